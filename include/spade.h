@@ -1,0 +1,225 @@
+/*
+ * spade.h -- C ABI of the speculative-verify library for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The library implements the cloud side of speculative decoding as SPADE
+ * (arXiv 2608.13076) uses it: the verifier M_p scores d draft tokens in one
+ * forward pass over d+1 positions (Algorithm 1, the "Cloud" step), accepts
+ * the longest verified prefix, replaces the first rejected draft by a draw
+ * from p'(x) = norm(max(0, p(x) - q(x))) (Sec. III-C, "Verification
+ * criterion"), and updates the context (m <- m + k + 1).  The draft length d
+ * is called gamma below.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All device memory belongs to the caller: weights, workspace, KV cache,
+ *   inputs and outputs.  The library never allocates or frees device memory;
+ *   its handles own small host structures only.
+ * - Pointers prefixed d_ are device pointers, h_ are host pointers.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *   call that takes a stream is asynchronous and stream-ordered unless its
+ *   comment says it synchronises.
+ * - Calls return SPADE_OK or a negative spade_status and never throw.  On
+ *   error nothing is launched and spade_last_error() holds a message (per
+ *   thread).
+ * - Token ids are int32 in [0, vocab).  Out-of-range ids found on the device
+ *   are clamped and flagged in the device error word (spade_get_device_error).
+ * - A model and the KV handles built on it must be used from one stream at a
+ *   time: calls share the workspace.
+ */
+#ifndef SPADE_H
+#define SPADE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct spade_model_s* spade_model;
+typedef struct spade_kv_s* spade_kv;
+
+typedef enum {
+  SPADE_OK = 0,
+  SPADE_EINVAL = -1,       /* bad argument (null pointer, range, shape)        */
+  SPADE_ECAPACITY = -2,    /* batch, gamma or KV capacity exceeded             */
+  SPADE_EHIP = -3,         /* a HIP runtime call failed                        */
+  SPADE_EUNSUPPORTED = -4, /* shape the kernels do not handle (see config)     */
+  SPADE_EDEVICE = -5       /* device error word non-zero                       */
+} spade_status;
+
+enum { SPADE_GREEDY = 0, SPADE_SAMPLE = 1 };
+enum { SPADE_F32 = 0, SPADE_BF16 = 1 };
+
+/* Bits of the device error word. */
+enum {
+  SPADE_DERR_TOKEN = 1u,    /* a token id was outside [0, vocab); clamped      */
+  SPADE_DERR_NAN = 2u,      /* a logit was NaN                                  */
+  SPADE_DERR_RESIDUAL = 4u, /* max(0, p - q) had no mass; drew from p instead   */
+  SPADE_DERR_NOQ = 8u       /* a sampling request got no draft_probs; greedy    */
+};
+
+/* Weight tensors, row-major [out_features, in_features] unless noted. */
+enum {
+  SPADE_WQ = 0,     /* [d_model, d_model]                                  */
+  SPADE_WK = 1,     /* [d_model, d_model]                                  */
+  SPADE_WV = 2,     /* [d_model, d_model]                                  */
+  SPADE_WO = 3,     /* [d_model, d_model]                                  */
+  SPADE_WGATE = 4,  /* [d_ffn, d_model]                                    */
+  SPADE_WUP = 5,    /* [d_ffn, d_model]                                    */
+  SPADE_WDOWN = 6,  /* [d_model, d_ffn]                                    */
+  SPADE_G_ATTN = 7, /* [d_model] float32 gain of the attention RMSNorm     */
+  SPADE_G_FFN = 8,  /* [d_model] float32 gain of the feed-forward RMSNorm  */
+  SPADE_EMBED = 9,  /* [vocab, d_model]                                    */
+  SPADE_G_FINAL = 10, /* [d_model] float32 gain of the final RMSNorm       */
+  SPADE_LM_HEAD = 11  /* [vocab, d_model]                                  */
+};
+
+/*
+ * The verifier: a pre-RMSNorm decoder (Sec. III-A: embedding, L blocks
+ * x_{l+1} = x_l + f_l(x_l) with f_l = attention then feed-forward, LM head,
+ * softmax).  Attention is multi-head with rotary position embedding
+ * (rotate-half pairing of feature i with i + head_dim/2, angle
+ * pos * rope_theta^(-2i/head_dim)); the feed-forward is SwiGLU
+ * (silu(h W_gate^T) * (h W_up^T)) W_down^T; RMSNorm(x) = x / sqrt(mean(x^2)
+ * + rms_eps) * g; no biases; the LM head is untied.
+ *
+ * weight_dtype: SPADE_BF16 or SPADE_F32 for every matrix (gains are float32).
+ * kv_dtype: storage type of K and V (RoPE is applied before storing).
+ * Supported: head_dim 64 or 128; d_model = n_heads * head_dim; d_model and
+ * d_ffn multiples of 256 (bf16 weights) or 128 (f32); any vocab >= 2; at most
+ * 15 drafts per request (gamma + 1 <= 16 rows).
+ */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab;
+  int32_t weight_dtype, kv_dtype;
+  float rms_eps, rope_theta;
+} spade_config;
+
+/* Bytes of the library's weight arena (its own tiled layout; filled by
+ * spade_model_load_tensor).  0 if the config is unsupported. */
+size_t spade_weight_bytes(const spade_config* cfg);
+
+/* Bytes of the workspace for calls with up to max_batch requests of up to
+ * max_gamma drafts each and caches of up to max_len positions. */
+size_t spade_workspace_bytes(const spade_config* cfg, int max_batch, int max_gamma, int max_len);
+
+/* Bytes of a KV cache holding max_batch requests of max_len positions:
+ * K then V, each [n_layers][max_batch][n_heads][max_len][head_dim]. */
+size_t spade_kv_bytes(const spade_config* cfg, int max_batch, int max_len);
+
+/* Create a model over caller-owned device buffers: d_weights of
+ * spade_weight_bytes() and d_workspace of spade_workspace_bytes() bytes
+ * (256-byte aligned).  Synchronises once: writes the RoPE table and clears the
+ * workspace's counters and error word on the current device. */
+spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* d_workspace,
+                                int max_batch, int max_gamma, int max_len, spade_model* out);
+
+/* Copy one tensor (kind = SPADE_WQ .. SPADE_LM_HEAD; layer ignored for the
+ * three global tensors) from a row-major device buffer into the arena,
+ * re-tiling matrices for the GEMM kernels.  d_src holds bf16 bits (uint16) or
+ * float32 as weight_dtype says; gains are always float32.  The source may be
+ * freed once the stream has passed this call. */
+spade_status spade_model_load_tensor(spade_model m, int kind, int layer, const void* d_src, void* stream);
+
+/* Wrap a caller-owned KV buffer of spade_kv_bytes(cfg, max_batch, max_len)
+ * bytes plus device int32 arrays lens[max_batch] (cached positions per
+ * request) and pending[max_batch] (the token whose row has not been computed
+ * yet: the last prompt token, then each round's correction).  lens and
+ * pending start at 0. */
+spade_status spade_kv_create(spade_model m, void* d_kv, int max_batch, int max_len,
+                             int32_t* d_lens, int32_t* d_pending, spade_kv* out);
+
+/* Set lens[0..B) and pending[0..B) from host arrays (a snapshot restore). */
+spade_status spade_kv_set_state(spade_kv kv, int B, const int32_t* h_lens,
+                                const int32_t* h_pending, void* stream);
+
+/* Read lens and pending to the host.  Synchronises the stream. */
+spade_status spade_kv_get_state(spade_kv kv, int B, int32_t* h_lens, int32_t* h_pending, void* stream);
+
+/* Device-to-device restore of lens/pending from d_lens/d_pending [B]. */
+spade_status spade_kv_restore(spade_kv kv, int B, const int32_t* d_lens, const int32_t* d_pending,
+                              void* stream);
+
+/* Prefill request b: run d_tokens[0 .. n_tokens-2] through the verifier,
+ * appending their K/V at positions lens[b] .. lens[b] + n_tokens - 2, and make
+ * d_tokens[n_tokens-1] the pending token (no logits are produced).  This is
+ * the context y_{1:m} of Algorithm 1's input. */
+spade_status spade_prefill(spade_model m, spade_kv kv, int b, const int32_t* d_tokens,
+                           int n_tokens, void* stream);
+
+/*
+ * spade_verify -- one cloud verification of gamma drafts for B requests
+ * (Algorithm 1, Cloud step; Sec. III-C).
+ *
+ * For request b the rows [pending_b, d_b,1 .. d_b,gamma] are appended at
+ * positions lens[b] .. lens[b] + gamma and run through the verifier in one
+ * pass; row i gives p_i = softmax(logits_i / T), the distribution of the token
+ * after d_b,i (row gamma: after the last draft).  Then, left to right:
+ *   greedy (mode SPADE_GREEDY): d_b,i+1 is accepted iff it is the argmax of
+ *     row i (ties: lowest id);
+ *   sampling (SPADE_SAMPLE): accepted iff u_b,i * q_b,i(d) < p_b,i(d), in
+ *     float32, i.e. with probability min(1, p/q).
+ * n_accepted[b] = k, the number accepted before the first rejection (0..gamma).
+ * correction[b] = the token that follows the k accepted drafts:
+ *   greedy: the argmax of row k;
+ *   sampling, k < gamma: a draw from norm(max(0, p_k - q_k));
+ *   sampling, k = gamma: a draw from p_gamma (no draft distribution there).
+ * Draws use Gumbel-max, argmax_v (log w_v + G_v), with G_v = -log(-log U_v),
+ * U_v = ((x_v >> 41) + 0.5) * 2^-23 and x_v output v (0-based) of a SplitMix64
+ * stream seeded with the float32 bits of u_b,gamma.
+ *
+ * d_draft_tokens  int32 [B, gamma] (may be NULL when gamma == 0)
+ * d_draft_probs   float32 [B, gamma, vocab] draft distributions q, already
+ *                 tempered, used as given; may be NULL if no request samples
+ *                 or gamma == 0 (a sampling request without q is verified
+ *                 greedily and flags SPADE_DERR_NOQ)
+ * d_uniforms      float32 [B, gamma + 1] in [0, 1); NULL if no request samples
+ * d_mode          uint8 [B], SPADE_GREEDY or SPADE_SAMPLE
+ * temperature     finite and > 0; applied to sampling requests (greedy ignores it)
+ * d_n_accepted    int32 [B] out
+ * d_correction    int32 [B] out
+ * d_logits        float32 [B, gamma + 1, vocab] out (raw logits), or NULL
+ *
+ * The KV rows of all gamma+1 positions are written but lens is unchanged, so
+ * the call can be repeated (idempotent) until spade_kv_commit.  Requires
+ * lens[b] + gamma + 1 <= max_len (checked against the host-side upper bound
+ * of lens) and B <= max_batch, gamma <= max_gamma.
+ */
+spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma,
+                          const int32_t* d_draft_tokens, const float* d_draft_probs,
+                          const float* d_uniforms, const uint8_t* d_mode, float temperature,
+                          int32_t* d_n_accepted, int32_t* d_correction, float* d_logits,
+                          void* stream);
+
+/* Context update after spade_verify (Algorithm 1: append the k accepted
+ * tokens and the correction, m <- m + k + 1): lens[b] += n_accepted[b] + 1 and
+ * pending[b] = correction[b], on the device.  KV rows past the new length are
+ * the rolled-back drafts; they are overwritten by the next round. */
+spade_status spade_kv_commit(spade_kv kv, int B, const int32_t* d_n_accepted,
+                             const int32_t* d_correction, void* stream);
+
+/* Accept/reject and correction alone, from given logits (the last stage of
+ * spade_verify).  d_logits float32 [B, gamma + 1, V]; other arguments as in
+ * spade_verify.  Needs a model only for its workspace: V <= cfg.vocab. */
+spade_status spade_accept_from_logits(spade_model m, int B, int gamma, int V, const float* d_logits,
+                                      const int32_t* d_draft_tokens, const float* d_draft_probs,
+                                      const float* d_uniforms, const uint8_t* d_mode,
+                                      float temperature, int32_t* d_n_accepted,
+                                      int32_t* d_correction, void* stream);
+
+/* Read and clear the device error word.  Synchronises the stream. */
+spade_status spade_get_device_error(spade_model m, uint32_t* h_flags, void* stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* spade_last_error(void);
+
+void spade_model_destroy(spade_model m);
+void spade_kv_destroy(spade_kv kv);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPADE_H */

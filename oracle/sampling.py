@@ -13,7 +13,7 @@ sampling method.  Two exact samplers are stated here:
               (Steele, Lea and Flood, OOPSLA 2014: the state advances by
               0x9E3779B97F4A7C15 and each output is the state passed through
               the variant-13 mixer 30/0xBF58476D1CE4E5B9/27/0x94D049BB133111EB/31),
-      U_v   = ((x_v >> 40) + 0.5) * 2^-24   (exact in float32 and float64),
+      U_v   = ((x_v >> 41) + 0.5) * 2^-23   (exact in float32 and float64),
       G_v   = -log(-log(U_v)).
 * ``inverse_cdf_draw``: the smallest v whose cumulative mass exceeds u * sum(w),
   in ascending token order -- the literal reading, used only as a second,
@@ -47,7 +47,7 @@ def uniform_seed(u: float) -> int:
 def gumbel_noise(seed: int, n: int) -> np.ndarray:
     """G_v, v < n, in float64."""
     x = splitmix64_stream(seed, n)
-    U = ((x >> np.uint64(40)).astype(np.float64) + 0.5) * 2.0 ** -24
+    U = ((x >> np.uint64(41)).astype(np.float64) + 0.5) * 2.0 ** -23
     return -np.log(-np.log(U))
 
 

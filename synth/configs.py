@@ -121,11 +121,11 @@ def workload(name: str) -> Workload:
 # 16-row panels and several 256-wide k-blocks; the vocab has a ragged tail
 # (not a multiple of 16); gains are random.
 MINI_BF16 = ModelShape("mini-bf16", n_layers=2, d_model=512, n_heads=4, head_dim=128,
-                       d_ffn=1536, vocab=4001, gain_std=0.1)
+                       d_ffn=1536, vocab=4001, init_std=0.06, gain_std=0.1)
 MINI_BF16_WIDE = ModelShape("mini-bf16-wide", n_layers=3, d_model=1024, n_heads=8,
-                            head_dim=128, d_ffn=2816, vocab=8011, gain_std=0.1)
+                            head_dim=128, d_ffn=2816, vocab=8011, init_std=0.05, gain_std=0.1)
 MINI_F32 = ModelShape("mini-f32", n_layers=2, d_model=256, n_heads=4, head_dim=64,
-                      d_ffn=768, vocab=1999, weight_dtype="f32", kv_dtype="f32",
+                      d_ffn=768, vocab=1999, weight_dtype="f32", kv_dtype="f32", init_std=0.06,
                       gain_std=0.1)
 
 

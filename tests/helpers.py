@@ -1,0 +1,139 @@
+"""Shared test helpers: build a workload's inputs with the oracle, run the
+oracle verify, run the HIP verify through the C ABI, compare them."""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+from oracle import GREEDY, SAMPLE, Decoder, verify as oracle_verify
+from oracle.speculative import _argmax_f32
+from synth import ModelWeights, make_inputs
+from synth.inputs import draw_from, softmax64
+
+LOGIT_TOL = {"f32": 1e-4, "bf16": 5e-2}
+
+
+@dataclass
+class OracleRun:
+    inputs: object
+    results: list
+    caches: list
+    chains: list = field(default_factory=list)
+
+
+def complete_drafts(dec: Decoder, inp, caches) -> None:
+    """Fill the draft slots that depend on the verifier (chain_half,
+    draft_model recipes) using the oracle, in place."""
+    w = inp.workload
+    G, V = w.gamma, w.model.vocab
+    for b, rec in enumerate(inp.recipe):
+        if rec == "chain_half" and G > 0:
+            c = caches[b].copy()
+            cur, chain = int(inp.pending[b]), []
+            for _ in range(min(inp.chain_slots + 1, G + 1)):
+                cur = _argmax_f32(dec.forward(c, [cur])[0])
+                chain.append(cur)
+            k = inp.chain_slots
+            inp.drafts[b, :k] = chain[:k]
+            if k < G and inp.drafts[b, k] == chain[k]:
+                inp.drafts[b, k] = (chain[k] + 1) % V
+        elif rec == "draft_model":
+            c = caches[b].copy()
+            cur = int(inp.pending[b])
+            for i in range(G):
+                lg = dec.forward(c, [cur])[0]
+                q = softmax64(lg / inp.temperature + inp.q_noise[b, i].astype(np.float64))
+                inp.draft_probs[b, i] = q.astype(np.float32)
+                cur = draw_from(inp.draft_probs[b, i], inp.draft_u[b, i])
+                inp.drafts[b, i] = cur
+
+
+def oracle_run(w, inp=None, weights: Optional[ModelWeights] = None, cap: Optional[int] = None,
+               keep_f64: bool = True) -> OracleRun:
+    shape = w.model
+    weights = weights or ModelWeights(shape, w.seed)
+    dec = Decoder(shape, weights.get, keep_f64=keep_f64)
+    inp = inp or make_inputs(w)
+    cap = cap or int(inp.lens.max()) + 2 * (w.gamma + 1) + 1
+    caches = []
+    for b in range(w.batch):
+        c = dec.new_cache(cap)
+        dec.prefill(c, inp.prompts[b][:-1])
+        caches.append(c)
+    complete_drafts(dec, inp, caches)
+    results = []
+    for b in range(w.batch):
+        q = inp.draft_probs[b] if inp.modes[b] == SAMPLE else None
+        results.append(oracle_verify(dec, caches[b], inp.pending[b], inp.drafts[b], q, inp.uniforms[b],
+                                     int(inp.modes[b]), inp.temperature))
+    return OracleRun(inp, results, caches)
+
+
+@dataclass
+class Parity:
+    logit_err: float
+    n_match_all: int
+    corr_match_all: int
+    pinned_n: int
+    pinned_corr: int
+    pinned_n_fail: List[int]
+    pinned_corr_fail: List[int]
+    excluded_n: int
+    excluded_corr: int
+    total: int
+
+
+def compare(orun: OracleRun, gpu_logits: np.ndarray, gpu_n: np.ndarray, gpu_corr: np.ndarray) -> Parity:
+    errs = [np.abs(gpu_logits[b].astype(np.float64) - r.logits).max() for b, r in enumerate(orun.results)]
+    p = Parity(float(max(errs)), 0, 0, 0, 0, [], [], 0, 0, len(orun.results))
+    for b, r in enumerate(orun.results):
+        nm = int(gpu_n[b]) == r.n_accepted
+        cm = int(gpu_corr[b]) == r.correction
+        p.n_match_all += nm
+        p.corr_match_all += nm and cm
+        if r.pinned_n:
+            p.pinned_n += 1
+            if not nm:
+                p.pinned_n_fail.append(b)
+        else:
+            p.excluded_n += 1
+        if r.pinned_correction:
+            p.pinned_corr += 1
+            if not (nm and cm):
+                p.pinned_corr_fail.append(b)
+        else:
+            p.excluded_corr += 1
+    return p
+
+
+def gpu_setup(w, weights: Optional[ModelWeights] = None, max_len: Optional[int] = None, max_batch=None):
+    from paper_2608_13076_amd import spade
+    shape = w.model
+    weights = weights or ModelWeights(shape, w.seed)
+    max_len = max_len or (w.ctx[1] + 2 * (w.gamma + 1) + 8)
+    model = spade.Model(shape, max_batch or w.batch, w.gamma, max_len)
+    for layer in range(shape.n_layers):
+        for kind in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "g_attn", "g_ffn"):
+            model.load_numpy(kind, layer, weights.get(kind, layer))
+    for kind in ("embed", "g_final", "lm_head"):
+        model.load_numpy(kind, None, weights.get(kind))
+    kv = spade.KVCache(model, max_batch or w.batch, max_len)
+    return model, kv
+
+
+def gpu_prefill(kv, inp) -> None:
+    for b, pr in enumerate(inp.prompts):
+        kv.prefill(b, pr)
+
+
+def gpu_verify(model, kv, inp, want_logits=True):
+    import torch
+    from paper_2608_13076_amd import spade
+    buf = spade.VerifyBuffers(model, inp.drafts, inp.draft_probs, inp.uniforms, inp.modes, want_logits)
+    spade.verify(model, kv, buf, inp.temperature)
+    torch.cuda.synchronize()
+    lg = buf.logits.cpu().numpy() if want_logits else None
+    return lg, buf.n.cpu().numpy(), buf.corr.cpu().numpy(), buf

@@ -1,0 +1,66 @@
+"""HIP verify path vs the oracle on the same seeded inputs, through the C ABI.
+
+Bar (per request): logits within 1e-4 (fp32 weights) or 5e-2 (bf16) max
+abs error; n_accepted and the correction token bit-exact wherever the oracle
+marks the decision as decided (greedy top-2 margin > 0.1, |u - p/q| > 1e-3,
+draw gap > 1e-3).  Excluded positions are counted and printed.
+"""
+
+import numpy as np
+import pytest
+
+from synth import ModelWeights, make_inputs, mini_workloads, workload
+from tests.helpers import LOGIT_TOL, compare, gpu_prefill, gpu_setup, gpu_verify, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run_rounds(w, rounds):
+    weights = ModelWeights(w.model, w.seed)
+    model, kv = gpu_setup(w, weights)
+    agg = dict(n=0, pinned_n=0, pinned_c=0, excl_n=0, excl_c=0, all_n=0, all_c=0, err=0.0)
+    for k in range(rounds):
+        wk = w.with_(seed=w.seed * 1000 + k)
+        inp = make_inputs(wk)
+        orun = oracle_run(wk, inp, weights=weights)
+        print(f"[{w.name}] round {k}: prefill + verify", flush=True)
+        kv.set_state(np.zeros(w.batch, np.int32), np.zeros(w.batch, np.int32))
+        gpu_prefill(kv, inp)
+        lg, n, c, _ = gpu_verify(model, kv, inp)
+        p = compare(orun, lg, n, c)
+        assert not p.pinned_n_fail, (k, p)
+        assert not p.pinned_corr_fail, (k, p)
+        assert p.logit_err < LOGIT_TOL[w.model.weight_dtype], (k, p.logit_err)
+        agg["n"] += p.total
+        agg["pinned_n"] += p.pinned_n
+        agg["pinned_c"] += p.pinned_corr
+        agg["excl_n"] += p.excluded_n
+        agg["excl_c"] += p.excluded_corr
+        agg["all_n"] += p.n_match_all
+        agg["all_c"] += p.corr_match_all
+        agg["err"] = max(agg["err"], p.logit_err)
+    print(f"[{w.name}] {agg}", flush=True)
+    assert model.device_error() == 0
+    return agg
+
+
+def test_c1_tiny_greedy():
+    agg = _run_rounds(workload("c1_tiny_greedy"), 24)
+    assert agg["pinned_n"] > 0
+
+
+def test_c1_tiny_sample():
+    agg = _run_rounds(workload("c1_tiny_sample"), 24)
+    assert agg["pinned_n"] > 0
+
+
+@pytest.mark.parametrize("w", mini_workloads(), ids=lambda w: w.name)
+def test_mini(w):
+    _run_rounds(w, 2)
