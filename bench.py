@@ -1,0 +1,216 @@
+"""Benchmark of one speculative-verify step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2_7b_greedy]
+
+A step is one pass of the whole hot path for one batch of synthetic input:
+spade_verify (embedding, every decoder layer, LM head, softmax, accept /
+reject, correction draw) + spade_kv_commit, followed by a device-side restore
+of the request lengths so every step verifies the same configuration.  The
+default workload is the Llama-7B-shaped bf16 verifier (32 layers, d_model
+4096, 32 heads x 128, SwiGLU 11008, vocab 32000), batch 1, 1024 cached tokens,
+gamma = 5, greedy, weights N(0, 0.02) from a seed.
+
+Printed: one JSON line with verified draft tokens/s (B * gamma / step time),
+the step latency, the whole-pass algorithmic bytes and their rate against the
+8 TB/s HBM peak, the dominant kernel's roofline (HIP events around that
+kernel alone, same launch configuration), and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w, lens) -> dict:
+    """Bytes one verify pass must move at minimum: every weight matrix and
+    gain once, the M gathered embedding rows, the cached K/V of every request
+    read once, the new K/V rows written once, the q rows of sampling
+    requests (their draft tokens' entries and the residual row)."""
+    m = w.model
+    elt = 2 if m.weight_dtype == "bf16" else 4
+    kvelt = 2 if m.kv_dtype == "bf16" else 4
+    d, f, v, L = m.d_model, m.d_ffn, m.vocab, m.n_layers
+    R = w.gamma + 1
+    M = w.batch * R
+    weights = L * (4 * d * d + 3 * d * f) * elt + L * 2 * d * 4 + v * d * elt + d * 4
+    embed = M * d * elt
+    kv_read = sum(int(l) + R for l in lens) * L * 2 * d * kvelt
+    kv_write = M * L * 2 * d * kvelt
+    return {"weights": weights, "embed": embed, "kv_read": kv_read, "kv_write": kv_write,
+            "total": weights + embed + kv_read + kv_write}
+
+
+def cpu_baseline(w, inp, layers: int) -> dict:
+    """The oracle, unchanged, on the first `layers` decoder layers of the same
+    model (same weights, same cached context, same rows), scaled to all
+    layers; the LM head and accept/reject are timed in full."""
+    from oracle import Decoder
+    from oracle import verify as oracle_verify
+    from synth import ModelWeights
+    m = w.model
+    part = m.__class__(**{**m.__dict__, "n_layers": layers})
+    mw = ModelWeights(m, w.seed)
+    dec = Decoder(part, mw.get, keep_f64=True)
+    b = 0
+    cache = dec.new_cache(int(inp.lens[b]) + w.gamma + 2)
+    t0 = time.perf_counter()
+    dec.prefill(cache, inp.prompts[b][:-1])
+    t_prefill = time.perf_counter() - t0
+    # warm the converted weights, then time the verify pass
+    reps = []
+    for _ in range(3):
+        c = cache.copy()
+        t0 = time.perf_counter()
+        oracle_verify(dec, c, inp.pending[b], inp.drafts[b], None, inp.uniforms[b], int(inp.modes[b]))
+        reps.append(time.perf_counter() - t0)
+    t_part = float(np.median(reps))
+    # LM head + accept share: time the last-stage alone (x -> logits -> accept)
+    t0 = time.perf_counter()
+    lm = dec.w("lm_head")
+    h = np.random.default_rng(0).standard_normal((w.gamma + 1, m.d_model))
+    for _ in range(3):
+        _ = h @ lm.T
+    t_lm = (time.perf_counter() - t0) / 3
+    t_layers = max(t_part - t_lm, 1e-9)
+    t_full = t_layers * m.n_layers / layers + t_lm
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    threads = int(os.environ.get("OMP_NUM_THREADS", cores))
+    mw.close()
+    return {"value": round(w.batch * w.gamma / t_full, 3), "unit": "draft tokens/s", "cores": min(cores, threads),
+            "kind": "oracle",
+            "sample": f"float64 NumPy oracle verify of batch 1 over the first {layers} of {m.n_layers} layers "
+                      f"(median of 3, prefill of {int(inp.lens[b])} tokens excluded, weights pre-converted), "
+                      f"scaled by {m.n_layers}/{layers}, plus the LM head",
+            "latency_us": round(t_full * 1e6, 1), "prefill_s_sample": round(t_prefill, 2)}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c2_7b_greedy")
+    ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-reps", type=int, default=20)
+    ap.add_argument("--all-kernels", action="store_true", help="also time every other projection GEMM")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        print("bench.py: only --gpus 1 is supported (single-GPU build)", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2608_13076_amd import spade
+    from synth import iter_weights, make_inputs, workload
+    from tests.golden.drafts import load_drafts
+
+    w = workload(args.workload)
+    m = w.model
+    inp = make_inputs(w)
+    drafts_src = load_drafts(w, inp)
+    log(f"workload {w.name}: {w.description}; drafts: {drafts_src}")
+
+    R = w.gamma + 1
+    max_len = int(inp.lens.max()) + 2 * R + 8
+    model = spade.Model(m, w.batch, w.gamma, max_len)
+    t0 = time.perf_counter()
+    for kind, layer, arr in iter_weights(m, w.seed):
+        model.load_numpy(kind, layer, arr)
+    log(f"weights generated + loaded in {time.perf_counter() - t0:.1f}s "
+        f"({model.weight_bytes() / 1e9:.2f} GB arena)")
+    kv = spade.KVCache(model, w.batch, max_len)
+    t0 = time.perf_counter()
+    for b in range(w.batch):
+        kv.prefill(b, inp.prompts[b])
+    log(f"prefill of {inp.lens.tolist()} tokens in {time.perf_counter() - t0:.1f}s")
+    lens0, pend0 = kv.snapshot(w.batch)
+    buf = spade.VerifyBuffers(model, inp.drafts, inp.draft_probs, inp.uniforms, inp.modes, want_logits=False)
+
+    def step():
+        spade.verify(model, kv, buf, inp.temperature)
+        kv.commit(buf.n, buf.corr)
+        kv.restore(lens0, pend0)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    ms = t / args.steps * 1e3
+    n_acc = buf.n.cpu().numpy()
+    log(f"{args.steps} steps: {ms:.3f} ms/step; n_accepted {n_acc.tolist()}")
+    if model.device_error() != 0:
+        log("device error word set")
+        return 1
+
+    ab = algorithmic_bytes(w, inp.lens)
+    gbs = ab["total"] / (ms * 1e-3) / 1e9
+
+    # Dominant kernel: the gate/up GEMM (45% of the weight bytes at this shape),
+    # timed alone with HIP events on the current stream, same launch config.
+    roof = spade.gemm_roofline(model, kv, "gu", w.batch, w.gamma, args.kernel_reps, HBM_PEAK_GBS)
+    log(f"dominant kernel: {roof}")
+    if args.all_kernels:
+        for kind in ("qkv", "o", "down", "lm"):
+            r = spade.gemm_roofline(model, kv, kind, w.batch, w.gamma, args.kernel_reps, HBM_PEAK_GBS)
+            log(f"gemm {kind}: {r['avg_launch_us']} us, {r['achieved']} GB/s ({r['frac']:.3f})")
+    kv.restore(lens0, pend0)
+
+    out = {
+        "metric": "verified draft tokens/sec and verify-pass latency (us); achieved HBM GB/s vs peak",
+        "value": round(w.batch * w.gamma / (ms * 1e-3), 2),
+        "unit": "draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "verify_latency_us": round(ms * 1e3, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 weights+KV, f32 activations" if m.weight_dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,0.02) weights, uniform prompt ids; no trained weights)",
+        "config": {"workload": w.name, "model": m.name, "batch": w.batch, "gamma": w.gamma,
+                   "cached_tokens": inp.lens.tolist(), "mode": w.mode, "drafts": drafts_src},
+        "algorithmic_bytes_per_step": ab["total"],
+        "achieved_GBps_whole_pass": round(gbs, 1),
+        "hbm_frac_whole_pass": round(gbs / HBM_PEAK_GBS, 4),
+        "emitted_tokens_per_call": float(np.mean(n_acc + 1)),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle on {args.cpu_layers} layers")
+        t0 = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_layers)
+        log(f"cpu baseline done in {time.perf_counter() - t0:.1f}s")
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

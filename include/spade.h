@@ -138,7 +138,11 @@ spade_status spade_kv_set_state(spade_kv kv, int B, const int32_t* h_lens,
 /* Read lens and pending to the host.  Synchronises the stream. */
 spade_status spade_kv_get_state(spade_kv kv, int B, int32_t* h_lens, int32_t* h_pending, void* stream);
 
-/* Device-to-device restore of lens/pending from d_lens/d_pending [B]. */
+/* Snapshot lens/pending [B] into caller device buffers (device-to-device) and
+ * remember the host-side capacity bound; spade_kv_restore copies them back and
+ * restores that bound.  Rows past the restored lengths are stale and get
+ * overwritten, so verify -> commit -> restore replays a round exactly. */
+spade_status spade_kv_snapshot(spade_kv kv, int B, int32_t* d_lens, int32_t* d_pending, void* stream);
 spade_status spade_kv_restore(spade_kv kv, int B, const int32_t* d_lens, const int32_t* d_pending,
                               void* stream);
 
@@ -208,6 +212,15 @@ spade_status spade_accept_from_logits(spade_model m, int B, int gamma, int V, co
                                       const float* d_uniforms, const uint8_t* d_mode,
                                       float temperature, int32_t* d_n_accepted,
                                       int32_t* d_correction, void* stream);
+
+/* Measurement hook: launch the GEMM kernel of one projection alone, exactly
+ * as spade_verify launches it for B requests of gamma drafts, `launches`
+ * times (layer = i mod n_layers), on the workspace's current operands.
+ * kind: 0 QKV (+RoPE, KV append), 1 O (+residual), 2 gate/up (+SiLU),
+ * 3 down (+residual), 4 LM head.  It overwrites workspace activations and
+ * cache rows past lens, so run it between verify calls, not inside a round. */
+spade_status spade_profile_gemm(spade_model m, spade_kv kv, int kind, int B, int gamma, int launches,
+                                void* stream);
 
 /* Read and clear the device error word.  Synchronises the stream. */
 spade_status spade_get_device_error(spade_model m, uint32_t* h_flags, void* stream);

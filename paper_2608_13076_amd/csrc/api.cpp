@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -85,8 +86,7 @@ ArenaLayout layout_of(const Dims& D) {
 }
 
 struct WsPlan {
-  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, inv_temp, tokens, err,
-      total;
+  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, total;
   size_t act_split, actf_split;
   int Mmax, NCmax, Rmax;
 };
@@ -95,9 +95,9 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   WsPlan p{};
   p.Rmax = std::max(max_gamma + 1, kPrefillRows);
   p.Mmax = std::max(max_batch * (max_gamma + 1), kPrefillRows);
-  p.NCmax = (max_len + kAttnChunkMin - 1) / kAttnChunkMin;
+  p.NCmax = std::min(kAttnMaxChunks, (max_len + kAttnChunkMin - 1) / kAttnChunkMin);
   const bool wb = D.wdt == SPADE_BF16;
-  const size_t ae = wb ? 2 * 3 : 4;  // three bf16 terms or one float
+  const size_t ae = wb ? 2 * kActSplits : 4;  // bf16 terms or one float
   p.act_split = (size_t)p.Mmax * D.d;
   p.actf_split = (size_t)p.Mmax * D.F;
   const int NU = D.Vpad / 16;
@@ -119,8 +119,6 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.logits = take((size_t)p.Mmax * D.V * 4);
   p.stats = take((size_t)p.Mmax * NU * 3 * 4);
   p.rope = take((size_t)max_len * (D.hd / 2) * 2 * 4);
-  p.inv_temp = take((size_t)max_batch * 4);
-  p.tokens = take((size_t)p.Mmax * 4);
   p.err = take(4);
   p.total = off;
   return p;
@@ -156,6 +154,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   if (!d_weights || !d_workspace || !out) return fail(SPADE_EINVAL, "null pointer");
   if (((uintptr_t)d_weights | (uintptr_t)d_workspace) & 255) return fail(SPADE_EINVAL, "buffers must be 256-byte aligned");
   if (max_batch < 1 || max_len < 2) return fail(SPADE_EINVAL, "max_batch >= 1 and max_len >= 2 required");
+  if (max_len > kMaxLen) return fail(SPADE_ECAPACITY, "max_len must be <= %d", kMaxLen);
   if (max_gamma < 0 || max_gamma + 1 > kMaxR) return fail(SPADE_ECAPACITY, "max_gamma must be in [0, %d]", kMaxR - 1);
   spade_model m = new (std::nothrow) spade_model_s();
   if (!m) return fail(SPADE_EINVAL, "out of host memory");
@@ -167,8 +166,18 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->max_batch = max_batch;
   m->max_gamma = max_gamma;
   m->max_len = max_len;
-  m->S = 3;
   (void)hipGetDevice(&m->device);
+  m->n_cu = 0;
+  if (hipDeviceGetAttribute(&m->n_cu, hipDeviceAttributeMultiprocessorCount, m->device) != hipSuccess ||
+      m->n_cu < 1)
+    m->n_cu = 256;
+  // one 8-wave GEMM workgroup per compute unit (the kernel needs two waves per
+  // SIMD); SPADE_GEMM_WGS overrides for experiments
+  m->gemm_wgs = m->n_cu;
+  if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
+    const int v = std::atoi(ev);
+    if (v > 0) m->gemm_wgs = v;
+  }
   const WsPlan p = plan_ws(m->dims, max_batch, max_gamma, max_len);
   Workspace& w = m->ws;
   uint8_t* b = m->work;
@@ -184,8 +193,6 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.logits = (float*)(b + p.logits);
   w.stats = (float*)(b + p.stats);
   w.rope = (float*)(b + p.rope);
-  w.inv_temp = (float*)(b + p.inv_temp);
-  w.tokens = (int32_t*)(b + p.tokens);
   w.err = (uint32_t*)(b + p.err);
   w.act_split = p.act_split;
   w.actf_split = p.actf_split;
@@ -246,7 +253,10 @@ spade_status spade_kv_create(spade_model m, void* d_kv, int max_batch, int max_l
   kv->max_batch = max_batch;
   kv->max_len = max_len;
   kv->lens_ub = new (std::nothrow) int[max_batch]();
-  if (!kv->lens_ub) {
+  kv->snap_ub = new (std::nothrow) int[max_batch]();
+  if (!kv->lens_ub || !kv->snap_ub) {
+    delete[] kv->lens_ub;
+    delete[] kv->snap_ub;
     delete kv;
     return fail(SPADE_EINVAL, "out of host memory");
   }
@@ -257,6 +267,7 @@ spade_status spade_kv_create(spade_model m, void* d_kv, int max_batch, int max_l
 void spade_kv_destroy(spade_kv kv) {
   if (!kv) return;
   delete[] kv->lens_ub;
+  delete[] kv->snap_ub;
   delete kv;
 }
 
@@ -288,15 +299,25 @@ spade_status spade_kv_get_state(spade_kv kv, int B, int32_t* h_lens, int32_t* h_
   return SPADE_OK;
 }
 
+spade_status spade_kv_snapshot(spade_kv kv, int B, int32_t* d_lens, int32_t* d_pending, void* stream) {
+  if (!kv || !d_lens || !d_pending) return fail(SPADE_EINVAL, "null pointer");
+  if (B < 1 || B > kv->max_batch) return fail(SPADE_ECAPACITY, "B out of range");
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipMemcpyAsync(d_lens, kv->lens, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess) e = hipMemcpyAsync(d_pending, kv->pending, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
+  if (e != hipSuccess) return hipfail(e, "kv_snapshot");
+  for (int b = 0; b < kv->max_batch; ++b) kv->snap_ub[b] = kv->lens_ub[b];
+  return SPADE_OK;
+}
+
 spade_status spade_kv_restore(spade_kv kv, int B, const int32_t* d_lens, const int32_t* d_pending, void* stream) {
   if (!kv || !d_lens || !d_pending) return fail(SPADE_EINVAL, "null pointer");
   if (B < 1 || B > kv->max_batch) return fail(SPADE_ECAPACITY, "B out of range");
   hipStream_t st = (hipStream_t)stream;
-  // lens only grow between a snapshot and its restore, so the host upper
-  // bound stays valid.
   hipError_t e = hipMemcpyAsync(kv->lens, d_lens, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
   if (e == hipSuccess) e = hipMemcpyAsync(kv->pending, d_pending, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
   if (e != hipSuccess) return hipfail(e, "kv_restore");
+  for (int b = 0; b < B; ++b) kv->lens_ub[b] = kv->snap_ub[b];
   return SPADE_OK;
 }
 
@@ -350,10 +371,27 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
   fc.drafts = d_draft_tokens;
   fc.want_logits = true;
   fc.logits_out = d_logits ? d_logits : m->ws.logits;
+  fc.mode = d_mode;
+  fc.inv_T = 1.0f / temperature;
+  fc.have_q = d_uniforms != nullptr && (d_draft_probs != nullptr || gamma == 0);
   hipError_t e = launch_forward(m, kv, fc, st);
-  if (e == hipSuccess)
-    e = launch_accept(m, B, gamma, m->dims.V, fc.logits_out, false, d_draft_tokens, d_draft_probs, d_uniforms,
-                      d_mode, temperature, d_n_accepted, d_correction, st);
+  if (e == hipSuccess) {
+    AcceptCall ac{};
+    ac.B = B;
+    ac.gamma = gamma;
+    ac.V = m->dims.V;
+    ac.logits = fc.logits_out;
+    ac.stats = m->ws.stats;
+    ac.NU = m->dims.Vpad / 16;
+    ac.drafts = d_draft_tokens;
+    ac.q = d_draft_probs;
+    ac.u = d_uniforms;
+    ac.mode = d_mode;
+    ac.inv_T = fc.inv_T;
+    ac.n_out = d_n_accepted;
+    ac.corr_out = d_correction;
+    e = launch_accept(m, ac, st);
+  }
   if (e != hipSuccess) return hipfail(e, "verify");
   return SPADE_OK;
 }
@@ -381,9 +419,45 @@ spade_status spade_accept_from_logits(spade_model m, int B, int gamma, int V, co
   if (d_draft_probs && !d_uniforms) return fail(SPADE_EINVAL, "sampling needs uniforms");
   if (!(temperature > 0.f && std::isfinite(temperature)))
     return fail(SPADE_EINVAL, "temperature must be finite and > 0");
-  hipError_t e = launch_accept(m, B, gamma, V, d_logits, false, d_draft_tokens, d_draft_probs, d_uniforms, d_mode,
-                               temperature, d_n_accepted, d_correction, (hipStream_t)stream);
+  AcceptCall ac{};
+  ac.B = B;
+  ac.gamma = gamma;
+  ac.V = V;
+  ac.logits = d_logits;
+  ac.stats = nullptr;
+  ac.drafts = d_draft_tokens;
+  ac.q = d_draft_probs;
+  ac.u = d_uniforms;
+  ac.mode = d_mode;
+  ac.inv_T = 1.0f / temperature;
+  ac.n_out = d_n_accepted;
+  ac.corr_out = d_correction;
+  hipError_t e = launch_accept(m, ac, (hipStream_t)stream);
   if (e != hipSuccess) return hipfail(e, "accept_from_logits");
+  return SPADE_OK;
+}
+
+spade_status spade_profile_gemm(spade_model m, spade_kv kv, int kind, int B, int gamma, int launches,
+                                void* stream) {
+  if (!m || !kv) return fail(SPADE_EINVAL, "null pointer");
+  if (kv->model != m) return fail(SPADE_EINVAL, "kv belongs to another model");
+  if (kind < GEMM_QKV || kind > GEMM_LM) return fail(SPADE_EINVAL, "bad GEMM kind %d", kind);
+  if (B < 1 || B > m->max_batch || B > kv->max_batch) return fail(SPADE_ECAPACITY, "B out of range");
+  if (gamma < 0 || gamma > m->max_gamma) return fail(SPADE_ECAPACITY, "gamma out of range");
+  if (launches < 1) return fail(SPADE_EINVAL, "launches must be >= 1");
+  for (int b = 0; b < B; ++b)
+    if (kv->lens_ub[b] + gamma + 1 > kv->max_len) return fail(SPADE_ECAPACITY, "KV capacity");
+  const int R = gamma + 1;
+  for (int i = 0; i < launches; ++i) {
+    ForwardCall fc{};
+    fc.b0 = 0;
+    fc.nb = B;
+    fc.R = R;
+    fc.logits_out = m->ws.logits;
+    fc.inv_T = 1.0f;
+    hipError_t e = launch_layer_gemm(m, kv, kind, i % m->dims.L, fc, (hipStream_t)stream);
+    if (e != hipSuccess) return hipfail(e, "profile_gemm");
+  }
   return SPADE_OK;
 }
 

@@ -7,20 +7,21 @@
 // the device.
 //
 // Kernels
-//   embed_kernel      x = E[token]; first GEMM operand and RMS partials
-//   gemm_kernel       Y = X W^T for skinny X (<= 32 rows), bf16 or f32 weights
-//                     streamed from a tiled arena, MFMA 16x16x32 bf16 (the fp32
-//                     activations split into three bf16 terms) or 16x16x4 f32,
-//                     with fused epilogues: RMSNorm scale + RoPE + KV append
-//                     (QKV), residual add + next RMS partials (O, down),
-//                     SiLU-gate (gate/up), logits (LM head)
-//   attn_kernel       multi-query causal attention of the gamma+1 rows over
-//                     the cache, split over key chunks; the last chunk to
-//                     finish merges the partials in a fixed order
-//   accept_kernel     per request: vocabulary-wide max / log-sum-exp / argmax
-//                     per row, the accept chain, the correction draw
-//   commit_kernel     lens += n + 1, pending = correction
-//   pack_kernel       row-major weights -> tiled arena
+//   embed_kernel   x = E[token]; first GEMM operand and RMS partials
+//   gemm_kernel    Y = X W^T for skinny X (<= 32 rows) against bf16 or f32
+//                  weights streamed from a tiled arena by persistent
+//                  workgroups, double-buffered; MFMA 16x16x32 bf16 (fp32
+//                  activations split into two bf16 terms) or 16x16x4 f32;
+//                  fused epilogues: RMSNorm scale + RoPE + KV append (QKV),
+//                  residual add + next RMS partials (O, down), SiLU gate
+//                  (gate/up), logits + per-panel softmax statistics (LM head)
+//   attn_kernel    multi-query causal attention of the gamma+1 rows over the
+//                  cache, split over key chunks; the chunk that finishes last
+//                  for a (request, head) merges the partials in chunk order
+//   accept_kernel  per request: vocabulary-wide max / log-sum-exp / argmax
+//                  per row, the accept chain, the Gumbel-max correction draw
+//   commit_kernel  lens += n + 1, pending = correction
+//   pack_kernel    row-major weights -> tiled arena
 #include "spade_internal.h"
 
 #include <float.h>
@@ -33,8 +34,6 @@ namespace spade {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float floatx4;
 
-constexpr int kS = 3;  // bf16 terms per fp32 activation (hi, mid, lo)
-
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 __device__ __forceinline__ uint16_t f2bf(float f) {
@@ -44,15 +43,15 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
-// Store v as the next GEMM's operand: three bf16 terms (bf16 weights) or the
-// float itself (fp32 weights).
+// Store v as the next GEMM's operand: kActSplits bf16 terms (bf16 weights:
+// hi = rne(v), lo = rne(v - hi)) or the float itself (fp32 weights).
 template <bool ABF16>
 __device__ __forceinline__ void store_act(void* base, size_t split, size_t idx, float v) {
   if constexpr (ABF16) {
     uint16_t* p = (uint16_t*)base;
     float r = v;
 #pragma unroll
-    for (int s = 0; s < kS; ++s) {
+    for (int s = 0; s < kActSplits; ++s) {
       const uint16_t h = f2bf(r);
       p[s * split + idx] = h;
       r -= bf2f(h);
@@ -115,18 +114,23 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedParams p) {
 // ---------------------------------------------------------------------------
 // Skinny GEMM with fused epilogues.
 //
-// Work unit = P weight panels (16 rows each) x all of K; one workgroup per
-// unit, NW waves splitting K into contiguous k-block ranges.  A wave streams
-// its k-blocks (8 KB per panel) with 16-byte loads: in the arena, slice j of
-// a k-block holds for lane l the 8 bf16 (4 f32) weights of row l%16 at
-// k = kb*256 + 32j + 8(l/16) (f32: kb*128 + 16j + 4(l/16)), exactly the B
-// operand of MFMA j, so every load instruction reads 1 KB contiguous.  The
-// A operand (activations, <= 32 rows) is read from L2 with the same k map.
-// Partial sums of the waves are reduced in LDS in wave order.
+// The arena stores a weight matrix as panels of 16 rows, each panel as its
+// k-blocks (256 k for bf16, 128 for f32) of 8 KB.  Slice j of a k-block holds
+// for lane l the 8 bf16 (4 f32) weights of panel row l%16 at
+// k = kb*256 + 32j + 8(l/16) (f32: kb*128 + 16j + 4(l/16)) -- the B operand of
+// MFMA j -- so each wave load instruction reads 1 KB contiguous.
+//
+// A persistent workgroup takes panels u = blockIdx.x, + gridDim.x, ...; its
+// NW waves split K into contiguous k-block ranges and walk a stream of
+// (panel, k-block) items, loading item t+1 while the MFMAs consume item t, so
+// the weight stream keeps going across panel boundaries while the partial
+// sums of a finished panel are reduced in LDS (in wave order) and its
+// epilogue runs.  The activations (<= 32 rows, A operand) come from L2 with
+// the same k map.
 // ---------------------------------------------------------------------------
 struct GemmParams {
   const uint8_t* w;
-  int NKB;
+  int NKB, n_units;
   int M, m0;
   const void* act;
   size_t act_split;
@@ -156,175 +160,256 @@ struct GemmParams {
   // LM
   float* logits;
   int V;
+  float* stats;
+  int NU;
+  const uint8_t* mode;
+  float inv_T;
+  int have_q;
   uint32_t* err;
 };
 
-template <bool WBF16, int P, int NW, int MT, int KIND>
-__global__ void __launch_bounds__(NW * 64) gemm_kernel(GemmParams a) {
-  const int u = blockIdx.x;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  __shared__ float red[NW][P][MT][4][64];
-  __shared__ float rinv_s[MT * 16];
+template <bool WBF16, int MT>
+struct Item {
+  static constexpr int S = WBF16 ? kActSplits : 1;
+  uint4 w[8];
+  uint4 a[MT][S][8];
+};
 
-  if (tid < MT * 16) {
-    float r = 1.f;
-    if (a.ssq_in != nullptr && tid < a.M) {
-      const float* sp = a.ssq_in + (size_t)(a.m0 + tid) * a.n_ssq;
-      float s = 0.f;
-      for (int i = 0; i < a.n_ssq; ++i) s += sp[i];
-      r = 1.0f / sqrtf(s * a.inv_din + a.eps);
+template <bool WBF16, int MT>
+__device__ __forceinline__ void load_w(Item<WBF16, MT>& it, const uint8_t* wp) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) it.w[j] = *(const uint4*)(wp + j * 1024);
+}
+
+template <bool WBF16, int MT>
+__device__ __forceinline__ void load_a(Item<WBF16, MT>& it, const GemmParams& a, int kb, int arow, int ag) {
+  constexpr int S = Item<WBF16, MT>::S;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int row = mt * 16 + arow;
+    const bool ok = row < a.M;
+    if constexpr (WBF16) {
+      const uint16_t* ap = (const uint16_t*)a.act + (size_t)(a.m0 + row) * a.act_stride + kb * 256 + ag * 8;
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          it.a[mt][s][j] = ok ? *(const uint4*)(ap + s * a.act_split + j * 32) : make_uint4(0, 0, 0, 0);
+    } else {
+      const float* ap = (const float*)a.act + (size_t)(a.m0 + row) * a.act_stride + kb * 128 + ag * 4;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) it.a[mt][0][j] = ok ? *(const uint4*)(ap + j * 16) : make_uint4(0, 0, 0, 0);
     }
-    rinv_s[tid] = r;
   }
+}
 
-  floatx4 acc[P][MT];
+template <bool WBF16, int MT>
+__device__ __forceinline__ void mma_item(const Item<WBF16, MT>& wsrc, const Item<WBF16, MT>& asrc, floatx4* acc) {
+  constexpr int S = Item<WBF16, MT>::S;
 #pragma unroll
-  for (int pp = 0; pp < P; ++pp)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[pp][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  const int NKB = a.NKB;
-  const int kb0 = (NKB * wave) / NW, kb1 = (NKB * (wave + 1)) / NW;
-  const uint8_t* wp = a.w + (size_t)u * NKB * P * kTileBytes + lane * 16;
-  const int arow = lane & 15, ag = lane >> 4;
-
-  for (int kb = kb0; kb < kb1; ++kb) {
-    uint4 wv[P][8];
-#pragma unroll
-    for (int pp = 0; pp < P; ++pp)
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        wv[pp][j] = *(const uint4*)(wp + ((size_t)kb * P + pp) * kTileBytes + j * 1024);
+  for (int j = 0; j < 8; ++j)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const int row = mt * 16 + arow;
-      const bool ok = row < a.M;
       if constexpr (WBF16) {
-        const uint16_t* ap = (const uint16_t*)a.act + (size_t)(a.m0 + row) * a.act_stride + kb * 256 + ag * 8;
-        uint4 av[kS][8];
 #pragma unroll
-        for (int s = 0; s < kS; ++s)
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            av[s][j] = ok ? *(const uint4*)(ap + s * a.act_split + j * 32) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-#pragma unroll
-          for (int pp = 0; pp < P; ++pp)
-#pragma unroll
-            for (int s = kS - 1; s >= 0; --s)
-              acc[pp][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  __builtin_bit_cast(bf16x8, av[s][j]), __builtin_bit_cast(bf16x8, wv[pp][j]),
-                  acc[pp][mt], 0, 0, 0);
+        for (int s = S - 1; s >= 0; --s)
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, asrc.a[mt][s][j]),
+                                                            __builtin_bit_cast(bf16x8, wsrc.w[j]), acc[mt], 0, 0, 0);
       } else {
-        const float* ap = (const float*)a.act + (size_t)(a.m0 + row) * a.act_stride + kb * 128 + ag * 4;
-        float4 av[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) av[j] = ok ? *(const float4*)(ap + j * 16) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-#pragma unroll
-          for (int pp = 0; pp < P; ++pp) {
-            const float4 w4 = __builtin_bit_cast(float4, wv[pp][j]);
-            acc[pp][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j].x, w4.x, acc[pp][mt], 0, 0, 0);
-            acc[pp][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j].y, w4.y, acc[pp][mt], 0, 0, 0);
-            acc[pp][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j].z, w4.z, acc[pp][mt], 0, 0, 0);
-            acc[pp][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j].w, w4.w, acc[pp][mt], 0, 0, 0);
-          }
+        const float4 w4 = __builtin_bit_cast(float4, wsrc.w[j]);
+        const float4 a4 = __builtin_bit_cast(float4, asrc.a[mt][0][j]);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.x, w4.x, acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.y, w4.y, acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.z, w4.z, acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.w, w4.w, acc[mt], 0, 0, 0);
       }
     }
-  }
+}
 
-#pragma unroll
-  for (int pp = 0; pp < P; ++pp)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) red[wave][pp][mt][r][lane] = acc[pp][mt][r];
-  __syncthreads();
-
-  // Epilogue: thread t <-> accumulator element (mt, r, lane) of every panel;
-  // D[i][j] of a 16x16 MFMA sits in lane j + 16*(i/4), register i%4, so the
-  // element is row m = mt*16 + 4*(lane/16) + r, panel column n = lane%16.
-  if (tid >= MT * 256) return;
-  const int emt = tid >> 8, er = (tid >> 6) & 3, eln = tid & 63;
-  const int ml = emt * 16 + 4 * (eln >> 4) + er;  // row within this launch
-  const int n = eln & 15;
-  float val[P];
-#pragma unroll
-  for (int pp = 0; pp < P; ++pp) {
-    float s = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) s += red[w][pp][emt][er][eln];
-    val[pp] = s;
-  }
+// Epilogue of panel p for the thread's accumulator element: row ml of this
+// launch, panel row n = lane % 16 (D[i][j] of a 16x16 MFMA sits in lane
+// j + 16*(i/4), register i%4).
+template <bool WBF16, int KIND>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int p, int ml, int n, float val, float rinv) {
   const bool rowok = ml < a.M;
   const int m = a.m0 + ml;  // row within the forward call
-  const float rinv = rinv_s[ml];
-
   if constexpr (KIND == GEMM_QKV) {
+    const int pps = a.d / 16, pph = a.hd / 16;
+    const int sec = p / pps, pw = p % pps;
+    const int h = pw / pph, wg = pw % pph;
+    const int pair = wg * 8 + (n & 7);
+    const bool hi = n >= 8;
+    const int f = pair + (hi ? a.hd / 2 : 0);
+    float v = val * rinv;
+    const float pv = __shfl_xor(v, 8);  // the RoPE partner
     if (!rowok) return;
-    const int upsec = a.d / 32, uph = a.hd / 32;
-    const int sec = u / upsec, rem = u % upsec;
-    const int h = rem / uph, wpan = rem % uph;
-    const int f0 = wpan * 16 + n, f1 = f0 + a.hd / 2;
-    float v0 = val[0] * rinv, v1 = val[1] * rinv;
     const int bl = m / a.R, i = m % a.R;
     const int bg = a.b0 + bl;
     const int pos = a.lens[bg] + i;
     if (sec < 2) {
-      const float* cs = a.rope + ((size_t)pos * (a.hd / 2) + f0) * 2;
+      const float* cs = a.rope + ((size_t)pos * (a.hd / 2) + pair) * 2;
       const float c = cs[0], sn = cs[1];
-      const float o0 = v0 * c - v1 * sn, o1 = v0 * sn + v1 * c;
-      v0 = o0;
-      v1 = o1;
+      v = hi ? (pv * sn + v * c) : (v * c - pv * sn);
     }
     if (sec == 0) {
-      a.q_out[(size_t)m * a.d + h * a.hd + f0] = v0;
-      a.q_out[(size_t)m * a.d + h * a.hd + f1] = v1;
+      a.q_out[(size_t)m * a.d + h * a.hd + f] = v;
     } else {
       void* cache = sec == 1 ? a.kc : a.vc;
-      const size_t off = (((size_t)bg * a.H + h) * a.max_len + pos) * a.hd;
-      if (a.kv_bf16) {
-        ((uint16_t*)cache)[off + f0] = f2bf(v0);
-        ((uint16_t*)cache)[off + f1] = f2bf(v1);
-      } else {
-        ((float*)cache)[off + f0] = v0;
-        ((float*)cache)[off + f1] = v1;
-      }
+      const size_t off = (((size_t)bg * a.H + h) * a.max_len + pos) * a.hd + f;
+      if (a.kv_bf16) ((uint16_t*)cache)[off] = f2bf(v);
+      else ((float*)cache)[off] = v;
     }
   } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
-    const int col = u * 16 + n;
+    const int col = p * 16 + n;
     float xv = 0.f;
     if (rowok) {
-      xv = a.x[(size_t)m * a.d + col] + val[0];
+      xv = a.x[(size_t)m * a.d + col] + val;
       a.x[(size_t)m * a.d + col] = xv;
       store_act<WBF16>(a.act_out, a.act_out_split, (size_t)m * a.act_out_stride + col, xv * a.g_next[col]);
     }
     float sq = xv * xv;
 #pragma unroll
     for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off);
-    if (rowok && n == 0) a.ssq_out[(size_t)m * a.n_ssq_out + u] = sq;
+    if (rowok && n == 0) a.ssq_out[(size_t)m * a.n_ssq_out + p] = sq;
   } else if constexpr (KIND == GEMM_GU) {
-    if (!rowok) return;
-    const int col = u * 16 + n;
-    const float gv = val[0] * rinv, uv = val[1] * rinv;
-    const float act = gv / (1.0f + expf(-gv)) * uv;
-    store_act<WBF16>(a.act_out, a.act_out_split, (size_t)m * a.act_out_stride + col, act);
-  } else {  // GEMM_LM
-    const int col = u * 16 + n;
-    if (!rowok || col >= a.V) return;
-    const float lg = val[0] * rinv;
-    if (lg != lg) flag_error(a.err, SPADE_DERR_NAN);
-    a.logits[(size_t)m * a.V + col] = lg;
+    const float v = val * rinv;
+    const float up = __shfl_xor(v, 8);
+    if (rowok && n < 8) {
+      const float act = v / (1.0f + expf(-v)) * up;
+      store_act<WBF16>(a.act_out, a.act_out_split, (size_t)m * a.act_out_stride + p * 8 + n, act);
+    }
+  } else {  // GEMM_LM: logits and the panel's (max, sum exp, argmax) of z = logit / T
+    const int col = p * 16 + n;
+    const bool valid = rowok && col < a.V;
+    const float lg = val * rinv;
+    bool samp = false;
+    if (rowok && a.mode != nullptr) {
+      const int bl = m / a.R;
+      samp = a.mode[bl] == SPADE_SAMPLE && a.have_q;
+    }
+    float z = -INFINITY;
+    int id = 0x7fffffff;
+    if (valid) {
+      a.logits[(size_t)m * a.V + col] = lg;
+      if (lg != lg) flag_error(a.err, SPADE_DERR_NAN);
+      else {
+        z = samp ? lg * a.inv_T : lg;
+        id = col;
+      }
+    }
+    float zm = z;
+    int am = id;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) {
+      const float oz = __shfl_xor(zm, off);
+      const int oa = __shfl_xor(am, off);
+      if (oz > zm || (oz == zm && oa < am)) {
+        zm = oz;
+        am = oa;
+      }
+    }
+    float e = (z == -INFINITY) ? 0.f : expf(z - zm);
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) e += __shfl_xor(e, off);
+    if (rowok && n == 0) {
+      float* st = a.stats + ((size_t)m * a.NU + p) * 3;
+      st[0] = zm;
+      st[1] = e;
+      st[2] = __int_as_float(am);
+    }
+  }
+}
+
+template <bool WBF16, int NW, int MT, int KIND>
+__global__ void __launch_bounds__(NW * 64) gemm_kernel(GemmParams a) {
+  constexpr bool ADBL = (MT == 1);  // double-buffer the activations too
+  __shared__ float red[NW][MT][4][64];
+  __shared__ float rinv_s[MT * 16];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int arow = lane & 15, ag = lane >> 4;
+  const int NKB = a.NKB;
+  const int nkw = (NKB + NW - 1) / NW;  // items per panel per wave (uniform)
+  const int kbl = (NKB * wave) / NW;
+  const int cnt = (NKB * (wave + 1)) / NW - kbl;  // real items of this wave
+  const int G = gridDim.x;
+  const int my_units = (a.n_units - (int)blockIdx.x + G - 1) / G;
+  const int T = my_units * nkw;
+  const uint8_t* wl = a.w + lane * 16;
+  const size_t unit_bytes = (size_t)NKB * kTileBytes;
+
+  Item<WBF16, MT> b0, b1;
+  floatx4 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  auto issue = [&](int t, Item<WBF16, MT>& buf) {
+    const int i = t % nkw;
+    if (i < cnt) {
+      const int u = (int)blockIdx.x + (t / nkw) * G;
+      load_w(buf, wl + (size_t)u * unit_bytes + (size_t)(kbl + i) * kTileBytes);
+      if constexpr (ADBL) load_a(buf, a, kbl + i, arow, ag);
+    }
+  };
+  auto unit_end = [&](int t) {
+    const int u = (int)blockIdx.x + (t / nkw) * G;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wave][mt][r][lane] = acc[mt][r];
+    __syncthreads();
+    if (tid < MT * 256) {
+      const int emt = tid >> 8, er = (tid >> 6) & 3, eln = tid & 63;
+      const int ml = emt * 16 + 4 * (eln >> 4) + er;
+      float val = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) val += red[w][emt][er][eln];
+      gemm_epilogue<WBF16, KIND>(a, u, ml, eln & 15, val, rinv_s[ml]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  };
+
+  if (T > 0) issue(0, b0);
+
+  // 1/rms of every row from the producer's per-panel sums of squares
+  {
+    const int row = tid >> 4, sub = tid & 15;
+    float s = 0.f;
+    if (a.ssq_in != nullptr && row < MT * 16 && row < a.M) {
+      const float* sp = a.ssq_in + (size_t)(a.m0 + row) * a.n_ssq;
+      for (int q = sub; q < a.n_ssq; q += 16) s += sp[q];
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    if (sub == 0 && row < MT * 16)
+      rinv_s[row] = (a.ssq_in != nullptr && row < a.M) ? 1.0f / sqrtf(s * a.inv_din + a.eps) : 1.0f;
+  }
+
+  for (int t = 0; t < T; t += 2) {
+    if constexpr (!ADBL) {
+      if (t % nkw < cnt) load_a(b0, a, kbl + t % nkw, arow, ag);
+    }
+    if (t + 1 < T) issue(t + 1, b1);
+    if (t % nkw < cnt) mma_item(b0, b0, acc);
+    if (t % nkw == nkw - 1) unit_end(t);
+    if (t + 1 >= T) break;
+    if constexpr (!ADBL) {
+      if ((t + 1) % nkw < cnt) load_a(b0, a, kbl + (t + 1) % nkw, arow, ag);
+    }
+    if (t + 2 < T) issue(t + 2, b0);
+    if ((t + 1) % nkw < cnt) mma_item(b1, ADBL ? b1 : b0, acc);
+    if ((t + 1) % nkw == nkw - 1) unit_end(t + 1);
   }
 }
 
 // ---------------------------------------------------------------------------
 // Verify attention.  Workgroup (chunk c, head h, request b): the R query rows
-// of the request against keys [c*CK, min((c+1)*CK, L_b + R)), key j visible
-// to row i iff j <= L_b + i (causal inside the appended block).  Sixteen
-// lanes share a key (HD/16 features each), four keys per wave step.  Each
+// of the request against keys [c*CK, min((c+1)*CK, L_b + R)); key j is
+// visible to row i iff j <= L_b + i (causal inside the appended block).
+// Scores: sixteen lanes share a key (HD/16 features each), four keys per wave
+// step, and a reduce-scatter over the sixteen lanes leaves each row's dot
+// product in one lane.  P V: each lane owns HD/64 output features.  Each
 // chunk writes (max, sum, unnormalised output) per row; the workgroup that
 // finishes last for (b, h) merges the chunks in chunk order and writes the
 // O-projection operand.
@@ -345,14 +430,11 @@ struct AttnParams {
   size_t act_split;
 };
 
-constexpr int kAttnMaxCK = 256;
-
-template <int HD, bool KVBF16>
+template <int N, bool KVBF16>
 __device__ __forceinline__ void load_kv(const void* base, size_t off, float* out) {
-  constexpr int DPL = HD / 16;
   if constexpr (KVBF16) {
     const uint16_t* p = (const uint16_t*)base + off;
-    if constexpr (DPL == 8) {
+    if constexpr (N == 8) {
       const uint4 v = *(const uint4*)p;
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -360,26 +442,47 @@ __device__ __forceinline__ void load_kv(const void* base, size_t off, float* out
         out[2 * e] = __uint_as_float(w[e] << 16);
         out[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
       }
+    } else if constexpr (N == 4) {
+      const uint2 v = *(const uint2*)p;
+      out[0] = __uint_as_float(v.x << 16);
+      out[1] = __uint_as_float(v.x & 0xffff0000u);
+      out[2] = __uint_as_float(v.y << 16);
+      out[3] = __uint_as_float(v.y & 0xffff0000u);
+    } else if constexpr (N == 2) {
+      const uint32_t v = *(const uint32_t*)p;
+      out[0] = __uint_as_float(v << 16);
+      out[1] = __uint_as_float(v & 0xffff0000u);
     } else {
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) out[e] = bf2f(p[e]);
+      for (int e = 0; e < N; ++e) out[e] = bf2f(p[e]);
     }
   } else {
     const float* p = (const float*)base + off;
+    if constexpr (N % 4 == 0) {
 #pragma unroll
-    for (int e = 0; e < DPL; e += 4) {
-      const float4 v = *(const float4*)(p + e);
-      out[e] = v.x;
-      out[e + 1] = v.y;
-      out[e + 2] = v.z;
-      out[e + 3] = v.w;
+      for (int e = 0; e < N; e += 4) {
+        const float4 v = *(const float4*)(p + e);
+        out[e] = v.x;
+        out[e + 1] = v.y;
+        out[e + 2] = v.z;
+        out[e + 3] = v.w;
+      }
+    } else if constexpr (N == 2) {
+      const float2 v = *(const float2*)p;
+      out[0] = v.x;
+      out[1] = v.y;
+    } else {
+#pragma unroll
+      for (int e = 0; e < N; ++e) out[e] = p[e];
     }
   }
 }
 
-template <int HD, bool KVBF16, bool ABF16>
+template <int HD, int RMAX, bool KVBF16, bool ABF16>
 __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
-  constexpr int DPL = HD / 16;
+  constexpr int DPL = HD / 16;  // score phase: features per lane
+  constexpr int DPV = HD / 64;  // P V phase: output features per lane
+  constexpr int RSH = (RMAX == 16) ? 0 : (RMAX == 8 ? 1 : 2);  // lanes per row after reduce-scatter: 1 << RSH
   const int c = blockIdx.x, h = blockIdx.y, bl = blockIdx.z;
   const int bg = p.b0 + bl;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -390,9 +493,10 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   const int k_lo = c * p.CK;
   const int k_hi = min(k_lo + p.CK, nkeys);
 
-  __shared__ float s_lds[kMaxR][kAttnMaxCK];
-  __shared__ float o_lds[4][kMaxR][HD];
-  __shared__ float m_lds[kMaxR], l_lds[kMaxR];
+  __shared__ float s_lds[RMAX][kAttnChunkMax];
+  __shared__ float o_lds[4][RMAX][HD];
+  __shared__ float m_lds[RMAX], l_lds[RMAX];
+  __shared__ float sc_lds[kAttnMaxChunks][RMAX];
   __shared__ int last_s;
 
   const size_t bh = (size_t)bl * p.H + h;
@@ -401,39 +505,61 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   const size_t kvbase = ((size_t)bg * p.H + h) * p.max_len * HD;
 
   if (k_lo < k_hi) {
-    // scores
-    float qr[kMaxR][DPL];
+    float qr[RMAX][DPL];
 #pragma unroll
-    for (int r = 0; r < kMaxR; ++r)
+    for (int r = 0; r < RMAX; ++r) {
+      if (r < R) {
+        const float* qp = p.q + (size_t)(bl * R + r) * p.d + h * HD + dg * DPL;
 #pragma unroll
-      for (int e = 0; e < DPL; ++e)
-        qr[r][e] = r < R ? p.q[(size_t)(bl * R + r) * p.d + h * HD + dg * DPL + e] : 0.f;
+        for (int e = 0; e < DPL; e += 4) {
+          const float4 v = *(const float4*)(qp + e);
+          qr[r][e] = v.x;
+          qr[r][e + 1] = v.y;
+          qr[r][e + 2] = v.z;
+          qr[r][e + 3] = v.w;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qr[r][e] = 0.f;
+      }
+    }
+    const int rr = dg >> RSH;                            // row this lane ends with
+    const bool writer = (dg & ((1 << RSH) - 1)) == 0 && rr < R;
     for (int kb = k_lo + 4 * wave; kb < k_hi; kb += 16) {
       const int k = kb + kg;
       float kv[DPL];
-      if (k < k_hi) load_kv<HD, KVBF16>(p.kc, kvbase + (size_t)k * HD + dg * DPL, kv);
+      if (k < k_hi) load_kv<DPL, KVBF16>(p.kc, kvbase + (size_t)k * HD + dg * DPL, kv);
       else {
 #pragma unroll
         for (int e = 0; e < DPL; ++e) kv[e] = 0.f;
       }
-      float dot[kMaxR];
+      float v[RMAX];
 #pragma unroll
-      for (int r = 0; r < kMaxR; ++r) {
+      for (int r = 0; r < RMAX; ++r) {
         float s = 0.f;
 #pragma unroll
         for (int e = 0; e < DPL; ++e) s += qr[r][e] * kv[e];
-        dot[r] = s;
+        v[r] = s;
       }
+      // reduce-scatter over the 16 lanes of the key
 #pragma unroll
-      for (int r = 0; r < kMaxR; ++r) {
+      for (int st = 0; st < 4; ++st) {
+        const int off = 8 >> st;
+        const int cur = RMAX >> st;
+        if (cur > 1) {
+          const int half = cur >> 1;
+          const bool up = (dg & off) != 0;
 #pragma unroll
-        for (int off = 8; off >= 1; off >>= 1) dot[r] += __shfl_xor(dot[r], off);
+          for (int j = 0; j < half; ++j) {
+            const float mine = up ? v[half + j] : v[j];
+            const float oth = up ? v[j] : v[half + j];
+            v[j] = mine + __shfl_xor(oth, off);
+          }
+        } else {
+          v[0] += __shfl_xor(v[0], off);
+        }
       }
-      float mine = 0.f;
-#pragma unroll
-      for (int r = 0; r < kMaxR; ++r)
-        if (r == dg) mine = dot[r];
-      if (k < k_hi && dg < R) s_lds[dg][k - k_lo] = (k <= L + dg) ? mine * p.scale : -INFINITY;
+      if (k < k_hi && writer) s_lds[rr][k - k_lo] = (k <= L + rr) ? v[0] * p.scale : -INFINITY;
     }
     __syncthreads();
     // chunk softmax, one wave per row
@@ -457,57 +583,42 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
       }
     }
     __syncthreads();
-    // P V
-    float acc[kMaxR][DPL];
+    // P V: wave w takes keys k_lo + w, + 4, ...; lane owns features lane*DPV ..
+    float acc[RMAX][DPV];
 #pragma unroll
-    for (int r = 0; r < kMaxR; ++r)
+    for (int r = 0; r < RMAX; ++r)
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[r][e] = 0.f;
-    for (int kb = k_lo + 4 * wave; kb < k_hi; kb += 16) {
-      const int k = kb + kg;
-      if (k < k_hi) {
-        float vv[DPL];
-        load_kv<HD, KVBF16>(p.vc, kvbase + (size_t)k * HD + dg * DPL, vv);
+      for (int e = 0; e < DPV; ++e) acc[r][e] = 0.f;
+    for (int k = k_lo + wave; k < k_hi; k += 4) {
+      float vv[DPV];
+      load_kv<DPV, KVBF16>(p.vc, kvbase + (size_t)k * HD + lane * DPV, vv);
+      const int kk = k - k_lo;
 #pragma unroll
-        for (int r = 0; r < kMaxR; ++r) {
-          if (r < R) {
-            const float pr = s_lds[r][k - k_lo];
+      for (int r = 0; r < RMAX; ++r) {
+        if (r < R) {
+          const float pr = s_lds[r][kk];
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) acc[r][e] += pr * vv[e];
-          }
+          for (int e = 0; e < DPV; ++e) acc[r][e] += pr * vv[e];
         }
       }
     }
 #pragma unroll
-    for (int r = 0; r < kMaxR; ++r)
+    for (int r = 0; r < RMAX; ++r)
+      if (r < R)
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) {
-        float v = acc[r][e];
-        v += __shfl_xor(v, 16);
-        v += __shfl_xor(v, 32);
-        acc[r][e] = v;
-      }
-    if (kg == 0) {
-#pragma unroll
-      for (int r = 0; r < kMaxR; ++r)
-        if (r < R)
-#pragma unroll
-          for (int e = 0; e < DPL; ++e) o_lds[wave][r][dg * DPL + e] = acc[r][e];
-    }
+        for (int e = 0; e < DPV; ++e) o_lds[wave][r][lane * DPV + e] = acc[r][e];
     __syncthreads();
     for (int idx = tid; idx < R * HD; idx += 256) {
       const int r = idx / HD, dd = idx % HD;
-      po[r * HD + dd] = o_lds[0][r][dd] + o_lds[1][r][dd] + o_lds[2][r][dd] + o_lds[3][r][dd];
+      po[r * HD + dd] = ((o_lds[0][r][dd] + o_lds[1][r][dd]) + o_lds[2][r][dd]) + o_lds[3][r][dd];
     }
     if (tid < R) {
       pml[tid * 2] = m_lds[tid];
       pml[tid * 2 + 1] = l_lds[tid];
     }
-  } else {
-    if (tid < R) {
-      pml[tid * 2] = -INFINITY;
-      pml[tid * 2 + 1] = 0.f;
-    }
+  } else if (tid < R) {
+    pml[tid * 2] = -INFINITY;
+    pml[tid * 2 + 1] = 0.f;
   }
 
   // the last chunk of (b, h) to arrive merges
@@ -522,20 +633,35 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   __threadfence();
   const float* po0 = p.part_o + (bh * p.NC * p.Rmax) * HD;
   const float* pml0 = p.part_ml + (bh * p.NC * p.Rmax) * 2;
-  for (int idx = tid; idx < R * HD; idx += 256) {
-    const int r = idx / HD, dd = idx % HD;
+  if (tid < R) {
+    const int r = tid;
     float M = -INFINITY;
-    for (int cc = 0; cc < p.NC; ++cc) M = fmaxf(M, __builtin_nontemporal_load(pml0 + ((size_t)cc * p.Rmax + r) * 2));
-    float Ls = 0.f, O = 0.f;
     for (int cc = 0; cc < p.NC; ++cc) {
       const float mc = __builtin_nontemporal_load(pml0 + ((size_t)cc * p.Rmax + r) * 2);
-      if (mc == -INFINITY) continue;
-      const float sc = expf(mc - M);
-      Ls += __builtin_nontemporal_load(pml0 + ((size_t)cc * p.Rmax + r) * 2 + 1) * sc;
-      O += __builtin_nontemporal_load(po0 + ((size_t)cc * p.Rmax + r) * HD + dd) * sc;
+      sc_lds[cc][r] = mc;
+      M = fmaxf(M, mc);
+    }
+    float Ls = 0.f;
+    for (int cc = 0; cc < p.NC; ++cc) {
+      const float mc = sc_lds[cc][r];
+      const float e = (mc == -INFINITY) ? 0.f : expf(mc - M);
+      Ls += __builtin_nontemporal_load(pml0 + ((size_t)cc * p.Rmax + r) * 2 + 1) * e;
+      sc_lds[cc][r] = e;
+    }
+    const float inv = 1.0f / Ls;
+    for (int cc = 0; cc < p.NC; ++cc) sc_lds[cc][r] *= inv;
+  }
+  __syncthreads();
+  for (int idx = tid; idx < R * HD; idx += 256) {
+    const int r = idx / HD, dd = idx % HD;
+    float O = 0.f;
+#pragma unroll 4
+    for (int cc = 0; cc < p.NC; ++cc) {
+      const float sc = sc_lds[cc][r];
+      if (sc != 0.f) O += __builtin_nontemporal_load(po0 + ((size_t)cc * p.Rmax + r) * HD + dd) * sc;
     }
     const int m = bl * R + r;
-    store_act<ABF16>(p.act_out, p.act_split, (size_t)m * p.d + h * HD + dd, O / Ls);
+    store_act<ABF16>(p.act_out, p.act_split, (size_t)m * p.d + h * HD + dd, O);
   }
   if (tid == 0) p.cnt[bh] = 0u;
 }
@@ -546,6 +672,8 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
 // ---------------------------------------------------------------------------
 struct AcceptParams {
   const float* logits;
+  const float* stats;
+  int NU;
   int V, gamma, R;
   const int32_t* drafts;
   const float* q;
@@ -571,38 +699,23 @@ __device__ __forceinline__ float gumbel_at(uint64_t seed, int v) {
   return -logf(-logf(U));
 }
 
-// (max, sum exp(z - max), argmax) merge; ties keep the lower id.
+// (max, sum exp(z - max), argmax); ties keep the lower id.
 struct RowStat {
   float m, s;
   int a;
 };
 
 __device__ __forceinline__ RowStat merge_stat(RowStat x, RowStat y) {
-  if (y.m > x.m || (y.m == x.m && y.a < x.a && y.m != -INFINITY)) {
+  if (y.m > x.m || (y.m == x.m && y.a < x.a)) {
     const RowStat t = x;
     x = y;
     y = t;
   }
-  // x has the larger max (or equal max with lower id)
   RowStat o;
   o.m = x.m;
   o.a = x.a;
   o.s = x.s + ((y.m == -INFINITY) ? 0.f : y.s * expf(y.m - x.m));
   return o;
-}
-
-__device__ __forceinline__ RowStat wave_merge(RowStat st) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    RowStat o;
-    o.m = __shfl_xor(st.m, off);
-    o.s = __shfl_xor(st.s, off);
-    o.a = __shfl_xor(st.a, off);
-    // combine in lane order so every lane reaches the same result
-    const bool lower = (threadIdx.x & off) == 0;
-    st = lower ? merge_stat(st, o) : merge_stat(o, st);
-  }
-  return st;
 }
 
 struct Best {
@@ -615,14 +728,17 @@ __device__ __forceinline__ Best better(Best x, Best y) {
   return x;
 }
 
-__global__ void __launch_bounds__(256) accept_kernel(AcceptParams p) {
+constexpr int kAcceptThreads = 1024;
+
+__global__ void __launch_bounds__(kAcceptThreads) accept_kernel(AcceptParams p) {
+  constexpr int NWV = kAcceptThreads / 64;
   const int b = blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int R = p.R, V = p.V, G = p.gamma;
-  __shared__ float rmax[kMaxR + 1], rlse[kMaxR + 1];
-  __shared__ int rarg[kMaxR + 1];
-  __shared__ RowStat part[4];
-  __shared__ Best bpart[4];
+  __shared__ float rlse[kMaxR];
+  __shared__ int rarg[kMaxR];
+  __shared__ RowStat part[NWV];
+  __shared__ Best bpart[NWV];
   __shared__ int n_s;
 
   bool sample = p.mode[b] == SPADE_SAMPLE;
@@ -633,22 +749,38 @@ __global__ void __launch_bounds__(256) accept_kernel(AcceptParams p) {
   const float invT = sample ? p.inv_T : 1.0f;
   const float* lg = p.logits + (size_t)b * R * V;
 
-  // row statistics over the vocabulary
+  // row statistics over the vocabulary (from the LM head's per-panel partials
+  // when given), merged in a fixed order
   for (int r = 0; r < R; ++r) {
     RowStat st{-INFINITY, 0.f, 0x7fffffff};
-    for (int v = tid; v < V; v += 256) {
-      const float z = lg[(size_t)r * V + v] * invT;
-      if (z != z) continue;
-      RowStat one{z, 1.f, v};
-      st = merge_stat(st, one);
+    if (p.stats != nullptr) {
+      const float* sp = p.stats + (size_t)(b * R + r) * p.NU * 3;
+#pragma unroll 2
+      for (int q = tid; q < p.NU; q += kAcceptThreads) {
+        const RowStat one{sp[q * 3], sp[q * 3 + 1], __float_as_int(sp[q * 3 + 2])};
+        if (one.m != -INFINITY) st = merge_stat(st, one);
+      }
+    } else {
+#pragma unroll 4
+      for (int v = tid; v < V; v += kAcceptThreads) {
+        const float z = lg[(size_t)r * V + v] * invT;
+        if (z != z) continue;
+        st = merge_stat(st, RowStat{z, 1.f, v});
+      }
     }
-    st = wave_merge(st);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      RowStat o;
+      o.m = __shfl_xor(st.m, off);
+      o.s = __shfl_xor(st.s, off);
+      o.a = __shfl_xor(st.a, off);
+      st = (lane & off) ? merge_stat(o, st) : merge_stat(st, o);
+    }
     if (lane == 0) part[wave] = st;
     __syncthreads();
     if (tid == 0) {
       RowStat t = part[0];
-      for (int w = 1; w < 4; ++w) t = merge_stat(t, part[w]);
-      rmax[r] = t.m;
+      for (int w = 1; w < NWV; ++w) t = merge_stat(t, part[w]);
       rlse[r] = t.m + logf(t.s);
       rarg[r] = t.a;
     }
@@ -692,7 +824,8 @@ __global__ void __launch_bounds__(256) accept_kernel(AcceptParams p) {
     for (int pass = 0; pass < 2; ++pass) {
       const bool use_res = residual && pass == 0;
       Best bst{-INFINITY, 0x7fffffff};
-      for (int v = tid; v < V; v += 256) {
+#pragma unroll 4
+      for (int v = tid; v < V; v += kAcceptThreads) {
         const float z = row[v] * invT;
         float sc;
         if (use_res) {
@@ -706,13 +839,13 @@ __global__ void __launch_bounds__(256) accept_kernel(AcceptParams p) {
       }
 #pragma unroll
       for (int off = 32; off >= 1; off >>= 1) {
-        Best o{__shfl_xor(bst.s, off), __shfl_xor(bst.a, off)};
+        const Best o{__shfl_xor(bst.s, off), __shfl_xor(bst.a, off)};
         bst = better(bst, o);
       }
       if (lane == 0) bpart[wave] = bst;
       __syncthreads();
       Best t = bpart[0];
-      for (int w = 1; w < 4; ++w) t = better(t, bpart[w]);
+      for (int w = 1; w < NWV; ++w) t = better(t, bpart[w]);
       __syncthreads();
       if (t.s != -INFINITY || !use_res) {
         corr = t.a;
@@ -728,7 +861,7 @@ __global__ void __launch_bounds__(256) accept_kernel(AcceptParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Small kernels: commit, lens advance, inverse temperatures, packing.
+// Small kernels: commit, lens advance, packing.
 // ---------------------------------------------------------------------------
 __global__ void commit_kernel(int B, int32_t* lens, int32_t* pending, const int32_t* n, const int32_t* corr) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
@@ -749,23 +882,20 @@ struct PackParams {
   const uint8_t* src;
   uint8_t* dst;
   int kind, wbf16;
-  int N_src, row_off, K, NKB, KB, P, n_units, N_logical, pad_from;
+  int N_src, row_off, K, NKB, n_units, pad_from, N_logical;
   int d, hd, F;
 };
 
 __global__ void pack_kernel(PackParams p) {
   const size_t chunk = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t total = (size_t)p.n_units * p.NKB * p.P * 512;  // 16-byte chunks
+  const size_t total = (size_t)p.n_units * p.NKB * 512;  // 16-byte chunks
   if (chunk >= total) return;
   const int lane = (int)(chunk & 63);
   const int j = (int)((chunk >> 6) & 7);
-  size_t t = chunk >> 9;
-  const int pp = (int)(t % p.P);
-  t /= p.P;
+  const size_t t = chunk >> 9;
   const int kb = (int)(t % p.NKB);
   const int u = (int)(t / p.NKB);
-  const int panel = unit_panel(p.kind, u, pp, p.d, p.hd, p.F);
-  const int row = panel * 16 + (lane & 15);
+  const int row = panel_row(p.kind, u, lane & 15, p.d, p.hd, p.F);
   const int g = lane >> 4;
   const int k = p.wbf16 ? kb * 256 + 32 * j + 8 * g : kb * 128 + 16 * j + 4 * g;
   const int srow = row - p.row_off;
@@ -784,37 +914,143 @@ __global__ void pack_kernel(PackParams p) {
 // ---------------------------------------------------------------------------
 namespace {
 
-template <bool WBF16, int P, int KIND>
-hipError_t launch_gemm_kind(const GemmParams& gp, int units, int mt, hipStream_t st) {
-  constexpr int NW = 8;
+constexpr int kGemmWaves = 8;
+
+template <bool WBF16, int KIND>
+hipError_t launch_gemm_kind(const GemmParams& gp, int grid, int mt, hipStream_t st) {
   if (mt == 1)
-    hipLaunchKernelGGL((gemm_kernel<WBF16, P, NW, 1, KIND>), dim3(units), dim3(NW * 64), 0, st, gp);
+    hipLaunchKernelGGL((gemm_kernel<WBF16, kGemmWaves, 1, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
   else
-    hipLaunchKernelGGL((gemm_kernel<WBF16, P, NW, 2, KIND>), dim3(units), dim3(NW * 64), 0, st, gp);
+    hipLaunchKernelGGL((gemm_kernel<WBF16, kGemmWaves, 2, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
   return hipGetLastError();
 }
 
 template <bool WBF16>
-hipError_t launch_gemm(int kind, const GemmParams& gp, int units, int mt, hipStream_t st) {
+hipError_t launch_gemm(int kind, const GemmParams& gp, int grid, int mt, hipStream_t st) {
   switch (kind) {
-    case GEMM_QKV: return launch_gemm_kind<WBF16, 2, GEMM_QKV>(gp, units, mt, st);
-    case GEMM_O: return launch_gemm_kind<WBF16, 1, GEMM_O>(gp, units, mt, st);
-    case GEMM_GU: return launch_gemm_kind<WBF16, 2, GEMM_GU>(gp, units, mt, st);
-    case GEMM_DOWN: return launch_gemm_kind<WBF16, 1, GEMM_DOWN>(gp, units, mt, st);
-    default: return launch_gemm_kind<WBF16, 1, GEMM_LM>(gp, units, mt, st);
+    case GEMM_QKV: return launch_gemm_kind<WBF16, GEMM_QKV>(gp, grid, mt, st);
+    case GEMM_O: return launch_gemm_kind<WBF16, GEMM_O>(gp, grid, mt, st);
+    case GEMM_GU: return launch_gemm_kind<WBF16, GEMM_GU>(gp, grid, mt, st);
+    case GEMM_DOWN: return launch_gemm_kind<WBF16, GEMM_DOWN>(gp, grid, mt, st);
+    default: return launch_gemm_kind<WBF16, GEMM_LM>(gp, grid, mt, st);
   }
+}
+
+template <int HD, int RMAX>
+hipError_t launch_attn_r(const AttnParams& ap, bool kvbf16, bool abf16, dim3 grid, hipStream_t st) {
+  if (kvbf16 && abf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, true, true>), grid, dim3(256), 0, st, ap);
+  else if (kvbf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, true, false>), grid, dim3(256), 0, st, ap);
+  else if (abf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, false, true>), grid, dim3(256), 0, st, ap);
+  else hipLaunchKernelGGL((attn_kernel<HD, RMAX, false, false>), grid, dim3(256), 0, st, ap);
+  return hipGetLastError();
 }
 
 template <int HD>
 hipError_t launch_attn_hd(const AttnParams& ap, bool kvbf16, bool abf16, dim3 grid, hipStream_t st) {
-  if (kvbf16 && abf16) hipLaunchKernelGGL((attn_kernel<HD, true, true>), grid, dim3(256), 0, st, ap);
-  else if (kvbf16) hipLaunchKernelGGL((attn_kernel<HD, true, false>), grid, dim3(256), 0, st, ap);
-  else if (abf16) hipLaunchKernelGGL((attn_kernel<HD, false, true>), grid, dim3(256), 0, st, ap);
-  else hipLaunchKernelGGL((attn_kernel<HD, false, false>), grid, dim3(256), 0, st, ap);
-  return hipGetLastError();
+  if (ap.R <= 4) return launch_attn_r<HD, 4>(ap, kvbf16, abf16, grid, st);
+  if (ap.R <= 8) return launch_attn_r<HD, 8>(ap, kvbf16, abf16, grid, st);
+  return launch_attn_r<HD, 16>(ap, kvbf16, abf16, grid, st);
 }
 
 }  // namespace
+
+hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, const ForwardCall& fc,
+                             hipStream_t st) {
+  const Dims& D = md->dims;
+  const Workspace& W = md->ws;
+  const bool wb = D.wdt == SPADE_BF16;
+  const int KBd = kblock_of(D.wdt);
+  const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->max_len * D.hd;  // elements
+  const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
+  const uint8_t* lb = md->weights + (size_t)layer * md->lay.layer_bytes;
+  const int M = fc.nb * fc.R;
+
+  GemmParams g{};
+  g.R = fc.R;
+  g.b0 = fc.b0;
+  g.lens = kv->lens;
+  g.inv_din = 1.0f / (float)D.d;
+  g.eps = D.eps;
+  g.n_ssq = D.d / 16;
+  g.H = D.H;
+  g.hd = D.hd;
+  g.d = D.d;
+  g.F = D.F;
+  g.max_len = kv->max_len;
+  g.kv_bf16 = D.kvdt == SPADE_BF16;
+  g.rope = W.rope;
+  g.x = W.x;
+  g.V = D.V;
+  g.err = W.err;
+  const uint8_t* wmat;
+  int K, units;
+  const void* act;
+  size_t act_split;
+  switch (kind) {
+    case GEMM_QKV:
+      wmat = lb + md->lay.qkv; K = D.d; units = 3 * D.d / 16; act = W.act_n; act_split = W.act_split;
+      g.ssq_in = W.ssq;
+      g.q_out = W.q;
+      g.kc = kv->k + (size_t)layer * kv_layer * kv_elt;
+      g.vc = kv->v + (size_t)layer * kv_layer * kv_elt;
+      break;
+    case GEMM_O:
+      // O projection + residual; operand of gate/up = x * g_ffn
+      wmat = lb + md->lay.o; K = D.d; units = D.d / 16; act = W.act_o; act_split = W.act_split;
+      g.act_out = W.act_n;
+      g.act_out_split = W.act_split;
+      g.act_out_stride = D.d;
+      g.g_next = (const float*)(lb + md->lay.g_ffn);
+      g.ssq_out = W.ssq;
+      g.n_ssq_out = D.d / 16;
+      break;
+    case GEMM_GU:
+      wmat = lb + md->lay.gu; K = D.d; units = 2 * D.F / 16; act = W.act_n; act_split = W.act_split;
+      g.ssq_in = W.ssq;
+      g.act_out = W.act_f;
+      g.act_out_split = W.actf_split;
+      g.act_out_stride = D.F;
+      break;
+    case GEMM_DOWN:
+      // down + residual; operand of the next layer (or of the LM head)
+      wmat = lb + md->lay.down; K = D.F; units = D.d / 16; act = W.act_f; act_split = W.actf_split;
+      g.act_out = W.act_n;
+      g.act_out_split = W.act_split;
+      g.act_out_stride = D.d;
+      g.g_next = (layer + 1 < D.L)
+                     ? (const float*)(md->weights + (size_t)(layer + 1) * md->lay.layer_bytes + md->lay.g_attn)
+                     : (const float*)(md->weights + md->lay.g_final);
+      g.ssq_out = W.ssq;
+      g.n_ssq_out = D.d / 16;
+      break;
+    default:  // GEMM_LM
+      wmat = md->weights + md->lay.lm; K = D.d; units = D.Vpad / 16; act = W.act_n; act_split = W.act_split;
+      g.ssq_in = W.ssq;
+      g.logits = fc.logits_out;
+      g.stats = W.stats;
+      g.NU = D.Vpad / 16;
+      g.mode = fc.mode;
+      g.inv_T = fc.inv_T;
+      g.have_q = fc.have_q;
+      break;
+  }
+  const int grid = std::min(units, md->gemm_wgs);
+  for (int m0 = 0; m0 < M; m0 += kMaxRowsPerGemm) {
+    GemmParams gp = g;
+    gp.w = wmat;
+    gp.NKB = K / KBd;
+    gp.n_units = units;
+    gp.M = std::min(kMaxRowsPerGemm, M - m0);
+    gp.m0 = m0;
+    gp.act = act;
+    gp.act_split = act_split;
+    gp.act_stride = K;
+    const int mt = gp.M > 16 ? 2 : 1;
+    hipError_t r = wb ? launch_gemm<true>(kind, gp, grid, mt, st) : launch_gemm<false>(kind, gp, grid, mt, st);
+    if (r != hipSuccess) return r;
+  }
+  return hipSuccess;
+}
 
 hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hipStream_t st) {
   const Dims& D = md->dims;
@@ -842,68 +1078,25 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   else hipLaunchKernelGGL(embed_kernel<false>, dim3(M), dim3(256), 0, st, ep);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
-  const int KBd = kblock_of(D.wdt);
   const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->max_len * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
 
-  // attention chunking: enough workgroups to fill the chip
+  // attention chunking: about 512 workgroups, chunks of 64..256 keys
   int max_keys = 0;
   for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) max_keys = std::max(max_keys, kv->lens_ub[b] + fc.R);
   int CK = kAttnChunkMin;
-  while (CK < kAttnMaxCK && (long)fc.nb * D.H * ((max_keys + CK - 1) / CK) > 2048) CK *= 2;
+  while (CK < kAttnChunkMax && ((long)fc.nb * D.H * ((max_keys + CK - 1) / CK) > 512 ||
+                                (max_keys + CK - 1) / CK > kAttnMaxChunks))
+    CK *= 2;
   const int NC = (max_keys + CK - 1) / CK;
-  if (NC > W.NCmax) return hipErrorInvalidValue;
-
-  auto gemm = [&](int kind, const uint8_t* wmat, int K, int units, const void* act, size_t act_split,
-                  GemmParams base) -> hipError_t {
-    for (int m0 = 0; m0 < M; m0 += kMaxRowsPerGemm) {
-      GemmParams gp = base;
-      gp.w = wmat;
-      gp.NKB = K / KBd;
-      gp.M = std::min(kMaxRowsPerGemm, M - m0);
-      gp.m0 = m0;
-      gp.act = act;
-      gp.act_split = act_split;
-      gp.act_stride = K;
-      const int mt = gp.M > 16 ? 2 : 1;
-      hipError_t r = wb ? launch_gemm<true>(kind, gp, units, mt, st) : launch_gemm<false>(kind, gp, units, mt, st);
-      if (r != hipSuccess) return r;
-    }
-    return hipSuccess;
-  };
-
-  GemmParams common{};
-  common.R = fc.R;
-  common.b0 = fc.b0;
-  common.lens = kv->lens;
-  common.inv_din = 1.0f / (float)D.d;
-  common.eps = D.eps;
-  common.n_ssq = D.d / 16;
-  common.H = D.H;
-  common.hd = D.hd;
-  common.d = D.d;
-  common.F = D.F;
-  common.max_len = kv->max_len;
-  common.kv_bf16 = D.kvdt == SPADE_BF16;
-  common.rope = W.rope;
-  common.x = W.x;
-  common.V = D.V;
-  common.err = W.err;
+  if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
 
   for (int l = 0; l < D.L; ++l) {
-    const uint8_t* lb = md->weights + (size_t)l * md->lay.layer_bytes;
-    // QKV + RoPE + KV append
-    GemmParams g = common;
-    g.ssq_in = W.ssq;
-    g.q_out = W.q;
-    g.kc = kv->k + (size_t)l * kv_layer * kv_elt;
-    g.vc = kv->v + (size_t)l * kv_layer * kv_elt;
-    if ((e = gemm(GEMM_QKV, lb + md->lay.qkv, D.d, 3 * D.d / 32, W.act_n, W.act_split, g)) != hipSuccess) return e;
-    // attention
+    if ((e = launch_layer_gemm(md, kv, GEMM_QKV, l, fc, st)) != hipSuccess) return e;
     AttnParams ap{};
     ap.q = W.q;
-    ap.kc = g.kc;
-    ap.vc = g.vc;
+    ap.kc = kv->k + (size_t)l * kv_layer * kv_elt;
+    ap.vc = kv->v + (size_t)l * kv_layer * kv_elt;
     ap.lens = kv->lens;
     ap.b0 = fc.b0;
     ap.R = fc.R;
@@ -924,60 +1117,32 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     if (D.hd == 64) e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);
     else e = launch_attn_hd<128>(ap, kvb, wb, agrid, st);
     if (e != hipSuccess) return e;
-    // O projection + residual; operand of gate/up = x * g_ffn
-    g = common;
-    g.act_out = W.act_n;
-    g.act_out_split = W.act_split;
-    g.act_out_stride = D.d;
-    g.g_next = (const float*)(lb + md->lay.g_ffn);
-    g.ssq_out = W.ssq;
-    g.n_ssq_out = D.d / 16;
-    if ((e = gemm(GEMM_O, lb + md->lay.o, D.d, D.d / 16, W.act_o, W.act_split, g)) != hipSuccess) return e;
-    // gate/up + SiLU
-    g = common;
-    g.ssq_in = W.ssq;
-    g.act_out = W.act_f;
-    g.act_out_split = W.actf_split;
-    g.act_out_stride = D.F;
-    if ((e = gemm(GEMM_GU, lb + md->lay.gu, D.d, D.F / 16, W.act_n, W.act_split, g)) != hipSuccess) return e;
-    // down + residual; operand of the next layer (or the LM head)
-    g = common;
-    g.act_out = W.act_n;
-    g.act_out_split = W.act_split;
-    g.act_out_stride = D.d;
-    g.g_next = (l + 1 < D.L) ? (const float*)(md->weights + (size_t)(l + 1) * md->lay.layer_bytes + md->lay.g_attn)
-                             : (const float*)(md->weights + md->lay.g_final);
-    g.ssq_out = W.ssq;
-    g.n_ssq_out = D.d / 16;
-    if ((e = gemm(GEMM_DOWN, lb + md->lay.down, D.F, D.d / 16, W.act_f, W.actf_split, g)) != hipSuccess) return e;
+    if ((e = launch_layer_gemm(md, kv, GEMM_O, l, fc, st)) != hipSuccess) return e;
+    if ((e = launch_layer_gemm(md, kv, GEMM_GU, l, fc, st)) != hipSuccess) return e;
+    if ((e = launch_layer_gemm(md, kv, GEMM_DOWN, l, fc, st)) != hipSuccess) return e;
   }
-  if (fc.want_logits) {
-    GemmParams g = common;
-    g.ssq_in = W.ssq;
-    g.logits = fc.logits_out;
-    if ((e = gemm(GEMM_LM, md->weights + md->lay.lm, D.d, D.Vpad / 16, W.act_n, W.act_split, g)) != hipSuccess)
-      return e;
-  }
+  if (fc.want_logits)
+    if ((e = launch_layer_gemm(md, kv, GEMM_LM, 0, fc, st)) != hipSuccess) return e;
   return hipSuccess;
 }
 
-hipError_t launch_accept(spade_model md, int B, int gamma, int V, const float* logits, bool /*have_stats*/,
-                         const int32_t* drafts, const float* q, const float* u, const uint8_t* mode,
-                         float temperature, int32_t* n_out, int32_t* corr_out, hipStream_t st) {
+hipError_t launch_accept(spade_model md, const AcceptCall& ac, hipStream_t st) {
   AcceptParams p{};
-  p.logits = logits;
-  p.V = V;
-  p.gamma = gamma;
-  p.R = gamma + 1;
-  p.drafts = drafts;
-  p.q = q;
-  p.u = u;
-  p.mode = mode;
-  p.inv_T = temperature > 0.f ? 1.0f / temperature : 1.0f;
-  p.n_out = n_out;
-  p.corr_out = corr_out;
+  p.logits = ac.logits;
+  p.stats = ac.stats;
+  p.NU = ac.NU;
+  p.V = ac.V;
+  p.gamma = ac.gamma;
+  p.R = ac.gamma + 1;
+  p.drafts = ac.drafts;
+  p.q = ac.q;
+  p.u = ac.u;
+  p.mode = ac.mode;
+  p.inv_T = ac.inv_T;
+  p.n_out = ac.n_out;
+  p.corr_out = ac.corr_out;
   p.err = md->ws.err;
-  hipLaunchKernelGGL(accept_kernel, dim3(B), dim3(256), 0, st, p);
+  hipLaunchKernelGGL(accept_kernel, dim3(ac.B), dim3(kAcceptThreads), 0, st, p);
   return hipGetLastError();
 }
 
@@ -986,25 +1151,23 @@ hipError_t launch_pack(spade_model md, int kind, int layer, const void* src, hip
   const bool wb = D.wdt == SPADE_BF16;
   const size_t elt = wb ? 2 : 4;
   const uint8_t* lb = md->weights + (size_t)layer * md->lay.layer_bytes;
-  size_t bytes = 0;
   uint8_t* dst = nullptr;
   PackParams pp{};
   pp.src = (const uint8_t*)src;
   pp.wbf16 = wb;
-  pp.KB = kblock_of(D.wdt);
   pp.d = D.d;
   pp.hd = D.hd;
   pp.F = D.F;
   switch (kind) {
     case SPADE_WQ: case SPADE_WK: case SPADE_WV:
       pp.kind = GEMM_QKV; pp.K = D.d; pp.N_src = D.d; pp.row_off = (kind - SPADE_WQ) * D.d;
-      pp.N_logical = 3 * D.d; pp.n_units = 3 * D.d / 32; dst = (uint8_t*)lb + md->lay.qkv; break;
+      pp.N_logical = 3 * D.d; pp.n_units = 3 * D.d / 16; dst = (uint8_t*)lb + md->lay.qkv; break;
     case SPADE_WO:
       pp.kind = GEMM_O; pp.K = D.d; pp.N_src = D.d; pp.row_off = 0; pp.N_logical = D.d;
       pp.n_units = D.d / 16; dst = (uint8_t*)lb + md->lay.o; break;
     case SPADE_WGATE: case SPADE_WUP:
       pp.kind = GEMM_GU; pp.K = D.d; pp.N_src = D.F; pp.row_off = (kind - SPADE_WGATE) * D.F;
-      pp.N_logical = 2 * D.F; pp.n_units = D.F / 16; dst = (uint8_t*)lb + md->lay.gu; break;
+      pp.N_logical = 2 * D.F; pp.n_units = 2 * D.F / 16; dst = (uint8_t*)lb + md->lay.gu; break;
     case SPADE_WDOWN:
       pp.kind = GEMM_DOWN; pp.K = D.F; pp.N_src = D.d; pp.row_off = 0; pp.N_logical = D.d;
       pp.n_units = D.d / 16; dst = (uint8_t*)lb + md->lay.down; break;
@@ -1012,8 +1175,7 @@ hipError_t launch_pack(spade_model md, int kind, int layer, const void* src, hip
       pp.kind = GEMM_LM; pp.K = D.d; pp.N_src = D.V; pp.row_off = 0; pp.N_logical = D.Vpad;
       pp.n_units = D.Vpad / 16; dst = md->weights + md->lay.lm; break;
     case SPADE_EMBED:
-      bytes = (size_t)D.V * D.d * elt;
-      return hipMemcpyAsync(md->weights + md->lay.embed, src, bytes, hipMemcpyDeviceToDevice, st);
+      return hipMemcpyAsync(md->weights + md->lay.embed, src, (size_t)D.V * D.d * elt, hipMemcpyDeviceToDevice, st);
     case SPADE_G_ATTN:
       return hipMemcpyAsync((uint8_t*)lb + md->lay.g_attn, src, (size_t)D.d * 4, hipMemcpyDeviceToDevice, st);
     case SPADE_G_FFN:
@@ -1025,9 +1187,8 @@ hipError_t launch_pack(spade_model md, int kind, int layer, const void* src, hip
   }
   pp.dst = dst;
   pp.pad_from = kind == SPADE_LM_HEAD ? D.V : pp.N_logical;
-  pp.P = panels_per_unit(pp.kind);
-  pp.NKB = pp.K / pp.KB;
-  const size_t total = (size_t)pp.n_units * pp.NKB * pp.P * 512;
+  pp.NKB = pp.K / kblock_of(D.wdt);
+  const size_t total = (size_t)pp.n_units * pp.NKB * 512;
   const unsigned blocks = (unsigned)((total + 255) / 256);
   hipLaunchKernelGGL(pack_kernel, dim3(blocks), dim3(256), 0, st, pp);
   return hipGetLastError();

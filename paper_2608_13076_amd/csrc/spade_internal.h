@@ -10,35 +10,40 @@
 
 namespace spade {
 
-constexpr int kPanel = 16;          // weight rows per MFMA tile (one panel)
-constexpr int kTileBytes = 8192;    // one panel x one k-block, in the arena
-constexpr int kMaxRowsPerGemm = 32; // rows handled by one GEMM launch
-constexpr int kPrefillRows = 16;    // tokens per prefill forward
-constexpr int kMaxR = 16;           // rows per request in one forward (gamma <= 15)
+constexpr int kPanel = 16;           // weight rows per MFMA tile (one panel)
+constexpr int kTileBytes = 8192;     // one panel x one k-block, in the arena
+constexpr int kMaxRowsPerGemm = 32;  // rows handled by one GEMM launch
+constexpr int kPrefillRows = 16;     // tokens per prefill forward
+constexpr int kMaxR = 16;            // rows per request in one forward (gamma <= 15)
+constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
 constexpr int kAttnChunkMin = 64;
+constexpr int kAttnChunkMax = 256;
+constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
+constexpr int kMaxLen = kAttnChunkMax * kAttnMaxChunks;
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 
 inline int kblock_of(int weight_dtype) { return weight_dtype == SPADE_BF16 ? 256 : 128; }
-inline int panels_per_unit(int kind) { return (kind == GEMM_QKV || kind == GEMM_GU) ? 2 : 1; }
 
-// Weight panel (16 rows of the logical [N, K] matrix) held by panel slot pp of
-// unit u.  The arena stores units in order; within a unit, k-block major and
-// panel minor, so the k-range a wave streams is one contiguous block.
-//   QKV: N = 3d.  Unit u covers section s (q, k, v), head h and panel w of the
-//        first half of the head; its partner panel holds features + hd/2, so
-//        the RoPE pair (i, i + hd/2) lands in the same thread.
-//   GU:  N = 2F (gate rows, then up rows).  Unit u = gate panel u + up panel u.
-//   others: unit u = panel u.
-__host__ __device__ inline int unit_panel(int kind, int u, int pp, int d_model, int head_dim, int d_ffn) {
+// Row of the logical [N, K] weight matrix held by row r (0..15) of arena
+// panel p.  Panels are stored in order, each as its k-blocks in order.
+//   QKV (N = 3d, rows of Wq, Wk, Wv): panel p of section s holds, for head h
+//     and group w, features w*8 .. w*8+7 in rows 0..7 and their rotary
+//     partners w*8+hd/2 .. w*8+7+hd/2 in rows 8..15, so lanes n and n^8 of an
+//     MFMA output hold a RoPE pair.
+//   GU (N = 2F, gate rows then up rows): panel p holds gate rows p*8 .. p*8+7
+//     in rows 0..7 and the matching up rows in rows 8..15.
+//   O, DOWN, LM: panel p holds rows p*16 .. p*16+15.
+__host__ __device__ inline int panel_row(int kind, int p, int r, int d_model, int head_dim, int d_ffn) {
   if (kind == GEMM_QKV) {
-    const int upsec = d_model / 32, uph = head_dim / 32;
-    const int s = u / upsec, rem = u % upsec;
-    const int h = rem / uph, w = rem % uph;
-    return s * (d_model / 16) + h * (head_dim / 16) + w + pp * uph;
+    const int pps = d_model / 16, pph = head_dim / 16;
+    const int s = p / pps, pw = p % pps;
+    const int h = pw / pph, w = pw % pph;
+    const int f = w * 8 + (r & 7) + (r >= 8 ? head_dim / 2 : 0);
+    return s * d_model + h * head_dim + f;
   }
-  if (kind == GEMM_GU) return u + pp * (d_ffn / 16);
-  return u;
+  if (kind == GEMM_GU) return (r < 8) ? p * 8 + r : d_ffn + p * 8 + (r - 8);
+  return p * 16 + r;
 }
 
 struct Dims {
@@ -55,23 +60,21 @@ struct ArenaLayout {
 
 // Sub-buffers of the caller's workspace.
 struct Workspace {
-  float* x;          // [Mmax][d] residual stream
-  void* act_n;       // normed GEMM input, split bf16 [S][Mmax][d] or f32 [Mmax][d]
-  void* act_o;       // attention output (O-projection input)
-  void* act_f;       // SwiGLU output (down-projection input) [S][Mmax][F]
-  float* ssq;        // [Mmax][d/16] sum-of-squares partials of x
-  float* q;          // [Mmax][d] rotated queries
-  float* attn_o;     // [Bmax][H][NCmax][Rmax][hd] chunk partial outputs
-  float* attn_ml;    // [Bmax][H][NCmax][Rmax][2] chunk max / sum
-  uint32_t* attn_cnt;// [Bmax][H] arrival counters (kept at zero between calls)
-  float* logits;     // [Mmax][V]
-  float* stats;      // [Mmax][NU][3] LM-head per-unit max / sumexp / argmax
-  float* rope;       // [max_len][hd/2][2] cos, sin
-  float* inv_temp;   // [Bmax]
-  int32_t* tokens;   // [Mmax] staging for prefill tokens
-  uint32_t* err;     // device error word
-  size_t act_split;  // elements between splits of act_n / act_o
-  size_t actf_split; // elements between splits of act_f
+  float* x;           // [Mmax][d] residual stream
+  void* act_n;        // normed GEMM input, split bf16 [S][Mmax][d] or f32 [Mmax][d]
+  void* act_o;        // attention output (O-projection input)
+  void* act_f;        // SwiGLU output (down-projection input) [S][Mmax][F]
+  float* ssq;         // [Mmax][d/16] sum-of-squares partials of x
+  float* q;           // [Mmax][d] rotated queries
+  float* attn_o;      // [Bmax][H][NCmax][Rmax][hd] chunk partial outputs
+  float* attn_ml;     // [Bmax][H][NCmax][Rmax][2] chunk max / sum
+  uint32_t* attn_cnt; // [Bmax][H] arrival counters (kept at zero between calls)
+  float* logits;      // [Mmax][V]
+  float* stats;       // [Mmax][Vpad/16][3] LM-head per-panel max / sumexp / argmax
+  float* rope;        // [max_len][hd/2][2] cos, sin
+  uint32_t* err;      // device error word
+  size_t act_split;   // elements between splits of act_n / act_o
+  size_t actf_split;  // elements between splits of act_f
   int Mmax, NCmax, Rmax;
 };
 
@@ -85,8 +88,9 @@ struct spade_model_s {
   uint8_t* work;
   spade::Workspace ws;
   int max_batch, max_gamma, max_len;
-  int S;  // activation splits for bf16 GEMMs
   int device;
+  int n_cu;      // compute units of the device
+  int gemm_wgs;  // persistent GEMM workgroups
 };
 
 struct spade_kv_s {
@@ -97,27 +101,42 @@ struct spade_kv_s {
   int32_t* pending;
   int max_batch, max_len;
   int* lens_ub;  // host upper bound of lens per request
+  int* snap_ub;  // lens_ub at the last snapshot
 };
 
 namespace spade {
 
-// Launchers (kernels.hip).  All return hipError_t of the launch.
 struct ForwardCall {
-  int b0, nb, R;                  // requests [b0, b0+nb), R rows each
-  const int32_t* tokens;          // prefill: [R] ids; verify: NULL
-  const int32_t* drafts;          // verify: [nb][R-1]
+  int b0, nb, R;           // requests [b0, b0+nb), R rows each
+  const int32_t* tokens;   // prefill: [R] ids; verify: NULL
+  const int32_t* drafts;   // verify: [nb][R-1]
   bool want_logits;
-  float* logits_out;              // [nb*R][V] (user buffer or workspace)
+  float* logits_out;       // [nb*R][V] (user buffer or workspace)
+  const uint8_t* mode;     // verify: [nb] modes (LM-head statistics use 1/T on sampling rows)
+  float inv_T;
+  bool have_q;             // draft probabilities given
+};
+
+struct AcceptCall {
+  int B, gamma, V;
+  const float* logits;     // [B][gamma+1][V]
+  const float* stats;      // [B*(gamma+1)][NU][3] from the LM head, or NULL
+  int NU;
+  const int32_t* drafts;
+  const float* q;
+  const float* u;
+  const uint8_t* mode;
+  float inv_T;
+  int32_t* n_out;
+  int32_t* corr_out;
 };
 
 hipError_t launch_forward(spade_model m, spade_kv kv, const ForwardCall& fc, hipStream_t st);
-hipError_t launch_accept(spade_model m, int B, int gamma, int V, const float* logits, bool have_stats,
-                         const int32_t* drafts, const float* q, const float* u, const uint8_t* mode,
-                         float temperature, int32_t* n_out, int32_t* corr_out, hipStream_t st);
+hipError_t launch_layer_gemm(spade_model m, spade_kv kv, int kind, int layer, const ForwardCall& fc,
+                             hipStream_t st);
+hipError_t launch_accept(spade_model m, const AcceptCall& ac, hipStream_t st);
 hipError_t launch_pack(spade_model m, int kind, int layer, const void* src, hipStream_t st);
 hipError_t launch_commit(spade_kv kv, int B, const int32_t* n, const int32_t* corr, hipStream_t st);
 hipError_t launch_advance(spade_kv kv, int b, int count, const int32_t* pending_src, hipStream_t st);
-hipError_t launch_set_inv_temp(spade_model m, int B, const uint8_t* mode, float temperature,
-                               bool have_q, hipStream_t st);
 
 }  // namespace spade

@@ -28,8 +28,8 @@ DERR_TOKEN, DERR_NAN, DERR_RESIDUAL, DERR_NOQ = 1, 2, 4, 8
 EXPORTED = (
     "spade_weight_bytes", "spade_workspace_bytes", "spade_kv_bytes", "spade_model_create",
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
-    "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
-    "spade_accept_from_logits", "spade_get_device_error", "spade_last_error",
+    "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
+    "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
     "spade_model_destroy", "spade_kv_destroy",
 )
 
@@ -77,11 +77,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_kv_create": (I, [P, P, I, I, P, P, ctypes.POINTER(P)]),
         "spade_kv_set_state": (I, [P, I, P, P, P]),
         "spade_kv_get_state": (I, [P, I, P, P, P]),
+        "spade_kv_snapshot": (I, [P, I, P, P, P]),
         "spade_kv_restore": (I, [P, I, P, P, P]),
         "spade_prefill": (I, [P, P, I, P, I, P]),
         "spade_verify": (I, [P, P, I, I, P, P, P, P, F, P, P, P, P]),
         "spade_kv_commit": (I, [P, I, P, P, P]),
         "spade_accept_from_logits": (I, [P, I, I, I, P, P, P, P, P, F, P, P, P]),
+        "spade_profile_gemm": (I, [P, P, I, I, I, I, P]),
         "spade_get_device_error": (I, [P, P, P]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
@@ -217,6 +219,12 @@ class KVCache:
         _check(self.lib.spade_kv_get_state(self.handle, B, l.ctypes.data_as(P), p.ctypes.data_as(P), _stream()))
         return l, p
 
+    def snapshot(self, B: int):
+        lens = torch.empty(B, dtype=torch.int32, device=self.model.device)
+        pending = torch.empty(B, dtype=torch.int32, device=self.model.device)
+        _check(self.lib.spade_kv_snapshot(self.handle, B, _ptr(lens), _ptr(pending), _stream()))
+        return lens, pending
+
     def restore(self, lens: torch.Tensor, pending: torch.Tensor) -> None:
         _check(self.lib.spade_kv_restore(self.handle, lens.numel(), _ptr(lens), _ptr(pending), _stream()))
 
@@ -264,3 +272,41 @@ def verify(model: Model, kv: KVCache, buf: VerifyBuffers, temperature: float = 1
     _check(model.lib.spade_verify(model.handle, kv.handle, buf.B, buf.gamma, _ptr(buf.drafts), _ptr(buf.q),
                                   _ptr(buf.u), _ptr(buf.mode), float(temperature), _ptr(buf.n),
                                   _ptr(buf.corr), _ptr(buf.logits), _stream()))
+
+
+GEMM_KINDS = {"qkv": 0, "o": 1, "gu": 2, "down": 3, "lm": 4}
+
+
+def gemm_weight_bytes(shape, kind: str) -> int:
+    """Weight bytes one launch of a projection GEMM streams."""
+    elt = 2 if shape.weight_dtype == "bf16" else 4
+    d, f, v = shape.d_model, shape.d_ffn, shape.vocab
+    n_k = {"qkv": (3 * d, d), "o": (d, d), "gu": (2 * f, d), "down": (d, f), "lm": (v, d)}[kind]
+    return n_k[0] * n_k[1] * elt
+
+
+def gemm_roofline(model: Model, kv: KVCache, kind: str, B: int, gamma: int, reps: int, peak_gbs: float) -> dict:
+    """Average duration of one launch of a projection GEMM (HIP events on the
+    current stream around `reps` x n_layers launches of that kernel alone)
+    and its algorithmic bytes: the weight matrix once, the fp32 input rows
+    once, the fp32 output rows once."""
+    s = model.shape
+    L = s.n_layers if kind != "lm" else 1
+    n = reps * L
+    M = B * (gamma + 1)
+    d, f, v = s.d_model, s.d_ffn, s.vocab
+    k_in = f if kind == "down" else d
+    n_out = {"qkv": 3 * d, "o": d, "gu": f, "down": d, "lm": v}[kind]
+    alg = gemm_weight_bytes(s, kind) + M * k_in * 4 + M * n_out * 4
+    _check(model.lib.spade_profile_gemm(model.handle, kv.handle, GEMM_KINDS[kind], B, gamma, L, _stream()))
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    _check(model.lib.spade_profile_gemm(model.handle, kv.handle, GEMM_KINDS[kind], B, gamma, n, _stream()))
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / n
+    achieved = alg / (us * 1e-6) / 1e9
+    return {"kernel": f"gemm_kernel<{kind}>", "bound": "hbm", "achieved": round(achieved, 1),
+            "peak": peak_gbs, "unit": "GB/s", "frac": round(achieved / peak_gbs, 4), "traffic": None,
+            "avg_launch_us": round(us, 3), "algorithmic_bytes_per_launch": alg, "launches_timed": n}
