@@ -105,8 +105,12 @@ size_t spade_weight_bytes(const spade_config* cfg);
  * max_gamma drafts each and caches of up to max_len positions. */
 size_t spade_workspace_bytes(const spade_config* cfg, int max_batch, int max_gamma, int max_len);
 
-/* Bytes of a KV cache holding max_batch requests of max_len positions:
- * K then V, each [n_layers][max_batch][n_heads][max_len][head_dim]. */
+/* Bytes of a KV cache holding max_batch requests of max_len positions.  With
+ * S = max_len rounded up to a multiple of 32: K is
+ * [n_layers][max_batch][n_heads][S][head_dim] (a row per position) and V,
+ * stored transposed, is [n_layers][max_batch][n_heads][head_dim][S] (a row
+ * per feature), so the verify kernels read both as contiguous 16-byte
+ * fragments.  max_len <= 16384. */
 size_t spade_kv_bytes(const spade_config* cfg, int max_batch, int max_len);
 
 /* Create a model over caller-owned device buffers: d_weights of

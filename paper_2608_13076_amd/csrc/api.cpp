@@ -95,7 +95,7 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   WsPlan p{};
   p.Rmax = std::max(max_gamma + 1, kPrefillRows);
   p.Mmax = std::max(max_batch * (max_gamma + 1), kPrefillRows);
-  p.NCmax = std::min(kAttnMaxChunks, (max_len + kAttnChunkMin - 1) / kAttnChunkMin);
+  p.NCmax = std::min(kAttnMaxChunks, (max_len + kAttnChunk - 1) / kAttnChunk);
   const bool wb = D.wdt == SPADE_BF16;
   const size_t ae = wb ? 2 * kActSplits : 4;  // bf16 terms or one float
   p.act_split = (size_t)p.Mmax * D.d;
@@ -144,7 +144,7 @@ size_t spade_workspace_bytes(const spade_config* cfg, int max_batch, int max_gam
 size_t spade_kv_bytes(const spade_config* cfg, int max_batch, int max_len) {
   if (check_config(cfg) != SPADE_OK || max_batch < 1 || max_len < 1) return 0;
   const size_t e = cfg->kv_dtype == SPADE_BF16 ? 2 : 4;
-  return 2 * align256((size_t)cfg->n_layers * max_batch * cfg->n_heads * max_len * cfg->head_dim * e);
+  return 2 * align256((size_t)cfg->n_layers * max_batch * cfg->n_heads * kv_stride_of(max_len) * cfg->head_dim * e);
 }
 
 spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* d_workspace, int max_batch,
@@ -252,6 +252,7 @@ spade_status spade_kv_create(spade_model m, void* d_kv, int max_batch, int max_l
   kv->pending = d_pending;
   kv->max_batch = max_batch;
   kv->max_len = max_len;
+  kv->stride = kv_stride_of(max_len);
   kv->lens_ub = new (std::nothrow) int[max_batch]();
   kv->snap_ub = new (std::nothrow) int[max_batch]();
   if (!kv->lens_ub || !kv->snap_ub) {
@@ -303,8 +304,7 @@ spade_status spade_kv_snapshot(spade_kv kv, int B, int32_t* d_lens, int32_t* d_p
   if (!kv || !d_lens || !d_pending) return fail(SPADE_EINVAL, "null pointer");
   if (B < 1 || B > kv->max_batch) return fail(SPADE_ECAPACITY, "B out of range");
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = hipMemcpyAsync(d_lens, kv->lens, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
-  if (e == hipSuccess) e = hipMemcpyAsync(d_pending, kv->pending, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
+  hipError_t e = launch_copy_state(B, d_lens, d_pending, kv->lens, kv->pending, st);
   if (e != hipSuccess) return hipfail(e, "kv_snapshot");
   for (int b = 0; b < kv->max_batch; ++b) kv->snap_ub[b] = kv->lens_ub[b];
   return SPADE_OK;
@@ -314,8 +314,7 @@ spade_status spade_kv_restore(spade_kv kv, int B, const int32_t* d_lens, const i
   if (!kv || !d_lens || !d_pending) return fail(SPADE_EINVAL, "null pointer");
   if (B < 1 || B > kv->max_batch) return fail(SPADE_ECAPACITY, "B out of range");
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = hipMemcpyAsync(kv->lens, d_lens, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
-  if (e == hipSuccess) e = hipMemcpyAsync(kv->pending, d_pending, (size_t)B * 4, hipMemcpyDeviceToDevice, st);
+  hipError_t e = launch_copy_state(B, kv->lens, kv->pending, d_lens, d_pending, st);
   if (e != hipSuccess) return hipfail(e, "kv_restore");
   for (int b = 0; b < B; ++b) kv->lens_ub[b] = kv->snap_ub[b];
   return SPADE_OK;

@@ -16,8 +16,9 @@
 //                  residual add + next RMS partials (O, down), SiLU gate
 //                  (gate/up), logits + per-panel softmax statistics (LM head)
 //   attn_kernel    multi-query causal attention of the gamma+1 rows over the
-//                  cache, split over key chunks; the chunk that finishes last
-//                  for a (request, head) merges the partials in chunk order
+//                  cache, split over key chunks of 128 keys
+//   attn_combine_kernel  merges the chunk partials of each (request, head) in
+//                  chunk order into the O-projection operand
 //   accept_kernel  per request: vocabulary-wide max / log-sum-exp / argmax
 //                  per row, the accept chain, the Gumbel-max correction draw
 //   commit_kernel  lens += n + 1, pending = correction
@@ -145,7 +146,7 @@ struct GemmParams {
   float* q_out;
   void* kc;
   void* vc;
-  int H, hd, d, max_len, kv_bf16;
+  int H, hd, d, kv_stride, kv_bf16;
   const float* rope;
   // O / DOWN
   float* x;
@@ -254,8 +255,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int p, int ml
     if (sec == 0) {
       a.q_out[(size_t)m * a.d + h * a.hd + f] = v;
     } else {
+      // K rows [pos][hd]; V transposed, rows [feature][stride]
+      const size_t head = ((size_t)bg * a.H + h) * a.kv_stride * a.hd;
       void* cache = sec == 1 ? a.kc : a.vc;
-      const size_t off = (((size_t)bg * a.H + h) * a.max_len + pos) * a.hd + f;
+      const size_t off = sec == 1 ? head + (size_t)pos * a.hd + f : head + (size_t)f * a.kv_stride + pos;
       if (a.kv_bf16) ((uint16_t*)cache)[off] = f2bf(v);
       else ((float*)cache)[off] = v;
     }
@@ -403,6 +406,90 @@ __global__ void __launch_bounds__(NW * 64) gemm_kernel(GemmParams a) {
   }
 }
 
+// Variant for K <= 2 * NW k-blocks and <= 16 rows: each wave keeps the
+// activations of its (at most two) k-blocks in registers for the whole
+// launch and runs a three-deep weight pipeline (two items in flight while the
+// third is consumed).
+template <bool WBF16, int NW, int KIND>
+__global__ void __launch_bounds__(NW * 64) gemm_ares_kernel(GemmParams a) {
+  __shared__ float red[NW][1][4][64];
+  __shared__ float rinv_s[16];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int arow = lane & 15, ag = lane >> 4;
+  const int NKB = a.NKB;
+  const int nkw = (NKB + NW - 1) / NW;  // 1 or 2
+  const int kbl = (NKB * wave) / NW;
+  const int cnt = (NKB * (wave + 1)) / NW - kbl;
+  const int G = gridDim.x;
+  const int my_units = (a.n_units - (int)blockIdx.x + G - 1) / G;
+  const int T = my_units * nkw;
+  const uint8_t* wl = a.w + lane * 16;
+  const size_t unit_bytes = (size_t)NKB * kTileBytes;
+
+  Item<WBF16, 1> w0, w1, w2, a0, a1;
+  floatx4 acc[1] = {floatx4{0.f, 0.f, 0.f, 0.f}};
+
+  auto issue = [&](int t, Item<WBF16, 1>& buf) {
+    const int i = t % nkw;
+    if (i < cnt) {
+      const int u = (int)blockIdx.x + (t / nkw) * G;
+      load_w(buf, wl + (size_t)u * unit_bytes + (size_t)(kbl + i) * kTileBytes);
+    }
+  };
+  auto unit_end = [&](int t) {
+    const int u = (int)blockIdx.x + (t / nkw) * G;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][0][r][lane] = acc[0][r];
+    __syncthreads();
+    if (tid < 256) {
+      const int er = (tid >> 6) & 3, eln = tid & 63;
+      const int ml = 4 * (eln >> 4) + er;
+      float val = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) val += red[w][0][er][eln];
+      gemm_epilogue<WBF16, KIND>(a, u, ml, eln & 15, val, rinv_s[ml]);
+    }
+    __syncthreads();
+    acc[0] = floatx4{0.f, 0.f, 0.f, 0.f};
+  };
+  auto step = [&](int t, const Item<WBF16, 1>& wb) {
+    const int i = t % nkw;
+    if (i < cnt) {
+      if (i == 0) mma_item(wb, a0, acc);
+      else mma_item(wb, a1, acc);
+    }
+    if (i == nkw - 1) unit_end(t);
+  };
+
+  if (T > 0) issue(0, w0);
+  if (T > 1) issue(1, w1);
+  if (cnt > 0) load_a(a0, a, kbl, arow, ag);
+  if (cnt > 1) load_a(a1, a, kbl + 1, arow, ag);
+  {
+    const int row = tid >> 4, sub = tid & 15;
+    float s = 0.f;
+    if (a.ssq_in != nullptr && row < 16 && row < a.M) {
+      const float* sp = a.ssq_in + (size_t)(a.m0 + row) * a.n_ssq;
+      for (int q = sub; q < a.n_ssq; q += 16) s += sp[q];
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    if (sub == 0 && row < 16)
+      rinv_s[row] = (a.ssq_in != nullptr && row < a.M) ? 1.0f / sqrtf(s * a.inv_din + a.eps) : 1.0f;
+  }
+
+  for (int t = 0; t < T; t += 3) {
+    if (t + 2 < T) issue(t + 2, w2);
+    step(t, w0);
+    if (t + 1 >= T) break;
+    if (t + 3 < T) issue(t + 3, w0);
+    step(t + 1, w1);
+    if (t + 2 >= T) break;
+    if (t + 4 < T) issue(t + 4, w1);
+    step(t + 2, w2);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Verify attention.  Workgroup (chunk c, head h, request b): the R query rows
 // of the request against keys [c*CK, min((c+1)*CK, L_b + R)); key j is
@@ -410,16 +497,15 @@ __global__ void __launch_bounds__(NW * 64) gemm_kernel(GemmParams a) {
 // Scores: sixteen lanes share a key (HD/16 features each), four keys per wave
 // step, and a reduce-scatter over the sixteen lanes leaves each row's dot
 // product in one lane.  P V: each lane owns HD/64 output features.  Each
-// chunk writes (max, sum, unnormalised output) per row; the workgroup that
-// finishes last for (b, h) merges the chunks in chunk order and writes the
-// O-projection operand.
+// chunk writes (max, sum, unnormalised output) per row for the combine
+// kernel.
 // ---------------------------------------------------------------------------
 struct AttnParams {
   const float* q;
   const void* kc;
   const void* vc;
   const int32_t* lens;
-  int b0, R, H, d, max_len;
+  int b0, R, H, d, kv_stride;
   int CK, NC;
   float scale;
   float* part_o;
@@ -430,183 +516,345 @@ struct AttnParams {
   size_t act_split;
 };
 
+// Raw K/V bytes of one lane: N features of a cache row, loaded as wide as
+// their alignment allows, widened to float after the load has landed.
 template <int N, bool KVBF16>
-__device__ __forceinline__ void load_kv(const void* base, size_t off, float* out) {
-  if constexpr (KVBF16) {
-    const uint16_t* p = (const uint16_t*)base + off;
-    if constexpr (N == 8) {
-      const uint4 v = *(const uint4*)p;
-      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+struct KVRaw {
+  static constexpr int BYTES = N * (KVBF16 ? 2 : 4);
+  static constexpr int WORDS = BYTES >= 4 ? BYTES / 4 : 1;
+  uint32_t w[WORDS];
+};
+
+template <int N, bool KVBF16>
+__device__ __forceinline__ void kv_load(KVRaw<N, KVBF16>& r, const void* base, size_t off) {
+  constexpr int BYTES = KVRaw<N, KVBF16>::BYTES;
+  const uint8_t* p = (const uint8_t*)base + off * (KVBF16 ? 2 : 4);
+  if constexpr (BYTES >= 16) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        out[2 * e] = __uint_as_float(w[e] << 16);
-        out[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
-      }
-    } else if constexpr (N == 4) {
-      const uint2 v = *(const uint2*)p;
-      out[0] = __uint_as_float(v.x << 16);
-      out[1] = __uint_as_float(v.x & 0xffff0000u);
-      out[2] = __uint_as_float(v.y << 16);
-      out[3] = __uint_as_float(v.y & 0xffff0000u);
-    } else if constexpr (N == 2) {
-      const uint32_t v = *(const uint32_t*)p;
-      out[0] = __uint_as_float(v << 16);
-      out[1] = __uint_as_float(v & 0xffff0000u);
-    } else {
-#pragma unroll
-      for (int e = 0; e < N; ++e) out[e] = bf2f(p[e]);
+    for (int i = 0; i < BYTES / 16; ++i) {
+      const uint4 v = *(const uint4*)(p + 16 * i);
+      r.w[4 * i] = v.x;
+      r.w[4 * i + 1] = v.y;
+      r.w[4 * i + 2] = v.z;
+      r.w[4 * i + 3] = v.w;
     }
+  } else if constexpr (BYTES == 8) {
+    const uint2 v = *(const uint2*)p;
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+  } else if constexpr (BYTES == 4) {
+    r.w[0] = *(const uint32_t*)p;
   } else {
-    const float* p = (const float*)base + off;
-    if constexpr (N % 4 == 0) {
-#pragma unroll
-      for (int e = 0; e < N; e += 4) {
-        const float4 v = *(const float4*)(p + e);
-        out[e] = v.x;
-        out[e + 1] = v.y;
-        out[e + 2] = v.z;
-        out[e + 3] = v.w;
-      }
-    } else if constexpr (N == 2) {
-      const float2 v = *(const float2*)p;
-      out[0] = v.x;
-      out[1] = v.y;
-    } else {
-#pragma unroll
-      for (int e = 0; e < N; ++e) out[e] = p[e];
-    }
+    r.w[0] = *(const uint16_t*)p;
   }
 }
 
+template <int N, bool KVBF16>
+__device__ __forceinline__ void kv_zero(KVRaw<N, KVBF16>& r) {
+#pragma unroll
+  for (int i = 0; i < KVRaw<N, KVBF16>::WORDS; ++i) r.w[i] = 0u;
+}
+
+template <int N, bool KVBF16>
+__device__ __forceinline__ float kv_get(const KVRaw<N, KVBF16>& r, int e) {
+  if constexpr (KVBF16) {
+    const uint32_t w = r.w[e >> 1];
+    return (e & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
+  } else {
+    return __uint_as_float(r.w[e]);
+  }
+}
+
+constexpr int kAttnKeysPerWave = kAttnChunk / 4;
+
 template <int HD, int RMAX, bool KVBF16, bool ABF16>
 __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
-  constexpr int DPL = HD / 16;  // score phase: features per lane
-  constexpr int DPV = HD / 64;  // P V phase: output features per lane
-  constexpr int RSH = (RMAX == 16) ? 0 : (RMAX == 8 ? 1 : 2);  // lanes per row after reduce-scatter: 1 << RSH
+  constexpr int DPL = HD / 16;  // VALU score phase (f32 cache): features per lane
+  constexpr int DPV = HD / 64;  // VALU P V phase (f32 cache): features per lane
+  constexpr int KPW = kAttnKeysPerWave;
+  constexpr int FT = HD / 16;   // MFMA P V: feature tiles
   const int c = blockIdx.x, h = blockIdx.y, bl = blockIdx.z;
   const int bg = p.b0 + bl;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int kg = lane >> 4, dg = lane & 15;
   const int R = p.R;
   const int L = p.lens[bg];
   const int nkeys = L + R;
-  const int k_lo = c * p.CK;
-  const int k_hi = min(k_lo + p.CK, nkeys);
+  const int k_lo = c * kAttnChunk;
+  const int k_hi = min(k_lo + kAttnChunk, nkeys);
+  const int kw = k_lo + wave * KPW;  // this wave's first key
+  const int g = lane >> 4, kl = lane & 15;
 
-  __shared__ float s_lds[RMAX][kAttnChunkMax];
+  __shared__ float s_lds[RMAX][kAttnChunk];
   __shared__ float o_lds[4][RMAX][HD];
   __shared__ float m_lds[RMAX], l_lds[RMAX];
-  __shared__ float sc_lds[kAttnMaxChunks][RMAX];
-  __shared__ int last_s;
 
   const size_t bh = (size_t)bl * p.H + h;
   float* po = p.part_o + ((bh * p.NC + c) * p.Rmax) * HD;
   float* pml = p.part_ml + ((bh * p.NC + c) * p.Rmax) * 2;
-  const size_t kvbase = ((size_t)bg * p.H + h) * p.max_len * HD;
+  const size_t kbase = ((size_t)bg * p.H + h) * p.kv_stride * HD;  // K rows [key][HD]
+  const size_t vbase = kbase;                                       // V^T rows [feature][kv_stride]
 
   if (k_lo < k_hi) {
-    float qr[RMAX][DPL];
+    if constexpr (KVBF16) {
+      // -------- MFMA 16x16x32 bf16 for S = Q K^T and O = P V --------
+      constexpr int KS = HD / 32;
+      const uint16_t* kc = (const uint16_t*)p.kc;
+      const uint16_t* vc = (const uint16_t*)p.vc;
+      // loads first: K (B of S: 16 keys x 32 features per fragment) and V^T
+      // (B of O: 32 keys x 16 features per fragment)
+      uint4 kf[KPW / 16][KS];
 #pragma unroll
-    for (int r = 0; r < RMAX; ++r) {
-      if (r < R) {
-        const float* qp = p.q + (size_t)(bl * R + r) * p.d + h * HD + dg * DPL;
+      for (int grp = 0; grp < KPW / 16; ++grp) {
+        const int key = kw + 16 * grp + kl;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          kf[grp][ks] = key < k_hi ? *(const uint4*)(kc + kbase + (size_t)key * HD + 32 * ks + 8 * g)
+                                   : make_uint4(0, 0, 0, 0);
+      }
+      uint4 vf[FT];
+      const int kv0 = kw + 8 * g;  // first of this lane's 8 keys
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft) {
+        const uint16_t* vp = vc + vbase + (size_t)(16 * ft + kl) * p.kv_stride + kv0;
+        if (kv0 + 8 <= k_hi) {
+          vf[ft] = *(const uint4*)vp;
+        } else {
+          uint32_t w[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t lo = (kv0 + 2 * e < k_hi) ? vp[2 * e] : 0u;
+            const uint32_t hi = (kv0 + 2 * e + 1 < k_hi) ? vp[2 * e + 1] : 0u;
+            w[e] = lo | (hi << 16);
+          }
+          vf[ft] = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+      }
+      uint4 qh[KS], ql[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        qh[ks] = make_uint4(0, 0, 0, 0);
+        ql[ks] = make_uint4(0, 0, 0, 0);
+      }
+      if (kl < R) {
+        const float* qp = p.q + (size_t)(bl * R + kl) * p.d + h * HD + 8 * g;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const float4 x0 = *(const float4*)(qp + 32 * ks);
+          const float4 x1 = *(const float4*)(qp + 32 * ks + 4);
+          const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+          uint32_t hw[4], lw[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint16_t h0 = f2bf(xs[2 * e]), h1 = f2bf(xs[2 * e + 1]);
+            const uint16_t l0 = f2bf(xs[2 * e] - bf2f(h0)), l1 = f2bf(xs[2 * e + 1] - bf2f(h1));
+            hw[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            lw[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+          }
+          qh[ks] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+          ql[ks] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+        }
+      }
+#pragma unroll
+      for (int grp = 0; grp < KPW / 16; ++grp) {
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql[ks]),
+                                                        __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh[ks]),
+                                                        __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+        }
+        // D[i][j] sits in lane j + 16*(i/4), register i%4: rows 4g..4g+3 of key kl
+        const int key = kw + 16 * grp + kl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = 4 * g + i;
+          if (r < RMAX && key < k_hi) s_lds[r][key - k_lo] = (key <= L + r) ? acc[i] * p.scale : -INFINITY;
+        }
+      }
+      __syncthreads();
+      // chunk softmax, one wave per row; keys past the chunk end get p = 0
+      const int nk = k_hi - k_lo;
+      for (int r = wave; r < R; r += 4) {
+        float mx = -INFINITY;
+        for (int j = lane; j < nk; j += 64) mx = fmaxf(mx, s_lds[r][j]);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        float sum = 0.f;
+        for (int j = lane; j < kAttnChunk; j += 64) {
+          const float e = (j < nk && mx != -INFINITY) ? expf(s_lds[r][j] - mx) : 0.f;
+          s_lds[r][j] = e;
+          sum += e;
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+        if (lane == 0) {
+          m_lds[r] = mx;
+          l_lds[r] = sum;
+        }
+      }
+      __syncthreads();
+      // O = P V: A = P rows (fp32 from LDS split into two bf16 terms) over the
+      // wave's 32 keys, B = V^T fragments
+      uint4 ph = make_uint4(0, 0, 0, 0), pl = make_uint4(0, 0, 0, 0);
+      if (kl < R) {
+        const float* pp = &s_lds[kl][kw - k_lo + 8 * g];
+        const float4 x0 = *(const float4*)pp;
+        const float4 x1 = *(const float4*)(pp + 4);
+        const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        uint32_t hw[4], lw[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint16_t h0 = f2bf(xs[2 * e]), h1 = f2bf(xs[2 * e + 1]);
+          const uint16_t l0 = f2bf(xs[2 * e] - bf2f(h0)), l1 = f2bf(xs[2 * e + 1] - bf2f(h1));
+          hw[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          lw[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        }
+        ph = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+        pl = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+      }
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft) {
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl), __builtin_bit_cast(bf16x8, vf[ft]),
+                                                      acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph), __builtin_bit_cast(bf16x8, vf[ft]),
+                                                      acc, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = 4 * g + i;
+          if (r < RMAX) o_lds[wave][r][16 * ft + kl] = acc[i];
+        }
+      }
+    } else {
+      // -------- f32 cache: VALU --------
+      constexpr int KSTEPS = KPW / 4;
+      constexpr int RSH = (RMAX == 16) ? 0 : (RMAX == 8 ? 1 : 2);
+      const float* kc = (const float*)p.kc;
+      const float* vc = (const float*)p.vc;
+      const int kg = lane >> 4, dg = lane & 15;
+      float kr[KSTEPS][DPL];
+#pragma unroll
+      for (int s2 = 0; s2 < KSTEPS; ++s2) {
+        const int k = kw + 4 * s2 + kg;
 #pragma unroll
         for (int e = 0; e < DPL; e += 4) {
-          const float4 v = *(const float4*)(qp + e);
-          qr[r][e] = v.x;
-          qr[r][e + 1] = v.y;
-          qr[r][e + 2] = v.z;
-          qr[r][e + 3] = v.w;
+          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (k < k_hi) v = *(const float4*)(kc + kbase + (size_t)k * HD + dg * DPL + e);
+          kr[s2][e] = v.x;
+          kr[s2][e + 1] = v.y;
+          kr[s2][e + 2] = v.z;
+          kr[s2][e + 3] = v.w;
         }
-      } else {
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) qr[r][e] = 0.f;
       }
-    }
-    const int rr = dg >> RSH;                            // row this lane ends with
-    const bool writer = (dg & ((1 << RSH) - 1)) == 0 && rr < R;
-    for (int kb = k_lo + 4 * wave; kb < k_hi; kb += 16) {
-      const int k = kb + kg;
-      float kv[DPL];
-      if (k < k_hi) load_kv<DPL, KVBF16>(p.kc, kvbase + (size_t)k * HD + dg * DPL, kv);
-      else {
+      float vt[DPV][KPW];  // V^T: this lane's features over the wave's keys
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) kv[e] = 0.f;
-      }
-      float v[RMAX];
+      for (int e = 0; e < DPV; ++e) {
+        const float* vp = vc + vbase + (size_t)(lane * DPV + e) * p.kv_stride + kw;
 #pragma unroll
-      for (int r = 0; r < RMAX; ++r) {
-        float s = 0.f;
+        for (int j = 0; j < KPW; j += 4) {
+          if (kw + j + 4 <= k_hi) {
+            const float4 v = *(const float4*)(vp + j);
+            vt[e][j] = v.x;
+            vt[e][j + 1] = v.y;
+            vt[e][j + 2] = v.z;
+            vt[e][j + 3] = v.w;
+          } else {
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) s += qr[r][e] * kv[e];
-        v[r] = s;
-      }
-      // reduce-scatter over the 16 lanes of the key
-#pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const int off = 8 >> st;
-        const int cur = RMAX >> st;
-        if (cur > 1) {
-          const int half = cur >> 1;
-          const bool up = (dg & off) != 0;
-#pragma unroll
-          for (int j = 0; j < half; ++j) {
-            const float mine = up ? v[half + j] : v[j];
-            const float oth = up ? v[j] : v[half + j];
-            v[j] = mine + __shfl_xor(oth, off);
+            for (int jj = 0; jj < 4; ++jj) vt[e][j + jj] = (kw + j + jj < k_hi) ? vp[j + jj] : 0.f;
           }
-        } else {
-          v[0] += __shfl_xor(v[0], off);
         }
       }
-      if (k < k_hi && writer) s_lds[rr][k - k_lo] = (k <= L + rr) ? v[0] * p.scale : -INFINITY;
-    }
-    __syncthreads();
-    // chunk softmax, one wave per row
-    const int nk = k_hi - k_lo;
-    for (int r = wave; r < R; r += 4) {
-      float mx = -INFINITY;
-      for (int j = lane; j < nk; j += 64) mx = fmaxf(mx, s_lds[r][j]);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-      float sum = 0.f;
-      for (int j = lane; j < nk; j += 64) {
-        const float e = (mx == -INFINITY) ? 0.f : expf(s_lds[r][j] - mx);
-        s_lds[r][j] = e;
-        sum += e;
-      }
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
-      if (lane == 0) {
-        m_lds[r] = mx;
-        l_lds[r] = sum;
-      }
-    }
-    __syncthreads();
-    // P V: wave w takes keys k_lo + w, + 4, ...; lane owns features lane*DPV ..
-    float acc[RMAX][DPV];
-#pragma unroll
-    for (int r = 0; r < RMAX; ++r)
-#pragma unroll
-      for (int e = 0; e < DPV; ++e) acc[r][e] = 0.f;
-    for (int k = k_lo + wave; k < k_hi; k += 4) {
-      float vv[DPV];
-      load_kv<DPV, KVBF16>(p.vc, kvbase + (size_t)k * HD + lane * DPV, vv);
-      const int kk = k - k_lo;
+      float qr[RMAX][DPL];
 #pragma unroll
       for (int r = 0; r < RMAX; ++r) {
         if (r < R) {
-          const float pr = s_lds[r][kk];
+          const float* qp = p.q + (size_t)(bl * R + r) * p.d + h * HD + dg * DPL;
 #pragma unroll
-          for (int e = 0; e < DPV; ++e) acc[r][e] += pr * vv[e];
+          for (int e = 0; e < DPL; e += 4) {
+            const float4 v = *(const float4*)(qp + e);
+            qr[r][e] = v.x;
+            qr[r][e + 1] = v.y;
+            qr[r][e + 2] = v.z;
+            qr[r][e + 3] = v.w;
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) qr[r][e] = 0.f;
+        }
+      }
+      const int rr = dg >> RSH;
+      const bool writer = (dg & ((1 << RSH) - 1)) == 0 && rr < R;
+#pragma unroll
+      for (int s2 = 0; s2 < KSTEPS; ++s2) {
+        const int k = kw + 4 * s2 + kg;
+        float v[RMAX];
+#pragma unroll
+        for (int r = 0; r < RMAX; ++r) {
+          float acc = 0.f;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) acc += qr[r][e] * kr[s2][e];
+          v[r] = acc;
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+          const int off = 8 >> st;
+          const int cur = RMAX >> st;
+          if (cur > 1) {
+            const int half = cur >> 1;
+            const bool up = (dg & off) != 0;
+#pragma unroll
+            for (int j = 0; j < half; ++j) {
+              const float mine = up ? v[half + j] : v[j];
+              const float oth = up ? v[j] : v[half + j];
+              v[j] = mine + __shfl_xor(oth, off);
+            }
+          } else {
+            v[0] += __shfl_xor(v[0], off);
+          }
+        }
+        if (k < k_hi && writer) s_lds[rr][k - k_lo] = (k <= L + rr) ? v[0] * p.scale : -INFINITY;
+      }
+      __syncthreads();
+      const int nk = k_hi - k_lo;
+      for (int r = wave; r < R; r += 4) {
+        float mx = -INFINITY;
+        for (int j = lane; j < nk; j += 64) mx = fmaxf(mx, s_lds[r][j]);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        float sum = 0.f;
+        for (int j = lane; j < kAttnChunk; j += 64) {
+          const float e = (j < nk && mx != -INFINITY) ? expf(s_lds[r][j] - mx) : 0.f;
+          s_lds[r][j] = e;
+          sum += e;
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+        if (lane == 0) {
+          m_lds[r] = mx;
+          l_lds[r] = sum;
+        }
+      }
+      __syncthreads();
+      const int kk0 = kw - k_lo;
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) {
+        float a[DPV];
+#pragma unroll
+        for (int e = 0; e < DPV; ++e) a[e] = 0.f;
+        if (r < R) {
+#pragma unroll
+          for (int j = 0; j < KPW; j += 4) {
+            const float4 p4 = *(const float4*)&s_lds[r][kk0 + j];
+#pragma unroll
+            for (int e = 0; e < DPV; ++e)
+              a[e] += p4.x * vt[e][j] + p4.y * vt[e][j + 1] + p4.z * vt[e][j + 2] + p4.w * vt[e][j + 3];
+          }
+#pragma unroll
+          for (int e = 0; e < DPV; ++e) o_lds[wave][r][lane * DPV + e] = a[e];
         }
       }
     }
-#pragma unroll
-    for (int r = 0; r < RMAX; ++r)
-      if (r < R)
-#pragma unroll
-        for (int e = 0; e < DPV; ++e) o_lds[wave][r][lane * DPV + e] = acc[r][e];
     __syncthreads();
     for (int idx = tid; idx < R * HD; idx += 256) {
       const int r = idx / HD, dd = idx % HD;
@@ -620,32 +868,37 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
     pml[tid * 2] = -INFINITY;
     pml[tid * 2 + 1] = 0.f;
   }
+}
 
-  // the last chunk of (b, h) to arrive merges
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t old = atomicAdd(&p.cnt[bh], 1u);
-    last_s = (old == (uint32_t)(p.NC - 1));
-  }
-  __syncthreads();
-  if (!last_s) return;
-  __threadfence();
+// Merge of the chunk partials of every (request, head) in chunk order (a
+// second launch: the kernel boundary orders the partial writes before these
+// reads), written as the O-projection operand.
+template <int HD, int RMAX, bool ABF16>
+__global__ void __launch_bounds__(256) attn_combine_kernel(AttnParams p) {
+  const int h = blockIdx.x, bl = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int R = p.R;
+  __shared__ float sc_lds[kAttnMaxChunks][RMAX];
+  __shared__ float l_lds[kAttnMaxChunks][RMAX];
+  const size_t bh = (size_t)bl * p.H + h;
   const float* po0 = p.part_o + (bh * p.NC * p.Rmax) * HD;
   const float* pml0 = p.part_ml + (bh * p.NC * p.Rmax) * 2;
+  for (int idx = tid; idx < p.NC * R; idx += 256) {
+    const int cc = idx / R, r = idx % R;
+    const float2 ml = *(const float2*)(pml0 + ((size_t)cc * p.Rmax + r) * 2);
+    sc_lds[cc][r] = ml.x;
+    l_lds[cc][r] = ml.y;
+  }
+  __syncthreads();
   if (tid < R) {
     const int r = tid;
     float M = -INFINITY;
-    for (int cc = 0; cc < p.NC; ++cc) {
-      const float mc = __builtin_nontemporal_load(pml0 + ((size_t)cc * p.Rmax + r) * 2);
-      sc_lds[cc][r] = mc;
-      M = fmaxf(M, mc);
-    }
+    for (int cc = 0; cc < p.NC; ++cc) M = fmaxf(M, sc_lds[cc][r]);
     float Ls = 0.f;
     for (int cc = 0; cc < p.NC; ++cc) {
       const float mc = sc_lds[cc][r];
       const float e = (mc == -INFINITY) ? 0.f : expf(mc - M);
-      Ls += __builtin_nontemporal_load(pml0 + ((size_t)cc * p.Rmax + r) * 2 + 1) * e;
+      Ls += l_lds[cc][r] * e;
       sc_lds[cc][r] = e;
     }
     const float inv = 1.0f / Ls;
@@ -655,15 +908,15 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   for (int idx = tid; idx < R * HD; idx += 256) {
     const int r = idx / HD, dd = idx % HD;
     float O = 0.f;
-#pragma unroll 4
+#pragma unroll 8
     for (int cc = 0; cc < p.NC; ++cc) {
       const float sc = sc_lds[cc][r];
-      if (sc != 0.f) O += __builtin_nontemporal_load(po0 + ((size_t)cc * p.Rmax + r) * HD + dd) * sc;
+      const float v = po0[((size_t)cc * p.Rmax + r) * HD + dd];
+      O += sc != 0.f ? v * sc : 0.f;
     }
     const int m = bl * R + r;
     store_act<ABF16>(p.act_out, p.act_split, (size_t)m * p.d + h * HD + dd, O);
   }
-  if (tid == 0) p.cnt[bh] = 0u;
 }
 
 // ---------------------------------------------------------------------------
@@ -737,7 +990,6 @@ __global__ void __launch_bounds__(kAcceptThreads) accept_kernel(AcceptParams p) 
   const int R = p.R, V = p.V, G = p.gamma;
   __shared__ float rlse[kMaxR];
   __shared__ int rarg[kMaxR];
-  __shared__ RowStat part[NWV];
   __shared__ Best bpart[NWV];
   __shared__ int n_s;
 
@@ -749,20 +1001,21 @@ __global__ void __launch_bounds__(kAcceptThreads) accept_kernel(AcceptParams p) 
   const float invT = sample ? p.inv_T : 1.0f;
   const float* lg = p.logits + (size_t)b * R * V;
 
-  // row statistics over the vocabulary (from the LM head's per-panel partials
-  // when given), merged in a fixed order
-  for (int r = 0; r < R; ++r) {
+  // row statistics over the vocabulary: wave r merges row r from the LM
+  // head's per-panel partials (or, without them, from the logits), in a fixed
+  // order
+  for (int r = wave; r < R; r += NWV) {
     RowStat st{-INFINITY, 0.f, 0x7fffffff};
     if (p.stats != nullptr) {
       const float* sp = p.stats + (size_t)(b * R + r) * p.NU * 3;
-#pragma unroll 2
-      for (int q = tid; q < p.NU; q += kAcceptThreads) {
+#pragma unroll 8
+      for (int q = lane; q < p.NU; q += 64) {
         const RowStat one{sp[q * 3], sp[q * 3 + 1], __float_as_int(sp[q * 3 + 2])};
         if (one.m != -INFINITY) st = merge_stat(st, one);
       }
     } else {
-#pragma unroll 4
-      for (int v = tid; v < V; v += kAcceptThreads) {
+#pragma unroll 8
+      for (int v = lane; v < V; v += 64) {
         const float z = lg[(size_t)r * V + v] * invT;
         if (z != z) continue;
         st = merge_stat(st, RowStat{z, 1.f, v});
@@ -776,16 +1029,12 @@ __global__ void __launch_bounds__(kAcceptThreads) accept_kernel(AcceptParams p) 
       o.a = __shfl_xor(st.a, off);
       st = (lane & off) ? merge_stat(o, st) : merge_stat(st, o);
     }
-    if (lane == 0) part[wave] = st;
-    __syncthreads();
-    if (tid == 0) {
-      RowStat t = part[0];
-      for (int w = 1; w < NWV; ++w) t = merge_stat(t, part[w]);
-      rlse[r] = t.m + logf(t.s);
-      rarg[r] = t.a;
+    if (lane == 0) {
+      rlse[r] = st.m + logf(st.s);
+      rarg[r] = st.a;
     }
-    __syncthreads();
   }
+  __syncthreads();
 
   if (tid == 0) {
     int n = G;
@@ -871,6 +1120,15 @@ __global__ void commit_kernel(int B, int32_t* lens, int32_t* pending, const int3
   }
 }
 
+__global__ void copy_state_kernel(int B, int32_t* lens, int32_t* pending, const int32_t* src_lens,
+                                  const int32_t* src_pending) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) {
+    lens[b] = src_lens[b];
+    pending[b] = src_pending[b];
+  }
+}
+
 __global__ void advance_kernel(int b, int count, int32_t* lens, int32_t* pending, const int32_t* src) {
   if (threadIdx.x == 0) {
     lens[b] += count;
@@ -918,7 +1176,9 @@ constexpr int kGemmWaves = 8;
 
 template <bool WBF16, int KIND>
 hipError_t launch_gemm_kind(const GemmParams& gp, int grid, int mt, hipStream_t st) {
-  if (mt == 1)
+  if (mt == 1 && gp.NKB <= 2 * kGemmWaves)
+    hipLaunchKernelGGL((gemm_ares_kernel<WBF16, kGemmWaves, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
+  else if (mt == 1)
     hipLaunchKernelGGL((gemm_kernel<WBF16, kGemmWaves, 1, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
   else
     hipLaunchKernelGGL((gemm_kernel<WBF16, kGemmWaves, 2, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
@@ -942,6 +1202,11 @@ hipError_t launch_attn_r(const AttnParams& ap, bool kvbf16, bool abf16, dim3 gri
   else if (kvbf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, true, false>), grid, dim3(256), 0, st, ap);
   else if (abf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, false, true>), grid, dim3(256), 0, st, ap);
   else hipLaunchKernelGGL((attn_kernel<HD, RMAX, false, false>), grid, dim3(256), 0, st, ap);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 cgrid(grid.y, grid.z);
+  if (abf16) hipLaunchKernelGGL((attn_combine_kernel<HD, RMAX, true>), cgrid, dim3(256), 0, st, ap);
+  else hipLaunchKernelGGL((attn_combine_kernel<HD, RMAX, false>), cgrid, dim3(256), 0, st, ap);
   return hipGetLastError();
 }
 
@@ -960,7 +1225,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   const Workspace& W = md->ws;
   const bool wb = D.wdt == SPADE_BF16;
   const int KBd = kblock_of(D.wdt);
-  const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->max_len * D.hd;  // elements
+  const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->stride * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
   const uint8_t* lb = md->weights + (size_t)layer * md->lay.layer_bytes;
   const int M = fc.nb * fc.R;
@@ -976,7 +1241,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   g.hd = D.hd;
   g.d = D.d;
   g.F = D.F;
-  g.max_len = kv->max_len;
+  g.kv_stride = kv->stride;
   g.kv_bf16 = D.kvdt == SPADE_BF16;
   g.rope = W.rope;
   g.x = W.x;
@@ -1078,16 +1343,13 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   else hipLaunchKernelGGL(embed_kernel<false>, dim3(M), dim3(256), 0, st, ep);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
-  const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->max_len * D.hd;  // elements
+  const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->stride * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
 
-  // attention chunking: about 512 workgroups, chunks of 64..256 keys
+  // attention chunks of kAttnChunk keys over the longest request
   int max_keys = 0;
   for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) max_keys = std::max(max_keys, kv->lens_ub[b] + fc.R);
-  int CK = kAttnChunkMin;
-  while (CK < kAttnChunkMax && ((long)fc.nb * D.H * ((max_keys + CK - 1) / CK) > 512 ||
-                                (max_keys + CK - 1) / CK > kAttnMaxChunks))
-    CK *= 2;
+  const int CK = kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
 
@@ -1102,7 +1364,7 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     ap.R = fc.R;
     ap.H = D.H;
     ap.d = D.d;
-    ap.max_len = kv->max_len;
+    ap.kv_stride = kv->stride;
     ap.CK = CK;
     ap.NC = NC;
     ap.scale = 1.0f / sqrtf((float)D.hd);
@@ -1196,6 +1458,13 @@ hipError_t launch_pack(spade_model md, int kind, int layer, const void* src, hip
 
 hipError_t launch_commit(spade_kv kv, int B, const int32_t* n, const int32_t* corr, hipStream_t st) {
   hipLaunchKernelGGL(commit_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, kv->lens, kv->pending, n, corr);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_state(int B, int32_t* lens, int32_t* pending, const int32_t* src_lens,
+                             const int32_t* src_pending, hipStream_t st) {
+  hipLaunchKernelGGL(copy_state_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, lens, pending, src_lens,
+                     src_pending);
   return hipGetLastError();
 }
 

@@ -16,10 +16,10 @@ constexpr int kMaxRowsPerGemm = 32;  // rows handled by one GEMM launch
 constexpr int kPrefillRows = 16;     // tokens per prefill forward
 constexpr int kMaxR = 16;            // rows per request in one forward (gamma <= 15)
 constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
-constexpr int kAttnChunkMin = 64;
-constexpr int kAttnChunkMax = 256;
+constexpr int kAttnChunk = 128;      // keys per attention workgroup
 constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
-constexpr int kMaxLen = kAttnChunkMax * kAttnMaxChunks;
+constexpr int kMaxLen = kAttnChunk * kAttnMaxChunks;
+inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 
@@ -100,6 +100,7 @@ struct spade_kv_s {
   int32_t* lens;
   int32_t* pending;
   int max_batch, max_len;
+  int stride;    // positions per (request, head) row of the cache: max_len rounded up to 32
   int* lens_ub;  // host upper bound of lens per request
   int* snap_ub;  // lens_ub at the last snapshot
 };
@@ -138,5 +139,7 @@ hipError_t launch_accept(spade_model m, const AcceptCall& ac, hipStream_t st);
 hipError_t launch_pack(spade_model m, int kind, int layer, const void* src, hipStream_t st);
 hipError_t launch_commit(spade_kv kv, int B, const int32_t* n, const int32_t* corr, hipStream_t st);
 hipError_t launch_advance(spade_kv kv, int b, int count, const int32_t* pending_src, hipStream_t st);
+hipError_t launch_copy_state(int B, int32_t* lens, int32_t* pending, const int32_t* src_lens,
+                             const int32_t* src_pending, hipStream_t st);
 
 }  // namespace spade
