@@ -51,19 +51,27 @@ def gumbel_noise(seed: int, n: int) -> np.ndarray:
     return -np.log(-np.log(U))
 
 
+def gumbel_top2(log_w: np.ndarray, seed: int):
+    """Perturbed scores log_w[v] + G_v: the best token, the runner-up and the
+    gap between their scores.  Ties go to the lowest id."""
+    s = np.asarray(log_w, dtype=np.float64) + gumbel_noise(seed, len(log_w))
+    v = int(np.argmax(s))
+    rest = s.copy()
+    rest[v] = -np.inf
+    v2 = int(np.argmax(rest)) if rest.size > 1 else v
+    second = float(rest[v2]) if rest.size > 1 else -np.inf
+    return v, v2, float(s[v] - second)
+
+
 def gumbel_argmax(log_w: np.ndarray, seed: int):
     """Draw v with probability proportional to exp(log_w[v]).
 
     Entries with log_w = -inf (zero weight) can never be drawn.  Returns the
     token and the gap between the best and second-best perturbed scores (the
-    margin by which the draw is decided).  Ties go to the lowest id.
+    margin by which the draw is decided).
     """
-    s = np.asarray(log_w, dtype=np.float64) + gumbel_noise(seed, len(log_w))
-    v = int(np.argmax(s))
-    top = s[v]
-    rest = np.delete(s, v)
-    second = float(np.max(rest)) if rest.size else -np.inf
-    return v, float(top - second)
+    v, _, gap = gumbel_top2(log_w, seed)
+    return v, gap
 
 
 def inverse_cdf_draw(w: np.ndarray, u: float) -> int:

@@ -43,7 +43,7 @@ from typing import List, Optional
 import numpy as np
 
 from .decoder import Decoder, KVCache
-from .sampling import gumbel_argmax, uniform_seed
+from .sampling import gumbel_top2, uniform_seed
 
 GREEDY = 0
 SAMPLE = 1
@@ -85,6 +85,7 @@ def _top2_margin(row: np.ndarray) -> float:
 class RowDecision:
     accepted: bool
     margin: float  # greedy: top-2 logit margin; sampling: |u - p/q|
+    ratio: float = float("nan")  # sampling: p(x) / q(x)
 
 
 @dataclass
@@ -131,24 +132,28 @@ def speculative_rows(logits: np.ndarray, drafts: np.ndarray, q: Optional[np.ndar
         ok = accept_test(uniforms[i], p_x, q_x)
         ratio = np.inf if q_x == 0.0 else p_x / q_x
         gap = np.inf if not np.isfinite(ratio) else abs(float(uniforms[i]) - ratio)
-        rows.append(RowDecision(ok, gap))
+        rows.append(RowDecision(ok, gap, ratio))
         if not ok:
             n = i
             break
     seed = uniform_seed(uniforms[d])
     fallback = False
+    kind = "bonus"
     if n < d:
         p_n = np.exp(_log_softmax(z[n]))
         w = np.maximum(0.0, p_n - np.asarray(q[n], dtype=np.float64))
         if w.sum() > 0:
+            kind = "residual"
             with np.errstate(divide="ignore"):
-                corr, gap = gumbel_argmax(np.log(w), seed)
+                corr, second, gap = gumbel_top2(np.log(w), seed)
         else:
             fallback = True
-            corr, gap = gumbel_argmax(z[n], seed)
+            kind = "fallback"
+            corr, second, gap = gumbel_top2(z[n], seed)
     else:
-        corr, gap = gumbel_argmax(z[d], seed)
+        corr, second, gap = gumbel_top2(z[d], seed)
     res = VerifyResult(n, corr, rows, gap, fallback)
+    res.notes["draw"] = {"kind": kind, "row": n, "top": corr, "second": second}
     res.pinned_n = all(r.margin > RATIO_MARGIN for r in rows)
     res.pinned_correction = res.pinned_n and gap > DRAW_MARGIN and not fallback
     return res

@@ -84,9 +84,46 @@ class Parity:
     excluded_n: int
     excluded_corr: int
     total: int
+    stable_n: int = 0
+    stable_corr: int = 0
+    stable_n_fail: List[int] = field(default_factory=list)
+    stable_corr_fail: List[int] = field(default_factory=list)
+
+
+def stability(res, logits: np.ndarray, q: Optional[np.ndarray], mode: int, temperature: float,
+              eps: float):
+    """Whether n_accepted and the correction are decided beyond what logits
+    off by at most eps (max abs) could change.
+
+    greedy: a row's argmax cannot move when its top-2 margin exceeds 2 eps.
+    sampling: z = logit / T moves by at most eps/T, so p(x) / q(x) moves by a
+    factor within exp(+-2 eps / T); the test u q < p cannot flip when
+    |u - p/q| > (p/q)(exp(2 eps/T) - 1).  A bonus / fallback draw scores
+    z_v + G_v, each off by at most eps/T; a residual draw scores
+    log(p_v - q_v) + G_v, off by at most p_v (exp(2 eps/T) - 1) / (p_v - q_v).
+    Small constants cover the float32 evaluation of the same quantities."""
+    if mode == GREEDY:
+        n_ok = all(r.margin > 2 * eps + 1e-6 for r in res.rows)
+        return n_ok, n_ok and res.draw_margin > 2 * eps + 1e-6
+    f = float(np.expm1(2 * eps / temperature))
+    n_ok = all((not np.isfinite(r.ratio)) or r.margin > r.ratio * f + 2e-6 for r in res.rows)
+    d = res.notes["draw"]
+    if d["kind"] == "residual":
+        z = np.asarray(logits[d["row"]], dtype=np.float64) / temperature
+        pz = np.exp(z - z.max())
+        pz /= pz.sum()
+        bound = 0.0
+        for v in (d["top"], d["second"]):
+            w = pz[v] - float(q[d["row"], v])
+            bound += pz[v] * f / w if w > 0 else np.inf
+        c_ok = res.draw_margin > bound + 1e-5
+    else:
+        c_ok = res.draw_margin > 2 * eps / temperature + 1e-5
+    return n_ok, n_ok and c_ok
 
 
 def compare(orun: OracleRun, gpu_logits: np.ndarray, gpu_n: np.ndarray, gpu_corr: np.ndarray) -> Parity:
+    inp = orun.inputs
     errs = [np.abs(gpu_logits[b].astype(np.float64) - r.logits).max() for b, r in enumerate(orun.results)]
     p = Parity(float(max(errs)), 0, 0, 0, 0, [], [], 0, 0, len(orun.results))
     for b, r in enumerate(orun.results):
@@ -106,6 +143,16 @@ def compare(orun: OracleRun, gpu_logits: np.ndarray, gpu_n: np.ndarray, gpu_corr
                 p.pinned_corr_fail.append(b)
         else:
             p.excluded_corr += 1
+        q = inp.draft_probs[b] if inp.draft_probs is not None else None
+        sn, sc = stability(r, r.logits, q, int(inp.modes[b]), inp.temperature, errs[b])
+        if sn:
+            p.stable_n += 1
+            if not nm:
+                p.stable_n_fail.append(b)
+        if sc:
+            p.stable_corr += 1
+            if not (nm and cm):
+                p.stable_corr_fail.append(b)
     return p
 
 
@@ -137,3 +184,15 @@ def gpu_verify(model, kv, inp, want_logits=True):
     torch.cuda.synchronize()
     lg = buf.logits.cpu().numpy() if want_logits else None
     return lg, buf.n.cpu().numpy(), buf.corr.cpu().numpy(), buf
+
+
+def gpu_setup_streaming(w, max_len: int, max_batch: Optional[int] = None):
+    """Model + KV on the GPU with weights generated and uploaded one tensor at
+    a time (no host copy of the whole model)."""
+    from paper_2608_13076_amd import spade
+    from synth import iter_weights
+    model = spade.Model(w.model, max_batch or w.batch, w.gamma, max_len)
+    for kind, layer, arr in iter_weights(w.model, w.seed):
+        model.load_numpy(kind, layer, arr)
+    kv = spade.KVCache(model, max_batch or w.batch, max_len)
+    return model, kv

@@ -1,0 +1,201 @@
+"""Full-size workloads through the C ABI, in the launch configuration the
+benchmark times.
+
+* 7B greedy (1024 cached tokens, gamma 5) and 13B sampling (2048 cached,
+  gamma 8): against the float64 oracle's stored results (tests/golden, written
+  by make_golden.py): logits at a seeded sample of vocabulary ids per row
+  within 5e-2, n_accepted and correction exact where decided.
+* 7B batched (16 ragged requests, gamma 8, M = 144) and 33B (4 x 1536, gamma
+  6, commit + second round): properties that hold at any size -- requests are
+  independent of their batch, decisions agree with the emitted logits, layer-0
+  K rows equal the oracle's (they depend on one token only), and a second
+  round after commit is bit-identical to a fresh prefill of the committed
+  sequence.
+"""
+
+import numpy as np
+import pytest
+
+from synth import make_inputs, workload
+from tests.golden.drafts import load_golden
+from tests.helpers import gpu_prefill, gpu_setup_streaming, gpu_verify
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _golden_case(name):
+    g = load_golden(name)
+    if g is None:
+        pytest.skip(f"no stored oracle results for {name}")
+    w = workload(name)
+    inp = make_inputs(w)
+    inp.drafts[:] = np.asarray(g["drafts"], dtype=np.int32)
+    if g.get("draft_probs_file"):
+        import os
+        from tests.golden.drafts import HERE
+        inp.draft_probs = np.load(os.path.join(HERE, g["draft_probs_file"]))
+    max_len = int(inp.lens.max()) + 2 * (w.gamma + 1) + 8
+    print(f"[{name}] weights + prefill", flush=True)
+    model, kv = gpu_setup_streaming(w, max_len)
+    gpu_prefill(kv, inp)
+    print(f"[{name}] verify", flush=True)
+    lg, n, c, _ = gpu_verify(model, kv, inp)
+    assert model.device_error() == 0
+    for b, req in enumerate(g["requests"]):
+        err = 0.0
+        for i, row in enumerate(req["rows"]):
+            ids = np.asarray(row["ids"])
+            err = max(err, float(np.abs(lg[b, i, ids].astype(np.float64) - np.asarray(row["logits"])).max()))
+        print(f"[{name}] request {b}: logit err {err:.3e}; n gpu/oracle {n[b]}/{req['n_accepted']}, "
+              f"correction {c[b]}/{req['correction']}, pinned {req['pinned_n']}/{req['pinned_correction']}",
+              flush=True)
+        assert err < 5e-2
+        if req["mode"] == 0:
+            if all(m > max(0.1, 2 * err) for m in req["row_margins"]):
+                assert n[b] == req["n_accepted"]
+                if req["draw_margin"] > max(0.1, 2 * err):
+                    assert c[b] == req["correction"]
+        else:
+            f = float(np.expm1(2 * err / g["temperature"]))
+            ratios = req.get("row_ratios", [])
+            if ratios and all((not np.isfinite(r)) or m > r * f + 2e-6
+                              for m, r in zip(req["row_margins"], ratios)):
+                assert n[b] == req["n_accepted"]
+                if req.get("draw_bound") is not None and req["draw_margin"] > req["draw_bound"] * f + 2 * err + 1e-5:
+                    assert c[b] == req["correction"]
+    return lg, n, c
+
+
+def test_c2_7b_greedy_vs_oracle():
+    _golden_case("c2_7b_greedy")
+
+
+def test_c3_13b_sample_vs_oracle():
+    _golden_case("c3_13b_sample")
+
+
+def _greedy_consistent(lg_b, drafts_b, n_b, c_b):
+    G = len(drafts_b)
+    am = np.argmax(lg_b.astype(np.float32), axis=-1)
+    n_exp = G
+    for i in range(G):
+        if drafts_b[i] != am[i]:
+            n_exp = i
+            break
+    return n_b == n_exp and c_b == am[n_exp]
+
+
+def test_c4_7b_batched_properties():
+    w = workload("c4_7b_batched")
+    inp = make_inputs(w)
+    max_len = int(inp.lens.max()) + 2 * (w.gamma + 1) + 8
+    print(f"[c4] weights + prefill of {int(inp.lens.sum())} tokens", flush=True)
+    model, kv = gpu_setup_streaming(w, max_len)
+    gpu_prefill(kv, inp)
+    print("[c4] verify B=16", flush=True)
+    lg, n, c, _ = gpu_verify(model, kv, inp)
+    assert model.device_error() == 0
+    # batch independence: the first k requests alone give bit-identical rows
+    for k in (1, 5):
+        sub = make_inputs(w)
+        sub.drafts = inp.drafts[:k].copy()
+        sub.uniforms = inp.uniforms[:k].copy()
+        sub.modes = inp.modes[:k].copy()
+        sub.draft_probs = None if inp.draft_probs is None else inp.draft_probs[:k].copy()
+        sub.workload = w.with_(batch=k)
+        print(f"[c4] verify B={k}", flush=True)
+        lgk, nk, ck, _ = gpu_verify(model, kv, sub)
+        np.testing.assert_array_equal(lgk, lg[:k])
+        np.testing.assert_array_equal(nk, n[:k])
+        np.testing.assert_array_equal(ck, c[:k])
+    # decisions agree with the emitted logits
+    for b in range(w.batch):
+        if inp.modes[b] == 0:
+            assert _greedy_consistent(lg[b], inp.drafts[b], n[b], c[b]), b
+        else:
+            z = lg[b].astype(np.float64) / inp.temperature
+            p = np.exp(z - z.max(-1, keepdims=True))
+            p /= p.sum(-1, keepdims=True)
+            for i in range(n[b] + (1 if n[b] < w.gamma else 0)):
+                x = inp.drafts[b, i]
+                ratio = p[i, x] / inp.draft_probs[b, i, x]
+                if abs(inp.uniforms[b, i] - ratio) > 1e-4 * max(1.0, ratio):
+                    assert (inp.uniforms[b, i] < ratio) == (i < n[b]), (b, i)
+            if n[b] < w.gamma:  # a residual draw only yields tokens with p > q
+                assert p[n[b], c[b]] > inp.draft_probs[b, n[b], c[b]] * (1 - 1e-4), b
+    # layer-0 K rows depend on one token only: compare with the oracle there
+    _check_layer0_keys(w, inp, kv, max_len)
+
+
+def _check_layer0_keys(w, inp, kv, max_len, n_samples=24):
+    import torch
+    from oracle.decoder import Decoder, apply_rope, bf16_round, rms_norm, rope_tables
+    from synth import make_tensor
+    m = w.model
+    emb = make_tensor(m, "embed", None, w.seed)
+    g = make_tensor(m, "g_attn", 0, w.seed)
+    wk = make_tensor(m, "wk", 0, w.seed)
+    from oracle.decoder import bf16_bits_to_f64
+    E = bf16_bits_to_f64(emb) if emb.dtype == np.uint16 else emb.astype(np.float64)
+    Wk = bf16_bits_to_f64(wk) if wk.dtype == np.uint16 else wk.astype(np.float64)
+    stride = (max_len + 31) // 32 * 32
+    kcache = kv.buf[: kv.buf.numel() // 2].view(torch.int16 if m.kv_dtype == "bf16" else torch.float32)
+    rng = np.random.default_rng(5)
+    for _ in range(n_samples):
+        b = int(rng.integers(0, w.batch))
+        pos = int(rng.integers(0, int(inp.lens[b])))
+        tok = int(inp.prompts[b][pos])
+        h = rms_norm(E[tok][None], g.astype(np.float64), m.rms_eps)
+        k = (h @ Wk.T).reshape(1, m.n_heads, m.head_dim)
+        cs, sn = rope_tables(np.array([pos]), m.head_dim, m.rope_theta)
+        k = bf16_round(apply_rope(k, cs, sn))[0]
+        for hh in (0, m.n_heads - 1):
+            off = ((b * m.n_heads + hh) * stride + pos) * m.head_dim
+            row = kcache[off: off + m.head_dim].cpu().numpy()
+            got = (row.view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+            # equal up to one bf16 rounding step of float32 differences
+            np.testing.assert_allclose(got, k[hh], rtol=2 ** -7, atol=1e-6)
+
+
+def test_c5_33b_commit_round_two_equals_fresh_prefill():
+    import torch
+    w = workload("c5_33b_commit")
+    inp = make_inputs(w)
+    G = w.gamma
+    max_len = int(inp.lens.max()) + 3 * (G + 1) + 8
+    print("[c5] weights + prefill", flush=True)
+    model, kv = gpu_setup_streaming(w, max_len)
+    gpu_prefill(kv, inp)
+    print("[c5] round 1", flush=True)
+    lg1, n1, c1, buf = gpu_verify(model, kv, inp)
+    for b in range(w.batch):
+        assert _greedy_consistent(lg1[b], inp.drafts[b], n1[b], c1[b]), b
+    kv.commit(buf.n, buf.corr)
+    torch.cuda.synchronize()
+    lens2, pend2 = kv.get_state(w.batch)
+    np.testing.assert_array_equal(lens2, inp.lens + n1 + 1)
+    np.testing.assert_array_equal(pend2, c1)
+    inp2 = make_inputs(w, round_index=1)
+    print("[c5] round 2", flush=True)
+    lg2, n2, c2, _ = gpu_verify(model, kv, inp2)
+    # fresh cache holding the committed sequences
+    from paper_2608_13076_amd import spade
+    kv2 = spade.KVCache(model, w.batch, max_len)
+    for b in range(w.batch):
+        seq = np.concatenate([inp.prompts[b], inp.drafts[b, : n1[b]], [c1[b]]]).astype(np.int32)
+        kv2.prefill(b, seq)
+    print("[c5] round 2 on a fresh prefill", flush=True)
+    lg2f, n2f, c2f, _ = gpu_verify(model, kv2, inp2)
+    np.testing.assert_array_equal(lg2, lg2f)
+    np.testing.assert_array_equal(n2, n2f)
+    np.testing.assert_array_equal(c2, c2f)
+    for b in range(w.batch):
+        assert _greedy_consistent(lg2[b], inp2.drafts[b], n2[b], c2[b]), b
+    assert model.device_error() == 0
