@@ -194,5 +194,7 @@ def gpu_setup_streaming(w, max_len: int, max_batch: Optional[int] = None):
     model = spade.Model(w.model, max_batch or w.batch, w.gamma, max_len)
     for kind, layer, arr in iter_weights(w.model, w.seed):
         model.load_numpy(kind, layer, arr)
+        if kind == "wd" and layer is not None and layer % 8 == 7:
+            print(f"  [{w.name}] weights of layer {layer} loaded", flush=True)
     kv = spade.KVCache(model, max_batch or w.batch, max_len)
     return model, kv
