@@ -57,7 +57,9 @@ enum {
   SPADE_DERR_TOKEN = 1u,    /* a token id was outside [0, vocab); clamped      */
   SPADE_DERR_NAN = 2u,      /* a logit was NaN                                  */
   SPADE_DERR_RESIDUAL = 4u, /* max(0, p - q) had no mass; drew from p instead   */
-  SPADE_DERR_NOQ = 8u       /* a sampling request got no draft_probs; greedy    */
+  SPADE_DERR_NOQ = 8u,      /* a sampling request got no draft_probs; greedy    */
+  SPADE_DERR_SYNC = 16u     /* a grid barrier of the single-launch verify pass
+                               timed out; that call's outputs are invalid       */
 };
 
 /* Weight tensors, row-major [out_features, in_features] unless noted. */
@@ -200,6 +202,20 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma,
                           const float* d_uniforms, const uint8_t* d_mode, float temperature,
                           int32_t* d_n_accepted, int32_t* d_correction, float* d_logits,
                           void* stream);
+
+/* Execution path of spade_verify.  After spade_model_set_fused(m, 1), a call
+ * whose shape the single-launch pass handles -- bf16 weights and cache,
+ * head_dim 128, B * (gamma + 1) <= 16, a device with cooperative launches --
+ * runs as ONE persistent kernel over all compute units (grid barriers between
+ * the stages, the next stage's weights requested before each barrier wait);
+ * any other call runs as one kernel per stage.  Both paths compute bit-for-bit
+ * the same results (same tiling, summation orders and merge order).  The
+ * default at model creation is the per-stage path unless the environment
+ * variable SPADE_FUSED is "1".  enable != 0 on a device without cooperative
+ * launches returns SPADE_EUNSUPPORTED.  A persistent pass whose grid barrier
+ * does not complete within about a second sets SPADE_DERR_SYNC and returns
+ * early. */
+spade_status spade_model_set_fused(spade_model m, int enable);
 
 /* Context update after spade_verify (Algorithm 1: append the k accepted
  * tokens and the correction, m <- m + k + 1): lens[b] += n_accepted[b] + 1 and

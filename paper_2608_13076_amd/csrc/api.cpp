@@ -86,7 +86,9 @@ ArenaLayout layout_of(const Dims& D) {
 }
 
 struct WsPlan {
-  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, total;
+  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, bar, fused, total;
+  FusedArena fa;
+  bool has_fused;
   size_t act_split, actf_split;
   int Mmax, NCmax, Rmax;
 };
@@ -120,6 +122,13 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.stats = take((size_t)p.Mmax * NU * 3 * 4);
   p.rope = take((size_t)max_len * (D.hd / 2) * 2 * 4);
   p.err = take(4);
+  p.bar = take(kBarBytes);
+  // the single-launch pass handles bf16 weights and cache with head_dim 128
+  p.has_fused = wb && D.kvdt == SPADE_BF16 && D.hd == 128;
+  if (p.has_fused) {
+    p.fa = fused_arena_of(D.L, D.d, D.F);
+    p.fused = take(p.fa.total);
+  }
   p.total = off;
   return p;
 }
@@ -178,6 +187,14 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = v;
   }
+  // the single-launch verify pass needs cooperative launches (all workgroups
+  // resident); it is off by default (the per-stage path is faster at the
+  // measured shapes), SPADE_FUSED=1 or spade_model_set_fused turns it on
+  int coop = 0;
+  (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, m->device);
+  m->fused_ok = false;
+  if (const char* ev = std::getenv("SPADE_FUSED"))
+    if (std::atoi(ev) != 0 && coop != 0) m->fused_ok = true;
   const WsPlan p = plan_ws(m->dims, max_batch, max_gamma, max_len);
   Workspace& w = m->ws;
   uint8_t* b = m->work;
@@ -194,6 +211,9 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.stats = (float*)(b + p.stats);
   w.rope = (float*)(b + p.rope);
   w.err = (uint32_t*)(b + p.err);
+  w.bar = (uint32_t*)(b + p.bar);
+  w.fused = p.has_fused ? b + p.fused : nullptr;
+  w.fa = p.fa;
   w.act_split = p.act_split;
   w.actf_split = p.actf_split;
   w.Mmax = p.Mmax;
@@ -213,6 +233,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   hipError_t e = hipMemcpy(w.rope, rope.data(), rope.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemset(w.attn_cnt, 0, (size_t)max_batch * m->dims.H * 4);
   if (e == hipSuccess) e = hipMemset(w.err, 0, 4);
+  if (e == hipSuccess) e = hipMemset(w.bar, 0, kBarBytes);
   // activation buffers start at zero so rows past M never feed NaNs
   if (e == hipSuccess) e = hipMemset(b, 0, p.ssq);
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -373,25 +394,41 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
   fc.mode = d_mode;
   fc.inv_T = 1.0f / temperature;
   fc.have_q = d_uniforms != nullptr && (d_draft_probs != nullptr || gamma == 0);
-  hipError_t e = launch_forward(m, kv, fc, st);
-  if (e == hipSuccess) {
-    AcceptCall ac{};
-    ac.B = B;
-    ac.gamma = gamma;
-    ac.V = m->dims.V;
-    ac.logits = fc.logits_out;
-    ac.stats = m->ws.stats;
-    ac.NU = m->dims.Vpad / 16;
-    ac.drafts = d_draft_tokens;
-    ac.q = d_draft_probs;
-    ac.u = d_uniforms;
-    ac.mode = d_mode;
-    ac.inv_T = fc.inv_T;
-    ac.n_out = d_n_accepted;
-    ac.corr_out = d_correction;
-    e = launch_accept(m, ac, st);
+  AcceptCall ac{};
+  ac.B = B;
+  ac.gamma = gamma;
+  ac.V = m->dims.V;
+  ac.logits = fc.logits_out;
+  ac.stats = m->ws.stats;
+  ac.NU = m->dims.Vpad / 16;
+  ac.drafts = d_draft_tokens;
+  ac.q = d_draft_probs;
+  ac.u = d_uniforms;
+  ac.mode = d_mode;
+  ac.inv_T = fc.inv_T;
+  ac.n_out = d_n_accepted;
+  ac.corr_out = d_correction;
+  hipError_t e;
+  if (fused_eligible(m, kv, fc)) {
+    e = launch_verify_fused(m, kv, fc, ac, st);
+  } else {
+    e = launch_forward(m, kv, fc, st);
+    if (e == hipSuccess) e = launch_accept(m, ac, st);
   }
   if (e != hipSuccess) return hipfail(e, "verify");
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_fused(spade_model m, int enable) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (!enable) {
+    m->fused_ok = false;
+    return SPADE_OK;
+  }
+  int coop = 0;
+  if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, m->device) != hipSuccess || !coop)
+    return fail(SPADE_EUNSUPPORTED, "device has no cooperative launch");
+  m->fused_ok = true;
   return SPADE_OK;
 }
 

@@ -1,0 +1,206 @@
+// Accept / reject and the correction draw for one request (Sec. III-C;
+// Algorithm 1, the verify / accept / sample / correct steps), run by one
+// workgroup of NT threads.  Shared by the stand-alone accept kernel and the
+// persistent verify kernel (COH: logits and LM-head statistics were written
+// by other workgroups of the same launch and are read with sc1 loads).
+#pragma once
+
+#include "device_util.h"
+
+namespace spade {
+
+struct AcceptParams {
+  const float* logits;
+  const float* stats;
+  int NU;
+  int V, gamma, R;
+  const int32_t* drafts;
+  const float* q;
+  const float* u;
+  const uint8_t* mode;
+  float inv_T;
+  int32_t* n_out;
+  int32_t* corr_out;
+  uint32_t* err;
+};
+
+// SplitMix64 output v (0-based) of the stream seeded with `seed`.
+__device__ __forceinline__ uint64_t splitmix64_at(uint64_t seed, uint64_t v) {
+  uint64_t z = seed + (v + 1ull) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ float gumbel_at(uint64_t seed, int v) {
+  const uint64_t x = splitmix64_at(seed, (uint64_t)v);
+  const float U = ((float)(uint32_t)(x >> 41) + 0.5f) * 0x1p-23f;
+  return -logf(-logf(U));
+}
+
+// (max, sum exp(z - max), argmax); ties keep the lower id.
+struct RowStat {
+  float m, s;
+  int a;
+};
+
+__device__ __forceinline__ RowStat merge_stat(RowStat x, RowStat y) {
+  if (y.m > x.m || (y.m == x.m && y.a < x.a)) {
+    const RowStat t = x;
+    x = y;
+    y = t;
+  }
+  RowStat o;
+  o.m = x.m;
+  o.a = x.a;
+  o.s = x.s + ((y.m == -INFINITY) ? 0.f : y.s * expf(y.m - x.m));
+  return o;
+}
+
+struct Best {
+  float s;
+  int a;
+};
+
+__device__ __forceinline__ Best better(Best x, Best y) {
+  if (y.s > x.s || (y.s == x.s && y.a < x.a)) return y;
+  return x;
+}
+
+template <bool COH>
+__device__ __forceinline__ float ld_any(const float* p) {
+  if constexpr (COH) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else return *p;
+}
+
+struct AcceptSmem {
+  float rlse[kMaxR];
+  int rarg[kMaxR];
+  Best bpart[16];
+  int n_s;
+};
+
+template <int NT, bool COH>
+__device__ __forceinline__ void accept_request(const AcceptParams& p, int b, AcceptSmem& sm) {
+  constexpr int NWV = NT / 64;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int R = p.R, V = p.V, G = p.gamma;
+
+  bool sample = p.mode[b] == SPADE_SAMPLE;
+  if (sample && (p.u == nullptr || (G > 0 && p.q == nullptr))) {
+    if (tid == 0) flag_error(p.err, SPADE_DERR_NOQ);
+    sample = false;
+  }
+  const float invT = sample ? p.inv_T : 1.0f;
+  const float* lg = p.logits + (size_t)b * R * V;
+
+  // row statistics over the vocabulary: wave r merges row r from the LM
+  // head's per-panel partials (or, without them, from the logits), in a fixed
+  // order
+  for (int r = wave; r < R; r += NWV) {
+    RowStat st{-INFINITY, 0.f, 0x7fffffff};
+    if (p.stats != nullptr) {
+      const float* sp = p.stats + (size_t)(b * R + r) * p.NU * 3;
+#pragma unroll 8
+      for (int q = lane; q < p.NU; q += 64) {
+        const RowStat one{ld_any<COH>(sp + q * 3), ld_any<COH>(sp + q * 3 + 1),
+                          __float_as_int(ld_any<COH>(sp + q * 3 + 2))};
+        if (one.m != -INFINITY) st = merge_stat(st, one);
+      }
+    } else {
+#pragma unroll 8
+      for (int v = lane; v < V; v += 64) {
+        const float z = ld_any<COH>(lg + (size_t)r * V + v) * invT;
+        if (z != z) continue;
+        st = merge_stat(st, RowStat{z, 1.f, v});
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      RowStat o;
+      o.m = __shfl_xor(st.m, off);
+      o.s = __shfl_xor(st.s, off);
+      o.a = __shfl_xor(st.a, off);
+      st = (lane & off) ? merge_stat(o, st) : merge_stat(st, o);
+    }
+    if (lane == 0) {
+      sm.rlse[r] = st.m + logf(st.s);
+      sm.rarg[r] = st.a;
+    }
+  }
+  __syncthreads();
+
+  if (tid == 0) {
+    int n = G;
+    for (int i = 0; i < G; ++i) {
+      int x = p.drafts[(size_t)b * G + i];
+      if (x < 0 || x >= V) {
+        flag_error(p.err, SPADE_DERR_TOKEN);
+        x = x < 0 ? 0 : V - 1;
+      }
+      bool ok;
+      if (!sample) {
+        ok = (x == sm.rarg[i]);
+      } else {
+        const float px = expf(ld_any<COH>(lg + (size_t)i * V + x) * invT - sm.rlse[i]);
+        const float qx = p.q[((size_t)b * G + i) * V + x];
+        ok = p.u[(size_t)b * (G + 1) + i] * qx < px;
+      }
+      if (!ok) {
+        n = i;
+        break;
+      }
+    }
+    sm.n_s = n;
+  }
+  __syncthreads();
+  const int n = sm.n_s;
+  int corr = 0;
+  if (!sample) {
+    corr = sm.rarg[n];
+  } else {
+    const uint64_t seed = (uint64_t)__float_as_uint(p.u[(size_t)b * (G + 1) + G]);
+    const float* row = lg + (size_t)n * V;
+    const bool residual = n < G;
+    const float* qrow = residual ? p.q + ((size_t)b * G + n) * V : nullptr;
+    const float lse = sm.rlse[n];
+    for (int pass = 0; pass < 2; ++pass) {
+      const bool use_res = residual && pass == 0;
+      Best bst{-INFINITY, 0x7fffffff};
+#pragma unroll 4
+      for (int v = tid; v < V; v += NT) {
+        const float z = ld_any<COH>(row + v) * invT;
+        float sc;
+        if (use_res) {
+          const float w = expf(z - lse) - qrow[v];
+          sc = w > 0.f ? logf(w) + gumbel_at(seed, v) : -INFINITY;
+        } else {
+          sc = z + gumbel_at(seed, v);
+        }
+        if (sc != sc) continue;
+        bst = better(bst, Best{sc, v});
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const Best o{__shfl_xor(bst.s, off), __shfl_xor(bst.a, off)};
+        bst = better(bst, o);
+      }
+      if (lane == 0) sm.bpart[wave] = bst;
+      __syncthreads();
+      Best t = sm.bpart[0];
+      for (int w = 1; w < NWV; ++w) t = better(t, sm.bpart[w]);
+      __syncthreads();
+      if (t.s != -INFINITY || !use_res) {
+        corr = t.a;
+        break;
+      }
+      if (tid == 0) flag_error(p.err, SPADE_DERR_RESIDUAL);
+    }
+  }
+  if (tid == 0) {
+    p.n_out[b] = n;
+    p.corr_out[b] = corr;
+  }
+}
+
+}  // namespace spade

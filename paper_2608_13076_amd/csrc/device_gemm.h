@@ -1,0 +1,484 @@
+// Skinny GEMM engine with fused epilogues, shared by the per-stage kernels
+// and the persistent verify kernel.
+//
+// The arena stores a weight matrix as panels of 16 rows, each panel as its
+// k-blocks (256 k for bf16, 128 for f32) of 8 KB.  Slice j of a k-block holds
+// for lane l the 8 bf16 (4 f32) weights of panel row l%16 at
+// k = kb*256 + 32j + 8(l/16) (f32: kb*128 + 16j + 4(l/16)) -- the B operand of
+// MFMA j -- so each wave load instruction reads 1 KB contiguous.
+//
+// A workgroup of 8 waves takes panels ("units") u = bid, bid + G, ...; each
+// wave owns a contiguous k-block range of every unit and walks a stream of
+// (unit, k-block) items through a three-deep register pipeline: the weight
+// tile of item t+3 is requested while the MFMAs consume item t.  After the
+// last item of a unit the wave partials are summed in LDS (in wave order) and
+// the unit's epilogue runs.  Activation operands (<= 32 rows) are either
+// copied once per launch into LDS (rows <= 16 whose split operand fits: every
+// item reads its fragment from there) or fetched from L2 with every item, one
+// item ahead.
+//
+// Every memory access inside the item loop is an unconditional raw-buffer
+// instruction whose range check masks absent rows and items (offsets past the
+// resource read 0, stores are dropped), and the epilogue's inputs are fetched
+// two items ahead.  With no load under a branch the compiler's wait counts
+// stay exact, so a wait for item t leaves items t+1 and t+2 in flight.
+#pragma once
+
+#include "device_util.h"
+
+namespace spade {
+
+struct GemmParams {
+  const uint8_t* w;
+  int NKB, n_units;
+  int M, m0;
+  const void* act;
+  size_t act_split;
+  int act_stride;
+  // row scale 1/rms from partials (ssq_in == NULL: scale 1)
+  const float* ssq_in;
+  int n_ssq;
+  float inv_din, eps;
+  int R, b0;
+  const int32_t* lens;
+  // QKV
+  float* q_out;
+  void* kc;
+  void* vc;
+  uint32_t kv_bytes;  // bytes of one layer's K (or V) cache
+  int H, hd, d, kv_stride, kv_bf16;
+  const float* rope;
+  // O / DOWN
+  float* x;
+  void* act_out;
+  size_t act_out_split;
+  int act_out_stride;
+  const float* g_next;
+  float* ssq_out;
+  int n_ssq_out;
+  // GU
+  int F;
+  // LM
+  float* logits;
+  int V;
+  float* stats;
+  int NU;
+  const uint8_t* mode;
+  float inv_T;
+  int have_q;
+  uint32_t* err;
+};
+
+constexpr int kGemmWaves = 8;
+
+template <int MT>
+struct GemmSmem {
+  float red[kGemmWaves][MT][4][64];
+  float rinv[MT * 16];
+};
+
+// LDS copy of the activation operand: per split, rows 0..M-1 and a zero row
+// at index M, each K elements plus 16 bytes of padding (rows start 4 banks
+// apart, so the 16 rows of a fragment read hit distinct banks).
+inline __host__ __device__ uint32_t gemm_lds_row_bytes(int K, int wbf16) { return (uint32_t)K * (wbf16 ? 2u : 4u) + 16u; }
+inline __host__ __device__ uint32_t gemm_lds_a_bytes(int M, int K, int wbf16) {
+  return (uint32_t)(wbf16 ? kActSplits : 1) * (uint32_t)(M + 1) * gemm_lds_row_bytes(K, wbf16);
+}
+// the LDS copy moves whole 1 KB blocks of a row
+inline __host__ __device__ bool gemm_lds_a_ok(int K, int wbf16) { return ((K * (wbf16 ? 2 : 4)) & 1023) == 0; }
+constexpr uint32_t kGemmLdsABytes = 144 * 1024;  // largest LDS operand copy
+
+struct EpiIn {
+  float a, b;
+};
+
+// WBF16: bf16 weights (else f32); MT: 16-row tiles of activations (1 or 2);
+// ALDS: activation operand copied to LDS once (MT == 1); COH: every output is
+// a write-through (sc1) store and the residual stream is read with sc1 loads.
+// Operands and row partials are read with plain loads: within one launch the
+// caller gives every producer its own output region, so no L2 holds a stale
+// line of them.
+template <bool WBF16, int MT, bool ALDS, int KIND, bool COH>
+struct Gemm {
+  static constexpr int NW = kGemmWaves;
+  static constexpr int S = WBF16 ? kActSplits : 1;
+  static constexpr uint32_t ELT = WBF16 ? 2u : 4u;
+
+  const GemmParams& a;
+  GemmSmem<MT>& sm;
+  uint8_t* lds_a;  // ALDS: operand copy (gemm_lds_a_bytes)
+  int bid, G, tid, lane, wave;
+  int NKB, nkw, kbl, cnt, T;
+  // epilogue geometry of this thread: output row ml of the launch, column n of
+  // the panel; tok: the thread holds a real output (tid < MT * 256)
+  int ml, n, emtc, er;
+  bool tok, rok;
+  int pos, bg;  // QKV: position and request of row ml
+  bool samp;    // LM: row ml uses 1/T statistics
+  bool nan_seen;
+  Rsrc ra[S];
+  uint4 w0[8], w1[8], w2[8];
+  uint4 av[MT][S][8];
+  EpiIn e0, e1, e2;
+  floatx4 acc[MT];
+
+  __device__ __forceinline__ Gemm(const GemmParams& a_, GemmSmem<MT>& sm_, uint8_t* lds_a_, int bid_, int G_)
+      : a(a_), sm(sm_), lds_a(lds_a_), bid(bid_), G(G_) {
+    tid = threadIdx.x;
+    lane = tid & 63;
+    wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    NKB = a.NKB;
+    nkw = (NKB + NW - 1) / NW;
+    kbl = (NKB * wave) / NW;
+    cnt = (NKB * (wave + 1)) / NW - kbl;
+    const int my_units = (a.n_units - bid + G - 1) / G;
+    T = my_units * nkw;
+    const int emt = tid >> 8;
+    tok = emt < MT;
+    emtc = tok ? emt : MT - 1;
+    er = (tid >> 6) & 3;
+    ml = emtc * 16 + 4 * (lane >> 4) + er;
+    n = lane & 15;
+    rok = tok && ml < a.M;
+    nan_seen = false;
+    pos = 0;
+    bg = 0;
+    samp = false;
+    if constexpr (KIND == GEMM_QKV || KIND == GEMM_LM) {
+      const int m = a.m0 + ml;
+      const int bl = m / a.R, i = m - bl * a.R;
+      bg = a.b0 + bl;
+      if constexpr (KIND == GEMM_QKV) {
+        if (rok) pos = a.lens[bg] + i;
+      } else {
+        if (rok && a.mode != nullptr) samp = a.mode[bl] == SPADE_SAMPLE && a.have_q;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+      ra[s] = make_rsrc((const uint8_t*)a.act + ((size_t)s * a.act_split + (size_t)a.m0 * a.act_stride) * ELT,
+                        (uint32_t)((size_t)a.M * a.act_stride * ELT));
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // weight tile of item t (zeros past the stream or the wave's k-range)
+  __device__ __forceinline__ void issue_w(int t, uint4 (&w)[8]) const {
+    const int i = t / nkw, k = t - i * nkw;
+    const bool ok = t < T && k < cnt;
+    const int u = ok ? bid + i * G : 0;
+    const uint8_t* tile = a.w + ((size_t)u * NKB + kbl + (ok ? k : 0)) * kTileBytes;
+    const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = ld_b128<false>(r, (uint32_t)(lane * 16 + j * 1024));
+  }
+
+  // activation operand of k-block kbl + k (k >= cnt: zeros)
+  __device__ __forceinline__ void issue_a_k(int k, uint4 (&dst)[MT][S][8]) const {
+    const bool ok = k < cnt;
+    const int kb = kbl + k;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int row = mt * 16 + (lane & 15);
+      uint32_t off;
+      if constexpr (WBF16) off = (uint32_t)(row * a.act_stride + kb * 256 + (lane >> 4) * 8) * 2u;
+      else off = (uint32_t)(row * a.act_stride + kb * 128 + (lane >> 4) * 4) * 4u;
+      off = ok ? off : kOob;
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dst[mt][s][j] = ld_b128<false>(ra[s], off + (uint32_t)j * (WBF16 ? 64u : 64u));
+    }
+  }
+
+  // activation operand of item t (streamed operand)
+  __device__ __forceinline__ void issue_a_t(int t, uint4 (&dst)[MT][S][8]) const {
+    const int i = t / nkw, k = t - i * nkw;
+    issue_a_k(t < T ? k : cnt, dst);
+  }
+
+  // ALDS: copy rows [0, M) of every split into LDS with direct buffer->LDS
+  // loads (no registers: each wave instruction moves 64 consecutive 16-byte
+  // chunks of one row; rows are a multiple of 1 KB, gemm_lds_a_ok) and write
+  // the zero rows with LDS stores.
+  __device__ __forceinline__ void fill_lds_a() {
+    const uint32_t rowb = gemm_lds_row_bytes(a.act_stride, WBF16);
+    const int row_bytes = a.act_stride * (int)ELT;
+    const int per_row = row_bytes >> 10;  // wave instructions per row
+    const int per_split = a.M * per_row;
+    for (int i = wave; i < S * per_split; i += NW) {
+      const int s = i / per_split, rem = i - s * per_split;
+      const int row = rem / per_row, blk = rem - row * per_row;
+      const Rsrc rs = (S == 1 || s == 0) ? ra[0] : ra[S - 1];  // no dynamic index into ra
+      __attribute__((address_space(3))) void* dst =
+          (__attribute__((address_space(3))) void*)(lds_a + (uint32_t)(s * (a.M + 1) + row) * rowb + (uint32_t)blk * 1024u);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 16, (uint32_t)(row * row_bytes + blk * 1024 + lane * 16), 0, 0, 0);
+    }
+    const int cpr = row_bytes >> 4;
+    for (int c = tid; c < S * cpr; c += NW * 64) {
+      const int s = c / cpr, cc = c - s * cpr;
+      *(uint4*)(lds_a + (uint32_t)(s * (a.M + 1) + a.M) * rowb + (uint32_t)cc * 16u) = make_uint4(0, 0, 0, 0);
+    }
+  }
+
+  // ALDS: fragment of k-block kbl + k for this lane (k >= cnt reads block kbl:
+  // finite values that meet a zero weight tile)
+  __device__ __forceinline__ void read_a_lds(int k) {
+    const uint32_t rowb = gemm_lds_row_bytes(a.act_stride, WBF16);
+    const int r = lane & 15;
+    const int rr = r < a.M ? r : a.M;
+    const int kb = kbl + (k < cnt ? k : 0);
+    uint32_t off;
+    if constexpr (WBF16) off = (uint32_t)rr * rowb + (uint32_t)(kb * 256 + (lane >> 4) * 8) * 2u;
+    else off = (uint32_t)rr * rowb + (uint32_t)(kb * 128 + (lane >> 4) * 4) * 4u;
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        av[0][s][j] = *(const uint4*)(lds_a + (uint32_t)(s * (a.M + 1)) * rowb + off + (uint32_t)j * 64u);
+  }
+
+  // epilogue inputs of the unit of item t
+  __device__ __forceinline__ EpiIn epi_load(int t) const {
+    EpiIn e{0.f, 0.f};
+    const int u = bid + (t / nkw) * G;
+    const bool ok = rok && t < T;
+    if constexpr (KIND == GEMM_QKV) {
+      const int pps = a.d >> 4, pph = a.hd >> 4;
+      const int pw = u % pps;
+      const int pair = (pw % pph) * 8 + (n & 7);
+      const Rsrc rr = make_rsrc(a.rope, 0x7ffffff0u);
+      const float2 cs = ld_f32x2<false>(rr, ok ? (uint32_t)((pos * (a.hd >> 1) + pair) * 2) * 4u : kOob);
+      e.a = cs.x;
+      e.b = cs.y;
+    } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
+      const int col = u * 16 + n;
+      const Rsrc rx = make_rsrc(a.x + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
+      const Rsrc rg = make_rsrc(a.g_next, (uint32_t)(a.d * 4));
+      e.a = ld_f32<COH>(rx, ok ? (uint32_t)(ml * a.d + col) * 4u : kOob);
+      e.b = ld_f32<false>(rg, ok ? (uint32_t)col * 4u : kOob);
+    }
+    return e;
+  }
+
+  __device__ __forceinline__ void mma(const uint4 (&w)[8], const uint4 (&x)[MT][S][8]) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        if constexpr (WBF16) {
+#pragma unroll
+          for (int s = S - 1; s >= 0; --s)
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, x[mt][s][j]),
+                                                              __builtin_bit_cast(bf16x8, w[j]), acc[mt], 0, 0, 0);
+        } else {
+          const float4 w4 = __builtin_bit_cast(float4, w[j]);
+          const float4 a4 = __builtin_bit_cast(float4, x[mt][0][j]);
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.x, w4.x, acc[mt], 0, 0, 0);
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.y, w4.y, acc[mt], 0, 0, 0);
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.z, w4.z, acc[mt], 0, 0, 0);
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.w, w4.w, acc[mt], 0, 0, 0);
+        }
+      }
+  }
+
+  // Epilogue of unit u for this thread's output (row ml, column n): val is
+  // the full dot product.  D[i][j] of a 16x16 MFMA sits in lane j + 16*(i/4),
+  // register i%4.
+  __device__ __forceinline__ void epilogue(int u, float val, const EpiIn& e) {
+    const float rinv = sm.rinv[ml];
+    if constexpr (KIND == GEMM_QKV) {
+      const int pps = a.d >> 4, pph = a.hd >> 4;
+      const int sec = u / pps, pw = u - sec * pps;
+      const int h = pw / pph, wg = pw - h * pph;
+      const int pair = wg * 8 + (n & 7);
+      const bool hi = n >= 8;
+      const int f = pair + (hi ? (a.hd >> 1) : 0);
+      float v = val * rinv;
+      const float pv = __shfl_xor(v, 8);  // the RoPE partner
+      const bool rot = sec < 2;
+      const float c = rot ? e.a : 1.f, sn = rot ? e.b : 0.f;
+      v = hi ? (pv * sn + v * c) : (v * c - pv * sn);
+      const Rsrc rq = make_rsrc(a.q_out + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
+      st_f32<COH>(rq, (rok && sec == 0) ? (uint32_t)(ml * a.d + h * a.hd + f) * 4u : kOob, v);
+      // K rows [pos][hd]; V transposed, rows [feature][stride]
+      const uint32_t head = (uint32_t)(bg * a.H + h) * (uint32_t)a.kv_stride * (uint32_t)a.hd;
+      const uint32_t elem = sec == 1 ? head + (uint32_t)(pos * a.hd + f) : head + (uint32_t)(f * a.kv_stride + pos);
+      const Rsrc rkv = make_rsrc(sec == 1 ? a.kc : a.vc, a.kv_bytes);
+      const bool kok = rok && sec > 0;
+      if (a.kv_bf16) st_b16<COH>(rkv, kok ? elem * 2u : kOob, f2bf(v));
+      else st_f32<COH>(rkv, kok ? elem * 4u : kOob, v);
+    } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
+      const int col = u * 16 + n;
+      const float xv = e.a + val;
+      const Rsrc rx = make_rsrc(a.x + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
+      st_f32<COH>(rx, rok ? (uint32_t)(ml * a.d + col) * 4u : kOob, xv);
+      const uint32_t split_b = (uint32_t)(a.act_out_split * ELT);
+      const Rsrc ro = make_rsrc((const uint8_t*)a.act_out + (size_t)a.m0 * a.act_out_stride * ELT,
+                                (uint32_t)((S - 1) * (size_t)split_b + (size_t)a.M * a.act_out_stride * ELT));
+      st_act<WBF16, COH>(ro, split_b, (uint32_t)(ml * a.act_out_stride + col), rok, xv * e.b);
+      float sq = rok ? xv * xv : 0.f;
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off);
+      const Rsrc rs = make_rsrc(a.ssq_out + (size_t)a.m0 * a.n_ssq_out, (uint32_t)((size_t)a.M * a.n_ssq_out * 4));
+      st_f32<COH>(rs, (rok && n == 0) ? (uint32_t)(ml * a.n_ssq_out + u) * 4u : kOob, sq);
+    } else if constexpr (KIND == GEMM_GU) {
+      const float v = val * rinv;
+      const float up = __shfl_xor(v, 8);
+      const float act = v / (1.0f + expf(-v)) * up;
+      const uint32_t split_b = (uint32_t)(a.act_out_split * ELT);
+      const Rsrc ro = make_rsrc((const uint8_t*)a.act_out + (size_t)a.m0 * a.act_out_stride * ELT,
+                                (uint32_t)((S - 1) * (size_t)split_b + (size_t)a.M * a.act_out_stride * ELT));
+      st_act<WBF16, COH>(ro, split_b, (uint32_t)(ml * a.act_out_stride + u * 8 + n), rok && n < 8, act);
+    } else {  // GEMM_LM: logits and the panel's (max, sum exp, argmax) of z = logit / T
+      const int col = u * 16 + n;
+      const bool valid = rok && col < a.V;
+      const float lg = val * rinv;
+      const Rsrc rl = make_rsrc(a.logits + (size_t)a.m0 * a.V, (uint32_t)((size_t)a.M * a.V * 4));
+      st_f32<COH>(rl, valid ? (uint32_t)(ml * a.V + col) * 4u : kOob, lg);
+      const bool isnan = lg != lg;
+      nan_seen = nan_seen || (valid && isnan);
+      const bool use = valid && !isnan;
+      const float z = use ? (samp ? lg * a.inv_T : lg) : -INFINITY;
+      const int id = use ? col : 0x7fffffff;
+      float zm = z;
+      int am = id;
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) {
+        const float oz = __shfl_xor(zm, off);
+        const int oa = __shfl_xor(am, off);
+        const bool take = oz > zm || (oz == zm && oa < am);
+        zm = take ? oz : zm;
+        am = take ? oa : am;
+      }
+      float ex = (z == -INFINITY) ? 0.f : expf(z - zm);
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) ex += __shfl_xor(ex, off);
+      const Rsrc rst = make_rsrc(a.stats + (size_t)a.m0 * a.NU * 3, (uint32_t)((size_t)a.M * a.NU * 12));
+      const uint32_t so = (rok && n == 0) ? (uint32_t)((ml * a.NU + u) * 3) * 4u : kOob;
+      st_f32<COH>(rst, so, zm);
+      st_f32<COH>(rst, so == kOob ? kOob : so + 4u, ex);
+      st_f32<COH>(rst, so == kOob ? kOob : so + 8u, __int_as_float(am));
+    }
+  }
+
+  __device__ __forceinline__ void unit_end(int t, const EpiIn& e) {
+    const int u = bid + (t / nkw) * G;
+    const bool keep = rok;
+    rok = rok && t < T;  // padding units store nothing
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm.red[wave][mt][r][lane] = acc[mt][r];
+    __syncthreads();
+    float val = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) val += sm.red[w][emtc][er][lane];
+    epilogue(u, val, e);
+    rok = keep;
+    __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // 1/rms of every row from the producer's per-16-column sums of squares:
+  // thread (row, sub) sums partials sub, sub + 16, ... in that order, then the
+  // sixteen subs combine in a butterfly.  The first sixteen partials of each
+  // thread are requested with the other prologue loads (ssq_issue).
+  __device__ __forceinline__ Rsrc ssq_rsrc() const {
+    return make_rsrc(a.ssq_in + (size_t)a.m0 * a.n_ssq, (uint32_t)((size_t)a.M * a.n_ssq * 4));
+  }
+
+  __device__ __forceinline__ void ssq_issue(float (&v)[16]) const {
+    const int row = tid >> 4, sub = tid & 15;
+    const Rsrc rs = ssq_rsrc();
+    const uint32_t base = (uint32_t)(row * a.n_ssq) * 4u;
+#pragma unroll
+    for (int f = 0; f < 16; ++f) {
+      const int q = sub + f * 16;
+      v[f] = ld_f32<false>(rs, (a.ssq_in != nullptr && q < a.n_ssq) ? base + (uint32_t)q * 4u : kOob);
+    }
+  }
+
+  __device__ __forceinline__ void row_scales(const float (&v0)[16]) {
+    const int row = tid >> 4, sub = tid & 15;
+    float s = 0.f;
+#pragma unroll
+    for (int f = 0; f < 16; ++f) s += v0[f];
+    if (a.ssq_in != nullptr) {
+      const Rsrc rs = ssq_rsrc();
+      const uint32_t base = (uint32_t)(row * a.n_ssq) * 4u;
+      for (int q0 = sub + 256; q0 < a.n_ssq; q0 += 256) {
+        float v[16];
+#pragma unroll
+        for (int f = 0; f < 16; ++f) {
+          const int q = q0 + f * 16;
+          v[f] = ld_f32<false>(rs, q < a.n_ssq ? base + (uint32_t)q * 4u : kOob);
+        }
+#pragma unroll
+        for (int f = 0; f < 16; ++f) s += v[f];
+      }
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    if (sub == 0 && row < MT * 16)
+      sm.rinv[row] = (a.ssq_in != nullptr && row < a.M) ? 1.0f / sqrtf(s * a.inv_din + a.eps) : 1.0f;
+  }
+
+  // The first three weight tiles: needs nothing the previous stage produces.
+  __device__ __forceinline__ void prefetch() {
+    issue_w(0, w0);
+    issue_w(1, w1);
+    issue_w(2, w2);
+  }
+
+  template <int P>
+  __device__ __forceinline__ void step(int t) {
+    if constexpr (P == 0) step_impl(t, w0, e0, e2);
+    else if constexpr (P == 1) step_impl(t, w1, e1, e0);
+    else step_impl(t, w2, e2, e1);
+  }
+
+  // item t: consume tile w, refill it with item t + 3, fetch the epilogue
+  // inputs of item t + 2 into enew, finish the unit with ecur
+  __device__ __forceinline__ void step_impl(int t, uint4 (&w)[8], EpiIn& ecur, EpiIn& enew) {
+    const int k = t - (t / nkw) * nkw;
+    if constexpr (ALDS) read_a_lds(k);
+    mma(w, av);
+    // the refills below reuse the registers just consumed: keep them after
+    // the MFMAs so no fourth tile is ever live
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (!ALDS) issue_a_t(t + 1, av);
+    issue_w(t + 3, w);
+    enew = epi_load(t + 2);
+    if (k == nkw - 1) unit_end(t, ecur);
+  }
+
+  // Everything after prefetch(): operands, row scales, the item loop.
+  __device__ __forceinline__ void run() {
+    // prologue: operand copy, epilogue inputs and row partials in one round trip
+    if constexpr (ALDS) fill_lds_a();
+    else issue_a_t(0, av);
+    e0 = epi_load(0);
+    e1 = epi_load(1);
+    float sv[16];
+    ssq_issue(sv);
+    row_scales(sv);
+    // the first item needs all of the above; starting the loop with nothing in
+    // flight lets the loop head take its wait counts from the loop body
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    // the item count is padded to a multiple of 3 (padding items load zeros
+    // and store nothing): a loop body without exits keeps the wait counts
+    // at the loop head exact
+    const int Tpad = (T + 2) / 3 * 3;
+    for (int t = 0; t < Tpad; t += 3) {
+      step<0>(t);
+      step<1>(t + 1);
+      step<2>(t + 2);
+    }
+    if (nan_seen) flag_error(a.err, SPADE_DERR_NAN);
+  }
+};
+
+}  // namespace spade

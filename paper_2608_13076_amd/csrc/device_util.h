@@ -1,0 +1,87 @@
+// Device helpers shared by the HIP kernels: bf16 conversion, MFMA operand
+// types, raw buffer resources and cache-policy-tagged loads and stores.
+#pragma once
+
+#include "spade_internal.h"
+
+#include <math.h>
+
+namespace spade {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float floatx4;
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+
+// sc1 cache policy: a load that sees every device-scope store completed
+// before it (it does not hit stale lines of another XCD's L2) and a store that
+// writes through to the device coherence point.  Data that one workgroup of a
+// persistent launch writes and another reads goes through these.
+constexpr int kAuxCoh = 16;
+// A byte offset past the end of every buffer resource: loads return 0, stores
+// are dropped.  Masks a lane's access without a branch.
+constexpr uint32_t kOob = 0x80000000u;
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// round to nearest even; NaN stays NaN
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Raw (unswizzled) buffer resource over [p, p + bytes); bytes < 2^31.
+__device__ __forceinline__ Rsrc make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+template <bool COH>
+__device__ __forceinline__ uint4 ld_b128(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, COH ? kAuxCoh : 0));
+}
+
+template <bool COH>
+__device__ __forceinline__ float ld_f32(Rsrc r, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, COH ? kAuxCoh : 0));
+}
+
+template <bool COH>
+__device__ __forceinline__ float2 ld_f32x2(Rsrc r, uint32_t off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, COH ? kAuxCoh : 0);
+  return make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
+}
+
+template <bool COH>
+__device__ __forceinline__ void st_f32(Rsrc r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, COH ? kAuxCoh : 0);
+}
+
+template <bool COH>
+__device__ __forceinline__ void st_b16(Rsrc r, uint32_t off, uint16_t v) {
+  __builtin_amdgcn_raw_buffer_store_b16(v, r, (int)off, 0, COH ? kAuxCoh : 0);
+}
+
+// Store v at element `elem` as a GEMM operand: kActSplits bf16 terms
+// (hi = rne(v), lo = rne(v - hi), split s at byte s * split_bytes) when the
+// weights are bf16, else the float itself.  ok == false drops the store.
+template <bool ABF16, bool COH>
+__device__ __forceinline__ void st_act(Rsrc r, uint32_t split_bytes, uint32_t elem, bool ok, float v) {
+  if constexpr (ABF16) {
+    float rem = v;
+#pragma unroll
+    for (int s = 0; s < kActSplits; ++s) {
+      const uint16_t h = f2bf(rem);
+      st_b16<COH>(r, ok ? s * split_bytes + elem * 2u : kOob, h);
+      rem -= bf2f(h);
+    }
+  } else {
+    st_f32<COH>(r, ok ? elem * 4u : kOob, v);
+  }
+}
+
+__device__ __forceinline__ void flag_error(uint32_t* err, uint32_t bits) {
+  if (err) atomicOr(err, bits);
+}
+
+}  // namespace spade

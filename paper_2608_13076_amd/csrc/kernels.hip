@@ -23,7 +23,9 @@
 //                  per row, the accept chain, the Gumbel-max correction draw
 //   commit_kernel  lens += n + 1, pending = correction
 //   pack_kernel    row-major weights -> tiled arena
-#include "spade_internal.h"
+#include "device_accept.h"
+#include "device_attn.h"
+#include "device_gemm.h"
 
 #include <float.h>
 #include <math.h>
@@ -31,18 +33,6 @@
 #include <algorithm>
 
 namespace spade {
-
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) float floatx4;
-
-__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
-
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
 
 // Store v as the next GEMM's operand: kActSplits bf16 terms (bf16 weights:
 // hi = rne(v), lo = rne(v - hi)) or the float itself (fp32 weights).
@@ -60,10 +50,6 @@ __device__ __forceinline__ void store_act(void* base, size_t split, size_t idx, 
   } else {
     ((float*)base)[idx] = v;
   }
-}
-
-__device__ __forceinline__ void flag_error(uint32_t* err, uint32_t bits) {
-  if (err) atomicOr(err, bits);
 }
 
 // ---------------------------------------------------------------------------
@@ -95,399 +81,37 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedParams p) {
     if (threadIdx.x == 0) flag_error(p.err, SPADE_DERR_TOKEN);
     t = t < 0 ? 0 : p.V - 1;
   }
+  // one column per thread; the sixteen lanes of a panel sum x^2 in a fixed
+  // butterfly order (the same order as the single-launch pass)
   const int npan = p.d / 16;
-  for (int pn = threadIdx.x; pn < npan; pn += blockDim.x) {
-    float ss = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int n = pn * 16 + e;
-      float v;
+  for (int n0 = 0; n0 < p.d; n0 += blockDim.x) {
+    const int n = n0 + (int)threadIdx.x;
+    const bool ok = n < p.d;
+    float v = 0.f;
+    if (ok) {
       if constexpr (WBF16) v = bf2f(((const uint16_t*)p.E)[(size_t)t * p.d + n]);
       else v = ((const float*)p.E)[(size_t)t * p.d + n];
       p.x[(size_t)m * p.d + n] = v;
-      ss += v * v;
       store_act<WBF16>(p.act, p.act_split, (size_t)m * p.d + n, v * p.g[n]);
     }
-    p.ssq[(size_t)m * npan + pn] = ss;
+    float ss = v * v;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    if (ok && (n & 15) == 0) p.ssq[(size_t)m * npan + (n >> 4)] = ss;
   }
 }
 
 // ---------------------------------------------------------------------------
-// Skinny GEMM with fused epilogues.
-//
-// The arena stores a weight matrix as panels of 16 rows, each panel as its
-// k-blocks (256 k for bf16, 128 for f32) of 8 KB.  Slice j of a k-block holds
-// for lane l the 8 bf16 (4 f32) weights of panel row l%16 at
-// k = kb*256 + 32j + 8(l/16) (f32: kb*128 + 16j + 4(l/16)) -- the B operand of
-// MFMA j -- so each wave load instruction reads 1 KB contiguous.
-//
-// A persistent workgroup takes panels u = blockIdx.x, + gridDim.x, ...; its
-// NW waves split K into contiguous k-block ranges and walk a stream of
-// (panel, k-block) items, loading item t+1 while the MFMAs consume item t, so
-// the weight stream keeps going across panel boundaries while the partial
-// sums of a finished panel are reduced in LDS (in wave order) and its
-// epilogue runs.  The activations (<= 32 rows, A operand) come from L2 with
-// the same k map.
+// Projection GEMMs (engine in device_gemm.h): one launch per (layer, kind,
+// block of <= 32 rows), persistent workgroups.
 // ---------------------------------------------------------------------------
-struct GemmParams {
-  const uint8_t* w;
-  int NKB, n_units;
-  int M, m0;
-  const void* act;
-  size_t act_split;
-  int act_stride;
-  // row scale 1/rms from partials (ssq_in == NULL: scale 1)
-  const float* ssq_in;
-  int n_ssq;
-  float inv_din, eps;
-  int R, b0;
-  const int32_t* lens;
-  // QKV
-  float* q_out;
-  void* kc;
-  void* vc;
-  int H, hd, d, kv_stride, kv_bf16;
-  const float* rope;
-  // O / DOWN
-  float* x;
-  void* act_out;
-  size_t act_out_split;
-  int act_out_stride;
-  const float* g_next;
-  float* ssq_out;
-  int n_ssq_out;
-  // GU
-  int F;
-  // LM
-  float* logits;
-  int V;
-  float* stats;
-  int NU;
-  const uint8_t* mode;
-  float inv_T;
-  int have_q;
-  uint32_t* err;
-};
-
-template <bool WBF16, int MT>
-struct Item {
-  static constexpr int S = WBF16 ? kActSplits : 1;
-  uint4 w[8];
-  uint4 a[MT][S][8];
-};
-
-template <bool WBF16, int MT>
-__device__ __forceinline__ void load_w(Item<WBF16, MT>& it, const uint8_t* wp) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) it.w[j] = *(const uint4*)(wp + j * 1024);
-}
-
-template <bool WBF16, int MT>
-__device__ __forceinline__ void load_a(Item<WBF16, MT>& it, const GemmParams& a, int kb, int arow, int ag) {
-  constexpr int S = Item<WBF16, MT>::S;
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int row = mt * 16 + arow;
-    const bool ok = row < a.M;
-    if constexpr (WBF16) {
-      const uint16_t* ap = (const uint16_t*)a.act + (size_t)(a.m0 + row) * a.act_stride + kb * 256 + ag * 8;
-#pragma unroll
-      for (int s = 0; s < S; ++s)
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          it.a[mt][s][j] = ok ? *(const uint4*)(ap + s * a.act_split + j * 32) : make_uint4(0, 0, 0, 0);
-    } else {
-      const float* ap = (const float*)a.act + (size_t)(a.m0 + row) * a.act_stride + kb * 128 + ag * 4;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) it.a[mt][0][j] = ok ? *(const uint4*)(ap + j * 16) : make_uint4(0, 0, 0, 0);
-    }
-  }
-}
-
-template <bool WBF16, int MT>
-__device__ __forceinline__ void mma_item(const Item<WBF16, MT>& wsrc, const Item<WBF16, MT>& asrc, floatx4* acc) {
-  constexpr int S = Item<WBF16, MT>::S;
-#pragma unroll
-  for (int j = 0; j < 8; ++j)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      if constexpr (WBF16) {
-#pragma unroll
-        for (int s = S - 1; s >= 0; --s)
-          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, asrc.a[mt][s][j]),
-                                                            __builtin_bit_cast(bf16x8, wsrc.w[j]), acc[mt], 0, 0, 0);
-      } else {
-        const float4 w4 = __builtin_bit_cast(float4, wsrc.w[j]);
-        const float4 a4 = __builtin_bit_cast(float4, asrc.a[mt][0][j]);
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.x, w4.x, acc[mt], 0, 0, 0);
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.y, w4.y, acc[mt], 0, 0, 0);
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.z, w4.z, acc[mt], 0, 0, 0);
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.w, w4.w, acc[mt], 0, 0, 0);
-      }
-    }
-}
-
-// Epilogue of panel p for the thread's accumulator element: row ml of this
-// launch, panel row n = lane % 16 (D[i][j] of a 16x16 MFMA sits in lane
-// j + 16*(i/4), register i%4).
-template <bool WBF16, int KIND>
-__device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int p, int ml, int n, float val, float rinv) {
-  const bool rowok = ml < a.M;
-  const int m = a.m0 + ml;  // row within the forward call
-  if constexpr (KIND == GEMM_QKV) {
-    const int pps = a.d / 16, pph = a.hd / 16;
-    const int sec = p / pps, pw = p % pps;
-    const int h = pw / pph, wg = pw % pph;
-    const int pair = wg * 8 + (n & 7);
-    const bool hi = n >= 8;
-    const int f = pair + (hi ? a.hd / 2 : 0);
-    float v = val * rinv;
-    const float pv = __shfl_xor(v, 8);  // the RoPE partner
-    if (!rowok) return;
-    const int bl = m / a.R, i = m % a.R;
-    const int bg = a.b0 + bl;
-    const int pos = a.lens[bg] + i;
-    if (sec < 2) {
-      const float* cs = a.rope + ((size_t)pos * (a.hd / 2) + pair) * 2;
-      const float c = cs[0], sn = cs[1];
-      v = hi ? (pv * sn + v * c) : (v * c - pv * sn);
-    }
-    if (sec == 0) {
-      a.q_out[(size_t)m * a.d + h * a.hd + f] = v;
-    } else {
-      // K rows [pos][hd]; V transposed, rows [feature][stride]
-      const size_t head = ((size_t)bg * a.H + h) * a.kv_stride * a.hd;
-      void* cache = sec == 1 ? a.kc : a.vc;
-      const size_t off = sec == 1 ? head + (size_t)pos * a.hd + f : head + (size_t)f * a.kv_stride + pos;
-      if (a.kv_bf16) ((uint16_t*)cache)[off] = f2bf(v);
-      else ((float*)cache)[off] = v;
-    }
-  } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
-    const int col = p * 16 + n;
-    float xv = 0.f;
-    if (rowok) {
-      xv = a.x[(size_t)m * a.d + col] + val;
-      a.x[(size_t)m * a.d + col] = xv;
-      store_act<WBF16>(a.act_out, a.act_out_split, (size_t)m * a.act_out_stride + col, xv * a.g_next[col]);
-    }
-    float sq = xv * xv;
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off);
-    if (rowok && n == 0) a.ssq_out[(size_t)m * a.n_ssq_out + p] = sq;
-  } else if constexpr (KIND == GEMM_GU) {
-    const float v = val * rinv;
-    const float up = __shfl_xor(v, 8);
-    if (rowok && n < 8) {
-      const float act = v / (1.0f + expf(-v)) * up;
-      store_act<WBF16>(a.act_out, a.act_out_split, (size_t)m * a.act_out_stride + p * 8 + n, act);
-    }
-  } else {  // GEMM_LM: logits and the panel's (max, sum exp, argmax) of z = logit / T
-    const int col = p * 16 + n;
-    const bool valid = rowok && col < a.V;
-    const float lg = val * rinv;
-    bool samp = false;
-    if (rowok && a.mode != nullptr) {
-      const int bl = m / a.R;
-      samp = a.mode[bl] == SPADE_SAMPLE && a.have_q;
-    }
-    float z = -INFINITY;
-    int id = 0x7fffffff;
-    if (valid) {
-      a.logits[(size_t)m * a.V + col] = lg;
-      if (lg != lg) flag_error(a.err, SPADE_DERR_NAN);
-      else {
-        z = samp ? lg * a.inv_T : lg;
-        id = col;
-      }
-    }
-    float zm = z;
-    int am = id;
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) {
-      const float oz = __shfl_xor(zm, off);
-      const int oa = __shfl_xor(am, off);
-      if (oz > zm || (oz == zm && oa < am)) {
-        zm = oz;
-        am = oa;
-      }
-    }
-    float e = (z == -INFINITY) ? 0.f : expf(z - zm);
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) e += __shfl_xor(e, off);
-    if (rowok && n == 0) {
-      float* st = a.stats + ((size_t)m * a.NU + p) * 3;
-      st[0] = zm;
-      st[1] = e;
-      st[2] = __int_as_float(am);
-    }
-  }
-}
-
-template <bool WBF16, int NW, int MT, int KIND>
-__global__ void __launch_bounds__(NW * 64) gemm_kernel(GemmParams a) {
-  constexpr bool ADBL = (MT == 1);  // double-buffer the activations too
-  __shared__ float red[NW][MT][4][64];
-  __shared__ float rinv_s[MT * 16];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int arow = lane & 15, ag = lane >> 4;
-  const int NKB = a.NKB;
-  const int nkw = (NKB + NW - 1) / NW;  // items per panel per wave (uniform)
-  const int kbl = (NKB * wave) / NW;
-  const int cnt = (NKB * (wave + 1)) / NW - kbl;  // real items of this wave
-  const int G = gridDim.x;
-  const int my_units = (a.n_units - (int)blockIdx.x + G - 1) / G;
-  const int T = my_units * nkw;
-  const uint8_t* wl = a.w + lane * 16;
-  const size_t unit_bytes = (size_t)NKB * kTileBytes;
-
-  Item<WBF16, MT> b0, b1;
-  floatx4 acc[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  auto issue = [&](int t, Item<WBF16, MT>& buf) {
-    const int i = t % nkw;
-    if (i < cnt) {
-      const int u = (int)blockIdx.x + (t / nkw) * G;
-      load_w(buf, wl + (size_t)u * unit_bytes + (size_t)(kbl + i) * kTileBytes);
-      if constexpr (ADBL) load_a(buf, a, kbl + i, arow, ag);
-    }
-  };
-  auto unit_end = [&](int t) {
-    const int u = (int)blockIdx.x + (t / nkw) * G;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) red[wave][mt][r][lane] = acc[mt][r];
-    __syncthreads();
-    if (tid < MT * 256) {
-      const int emt = tid >> 8, er = (tid >> 6) & 3, eln = tid & 63;
-      const int ml = emt * 16 + 4 * (eln >> 4) + er;
-      float val = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) val += red[w][emt][er][eln];
-      gemm_epilogue<WBF16, KIND>(a, u, ml, eln & 15, val, rinv_s[ml]);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  };
-
-  if (T > 0) issue(0, b0);
-
-  // 1/rms of every row from the producer's per-panel sums of squares
-  {
-    const int row = tid >> 4, sub = tid & 15;
-    float s = 0.f;
-    if (a.ssq_in != nullptr && row < MT * 16 && row < a.M) {
-      const float* sp = a.ssq_in + (size_t)(a.m0 + row) * a.n_ssq;
-      for (int q = sub; q < a.n_ssq; q += 16) s += sp[q];
-    }
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-    if (sub == 0 && row < MT * 16)
-      rinv_s[row] = (a.ssq_in != nullptr && row < a.M) ? 1.0f / sqrtf(s * a.inv_din + a.eps) : 1.0f;
-  }
-
-  for (int t = 0; t < T; t += 2) {
-    if constexpr (!ADBL) {
-      if (t % nkw < cnt) load_a(b0, a, kbl + t % nkw, arow, ag);
-    }
-    if (t + 1 < T) issue(t + 1, b1);
-    if (t % nkw < cnt) mma_item(b0, b0, acc);
-    if (t % nkw == nkw - 1) unit_end(t);
-    if (t + 1 >= T) break;
-    if constexpr (!ADBL) {
-      if ((t + 1) % nkw < cnt) load_a(b0, a, kbl + (t + 1) % nkw, arow, ag);
-    }
-    if (t + 2 < T) issue(t + 2, b0);
-    if ((t + 1) % nkw < cnt) mma_item(b1, ADBL ? b1 : b0, acc);
-    if ((t + 1) % nkw == nkw - 1) unit_end(t + 1);
-  }
-}
-
-// Variant for K <= 2 * NW k-blocks and <= 16 rows: each wave keeps the
-// activations of its (at most two) k-blocks in registers for the whole
-// launch and runs a three-deep weight pipeline (two items in flight while the
-// third is consumed).
-template <bool WBF16, int NW, int KIND>
-__global__ void __launch_bounds__(NW * 64) gemm_ares_kernel(GemmParams a) {
-  __shared__ float red[NW][1][4][64];
-  __shared__ float rinv_s[16];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int arow = lane & 15, ag = lane >> 4;
-  const int NKB = a.NKB;
-  const int nkw = (NKB + NW - 1) / NW;  // 1 or 2
-  const int kbl = (NKB * wave) / NW;
-  const int cnt = (NKB * (wave + 1)) / NW - kbl;
-  const int G = gridDim.x;
-  const int my_units = (a.n_units - (int)blockIdx.x + G - 1) / G;
-  const int T = my_units * nkw;
-  const uint8_t* wl = a.w + lane * 16;
-  const size_t unit_bytes = (size_t)NKB * kTileBytes;
-
-  Item<WBF16, 1> w0, w1, w2, a0, a1;
-  floatx4 acc[1] = {floatx4{0.f, 0.f, 0.f, 0.f}};
-
-  auto issue = [&](int t, Item<WBF16, 1>& buf) {
-    const int i = t % nkw;
-    if (i < cnt) {
-      const int u = (int)blockIdx.x + (t / nkw) * G;
-      load_w(buf, wl + (size_t)u * unit_bytes + (size_t)(kbl + i) * kTileBytes);
-    }
-  };
-  auto unit_end = [&](int t) {
-    const int u = (int)blockIdx.x + (t / nkw) * G;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) red[wave][0][r][lane] = acc[0][r];
-    __syncthreads();
-    if (tid < 256) {
-      const int er = (tid >> 6) & 3, eln = tid & 63;
-      const int ml = 4 * (eln >> 4) + er;
-      float val = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) val += red[w][0][er][eln];
-      gemm_epilogue<WBF16, KIND>(a, u, ml, eln & 15, val, rinv_s[ml]);
-    }
-    __syncthreads();
-    acc[0] = floatx4{0.f, 0.f, 0.f, 0.f};
-  };
-  auto step = [&](int t, const Item<WBF16, 1>& wb) {
-    const int i = t % nkw;
-    if (i < cnt) {
-      if (i == 0) mma_item(wb, a0, acc);
-      else mma_item(wb, a1, acc);
-    }
-    if (i == nkw - 1) unit_end(t);
-  };
-
-  if (T > 0) issue(0, w0);
-  if (T > 1) issue(1, w1);
-  if (cnt > 0) load_a(a0, a, kbl, arow, ag);
-  if (cnt > 1) load_a(a1, a, kbl + 1, arow, ag);
-  {
-    const int row = tid >> 4, sub = tid & 15;
-    float s = 0.f;
-    if (a.ssq_in != nullptr && row < 16 && row < a.M) {
-      const float* sp = a.ssq_in + (size_t)(a.m0 + row) * a.n_ssq;
-      for (int q = sub; q < a.n_ssq; q += 16) s += sp[q];
-    }
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-    if (sub == 0 && row < 16)
-      rinv_s[row] = (a.ssq_in != nullptr && row < a.M) ? 1.0f / sqrtf(s * a.inv_din + a.eps) : 1.0f;
-  }
-
-  for (int t = 0; t < T; t += 3) {
-    if (t + 2 < T) issue(t + 2, w2);
-    step(t, w0);
-    if (t + 1 >= T) break;
-    if (t + 3 < T) issue(t + 3, w0);
-    step(t + 1, w1);
-    if (t + 2 >= T) break;
-    if (t + 4 < T) issue(t + 4, w1);
-    step(t + 2, w2);
-  }
+template <bool WBF16, int MT, bool ALDS, int KIND>
+__global__ void __launch_bounds__(kGemmWaves * 64) gemm_kernel(GemmParams a) {
+  __shared__ GemmSmem<MT> sm;
+  extern __shared__ uint4 lds_dyn[];
+  Gemm<WBF16, MT, ALDS, KIND, false> g(a, sm, (uint8_t*)lds_dyn, (int)blockIdx.x, (int)gridDim.x);
+  g.prefetch();
+  g.run();
 }
 
 // ---------------------------------------------------------------------------
@@ -919,194 +543,81 @@ __global__ void __launch_bounds__(256) attn_combine_kernel(AttnParams p) {
   }
 }
 
-// ---------------------------------------------------------------------------
-// Accept / reject and the correction draw, one workgroup per request
-// (Sec. III-C; Algorithm 1, the verify / accept / sample / correct steps).
-// ---------------------------------------------------------------------------
-struct AcceptParams {
-  const float* logits;
-  const float* stats;
-  int NU;
-  int V, gamma, R;
-  const int32_t* drafts;
-  const float* q;
-  const float* u;
-  const uint8_t* mode;
-  float inv_T;
-  int32_t* n_out;
-  int32_t* corr_out;
-  uint32_t* err;
-};
-
-// SplitMix64 output v (0-based) of the stream seeded with `seed`.
-__device__ __forceinline__ uint64_t splitmix64_at(uint64_t seed, uint64_t v) {
-  uint64_t z = seed + (v + 1ull) * 0x9E3779B97F4A7C15ull;
-  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-  return z ^ (z >> 31);
-}
-
-__device__ __forceinline__ float gumbel_at(uint64_t seed, int v) {
-  const uint64_t x = splitmix64_at(seed, (uint64_t)v);
-  const float U = ((float)(uint32_t)(x >> 41) + 0.5f) * 0x1p-23f;
-  return -logf(-logf(U));
-}
-
-// (max, sum exp(z - max), argmax); ties keep the lower id.
-struct RowStat {
-  float m, s;
-  int a;
-};
-
-__device__ __forceinline__ RowStat merge_stat(RowStat x, RowStat y) {
-  if (y.m > x.m || (y.m == x.m && y.a < x.a)) {
-    const RowStat t = x;
-    x = y;
-    y = t;
+// bf16 cache, head_dim 128: chunks of kAttnChunkB keys, one 8-wave workgroup
+// per (chunk, head, request) (device_attn.h), and the chunk merge.
+__global__ void __launch_bounds__(512) attn_b_kernel(AttnParams p) {
+  __shared__ AttnSmemB sm;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  AttnItemB it;
+  it.active = true;
+  it.c = blockIdx.x;
+  it.h = blockIdx.y;
+  it.bl = blockIdx.z;
+  const int bg = p.b0 + it.bl;
+  it.L = p.lens[bg];
+  it.k_lo = it.c * kAttnChunkB;
+  it.k_hi = min(it.k_lo + kAttnChunkB, it.L + p.R);
+  const size_t base = ((size_t)bg * p.H + it.h) * p.kv_stride * kAttnHd;
+  it.kc = (const uint16_t*)p.kc + base;
+  it.vc = (const uint16_t*)p.vc + base;
+  AttnRegsB r;
+  attn_zero_regs(r);
+  if (it.k_lo < it.k_hi) {
+    attn_load_plain(it, p.kv_stride, it.k_lo, (it.k_hi + 7) & ~7, wave, lane, r);
+    attn_mask_tail(it, wave, lane, r);
   }
-  RowStat o;
-  o.m = x.m;
-  o.a = x.a;
-  o.s = x.s + ((y.m == -INFINITY) ? 0.f : y.s * expf(y.m - x.m));
-  return o;
+  attn_chunk(it, p.q + (size_t)(it.bl * p.R) * p.d + it.h * kAttnHd, p.d, p.R, p.scale, r, sm);
+  const size_t bh = (size_t)it.bl * p.H + it.h;
+  float* po = p.part_o + ((bh * p.NC + it.c) * p.Rmax) * kAttnHd;
+  float* pml = p.part_ml + ((bh * p.NC + it.c) * p.Rmax) * 2;
+  for (int idx = tid; idx < p.R * kAttnHd; idx += 512) {
+    const int row = idx / kAttnHd, dd = idx - row * kAttnHd;
+    po[row * kAttnHd + dd] = attn_chunk_out(sm, row, dd);
+  }
+  if (tid < p.R) {
+    pml[tid * 2] = sm.m[tid];
+    pml[tid * 2 + 1] = sm.l[tid];
+  }
 }
 
-struct Best {
-  float s;
-  int a;
-};
-
-__device__ __forceinline__ Best better(Best x, Best y) {
-  if (y.s > x.s || (y.s == x.s && y.a < x.a)) return y;
-  return x;
+template <bool ABF16>
+__global__ void __launch_bounds__(512) attn_b_combine_kernel(AttnParams p) {
+  __shared__ float ml[2 * kAttnMaxChunks * kAttnRows];
+  __shared__ float sc[kAttnMaxChunks * kAttnRows];
+  const int h = blockIdx.x, bl = blockIdx.y, tid = threadIdx.x;
+  const int R = p.R;
+  const size_t bh = (size_t)bl * p.H + h;
+  const float* po0 = p.part_o + (bh * p.NC * p.Rmax) * kAttnHd;
+  const float* pml0 = p.part_ml + (bh * p.NC * p.Rmax) * 2;
+  for (int i = tid; i < p.NC * R; i += 512) {
+    const int c = i / R, row = i - c * R;
+    ml[2 * i] = pml0[((size_t)c * p.Rmax + row) * 2];
+    ml[2 * i + 1] = pml0[((size_t)c * p.Rmax + row) * 2 + 1];
+  }
+  __syncthreads();
+  if (tid < R) attn_merge_weights(ml, sc, p.NC, R, tid);
+  __syncthreads();
+  for (int idx = tid; idx < R * kAttnHd; idx += 512) {
+    const int row = idx / kAttnHd, dd = idx - row * kAttnHd;
+    float O = 0.f;
+    for (int c = 0; c < p.NC; ++c) {
+      const float w = sc[c * R + row];
+      const float v = po0[((size_t)c * p.Rmax + row) * kAttnHd + dd];
+      O += w != 0.f ? v * w : 0.f;
+    }
+    store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * R + row) * p.d + h * kAttnHd + dd, O);
+  }
 }
 
+// ---------------------------------------------------------------------------
+// Accept / reject and the correction draw (device_accept.h), one workgroup per
+// request.
+// ---------------------------------------------------------------------------
 constexpr int kAcceptThreads = 1024;
 
 __global__ void __launch_bounds__(kAcceptThreads) accept_kernel(AcceptParams p) {
-  constexpr int NWV = kAcceptThreads / 64;
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int R = p.R, V = p.V, G = p.gamma;
-  __shared__ float rlse[kMaxR];
-  __shared__ int rarg[kMaxR];
-  __shared__ Best bpart[NWV];
-  __shared__ int n_s;
-
-  bool sample = p.mode[b] == SPADE_SAMPLE;
-  if (sample && (p.u == nullptr || (G > 0 && p.q == nullptr))) {
-    if (tid == 0) flag_error(p.err, SPADE_DERR_NOQ);
-    sample = false;
-  }
-  const float invT = sample ? p.inv_T : 1.0f;
-  const float* lg = p.logits + (size_t)b * R * V;
-
-  // row statistics over the vocabulary: wave r merges row r from the LM
-  // head's per-panel partials (or, without them, from the logits), in a fixed
-  // order
-  for (int r = wave; r < R; r += NWV) {
-    RowStat st{-INFINITY, 0.f, 0x7fffffff};
-    if (p.stats != nullptr) {
-      const float* sp = p.stats + (size_t)(b * R + r) * p.NU * 3;
-#pragma unroll 8
-      for (int q = lane; q < p.NU; q += 64) {
-        const RowStat one{sp[q * 3], sp[q * 3 + 1], __float_as_int(sp[q * 3 + 2])};
-        if (one.m != -INFINITY) st = merge_stat(st, one);
-      }
-    } else {
-#pragma unroll 8
-      for (int v = lane; v < V; v += 64) {
-        const float z = lg[(size_t)r * V + v] * invT;
-        if (z != z) continue;
-        st = merge_stat(st, RowStat{z, 1.f, v});
-      }
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      RowStat o;
-      o.m = __shfl_xor(st.m, off);
-      o.s = __shfl_xor(st.s, off);
-      o.a = __shfl_xor(st.a, off);
-      st = (lane & off) ? merge_stat(o, st) : merge_stat(st, o);
-    }
-    if (lane == 0) {
-      rlse[r] = st.m + logf(st.s);
-      rarg[r] = st.a;
-    }
-  }
-  __syncthreads();
-
-  if (tid == 0) {
-    int n = G;
-    for (int i = 0; i < G; ++i) {
-      int x = p.drafts[(size_t)b * G + i];
-      if (x < 0 || x >= V) {
-        flag_error(p.err, SPADE_DERR_TOKEN);
-        x = x < 0 ? 0 : V - 1;
-      }
-      bool ok;
-      if (!sample) {
-        ok = (x == rarg[i]);
-      } else {
-        const float px = expf(lg[(size_t)i * V + x] * invT - rlse[i]);
-        const float qx = p.q[((size_t)b * G + i) * V + x];
-        ok = p.u[(size_t)b * (G + 1) + i] * qx < px;
-      }
-      if (!ok) {
-        n = i;
-        break;
-      }
-    }
-    n_s = n;
-  }
-  __syncthreads();
-  const int n = n_s;
-  int corr = 0;
-  if (!sample) {
-    corr = rarg[n];
-  } else {
-    const uint64_t seed = (uint64_t)__float_as_uint(p.u[(size_t)b * (G + 1) + G]);
-    const float* row = lg + (size_t)n * V;
-    const bool residual = n < G;
-    const float* qrow = residual ? p.q + ((size_t)b * G + n) * V : nullptr;
-    const float lse = rlse[n];
-    for (int pass = 0; pass < 2; ++pass) {
-      const bool use_res = residual && pass == 0;
-      Best bst{-INFINITY, 0x7fffffff};
-#pragma unroll 4
-      for (int v = tid; v < V; v += kAcceptThreads) {
-        const float z = row[v] * invT;
-        float sc;
-        if (use_res) {
-          const float w = expf(z - lse) - qrow[v];
-          sc = w > 0.f ? logf(w) + gumbel_at(seed, v) : -INFINITY;
-        } else {
-          sc = z + gumbel_at(seed, v);
-        }
-        if (sc != sc) continue;
-        bst = better(bst, Best{sc, v});
-      }
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) {
-        const Best o{__shfl_xor(bst.s, off), __shfl_xor(bst.a, off)};
-        bst = better(bst, o);
-      }
-      if (lane == 0) bpart[wave] = bst;
-      __syncthreads();
-      Best t = bpart[0];
-      for (int w = 1; w < NWV; ++w) t = better(t, bpart[w]);
-      __syncthreads();
-      if (t.s != -INFINITY || !use_res) {
-        corr = t.a;
-        break;
-      }
-      if (tid == 0) flag_error(p.err, SPADE_DERR_RESIDUAL);
-    }
-  }
-  if (tid == 0) {
-    p.n_out[b] = n;
-    p.corr_out[b] = corr;
-  }
+  __shared__ AcceptSmem sm;
+  accept_request<kAcceptThreads, false>(p, (int)blockIdx.x, sm);
 }
 
 // ---------------------------------------------------------------------------
@@ -1172,16 +683,27 @@ __global__ void pack_kernel(PackParams p) {
 // ---------------------------------------------------------------------------
 namespace {
 
-constexpr int kGemmWaves = 8;
+// The LDS operand copy needs more than the default dynamic LDS limit.
+template <bool WBF16, int KIND>
+hipError_t enable_lds_a() {
+  static hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<WBF16, 1, true, KIND>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGemmLdsABytes);
+  return once;
+}
 
 template <bool WBF16, int KIND>
 hipError_t launch_gemm_kind(const GemmParams& gp, int grid, int mt, hipStream_t st) {
-  if (mt == 1 && gp.NKB <= 2 * kGemmWaves)
-    hipLaunchKernelGGL((gemm_ares_kernel<WBF16, kGemmWaves, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
-  else if (mt == 1)
-    hipLaunchKernelGGL((gemm_kernel<WBF16, kGemmWaves, 1, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
-  else
-    hipLaunchKernelGGL((gemm_kernel<WBF16, kGemmWaves, 2, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
+  // the LDS operand copy pays off once a workgroup reuses it for a second unit
+  const uint32_t lds = gemm_lds_a_bytes(gp.M, gp.act_stride, WBF16);
+  if (mt == 1 && lds <= kGemmLdsABytes && gemm_lds_a_ok(gp.act_stride, WBF16) && gp.n_units >= 2 * grid) {
+    hipError_t e = enable_lds_a<WBF16, KIND>();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_kernel<WBF16, 1, true, KIND>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp);
+  } else if (mt == 1) {
+    hipLaunchKernelGGL((gemm_kernel<WBF16, 1, false, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
+  } else {
+    hipLaunchKernelGGL((gemm_kernel<WBF16, 2, false, KIND>), dim3(grid), dim3(kGemmWaves * 64), 0, st, gp);
+  }
   return hipGetLastError();
 }
 
@@ -1243,6 +765,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   g.F = D.F;
   g.kv_stride = kv->stride;
   g.kv_bf16 = D.kvdt == SPADE_BF16;
+  g.kv_bytes = (uint32_t)(kv_layer * kv_elt);
   g.rope = W.rope;
   g.x = W.x;
   g.V = D.V;
@@ -1346,10 +869,12 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->stride * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
 
-  // attention chunks of kAttnChunk keys over the longest request
+  // attention chunks over the longest request: kAttnChunkB keys for a bf16
+  // cache with head_dim 128 (8-wave MFMA kernel), else kAttnChunk
   int max_keys = 0;
   for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) max_keys = std::max(max_keys, kv->lens_ub[b] + fc.R);
-  const int CK = kAttnChunk;
+  const bool attn_b = D.kvdt == SPADE_BF16 && D.hd == kAttnHd && fc.R <= kAttnRows;
+  const int CK = attn_b ? kAttnChunkB : kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
 
@@ -1376,8 +901,17 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     ap.act_split = W.act_split;
     const dim3 agrid(NC, D.H, fc.nb);
     const bool kvb = D.kvdt == SPADE_BF16;
-    if (D.hd == 64) e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);
-    else e = launch_attn_hd<128>(ap, kvb, wb, agrid, st);
+    if (attn_b) {
+      hipLaunchKernelGGL(attn_b_kernel, agrid, dim3(512), 0, st, ap);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      if (wb) hipLaunchKernelGGL(attn_b_combine_kernel<true>, dim3(D.H, fc.nb), dim3(512), 0, st, ap);
+      else hipLaunchKernelGGL(attn_b_combine_kernel<false>, dim3(D.H, fc.nb), dim3(512), 0, st, ap);
+      e = hipGetLastError();
+    } else if (D.hd == 64) {
+      e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);
+    } else {
+      e = launch_attn_hd<128>(ap, kvb, wb, agrid, st);
+    }
     if (e != hipSuccess) return e;
     if ((e = launch_layer_gemm(md, kv, GEMM_O, l, fc, st)) != hipSuccess) return e;
     if ((e = launch_layer_gemm(md, kv, GEMM_GU, l, fc, st)) != hipSuccess) return e;

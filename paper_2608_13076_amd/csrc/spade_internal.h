@@ -19,6 +19,8 @@ constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
 constexpr int kAttnChunk = 128;      // keys per attention workgroup
 constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
 constexpr int kMaxLen = kAttnChunk * kAttnMaxChunks;
+constexpr uint32_t kFusedLdsBytes = 159 * 1024;  // dynamic LDS of the single-launch verify kernel
+constexpr size_t kBarBytes = 4096;               // its grid-barrier words
 inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
@@ -44,6 +46,47 @@ __host__ __device__ inline int panel_row(int kind, int p, int r, int d_model, in
   }
   if (kind == GEMM_GU) return (r < 8) ? p * 8 + r : d_ffn + p * 8 + (r - 8);
   return p * 16 + r;
+}
+
+// Activation arena of the single-launch verify pass.  Every buffer one stage
+// writes and a later stage of the same launch reads has its own region per
+// layer (and one for the embedding), so no L2 holds a line of it before it is
+// written: readers use plain cached loads, writers write-through stores.
+constexpr int kFusedRows = 16;  // rows (requests x (gamma + 1)) of the single-launch pass
+struct FusedArena {
+  // per-layer block: rotated q; attention output (O operand); O output (gate/up
+  // operand) and its RMS partials; SwiGLU output (down operand); down output
+  // (next QKV / LM operand) and its RMS partials.  Split operands hold two
+  // bf16 terms, split s at element s * kFusedRows * K.
+  size_t q, act_o, act_no, ssq_o, act_f, act_nd, ssq_d, layer_bytes;
+  size_t e_act, e_ssq;  // embedding output, after the layer blocks
+  size_t total;
+};
+
+inline size_t fused_align(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline FusedArena fused_arena_of(int L, int d, int F) {
+  FusedArena a{};
+  const size_t rows = kFusedRows;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += fused_align(bytes);
+    return o;
+  };
+  a.q = take(rows * d * 4);
+  a.act_o = take(rows * d * 4);
+  a.act_no = take(rows * d * 4);
+  a.ssq_o = take(rows * (d / 16) * 4);
+  a.act_f = take(rows * F * 4);
+  a.act_nd = take(rows * d * 4);
+  a.ssq_d = take(rows * (d / 16) * 4);
+  a.layer_bytes = off;
+  off = a.layer_bytes * L;
+  a.e_act = take(rows * d * 4);
+  a.e_ssq = take(rows * (d / 16) * 4);
+  a.total = off;
+  return a;
 }
 
 struct Dims {
@@ -73,6 +116,9 @@ struct Workspace {
   float* stats;       // [Mmax][Vpad/16][3] LM-head per-panel max / sumexp / argmax
   float* rope;        // [max_len][hd/2][2] cos, sin
   uint32_t* err;      // device error word
+  uint32_t* bar;      // grid-barrier words of the single-launch verify pass (kept at zero between calls)
+  uint8_t* fused;     // activation arena of the single-launch verify pass (NULL if the model cannot use it)
+  FusedArena fa;
   size_t act_split;   // elements between splits of act_n / act_o
   size_t actf_split;  // elements between splits of act_f
   int Mmax, NCmax, Rmax;
@@ -91,6 +137,7 @@ struct spade_model_s {
   int device;
   int n_cu;      // compute units of the device
   int gemm_wgs;  // persistent GEMM workgroups
+  bool fused_ok; // cooperative launches available and the single-launch verify pass enabled
 };
 
 struct spade_kv_s {
@@ -133,6 +180,10 @@ struct AcceptCall {
 };
 
 hipError_t launch_forward(spade_model m, spade_kv kv, const ForwardCall& fc, hipStream_t st);
+// single-launch verify pass (verify_fused.hip): eligibility and launch
+bool fused_eligible(spade_model m, spade_kv kv, const ForwardCall& fc);
+hipError_t launch_verify_fused(spade_model m, spade_kv kv, const ForwardCall& fc, const AcceptCall& ac,
+                               hipStream_t st);
 hipError_t launch_layer_gemm(spade_model m, spade_kv kv, int kind, int layer, const ForwardCall& fc,
                              hipStream_t st);
 hipError_t launch_accept(spade_model m, const AcceptCall& ac, hipStream_t st);

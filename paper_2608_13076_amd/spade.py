@@ -30,7 +30,7 @@ EXPORTED = (
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
     "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
-    "spade_model_destroy", "spade_kv_destroy",
+    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused",
 )
 
 
@@ -85,6 +85,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_accept_from_logits": (I, [P, I, I, I, P, P, P, P, P, F, P, P, P]),
         "spade_profile_gemm": (I, [P, P, I, I, I, I, P]),
         "spade_get_device_error": (I, [P, P, P]),
+        "spade_model_set_fused": (I, [P, I]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
         "spade_kv_destroy": (None, [P]),
@@ -162,6 +163,11 @@ class Model:
     def load_all(self, tensors: Iterable[Tuple[str, Optional[int], np.ndarray]]) -> None:
         for kind, layer, arr in tensors:
             self.load_numpy(kind, layer, arr)
+
+    def set_fused(self, enable: bool) -> None:
+        """Single persistent launch per verify call where the shape allows it
+        (default), or one kernel per stage."""
+        _check(self.lib.spade_model_set_fused(self.handle, 1 if enable else 0))
 
     def device_error(self) -> int:
         v = ctypes.c_uint32()
