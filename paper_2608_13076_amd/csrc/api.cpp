@@ -119,7 +119,7 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.attn_ml = take((size_t)max_batch * D.H * p.NCmax * p.Rmax * 2 * 4);
   p.attn_cnt = take((size_t)max_batch * D.H * 4);
   p.logits = take((size_t)p.Mmax * D.V * 4);
-  p.stats = take((size_t)p.Mmax * NU * 3 * 4);
+  p.stats = take((size_t)p.Mmax * std::max(NU, kMaxStatGroups) * 3 * 4);
   p.rope = take((size_t)max_len * (D.hd / 2) * 2 * 4);
   p.err = take(4);
   p.bar = take(kBarBytes);
@@ -185,7 +185,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->gemm_wgs = m->n_cu;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
-    if (v > 0) m->gemm_wgs = v;
+    if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
   }
   // the single-launch verify pass needs cooperative launches (all workgroups
   // resident); it is off by default (the per-stage path is faster at the
@@ -400,7 +400,7 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
   ac.V = m->dims.V;
   ac.logits = fc.logits_out;
   ac.stats = m->ws.stats;
-  ac.NU = m->dims.Vpad / 16;
+  ac.NU = std::min(m->dims.Vpad / 16, m->gemm_wgs);  // LM-head workgroups (fused: n_cu, set there)
   ac.drafts = d_draft_tokens;
   ac.q = d_draft_probs;
   ac.u = d_uniforms;

@@ -38,25 +38,6 @@ __device__ __forceinline__ float gumbel_at(uint64_t seed, int v) {
   return -logf(-logf(U));
 }
 
-// (max, sum exp(z - max), argmax); ties keep the lower id.
-struct RowStat {
-  float m, s;
-  int a;
-};
-
-__device__ __forceinline__ RowStat merge_stat(RowStat x, RowStat y) {
-  if (y.m > x.m || (y.m == x.m && y.a < x.a)) {
-    const RowStat t = x;
-    x = y;
-    y = t;
-  }
-  RowStat o;
-  o.m = x.m;
-  o.a = x.a;
-  o.s = x.s + ((y.m == -INFINITY) ? 0.f : y.s * expf(y.m - x.m));
-  return o;
-}
-
 struct Best {
   float s;
   int a;
@@ -76,6 +57,8 @@ __device__ __forceinline__ float ld_any(const float* p) {
 struct AcceptSmem {
   float rlse[kMaxR];
   int rarg[kMaxR];
+  int x[kMaxR];                     // draft tokens (clamped)
+  float lx[kMaxR], qx[kMaxR], ux[kMaxR];  // sampling: logit and q at the draft, its uniform
   Best bpart[16];
   int n_s;
 };
@@ -94,9 +77,24 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
   const float invT = sample ? p.inv_T : 1.0f;
   const float* lg = p.logits + (size_t)b * R * V;
 
+  // the drafts and what the accept chain reads for them, one thread per draft
+  if (tid < G) {
+    int x = p.drafts[(size_t)b * G + tid];
+    if (x < 0 || x >= V) {
+      flag_error(p.err, SPADE_DERR_TOKEN);
+      x = x < 0 ? 0 : V - 1;
+    }
+    sm.x[tid] = x;
+    if (sample) {
+      sm.lx[tid] = ld_any<COH>(lg + (size_t)tid * V + x);
+      sm.qx[tid] = p.q[((size_t)b * G + tid) * V + x];
+      sm.ux[tid] = p.u[(size_t)b * (G + 1) + tid];
+    }
+  }
+
   // row statistics over the vocabulary: wave r merges row r from the LM
-  // head's per-panel partials (or, without them, from the logits), in a fixed
-  // order
+  // head's per-workgroup partials (or, without them, from the logits), in a
+  // fixed order
   for (int r = wave; r < R; r += NWV) {
     RowStat st{-INFINITY, 0.f, 0x7fffffff};
     if (p.stats != nullptr) {
@@ -133,18 +131,12 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
   if (tid == 0) {
     int n = G;
     for (int i = 0; i < G; ++i) {
-      int x = p.drafts[(size_t)b * G + i];
-      if (x < 0 || x >= V) {
-        flag_error(p.err, SPADE_DERR_TOKEN);
-        x = x < 0 ? 0 : V - 1;
-      }
       bool ok;
       if (!sample) {
-        ok = (x == sm.rarg[i]);
+        ok = (sm.x[i] == sm.rarg[i]);
       } else {
-        const float px = expf(ld_any<COH>(lg + (size_t)i * V + x) * invT - sm.rlse[i]);
-        const float qx = p.q[((size_t)b * G + i) * V + x];
-        ok = p.u[(size_t)b * (G + 1) + i] * qx < px;
+        const float px = expf(sm.lx[i] * invT - sm.rlse[i]);
+        ok = sm.ux[i] * sm.qx[i] < px;
       }
       if (!ok) {
         n = i;

@@ -4,8 +4,8 @@
 // kernel.
 //
 // Work item: (request, head, chunk of kAttnChunkB keys), one 8-wave
-// workgroup; wave w owns keys [k_lo + 64w, k_lo + 64w + 64) as two 32-key
-// sub-blocks.  Row i of the request sits at position L + i and sees keys
+// workgroup; wave w owns keys [k_lo + 32 S w, k_lo + 32 S (w + 1)) as S =
+// kAttnSub sub-blocks of 32 keys.  Row i of the request sits at position L + i and sees keys
 // <= L + i.  Scores S = Q K^T and O = P V run on MFMA 16x16x32 bf16 with Q and
 // P split into two bf16 terms (hi + lo); K is stored as rows [pos][hd] and V
 // transposed, rows [feature][stride], so both B operands are 16-byte loads.
@@ -18,7 +18,8 @@
 
 namespace spade {
 
-constexpr int kAttnChunkB = 512;  // keys per chunk
+constexpr int kAttnSub = 1;                    // 32-key sub-blocks per wave
+constexpr int kAttnChunkB = 8 * 32 * kAttnSub;  // keys per chunk (8 waves)
 constexpr int kAttnHd = 128;
 constexpr int kAttnRows = 16;      // rows per request (gamma + 1 <= 16)
 
@@ -29,8 +30,8 @@ struct AttnSmemB {
 };
 
 struct AttnRegsB {
-  uint4 kf[2][2][4];  // [sub-block][16-key group][32-feature slice]
-  uint4 vf[2][8];     // [sub-block][16-feature tile]: this lane's 8 keys
+  uint4 kf[kAttnSub][2][4];  // [sub-block][16-key group][32-feature slice]
+  uint4 vf[kAttnSub][8];     // [sub-block][16-feature tile]: this lane's 8 keys
 };
 
 struct AttnItemB {
@@ -44,7 +45,7 @@ struct AttnItemB {
 
 __device__ __forceinline__ void attn_zero_regs(AttnRegsB& r) {
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
+  for (int sb = 0; sb < kAttnSub; ++sb) {
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp)
 #pragma unroll
@@ -60,8 +61,8 @@ __device__ __forceinline__ void attn_load_plain(const AttnItemB& it, int stride,
                                                 AttnRegsB& r) {
   const int g = lane >> 4, kl = lane & 15;
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int kw = it.k_lo + 64 * wave + 32 * sb;
+  for (int sb = 0; sb < kAttnSub; ++sb) {
+    const int kw = it.k_lo + 32 * kAttnSub * wave + 32 * sb;
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
       const int key = kw + 16 * grp + kl;
@@ -85,8 +86,8 @@ __device__ __forceinline__ void attn_load_new(const AttnItemB& it, Rsrc rk, Rsrc
                                               AttnRegsB& r) {
   const int g = lane >> 4, kl = lane & 15;
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int kw = it.k_lo + 64 * wave + 32 * sb;
+  for (int sb = 0; sb < kAttnSub; ++sb) {
+    const int kw = it.k_lo + 32 * kAttnSub * wave + 32 * sb;
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
       const int key = kw + 16 * grp + kl;
@@ -109,8 +110,8 @@ __device__ __forceinline__ void attn_load_new(const AttnItemB& it, Rsrc rk, Rsrc
 __device__ __forceinline__ void attn_mask_tail(const AttnItemB& it, int wave, int lane, AttnRegsB& r) {
   const int g = lane >> 4;
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int kv0 = it.k_lo + 64 * wave + 32 * sb + 8 * g;
+  for (int sb = 0; sb < kAttnSub; ++sb) {
+    const int kv0 = it.k_lo + 32 * kAttnSub * wave + 32 * sb + 8 * g;
     if (kv0 + 8 > it.k_hi) {
 #pragma unroll
       for (int ft = 0; ft < 8; ++ft) {
@@ -166,7 +167,7 @@ __device__ __forceinline__ void attn_chunk(const AttnItemB& it, const float* q, 
   }
   // S = Q K^T; D[i][j] sits in lane j + 16*(i/4), register i%4: rows 4g..4g+3 of key kl
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
+  for (int sb = 0; sb < kAttnSub; ++sb)
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
       floatx4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -177,7 +178,7 @@ __device__ __forceinline__ void attn_chunk(const AttnItemB& it, const float* q, 
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh[ks]),
                                                       __builtin_bit_cast(bf16x8, r.kf[sb][grp][ks]), acc, 0, 0, 0);
       }
-      const int key = it.k_lo + 64 * wave + 32 * sb + 16 * grp + kl;
+      const int key = it.k_lo + 32 * kAttnSub * wave + 32 * sb + 16 * grp + kl;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 4 * g + i;
@@ -206,15 +207,15 @@ __device__ __forceinline__ void attn_chunk(const AttnItemB& it, const float* q, 
     }
   }
   __syncthreads();
-  // O = P V over the wave's 64 keys (sub-block 0, then 1)
+  // O = P V over the wave's keys (sub-blocks in order)
   floatx4 oacc[8];
 #pragma unroll
   for (int ft = 0; ft < 8; ++ft) oacc[ft] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
+  for (int sb = 0; sb < kAttnSub; ++sb) {
     uint4 ph = make_uint4(0, 0, 0, 0), pl = make_uint4(0, 0, 0, 0);
     if (kl < R) {
-      const float* pp = &sm.s[kl][64 * wave + 32 * sb + 8 * g];
+      const float* pp = &sm.s[kl][32 * kAttnSub * wave + 32 * sb + 8 * g];
       const float4 x0 = *(const float4*)pp;
       const float4 x1 = *(const float4*)(pp + 4);
       const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
@@ -258,6 +259,107 @@ __device__ __forceinline__ void attn_merge_weights(const float* ml, float* sc, i
   }
   const float inv = 1.0f / Ls;
   for (int c = 0; c < NC; ++c) sc[c * R + row] *= inv;
+}
+
+// Last-arrival merge of the chunks of one (request, head).
+struct AttnMergeSmem {
+  float ml[2 * kAttnMaxChunks * kAttnRows];  // (m, l) of every chunk, [c][row][2]
+  float sc[kAttnMaxChunks * kAttnRows];      // merge weights, [c][row]
+  int last;
+};
+
+// partials of output o (= row * kAttnHd + dd) for chunks 0..7 (sc1 loads)
+__device__ __forceinline__ void attn_load8(Rsrc rpo, int NC, int Rmax, int o, bool ok, float (&v)[8]) {
+  const int row = o / kAttnHd, dd = o - row * kAttnHd;
+#pragma unroll
+  for (int c = 0; c < 8; ++c)
+    v[c] = ld_b32_coh(rpo, (ok && c < NC) ? (uint32_t)((c * Rmax + row) * kAttnHd + dd) * 4u : kOob);
+}
+
+// weighted sum of output o over the chunks, in chunk order
+__device__ __forceinline__ float attn_merged(Rsrc rpo, const AttnMergeSmem& ms, int NC, int Rmax, int R, int o,
+                                             const float (&v)[8]) {
+  const int row = o / kAttnHd, dd = o - row * kAttnHd;
+  float O = 0.f;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    if (c < NC) {
+      const float w = ms.sc[c * R + row];
+      O += w != 0.f ? v[c] * w : 0.f;
+    }
+  }
+  for (int c = 8; c < NC; ++c) {
+    const float w = ms.sc[c * R + row];
+    const float val = ld_b32_coh(rpo, (uint32_t)((c * Rmax + row) * kAttnHd + dd) * 4u);
+    O += w != 0.f ? val * w : 0.f;
+  }
+  return O;
+}
+
+// Publish this chunk's partial with write-through stores, arrive on the
+// counter of its (request, head) once the stores have landed, and, in the
+// workgroup that arrives last, merge all chunks in chunk order (weights
+// attn_merge_weights) and pass each merged output o = row * kAttnHd + dd to
+// out(o, value).  The last arrival resets the counter.  part_o / part_ml:
+// [bh][NC][Rmax][kAttnHd] / [bh][NC][Rmax][2].  All 512 threads call it.
+template <class Out>
+__device__ __forceinline__ void attn_publish_merge(const AttnItemB& it, const AttnSmemB& sa, AttnMergeSmem& ms,
+                                                   float* part_o, float* part_ml, uint32_t* attn_cnt, int H,
+                                                   int NC, int Rmax, int R, Out&& out) {
+  const int tid = threadIdx.x;
+  const size_t bh = (size_t)it.bl * H + it.h;
+  if (it.active) {
+    float* po = part_o + ((bh * NC + it.c) * Rmax) * kAttnHd;
+    float* pml = part_ml + ((bh * NC + it.c) * Rmax) * 2;
+    for (int idx = tid; idx < R * kAttnHd; idx += 512) {
+      const int row = idx / kAttnHd, dd = idx - row * kAttnHd;
+      __hip_atomic_store(po + row * kAttnHd + dd, attn_chunk_out(sa, row, dd), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (tid < R) {
+      __hip_atomic_store(pml + tid * 2, sa.m[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(pml + tid * 2 + 1, sa.l[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) {
+    int last = 0;
+    if (it.active) {
+      uint32_t* cnt = attn_cnt + bh;
+      const uint32_t o = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (o == (uint32_t)NC - 1u) {
+        __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last = 1;
+      }
+    }
+    ms.last = last;
+  }
+  __syncthreads();
+  if (!ms.last) return;  // uniform across the workgroup
+  // the (m, l) pairs and this thread's first partials in one round trip
+  const Rsrc rpo = wave_rsrc(part_o + (bh * NC * Rmax) * kAttnHd);
+  const Rsrc rpm = wave_rsrc(part_ml + (bh * NC * Rmax) * 2);
+  const int nout = R * kAttnHd;
+  float v0[8], v1[8];
+  attn_load8(rpo, NC, Rmax, tid, tid < nout, v0);
+  attn_load8(rpo, NC, Rmax, tid + 512, tid + 512 < nout, v1);
+  for (int i = tid; i < NC * R; i += 512) {
+    const int c = i / R, row = i - c * R;
+    const uint32_t off = (uint32_t)((c * Rmax + row) * 2) * 4u;
+    ms.ml[2 * i] = ld_b32_coh(rpm, off);
+    ms.ml[2 * i + 1] = ld_b32_coh(rpm, off + 4u);
+  }
+  __syncthreads();
+  if (tid < R) attn_merge_weights(ms.ml, ms.sc, NC, R, tid);
+  __syncthreads();
+  if (tid < nout) out(tid, attn_merged(rpo, ms, NC, Rmax, R, tid, v0));
+  if (tid + 512 < nout) out(tid + 512, attn_merged(rpo, ms, NC, Rmax, R, tid + 512, v1));
+  for (int o = tid + 1024; o < nout; o += 512) {
+    float v[8];
+    attn_load8(rpo, NC, Rmax, o, true, v);
+    out(o, attn_merged(rpo, ms, NC, Rmax, R, o, v));
+  }
 }
 
 }  // namespace spade

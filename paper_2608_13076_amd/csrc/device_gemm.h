@@ -61,8 +61,8 @@ struct GemmParams {
   // LM
   float* logits;
   int V;
-  float* stats;
-  int NU;
+  float* stats;  // [M][NU][3]: (max, sum exp, argmax) of z = logit (/T) per row and workgroup
+  int NU;        // workgroups of the LM-head launch
   const uint8_t* mode;
   float inv_T;
   int have_q;
@@ -116,6 +116,7 @@ struct Gemm {
   int pos, bg;  // QKV: position and request of row ml
   bool samp;    // LM: row ml uses 1/T statistics
   bool nan_seen;
+  RowStat lmrun;  // LM: this workgroup's running (max, sum, argmax) of row ml over its units
   Rsrc ra[S];
   uint4 w0[8], w1[8], w2[8];
   uint4 av[MT][S][8];
@@ -141,6 +142,7 @@ struct Gemm {
     n = lane & 15;
     rok = tok && ml < a.M;
     nan_seen = false;
+    lmrun = RowStat{-INFINITY, 0.f, 0x7fffffff};
     pos = 0;
     bg = 0;
     samp = false;
@@ -354,11 +356,9 @@ struct Gemm {
       float ex = (z == -INFINITY) ? 0.f : expf(z - zm);
 #pragma unroll
       for (int off = 8; off >= 1; off >>= 1) ex += __shfl_xor(ex, off);
-      const Rsrc rst = make_rsrc(a.stats + (size_t)a.m0 * a.NU * 3, (uint32_t)((size_t)a.M * a.NU * 12));
-      const uint32_t so = (rok && n == 0) ? (uint32_t)((ml * a.NU + u) * 3) * 4u : kOob;
-      st_f32<COH>(rst, so, zm);
-      st_f32<COH>(rst, so == kOob ? kOob : so + 4u, ex);
-      st_f32<COH>(rst, so == kOob ? kOob : so + 8u, __int_as_float(am));
+      // fold the panel into this workgroup's running statistics of the row
+      // (panels in the workgroup's unit order); stored once after the loop
+      if (zm != -INFINITY) lmrun = merge_stat(lmrun, RowStat{zm, ex, am});
     }
   }
 
@@ -476,6 +476,14 @@ struct Gemm {
       step<0>(t);
       step<1>(t + 1);
       step<2>(t + 2);
+    }
+    if constexpr (KIND == GEMM_LM) {
+      // one (max, sum exp, argmax) per (row, workgroup): stats[m][bid], NU = grid size
+      const Rsrc rst = make_rsrc(a.stats + (size_t)a.m0 * a.NU * 3, (uint32_t)((size_t)a.M * a.NU * 12));
+      const uint32_t so = (rok && n == 0) ? (uint32_t)((ml * a.NU + bid) * 3) * 4u : kOob;
+      st_f32<COH>(rst, so, lmrun.m);
+      st_f32<COH>(rst, so == kOob ? kOob : so + 4u, lmrun.s);
+      st_f32<COH>(rst, so == kOob ? kOob : so + 8u, __int_as_float(lmrun.a));
     }
     if (nan_seen) flag_error(a.err, SPADE_DERR_NAN);
   }

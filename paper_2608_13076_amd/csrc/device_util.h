@@ -80,6 +80,36 @@ __device__ __forceinline__ void st_act(Rsrc r, uint32_t split_bytes, uint32_t el
   }
 }
 
+__device__ __forceinline__ float ld_b32_coh(Rsrc r, uint32_t off) { return ld_f32<true>(r, off); }
+
+// buffer resource over memory from `base` on, where base is the same in every
+// lane of the wave (offsets are the caller's to keep in bounds)
+__device__ __forceinline__ Rsrc wave_rsrc(const void* base) {
+  const uint64_t b = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  return make_rsrc((const void*)(((uint64_t)hi << 32) | lo), 0x7ffffff0u);
+}
+
+// (max, sum exp(z - max), argmax); ties keep the lower id.
+struct RowStat {
+  float m, s;
+  int a;
+};
+
+__device__ __forceinline__ RowStat merge_stat(RowStat x, RowStat y) {
+  if (y.m > x.m || (y.m == x.m && y.a < x.a)) {
+    const RowStat t = x;
+    x = y;
+    y = t;
+  }
+  RowStat o;
+  o.m = x.m;
+  o.a = x.a;
+  o.s = x.s + ((y.m == -INFINITY) ? 0.f : y.s * expf(y.m - x.m));
+  return o;
+}
+
 __device__ __forceinline__ void flag_error(uint32_t* err, uint32_t bits) {
   if (err) atomicOr(err, bits);
 }

@@ -78,13 +78,13 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedParams p) {
   if (p.tokens) t = p.tokens[i];
   else t = (i == 0) ? p.pending[p.b0 + bl] : p.drafts[bl * (p.R - 1) + i - 1];
   if (t < 0 || t >= p.V) {
-    if (threadIdx.x == 0) flag_error(p.err, SPADE_DERR_TOKEN);
+    if (threadIdx.x == 0 && blockIdx.y == 0) flag_error(p.err, SPADE_DERR_TOKEN);
     t = t < 0 ? 0 : p.V - 1;
   }
   // one column per thread; the sixteen lanes of a panel sum x^2 in a fixed
   // butterfly order (the same order as the single-launch pass)
   const int npan = p.d / 16;
-  for (int n0 = 0; n0 < p.d; n0 += blockDim.x) {
+  for (int n0 = (int)(blockIdx.y * blockDim.x); n0 < p.d; n0 += (int)(blockDim.x * gridDim.y)) {
     const int n = n0 + (int)threadIdx.x;
     const bool ok = n < p.d;
     float v = 0.f;
@@ -544,9 +544,12 @@ __global__ void __launch_bounds__(256) attn_combine_kernel(AttnParams p) {
 }
 
 // bf16 cache, head_dim 128: chunks of kAttnChunkB keys, one 8-wave workgroup
-// per (chunk, head, request) (device_attn.h), and the chunk merge.
+// per (chunk, head, request) (device_attn.h); the last chunk of a (request,
+// head) to finish merges them into the O-projection operand.
+template <bool ABF16>
 __global__ void __launch_bounds__(512) attn_b_kernel(AttnParams p) {
   __shared__ AttnSmemB sm;
+  __shared__ AttnMergeSmem ms;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   AttnItemB it;
   it.active = true;
@@ -567,46 +570,10 @@ __global__ void __launch_bounds__(512) attn_b_kernel(AttnParams p) {
     attn_mask_tail(it, wave, lane, r);
   }
   attn_chunk(it, p.q + (size_t)(it.bl * p.R) * p.d + it.h * kAttnHd, p.d, p.R, p.scale, r, sm);
-  const size_t bh = (size_t)it.bl * p.H + it.h;
-  float* po = p.part_o + ((bh * p.NC + it.c) * p.Rmax) * kAttnHd;
-  float* pml = p.part_ml + ((bh * p.NC + it.c) * p.Rmax) * 2;
-  for (int idx = tid; idx < p.R * kAttnHd; idx += 512) {
-    const int row = idx / kAttnHd, dd = idx - row * kAttnHd;
-    po[row * kAttnHd + dd] = attn_chunk_out(sm, row, dd);
-  }
-  if (tid < p.R) {
-    pml[tid * 2] = sm.m[tid];
-    pml[tid * 2 + 1] = sm.l[tid];
-  }
-}
-
-template <bool ABF16>
-__global__ void __launch_bounds__(512) attn_b_combine_kernel(AttnParams p) {
-  __shared__ float ml[2 * kAttnMaxChunks * kAttnRows];
-  __shared__ float sc[kAttnMaxChunks * kAttnRows];
-  const int h = blockIdx.x, bl = blockIdx.y, tid = threadIdx.x;
-  const int R = p.R;
-  const size_t bh = (size_t)bl * p.H + h;
-  const float* po0 = p.part_o + (bh * p.NC * p.Rmax) * kAttnHd;
-  const float* pml0 = p.part_ml + (bh * p.NC * p.Rmax) * 2;
-  for (int i = tid; i < p.NC * R; i += 512) {
-    const int c = i / R, row = i - c * R;
-    ml[2 * i] = pml0[((size_t)c * p.Rmax + row) * 2];
-    ml[2 * i + 1] = pml0[((size_t)c * p.Rmax + row) * 2 + 1];
-  }
-  __syncthreads();
-  if (tid < R) attn_merge_weights(ml, sc, p.NC, R, tid);
-  __syncthreads();
-  for (int idx = tid; idx < R * kAttnHd; idx += 512) {
-    const int row = idx / kAttnHd, dd = idx - row * kAttnHd;
-    float O = 0.f;
-    for (int c = 0; c < p.NC; ++c) {
-      const float w = sc[c * R + row];
-      const float v = po0[((size_t)c * p.Rmax + row) * kAttnHd + dd];
-      O += w != 0.f ? v * w : 0.f;
-    }
-    store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * R + row) * p.d + h * kAttnHd + dd, O);
-  }
+  attn_publish_merge(it, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int o, float O) {
+    const int row = o / kAttnHd, dd = o - row * kAttnHd;
+    store_act<ABF16>(p.act_out, p.act_split, (size_t)(it.bl * p.R + row) * p.d + it.h * kAttnHd + dd, O);
+  });
 }
 
 // ---------------------------------------------------------------------------
@@ -693,9 +660,9 @@ hipError_t enable_lds_a() {
 
 template <bool WBF16, int KIND>
 hipError_t launch_gemm_kind(const GemmParams& gp, int grid, int mt, hipStream_t st) {
-  // the LDS operand copy pays off once a workgroup reuses it for a second unit
+  // activation operand copied to LDS once per workgroup where it fits
   const uint32_t lds = gemm_lds_a_bytes(gp.M, gp.act_stride, WBF16);
-  if (mt == 1 && lds <= kGemmLdsABytes && gemm_lds_a_ok(gp.act_stride, WBF16) && gp.n_units >= 2 * grid) {
+  if (mt == 1 && lds <= kGemmLdsABytes && gemm_lds_a_ok(gp.act_stride, WBF16)) {
     hipError_t e = enable_lds_a<WBF16, KIND>();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((gemm_kernel<WBF16, 1, true, KIND>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp);
@@ -816,13 +783,13 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
       g.ssq_in = W.ssq;
       g.logits = fc.logits_out;
       g.stats = W.stats;
-      g.NU = D.Vpad / 16;
       g.mode = fc.mode;
       g.inv_T = fc.inv_T;
       g.have_q = fc.have_q;
       break;
   }
   const int grid = std::min(units, md->gemm_wgs);
+  g.NU = grid;  // LM head: one statistics entry per workgroup and row
   for (int m0 = 0; m0 < M; m0 += kMaxRowsPerGemm) {
     GemmParams gp = g;
     gp.w = wmat;
@@ -862,8 +829,10 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   ep.act_split = W.act_split;
   ep.ssq = W.ssq;
   ep.err = W.err;
-  if (wb) hipLaunchKernelGGL(embed_kernel<true>, dim3(M), dim3(256), 0, st, ep);
-  else hipLaunchKernelGGL(embed_kernel<false>, dim3(M), dim3(256), 0, st, ep);
+  // one workgroup per (row, 256 columns)
+  const dim3 egrid(M, (D.d + 255) / 256);
+  if (wb) hipLaunchKernelGGL(embed_kernel<true>, egrid, dim3(256), 0, st, ep);
+  else hipLaunchKernelGGL(embed_kernel<false>, egrid, dim3(256), 0, st, ep);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->stride * D.hd;  // elements
@@ -902,10 +871,8 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     const dim3 agrid(NC, D.H, fc.nb);
     const bool kvb = D.kvdt == SPADE_BF16;
     if (attn_b) {
-      hipLaunchKernelGGL(attn_b_kernel, agrid, dim3(512), 0, st, ap);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-      if (wb) hipLaunchKernelGGL(attn_b_combine_kernel<true>, dim3(D.H, fc.nb), dim3(512), 0, st, ap);
-      else hipLaunchKernelGGL(attn_b_combine_kernel<false>, dim3(D.H, fc.nb), dim3(512), 0, st, ap);
+      if (wb) hipLaunchKernelGGL(attn_b_kernel<true>, agrid, dim3(512), 0, st, ap);
+      else hipLaunchKernelGGL(attn_b_kernel<false>, agrid, dim3(512), 0, st, ap);
       e = hipGetLastError();
     } else if (D.hd == 64) {
       e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);

@@ -21,6 +21,7 @@ constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
 constexpr int kMaxLen = kAttnChunk * kAttnMaxChunks;
 constexpr uint32_t kFusedLdsBytes = 159 * 1024;  // dynamic LDS of the single-launch verify kernel
 constexpr size_t kBarBytes = 4096;               // its grid-barrier words
+constexpr int kMaxStatGroups = 2048;             // LM-head statistics entries per row (workgroups)
 inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
@@ -113,7 +114,7 @@ struct Workspace {
   float* attn_ml;     // [Bmax][H][NCmax][Rmax][2] chunk max / sum
   uint32_t* attn_cnt; // [Bmax][H] arrival counters (kept at zero between calls)
   float* logits;      // [Mmax][V]
-  float* stats;       // [Mmax][Vpad/16][3] LM-head per-panel max / sumexp / argmax
+  float* stats;       // [Mmax][groups][3] LM-head per-workgroup max / sumexp / argmax
   float* rope;        // [max_len][hd/2][2] cos, sin
   uint32_t* err;      // device error word
   uint32_t* bar;      // grid-barrier words of the single-launch verify pass (kept at zero between calls)

@@ -91,14 +91,6 @@ __device__ __forceinline__ void st_coh(float* p, float v) {
 __device__ __forceinline__ void st_coh_u16(uint16_t* p, uint16_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// sc1 loads at base + off where base is the same in every lane of the wave
-__device__ __forceinline__ Rsrc wave_rsrc(const void* base) {
-  const uint64_t b = (uint64_t)base;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
-  return make_rsrc((const void*)(((uint64_t)hi << 32) | lo), 0x7ffffff0u);
-}
-
 struct GridSync {
   uint32_t* w;
   uint32_t epoch;
@@ -267,7 +259,7 @@ __device__ __forceinline__ GemmParams fused_gemm_params(const FusedParams& P, in
     g.ssq_in = (const float*)(ar + P.fa.ssq_d);
     g.logits = P.logits;
     g.stats = P.stats;
-    g.NU = P.Vpad / 16;
+    g.NU = gridDim.x;  // one statistics entry per workgroup and row
     g.mode = P.mode;
     g.inv_T = P.inv_T;
     g.have_q = P.have_q;
@@ -298,9 +290,7 @@ __device__ __forceinline__ bool fused_gemm(const FusedParams& P, int layer, Grid
 // ---------------------------------------------------------------------------
 struct FusedAttnSmem {
   AttnSmemB a;
-  float ml[2 * kAttnMaxChunks * kAttnRows];  // (m, l) of every chunk, [c][row][2]
-  float sc[kAttnMaxChunks * kAttnRows];      // merge weights, [c][row]
-  int last;
+  AttnMergeSmem ms;
 };
 
 __device__ __forceinline__ AttnItemB fused_attn_item(const FusedParams& P, int layer, int item) {
@@ -328,107 +318,28 @@ __device__ __forceinline__ void fused_attn_prefetch(const FusedParams& P, const 
   if (it.active) attn_load_plain(it, P.kv_stride, it.k_lo, min(it.k_hi, it.L), wave, lane, r);
 }
 
-// merged output of (row, dd) = o-th output of the (request, head); v holds
-// the partials of chunks 0..7 already loaded
-__device__ __forceinline__ void fused_attn_out(const FusedParams& P, int layer, const AttnItemB& it, Rsrc rpo,
-                                               const FusedAttnSmem& sm, int o, const float (&v)[8]) {
-  const int R = P.R;
-  const int row = o / kAttnHd, dd = o - row * kAttnHd;
-  float O = 0.f;
-#pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    if (c < P.NC) {
-      const float w = sm.sc[c * R + row];
-      O += w != 0.f ? v[c] * w : 0.f;
-    }
-  }
-  for (int c = 8; c < P.NC; ++c) {
-    const float w = sm.sc[c * R + row];
-    const float val = ld_f32<true>(rpo, (uint32_t)((c * P.Rmax + row) * kAttnHd + dd) * 4u);
-    O += w != 0.f ? val * w : 0.f;
-  }
-  uint16_t* act = (uint16_t*)(P.arena + (size_t)layer * P.fa.layer_bytes + P.fa.act_o);
-  const size_t split = (size_t)kFusedRows * P.d;
-  const size_t e = (size_t)(it.bl * R + row) * P.d + it.h * kAttnHd + dd;
-  float rem = O;
-#pragma unroll
-  for (int s = 0; s < kActSplits; ++s) {
-    const uint16_t hb = f2bf(rem);
-    st_coh_u16(act + s * split + e, hb);
-    rem -= bf2f(hb);
-  }
-}
-
-__device__ __forceinline__ void fused_attn_load8(const FusedParams& P, Rsrc rpo, int o, bool ok, float (&v)[8]) {
-  const int row = o / kAttnHd, dd = o - row * kAttnHd;
-#pragma unroll
-  for (int c = 0; c < 8; ++c)
-    v[c] = ld_f32<true>(rpo, (ok && c < P.NC) ? (uint32_t)((c * P.Rmax + row) * kAttnHd + dd) * 4u : kOob);
-}
-
 __device__ __forceinline__ void fused_attn_run(const FusedParams& P, int layer, const AttnItemB& it, AttnRegsB& r,
                                                FusedAttnSmem& sm, int wave, int lane) {
-  const int tid = threadIdx.x;
   const int R = P.R;
   if (it.active) attn_load_new(it, wave_rsrc(it.kc), wave_rsrc(it.vc), P.kv_stride, wave, lane, r);
   attn_mask_tail(it, wave, lane, r);
   const float* q = (const float*)(P.arena + (size_t)layer * P.fa.layer_bytes + P.fa.q) +
                    (size_t)(it.bl * R) * P.d + it.h * kAttnHd;
   attn_chunk(it, q, P.d, R, P.scale, r, sm.a);
-  // chunk partial, then the arrival once it has landed
-  const size_t bh = (size_t)it.bl * P.H + it.h;
-  if (it.active) {
-    float* po = P.part_o + ((bh * P.NC + it.c) * P.Rmax) * kAttnHd;
-    float* pml = P.part_ml + ((bh * P.NC + it.c) * P.Rmax) * 2;
-    for (int idx = tid; idx < R * kAttnHd; idx += kFusedThreads) {
-      const int row = idx / kAttnHd, dd = idx - row * kAttnHd;
-      st_coh(po + row * kAttnHd + dd, attn_chunk_out(sm.a, row, dd));
+  // publish, arrive, and merge in the last arrival into this layer's O operand
+  uint16_t* act = (uint16_t*)(P.arena + (size_t)layer * P.fa.layer_bytes + P.fa.act_o);
+  const size_t split = (size_t)kFusedRows * P.d;
+  attn_publish_merge(it, sm.a, sm.ms, P.part_o, P.part_ml, P.attn_cnt, P.H, P.NC, P.Rmax, R, [&](int o, float O) {
+    const int row = o / kAttnHd, dd = o - row * kAttnHd;
+    const size_t e = (size_t)(it.bl * R + row) * P.d + it.h * kAttnHd + dd;
+    float rem = O;
+#pragma unroll
+    for (int s = 0; s < kActSplits; ++s) {
+      const uint16_t hb = f2bf(rem);
+      st_coh_u16(act + s * split + e, hb);
+      rem -= bf2f(hb);
     }
-    if (tid < R) {
-      st_coh(pml + tid * 2, sm.a.m[tid]);
-      st_coh(pml + tid * 2 + 1, sm.a.l[tid]);
-    }
-  }
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (tid == 0) {
-    int last = 0;
-    if (it.active) {
-      uint32_t* cnt = P.attn_cnt + bh;
-      const uint32_t o = add_rlx(cnt, 1u);
-      if (o == (uint32_t)P.NC - 1u) {
-        st_rlx(cnt, 0u);
-        last = 1;
-      }
-    }
-    sm.last = last;
-  }
-  __syncthreads();
-  if (!sm.last) return;  // uniform across the workgroup
-  // merge (chunk order, the arithmetic of the stage path's combine): the
-  // (m, l) pairs and this thread's first partials in one round trip
-  const Rsrc rpo = wave_rsrc(P.part_o + (bh * P.NC * P.Rmax) * kAttnHd);
-  const Rsrc rpm = wave_rsrc(P.part_ml + (bh * P.NC * P.Rmax) * 2);
-  const int nout = R * kAttnHd;
-  float v0[8], v1[8];
-  fused_attn_load8(P, rpo, tid, tid < nout, v0);
-  fused_attn_load8(P, rpo, tid + kFusedThreads, tid + kFusedThreads < nout, v1);
-  for (int i = tid; i < P.NC * R; i += kFusedThreads) {
-    const int c = i / R, row = i - c * R;
-    const uint32_t off = (uint32_t)((c * P.Rmax + row) * 2) * 4u;
-    sm.ml[2 * i] = ld_f32<true>(rpm, off);
-    sm.ml[2 * i + 1] = ld_f32<true>(rpm, off + 4u);
-  }
-  __syncthreads();
-  if (tid < R) attn_merge_weights(sm.ml, sm.sc, P.NC, R, tid);
-  __syncthreads();
-  if (tid < nout) fused_attn_out(P, layer, it, rpo, sm, tid, v0);
-  if (tid + kFusedThreads < nout) fused_attn_out(P, layer, it, rpo, sm, tid + kFusedThreads, v1);
-  for (int o = tid + 2 * kFusedThreads; o < nout; o += kFusedThreads) {
-    float v[8];
-    fused_attn_load8(P, rpo, o, true, v);
-    fused_attn_out(P, layer, it, rpo, sm, o, v);
-  }
+  });
 }
 
 __device__ __forceinline__ bool fused_attention(const FusedParams& P, int layer, GridSync& gs, uint8_t* lds,
@@ -481,7 +392,7 @@ __global__ void __launch_bounds__(kFusedThreads) verify_fused_kernel(FusedParams
     AcceptParams ap{};
     ap.logits = P.logits;
     ap.stats = P.stats;
-    ap.NU = P.Vpad / 16;
+    ap.NU = gs.G;
     ap.V = P.V;
     ap.gamma = P.R - 1;
     ap.R = P.R;
