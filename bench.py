@@ -103,6 +103,73 @@ def cpu_baseline(w, inp, layers: int) -> dict:
             "latency_us": round(t_full * 1e6, 1), "prefill_s_sample": round(t_prefill, 2)}
 
 
+COUNTER_FILE = os.path.join(ROOT, "profiles", "gu_gemm_hbm_traffic.txt")
+COPY_BYTES = 256 << 20  # the calibration copy reads and writes this many bytes
+
+
+def gemm_source_digest() -> str:
+    """Digest of the sources the gate/up GEMM kernel is built from."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("device_util.h", "device_gemm.h", "kernels.hip"):
+        with open(os.path.join(ROOT, "paper_2608_13076_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic():
+    """Measured HBM bytes per gate/up launch from the committed counter
+    summary, or None if it is missing or the kernel sources changed since."""
+    try:
+        txt = open(COUNTER_FILE).read()
+    except OSError:
+        return None
+    vals = dict(line.split(":", 1) for line in txt.splitlines() if line.startswith(("traffic_bytes", "source_digest")))
+    if vals.get("source_digest", "").strip() != gemm_source_digest():
+        return None
+    return int(vals["traffic_bytes"].strip())
+
+
+def summarize_counters(fetch_dir: str, write_dir: str, cmd_fetch: str, cmd_write: str) -> int:
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the calibration copy and of
+    the gate/up GEMM launches from two rocprofv3 --pmc runs of --counters; the
+    copy's known bytes give the scale of each counter."""
+    import csv
+    import glob
+
+    def per_kernel(d, counter):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        acc = {}
+        for r in csv.DictReader(open(f)):
+            if r.get("Counter_Name") != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = "copy" if "neg" in name else ("gu" if "gemm_kernel" in name else None)
+            if key:
+                acc.setdefault(key, []).append(float(r["Counter_Value"]))
+        return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
+
+    fe = per_kernel(fetch_dir, "FETCH_SIZE")
+    wr = per_kernel(write_dir, "WRITE_SIZE")
+    f_fetch = COPY_BYTES / fe["copy"][0]
+    f_write = COPY_BYTES / wr["copy"][0]
+    traffic = int(round(fe["gu"][0] * f_fetch + wr["gu"][0] * f_write))
+    with open(COUNTER_FILE, "w") as f:
+        f.write("# HBM traffic of the gate/up GEMM launch (7B, batch 1, gamma 5)\n\n")
+        f.write("Two rocprofv3 counter runs of `bench.py --counters` (a calibration copy of a known size,\n"
+                "then the gate/up GEMM launches of the measurement hook), from the repository root:\n\n")
+        f.write(f"    {cmd_fetch}\n    {cmd_write}\n\n")
+        f.write("| kernel | FETCH_SIZE (KiB/dispatch) | WRITE_SIZE (KiB/dispatch) | dispatches |\n|---|---|---|---|\n")
+        f.write(f"| calibration copy ({COPY_BYTES} B read, {COPY_BYTES} B written) | {fe['copy'][0]:.1f} | "
+                f"{wr['copy'][0]:.1f} | {fe['copy'][1]} |\n")
+        f.write(f"| gate/up GEMM | {fe['gu'][0]:.1f} | {wr['gu'][0]:.1f} | {fe['gu'][1]} |\n\n")
+        f.write(f"Scale (bytes per counter unit): fetch {f_fetch:.2f}, write {f_write:.2f}.\n\n")
+        f.write(f"traffic_bytes: {traffic}\n")
+        f.write(f"source_digest: {gemm_source_digest()}\n")
+    print(open(COUNTER_FILE).read())
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -114,7 +181,15 @@ def main() -> int:
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--all-kernels", action="store_true", help="also time every other projection GEMM")
     ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    ap.add_argument("--counters", action="store_true",
+                    help="counter-collection run: a calibration copy, then the gate/up GEMM launches; no timing")
+    ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH", "CMD_WRITE"),
+                    help="write the HBM traffic summary from two rocprofv3 --pmc runs of --counters")
+    ap.add_argument("--fused", type=int, default=None,
+                    help="1: single-launch verify kernel, 0: one kernel per stage (default: the library's)")
     args = ap.parse_args()
+    if args.summarize_counters:
+        return summarize_counters(*args.summarize_counters)
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
@@ -141,6 +216,19 @@ def main() -> int:
     log(f"weights generated + loaded in {time.perf_counter() - t0:.1f}s "
         f"({model.weight_bytes() / 1e9:.2f} GB arena)")
     kv = spade.KVCache(model, w.batch, max_len)
+    if args.fused is not None:
+        model.set_fused(bool(args.fused))
+    if args.counters:
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)  # calibration: reads and writes COPY_BYTES
+        torch.cuda.synchronize()
+        _check = spade._check
+        _check(model.lib.spade_profile_gemm(model.handle, kv.handle, spade.GEMM_KINDS["gu"], w.batch, w.gamma,
+                                            4, spade._stream()))
+        torch.cuda.synchronize()
+        log("counter run done: 1 calibration copy, 4 gate/up launches")
+        return 0
     t0 = time.perf_counter()
     for b in range(w.batch):
         kv.prefill(b, inp.prompts[b])
@@ -191,6 +279,8 @@ def main() -> int:
     # Dominant kernel: the gate/up GEMM (45% of the weight bytes at this shape),
     # timed alone with HIP events on the current stream, same launch config.
     roof = spade.gemm_roofline(model, kv, "gu", w.batch, w.gamma, args.kernel_reps, HBM_PEAK_GBS)
+    if w.name == "c2_7b_greedy":
+        roof["traffic"] = read_traffic()
     log(f"dominant kernel: {roof}")
     if args.all_kernels:
         for kind in ("qkv", "o", "down", "lm"):
