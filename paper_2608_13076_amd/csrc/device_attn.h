@@ -3,127 +3,146 @@
 // to each other), shared by the per-stage kernels and the persistent verify
 // kernel.
 //
-// Work item: (request, head, chunk of kAttnChunkB keys), one 8-wave
-// workgroup; wave w owns keys [k_lo + 32 S w, k_lo + 32 S (w + 1)) as S =
-// kAttnSub sub-blocks of 32 keys.  Row i of the request sits at position L + i and sees keys
-// <= L + i.  Scores S = Q K^T and O = P V run on MFMA 16x16x32 bf16 with Q and
-// P split into two bf16 terms (hi + lo); K is stored as rows [pos][hd] and V
-// transposed, rows [feature][stride], so both B operands are 16-byte loads.
-// A chunk writes its unnormalised output, row max and row sum; the chunks of
-// a (request, head) are merged in chunk order with weights
-// exp(m_c - max) / sum_c(l_c exp(m_c - max)) (attn_merge_weights).
+// Work item: (request, head, chunk of CK keys), one 8-wave workgroup.  Row i
+// of the request sits at position L + i and sees keys <= L + i.  Scores
+// S = Q K^T run with keys split over the waves (wave w: keys
+// [k_lo + w CK/8, k_lo + (w+1) CK/8)); the chunk softmax runs one wave per
+// row; O = P V runs with features split over the waves (wave w: features
+// [16 w, 16 w + 16) over every key of the chunk), so each wave ends with
+// final chunk outputs and no cross-wave sum is needed.  Both products use
+// MFMA 16x16x32 bf16 with Q and P split into two bf16 terms (hi + lo).  K is
+// stored as rows [pos][hd] and V transposed, rows [feature][stride], so both
+// B operands are 16-byte loads.  A chunk writes its unnormalised output, row
+// max and row sum; the chunks of a (request, head) are merged in chunk order
+// with weights exp(m_c - max) / sum_c(l_c exp(m_c - max)).
 #pragma once
 
 #include "device_util.h"
 
 namespace spade {
 
-constexpr int kAttnSub = 1;                    // 32-key sub-blocks per wave
-constexpr int kAttnChunkB = 8 * 32 * kAttnSub;  // keys per chunk (8 waves)
 constexpr int kAttnHd = 128;
-constexpr int kAttnRows = 16;      // rows per request (gamma + 1 <= 16)
+constexpr int kAttnRows = 16;  // rows per request (gamma + 1 <= 16)
+constexpr int kAttnThreads = 512;
 
-struct AttnSmemB {
-  float s[kAttnRows][kAttnChunkB];  // scores, then probabilities
-  float o[8][kAttnRows][kAttnHd];   // per-wave partial outputs
+template <int CK>
+struct AttnSmem {
+  static_assert(CK == 128 || CK == 256, "chunk of 128 or 256 keys");
+  // probabilities as two bf16 terms (the A operand of O = P V); rows padded by
+  // 16 bytes so the 16 rows of a fragment read start in different banks
+  uint16_t ph[kAttnRows][CK + 8], pl[kAttnRows][CK + 8];
+  float pm[kAttnRows][8], ps[kAttnRows][8];  // per-wave row max / row sum
   float m[kAttnRows], l[kAttnRows];
 };
 
-struct AttnRegsB {
-  uint4 kf[kAttnSub][2][4];  // [sub-block][16-key group][32-feature slice]
-  uint4 vf[kAttnSub][8];     // [sub-block][16-feature tile]: this lane's 8 keys
+template <int CK>
+struct AttnRegs {
+  uint4 kf[CK / 128][4];  // [16-key group][32-feature slice]: key k_lo + (CK/8) w + 16 grp + kl
+  uint4 vf[CK / 32];      // [32-key step]: V^T row 16 w + kl, keys k_lo + 32 ks + 8 g .. + 8
 };
 
-struct AttnItemB {
+struct AttnItem {
   bool active;
   int bl, h, c;
   int L;           // cached keys of the request (row i sits at L + i)
+  int nc;          // chunks of the request
   int k_lo, k_hi;  // keys of this chunk: [k_lo, k_hi)
   const uint16_t* kc;  // K rows of (request, head)
   const uint16_t* vc;  // V^T rows of (request, head)
 };
 
-__device__ __forceinline__ void attn_zero_regs(AttnRegsB& r) {
-#pragma unroll
-  for (int sb = 0; sb < kAttnSub; ++sb) {
-#pragma unroll
-    for (int grp = 0; grp < 2; ++grp)
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) r.kf[sb][grp][ks] = make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int ft = 0; ft < 8; ++ft) r.vf[sb][ft] = make_uint4(0, 0, 0, 0);
-  }
+// Item (request bl, head h, chunk c) of a request with L cached keys and R
+// rows; chunks at or past the request's last key are inactive.
+template <int CK>
+__device__ __forceinline__ AttnItem attn_item(bool valid, int bl, int h, int c, int L, int R, const void* kc,
+                                              const void* vc, size_t head_off) {
+  AttnItem it;
+  it.bl = bl;
+  it.h = h;
+  it.c = c;
+  it.L = L;
+  it.nc = (L + R + CK - 1) / CK;
+  it.active = valid && c < it.nc;
+  it.k_lo = c * CK;
+  it.k_hi = it.active ? min(it.k_lo + CK, L + R) : it.k_lo;
+  it.kc = (const uint16_t*)kc + head_off;
+  it.vc = (const uint16_t*)vc + head_off;
+  return it;
 }
 
-// Keys of this wave in [kb, ke) (plain loads).  V^T vectors load whole when
-// all their 8 keys are in [kb, ke); keys at or past k_hi read as zero.
-__device__ __forceinline__ void attn_load_plain(const AttnItemB& it, int stride, int kb, int ke, int wave, int lane,
-                                                AttnRegsB& r) {
+template <int CK>
+__device__ __forceinline__ void attn_zero_regs(AttnRegs<CK>& r) {
+#pragma unroll
+  for (int grp = 0; grp < CK / 128; ++grp)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) r.kf[grp][ks] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int ks = 0; ks < CK / 32; ++ks) r.vf[ks] = make_uint4(0, 0, 0, 0);
+}
+
+// Keys of this lane in [kb, ke) (plain loads).  V^T vectors load whole when
+// all their 8 keys are in [kb, ke); K rows at or past k_hi are not read.
+template <int CK>
+__device__ __forceinline__ void attn_load_plain(const AttnItem& it, int stride, int kb, int ke, int wave, int lane,
+                                                AttnRegs<CK>& r) {
   const int g = lane >> 4, kl = lane & 15;
 #pragma unroll
-  for (int sb = 0; sb < kAttnSub; ++sb) {
-    const int kw = it.k_lo + 32 * kAttnSub * wave + 32 * sb;
+  for (int grp = 0; grp < CK / 128; ++grp) {
+    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
+    if (key >= kb && key < ke && key < it.k_hi) {
 #pragma unroll
-    for (int grp = 0; grp < 2; ++grp) {
-      const int key = kw + 16 * grp + kl;
-      if (key >= kb && key < ke && key < it.k_hi) {
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) r.kf[sb][grp][ks] = *(const uint4*)(it.kc + (size_t)key * kAttnHd + 32 * ks + 8 * g);
-      }
+      for (int ks = 0; ks < 4; ++ks) r.kf[grp][ks] = *(const uint4*)(it.kc + (size_t)key * kAttnHd + 32 * ks + 8 * g);
     }
-    const int kv0 = kw + 8 * g;
-    if (kv0 >= kb && kv0 + 8 <= ke) {
+  }
+  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
 #pragma unroll
-      for (int ft = 0; ft < 8; ++ft) r.vf[sb][ft] = *(const uint4*)(it.vc + (size_t)(16 * ft + kl) * stride + kv0);
-    }
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const int kv0 = it.k_lo + 32 * ks + 8 * g;
+    if (kv0 >= kb && kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
   }
 }
 
 // The keys this verify call appended, [L, k_hi), written earlier in the same
 // launch by other workgroups: sc1 loads (rk, rv: resources over this (request,
 // head)'s K and V^T rows).  A V^T vector holding any such key loads whole.
-__device__ __forceinline__ void attn_load_new(const AttnItemB& it, Rsrc rk, Rsrc rv, int stride, int wave, int lane,
-                                              AttnRegsB& r) {
+template <int CK>
+__device__ __forceinline__ void attn_load_new(const AttnItem& it, Rsrc rk, Rsrc rv, int stride, int wave, int lane,
+                                              AttnRegs<CK>& r) {
   const int g = lane >> 4, kl = lane & 15;
 #pragma unroll
-  for (int sb = 0; sb < kAttnSub; ++sb) {
-    const int kw = it.k_lo + 32 * kAttnSub * wave + 32 * sb;
+  for (int grp = 0; grp < CK / 128; ++grp) {
+    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
+    if (key >= it.L && key < it.k_hi) {
 #pragma unroll
-    for (int grp = 0; grp < 2; ++grp) {
-      const int key = kw + 16 * grp + kl;
-      if (key >= it.L && key < it.k_hi) {
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-          r.kf[sb][grp][ks] = ld_b128<true>(rk, (uint32_t)(key * kAttnHd + 32 * ks + 8 * g) * 2u);
-      }
+      for (int ks = 0; ks < 4; ++ks)
+        r.kf[grp][ks] = ld_b128<true>(rk, (uint32_t)(key * kAttnHd + 32 * ks + 8 * g) * 2u);
     }
-    const int kv0 = kw + 8 * g;
-    if (kv0 + 8 > it.L && kv0 < it.k_hi) {
+  }
 #pragma unroll
-      for (int ft = 0; ft < 8; ++ft) r.vf[sb][ft] = ld_b128<true>(rv, (uint32_t)((16 * ft + kl) * stride + kv0) * 2u);
-    }
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const int kv0 = it.k_lo + 32 * ks + 8 * g;
+    if (kv0 + 8 > it.L && kv0 < it.k_hi)
+      r.vf[ks] = ld_b128<true>(rv, (uint32_t)((16 * wave + kl) * stride + kv0) * 2u);
   }
 }
 
 // Zero the V^T entries of keys at or past k_hi (their P is zero, but the
 // cache may hold anything there).
-__device__ __forceinline__ void attn_mask_tail(const AttnItemB& it, int wave, int lane, AttnRegsB& r) {
+template <int CK>
+__device__ __forceinline__ void attn_mask_tail(const AttnItem& it, int lane, AttnRegs<CK>& r) {
   const int g = lane >> 4;
 #pragma unroll
-  for (int sb = 0; sb < kAttnSub; ++sb) {
-    const int kv0 = it.k_lo + 32 * kAttnSub * wave + 32 * sb + 8 * g;
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const int kv0 = it.k_lo + 32 * ks + 8 * g;
     if (kv0 + 8 > it.k_hi) {
+      uint32_t w[4] = {r.vf[ks].x, r.vf[ks].y, r.vf[ks].z, r.vf[ks].w};
 #pragma unroll
-      for (int ft = 0; ft < 8; ++ft) {
-        uint32_t w[4] = {r.vf[sb][ft].x, r.vf[sb][ft].y, r.vf[sb][ft].z, r.vf[sb][ft].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int p0 = kv0 + 2 * e;
-          if (p0 >= it.k_hi) w[e] = 0u;
-          else if (p0 + 1 >= it.k_hi) w[e] &= 0xffffu;
-        }
-        r.vf[sb][ft] = make_uint4(w[0], w[1], w[2], w[3]);
+      for (int e = 0; e < 4; ++e) {
+        const int p0 = kv0 + 2 * e;
+        if (p0 >= it.k_hi) w[e] = 0u;
+        else if (p0 + 1 >= it.k_hi) w[e] &= 0xffffu;
       }
+      r.vf[ks] = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
 }
@@ -141,181 +160,216 @@ __device__ __forceinline__ void attn_split2(const float* xs, uint4& hi, uint4& l
   lo = make_uint4(lw[0], lw[1], lw[2], lw[3]);
 }
 
-// One chunk with K/V fragments in r.  q: row 0 of the request's rotated
-// queries for this head (rows R apart by q_stride floats).  On return
-// sm.o[0..7] hold the wave partials, sm.m / sm.l the row max / sum (for an
-// empty chunk -inf / 0).  All 512 threads call it (it synchronises).
-__device__ __forceinline__ void attn_chunk(const AttnItemB& it, const float* q, int q_stride, int R, float scale,
-                                           AttnRegsB& r, AttnSmemB& sm) {
+// Cross-lane moves within a row of 16 lanes (DPP): lane i reads lane i^1,
+// i^2, 7-i (within its half row) and 15-i; the four steps reduce the row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_f32<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_f32<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_f32<0x141>(v));  // row_half_mirror
+  return fmaxf(v, dpp_f32<0x140>(v));  // row_mirror
+}
+
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f32<0xB1>(v);
+  v += dpp_f32<0x4E>(v);
+  v += dpp_f32<0x141>(v);
+  return v + dpp_f32<0x140>(v);
+}
+
+// This lane's query slices of the request's rotated queries for this head
+// (q: row 0, rows q_stride floats apart): row kl, features 32 ks + 8 g .. + 8
+// for ks = 0..3 (rows >= R and inactive items: zeros).  Issued before the
+// K/V loads, so the wait for them does not wait for the cache rows.
+__device__ __forceinline__ void attn_load_q(const AttnItem& it, const float* q, int q_stride, int R, int lane,
+                                            float4 (&qr)[8]) {
+  const int g = lane >> 4, kl = lane & 15;
+  const bool ok = it.active && kl < R;
+  const Rsrc rq = wave_rsrc(q);  // wave-uniform base, per-lane offsets
+  const uint32_t base = (uint32_t)(kl * q_stride + 8 * g) * 4u;
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    qr[2 * ks] = __builtin_bit_cast(float4, ld_b128<false>(rq, ok ? base + (uint32_t)(32 * ks) * 4u : kOob));
+    qr[2 * ks + 1] = __builtin_bit_cast(float4, ld_b128<false>(rq, ok ? base + (uint32_t)(32 * ks + 4) * 4u : kOob));
+  }
+}
+
+// One chunk with K/V fragments in r and query slices in qr (attn_load_q).
+// Returns this lane's unnormalised chunk outputs: rows 4g + i (i = 0..3),
+// feature 16 wave + kl.  Threads tid < R also set sm.m[tid] / sm.l[tid], the
+// row max / sum (for a row that sees no key of the chunk -inf / 0).  All 512
+// threads call it (it synchronises).
+//
+// Chunk softmax: each lane holds the scores of rows 4g..4g+3 for its keys;
+// row maxima and sums reduce over the 16 lanes of a row (DPP) and then over
+// the eight waves (LDS, in wave order).  Probabilities (exp2 of the
+// log2(e)-scaled difference) go to LDS once, as two bf16 terms, and every
+// wave reads them as the A operand of O = P V.
+template <int CK>
+__device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (&qr)[8], int R, float scale,
+                                              const AttnRegs<CK>& r, AttnSmem<CK>& sm) {
+  constexpr int NG = CK / 128;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, kl = lane & 15;
   uint4 qh[4], ql[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
-    qh[ks] = make_uint4(0, 0, 0, 0);
-    ql[ks] = make_uint4(0, 0, 0, 0);
-  }
-  if (it.active && kl < R) {
-    const float* qp = q + (size_t)kl * q_stride + 8 * g;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const float4 x0 = *(const float4*)(qp + 32 * ks);
-      const float4 x1 = *(const float4*)(qp + 32 * ks + 4);
-      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      attn_split2(xs, qh[ks], ql[ks]);
-    }
+    const float4 x0 = qr[2 * ks], x1 = qr[2 * ks + 1];
+    const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+    attn_split2(xs, qh[ks], ql[ks]);
   }
   // S = Q K^T; D[i][j] sits in lane j + 16*(i/4), register i%4: rows 4g..4g+3 of key kl
+  float sv[NG][4];
 #pragma unroll
-  for (int sb = 0; sb < kAttnSub; ++sb)
+  for (int grp = 0; grp < NG; ++grp) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int grp = 0; grp < 2; ++grp) {
-      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql[ks]),
-                                                      __builtin_bit_cast(bf16x8, r.kf[sb][grp][ks]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh[ks]),
-                                                      __builtin_bit_cast(bf16x8, r.kf[sb][grp][ks]), acc, 0, 0, 0);
-      }
-      const int key = it.k_lo + 32 * kAttnSub * wave + 32 * sb + 16 * grp + kl;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = 4 * g + i;
-        if (key < it.k_hi) sm.s[row][key - it.k_lo] = (key <= it.L + row) ? acc[i] * scale : -INFINITY;
-      }
+    for (int ks = 0; ks < 4; ++ks) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql[ks]),
+                                                    __builtin_bit_cast(bf16x8, r.kf[grp][ks]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh[ks]),
+                                                    __builtin_bit_cast(bf16x8, r.kf[grp][ks]), acc, 0, 0, 0);
     }
-  __syncthreads();
-  // chunk softmax, one wave per row; keys past the chunk end get p = 0
-  const int nk = it.k_hi - it.k_lo;
-  for (int row = wave; row < R; row += 8) {
-    float mx = -INFINITY;
-    for (int j = lane; j < nk; j += 64) mx = fmaxf(mx, sm.s[row][j]);
+    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * g + i;
+      sv[grp][i] = (key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
+    }
+  }
+  // row maxima: over the wave's keys, then over the waves
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float mx = sv[0][i];
+#pragma unroll
+    for (int grp = 1; grp < NG; ++grp) mx = fmaxf(mx, sv[grp][i]);
+    mx = row16_max(mx);
+    if (kl == 0) sm.pm[4 * g + i][wave] = mx;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * g + i;
+    const float4 a = *(const float4*)&sm.pm[row][0];
+    const float4 b = *(const float4*)&sm.pm[row][4];
+    const float M = fmaxf(fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)), fmaxf(fmaxf(b.x, b.y), fmaxf(b.z, b.w)));
     float sum = 0.f;
-    for (int j = lane; j < kAttnChunkB; j += 64) {
-      const float e = (j < nk && mx != -INFINITY) ? expf(sm.s[row][j] - mx) : 0.f;
-      sm.s[row][j] = e;
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp) {
+      // masked keys: exp2(-inf) = 0
+      const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[grp][i] - M) * 1.44269504088896341f);
       sum += e;
+      const uint16_t h = f2bf(e);
+      const int kc = (CK / 8) * wave + 16 * grp + kl;
+      sm.ph[row][kc] = h;
+      sm.pl[row][kc] = f2bf(e - bf2f(h));
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
-    if (lane == 0) {
-      sm.m[row] = mx;
-      sm.l[row] = sum;
-    }
+    sum = row16_sum(sum);
+    if (kl == 0) sm.ps[row][wave] = sum;
   }
   __syncthreads();
-  // O = P V over the wave's keys (sub-blocks in order)
-  floatx4 oacc[8];
+  if (tid < R) {
+    float l = 0.f, M = -INFINITY;
 #pragma unroll
-  for (int ft = 0; ft < 8; ++ft) oacc[ft] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int sb = 0; sb < kAttnSub; ++sb) {
-    uint4 ph = make_uint4(0, 0, 0, 0), pl = make_uint4(0, 0, 0, 0);
-    if (kl < R) {
-      const float* pp = &sm.s[kl][32 * kAttnSub * wave + 32 * sb + 8 * g];
-      const float4 x0 = *(const float4*)pp;
-      const float4 x1 = *(const float4*)(pp + 4);
-      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      attn_split2(xs, ph, pl);
+    for (int w = 0; w < 8; ++w) {
+      l += sm.ps[tid][w];
+      M = fmaxf(M, sm.pm[tid][w]);
     }
-#pragma unroll
-    for (int ft = 0; ft < 8; ++ft) {
-      oacc[ft] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl),
-                                                         __builtin_bit_cast(bf16x8, r.vf[sb][ft]), oacc[ft], 0, 0, 0);
-      oacc[ft] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph),
-                                                         __builtin_bit_cast(bf16x8, r.vf[sb][ft]), oacc[ft], 0, 0, 0);
-    }
+    sm.m[tid] = M;
+    sm.l[tid] = l;
   }
+  // O = P V for features 16 wave .. 16 wave + 15, key steps in order
+  floatx4 o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int ft = 0; ft < 8; ++ft)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) sm.o[wave][4 * g + i][16 * ft + kl] = oacc[ft][i];
-  __syncthreads();
-}
-
-// Unnormalised chunk output of (row, dd): the eight wave partials in order.
-__device__ __forceinline__ float attn_chunk_out(const AttnSmemB& sm, int row, int dd) {
-  float v = sm.o[0][row][dd];
-#pragma unroll
-  for (int w = 1; w < 8; ++w) v += sm.o[w][row][dd];
-  return v;
-}
-
-// Merge weights of row `row` from (m, l) pairs ml[2 * (c * R + row)]: the
-// weight of chunk c is exp(m_c - max) / sum_c(l_c exp(m_c - max)), written to
-// sc[c * R + row].
-__device__ __forceinline__ void attn_merge_weights(const float* ml, float* sc, int NC, int R, int row) {
-  float Mx = -INFINITY;
-  for (int c = 0; c < NC; ++c) Mx = fmaxf(Mx, ml[2 * (c * R + row)]);
-  float Ls = 0.f;
-  for (int c = 0; c < NC; ++c) {
-    const float mc = ml[2 * (c * R + row)];
-    const float e = (mc == -INFINITY) ? 0.f : expf(mc - Mx);
-    Ls += ml[2 * (c * R + row) + 1] * e;
-    sc[c * R + row] = e;
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const uint4 ph = *(const uint4*)&sm.ph[kl][32 * ks + 8 * g];
+    const uint4 pl = *(const uint4*)&sm.pl[kl][32 * ks + 8 * g];
+    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
+                                                0, 0, 0);
+    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
+                                                0, 0, 0);
   }
-  const float inv = 1.0f / Ls;
-  for (int c = 0; c < NC; ++c) sc[c * R + row] *= inv;
+  return o;
 }
 
 // Last-arrival merge of the chunks of one (request, head).
 struct AttnMergeSmem {
-  float ml[2 * kAttnMaxChunks * kAttnRows];  // (m, l) of every chunk, [c][row][2]
-  float sc[kAttnMaxChunks * kAttnRows];      // merge weights, [c][row]
+  float sc[kAttnMaxChunks][kAttnRows];  // merge weights
   int last;
 };
 
-// partials of output o (= row * kAttnHd + dd) for chunks 0..7 (sc1 loads)
-__device__ __forceinline__ void attn_load8(Rsrc rpo, int NC, int Rmax, int o, bool ok, float (&v)[8]) {
+// partials of output o (= row * kAttnHd + dd) for chunks c0 .. c0 + 15
+// (sc1 loads; chunks past nc and ok == false read 0)
+__device__ __forceinline__ void attn_load16(Rsrc rpo, int c0, int nc, int Rmax, int o, bool ok, float (&v)[16]) {
   const int row = o / kAttnHd, dd = o - row * kAttnHd;
 #pragma unroll
-  for (int c = 0; c < 8; ++c)
-    v[c] = ld_b32_coh(rpo, (ok && c < NC) ? (uint32_t)((c * Rmax + row) * kAttnHd + dd) * 4u : kOob);
+  for (int j = 0; j < 16; ++j) {
+    const int c = c0 + j;
+    v[j] = ld_b32_coh(rpo, (ok && c < nc) ? (uint32_t)((c * Rmax + row) * kAttnHd + dd) * 4u : kOob);
+  }
 }
 
-// weighted sum of output o over the chunks, in chunk order
-__device__ __forceinline__ float attn_merged(Rsrc rpo, const AttnMergeSmem& ms, int NC, int Rmax, int R, int o,
-                                             const float (&v)[8]) {
-  const int row = o / kAttnHd, dd = o - row * kAttnHd;
-  float O = 0.f;
+// add chunks c0 .. c0 + 15 of output o to O, in chunk order
+__device__ __forceinline__ void attn_acc16(const AttnMergeSmem& ms, int c0, int nc, int o, const float (&v)[16],
+                                           float& O) {
+  const int row = o / kAttnHd;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    if (c < NC) {
-      const float w = ms.sc[c * R + row];
-      O += w != 0.f ? v[c] * w : 0.f;
+  for (int j = 0; j < 16; ++j) {
+    const int c = c0 + j;
+    if (c < nc) {
+      const float w = ms.sc[c][row];
+      O += w != 0.f ? v[j] * w : 0.f;
     }
   }
-  for (int c = 8; c < NC; ++c) {
-    const float w = ms.sc[c * R + row];
-    const float val = ld_b32_coh(rpo, (uint32_t)((c * Rmax + row) * kAttnHd + dd) * 4u);
-    O += w != 0.f ? val * w : 0.f;
-  }
-  return O;
 }
 
-// Publish this chunk's partial with write-through stores, arrive on the
-// counter of its (request, head) once the stores have landed, and, in the
-// workgroup that arrives last, merge all chunks in chunk order (weights
-// attn_merge_weights) and pass each merged output o = row * kAttnHd + dd to
-// out(o, value).  The last arrival resets the counter.  part_o / part_ml:
-// [bh][NC][Rmax][kAttnHd] / [bh][NC][Rmax][2].  All 512 threads call it.
+// merged outputs oa and oa + 512 (each where < nout); va / vb hold their
+// chunks 0..15 on entry
 template <class Out>
-__device__ __forceinline__ void attn_publish_merge(const AttnItemB& it, const AttnSmemB& sa, AttnMergeSmem& ms,
-                                                   float* part_o, float* part_ml, uint32_t* attn_cnt, int H,
-                                                   int NC, int Rmax, int R, Out&& out) {
-  const int tid = threadIdx.x;
+__device__ __forceinline__ void attn_merge_pair(Rsrc rpo, const AttnMergeSmem& ms, int nc, int Rmax, int nout,
+                                                int oa, float (&va)[16], float (&vb)[16], Out&& out) {
+  const int ob = oa + 512;
+  float Oa = 0.f, Ob = 0.f;
+  attn_acc16(ms, 0, nc, oa, va, Oa);
+  attn_acc16(ms, 0, nc, ob, vb, Ob);
+  for (int c0 = 16; c0 < nc; c0 += 16) {
+    attn_load16(rpo, c0, nc, Rmax, oa, oa < nout, va);
+    attn_load16(rpo, c0, nc, Rmax, ob, ob < nout, vb);
+    attn_acc16(ms, c0, nc, oa, va, Oa);
+    attn_acc16(ms, c0, nc, ob, vb, Ob);
+  }
+  if (oa < nout) out(oa, Oa);
+  if (ob < nout) out(ob, Ob);
+}
+
+// Publish this chunk's partial (o: attn_chunk's result) with write-through
+// stores, arrive on the counter of its (request, head) once the stores have
+// landed, and, in the workgroup that arrives last, merge the request's
+// chunks and pass each merged output o = row * kAttnHd + dd to out(o, value).
+// Merge weights of a row: one wave, chunks over its lanes; the weight of
+// chunk c is exp(m_c - max) / sum_c(l_c exp(m_c - max)).  The last arrival
+// resets the counter.  part_o / part_ml: [bh][NC][Rmax][kAttnHd] /
+// [bh][NC][Rmax][2].  All 512 threads call it; inactive items only
+// synchronise.
+template <int CK, class Out>
+__device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o, const AttnSmem<CK>& sa,
+                                                   AttnMergeSmem& ms, float* part_o, float* part_ml,
+                                                   uint32_t* attn_cnt, int H, int NC, int Rmax, int R, Out&& out) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, kl = lane & 15;
   const size_t bh = (size_t)it.bl * H + it.h;
   if (it.active) {
-    float* po = part_o + ((bh * NC + it.c) * Rmax) * kAttnHd;
-    float* pml = part_ml + ((bh * NC + it.c) * Rmax) * 2;
-    for (int idx = tid; idx < R * kAttnHd; idx += 512) {
-      const int row = idx / kAttnHd, dd = idx - row * kAttnHd;
-      __hip_atomic_store(po + row * kAttnHd + dd, attn_chunk_out(sa, row, dd), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+    float* po = part_o + ((bh * NC + it.c) * Rmax) * kAttnHd + 16 * wave + kl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * g + i;
+      if (row < R) __hip_atomic_store(po + row * kAttnHd, o[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    float* pml = part_ml + ((bh * NC + it.c) * Rmax) * 2;
     if (tid < R) {
       __hip_atomic_store(pml + tid * 2, sa.m[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(pml + tid * 2 + 1, sa.l[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -327,8 +381,8 @@ __device__ __forceinline__ void attn_publish_merge(const AttnItemB& it, const At
     int last = 0;
     if (it.active) {
       uint32_t* cnt = attn_cnt + bh;
-      const uint32_t o = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (o == (uint32_t)NC - 1u) {
+      const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (old == (uint32_t)it.nc - 1u) {
         __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         last = 1;
       }
@@ -337,28 +391,50 @@ __device__ __forceinline__ void attn_publish_merge(const AttnItemB& it, const At
   }
   __syncthreads();
   if (!ms.last) return;  // uniform across the workgroup
-  // the (m, l) pairs and this thread's first partials in one round trip
+  const int nc = it.nc;
+  // this thread's first partials, and each row's (m, l) pairs, in one round trip
   const Rsrc rpo = wave_rsrc(part_o + (bh * NC * Rmax) * kAttnHd);
   const Rsrc rpm = wave_rsrc(part_ml + (bh * NC * Rmax) * 2);
   const int nout = R * kAttnHd;
-  float v0[8], v1[8];
-  attn_load8(rpo, NC, Rmax, tid, tid < nout, v0);
-  attn_load8(rpo, NC, Rmax, tid + 512, tid + 512 < nout, v1);
-  for (int i = tid; i < NC * R; i += 512) {
-    const int c = i / R, row = i - c * R;
-    const uint32_t off = (uint32_t)((c * Rmax + row) * 2) * 4u;
-    ms.ml[2 * i] = ld_b32_coh(rpm, off);
-    ms.ml[2 * i + 1] = ld_b32_coh(rpm, off + 4u);
+  float va[16], vb[16];
+  attn_load16(rpo, 0, nc, Rmax, tid, tid < nout, va);
+  attn_load16(rpo, 0, nc, Rmax, tid + 512, tid + 512 < nout, vb);
+  for (int row = wave; row < R; row += 8) {
+    float mc[kAttnMaxChunks / 64], lc[kAttnMaxChunks / 64];
+#pragma unroll
+    for (int j = 0; j < kAttnMaxChunks / 64; ++j) {
+      const int c = lane + 64 * j;
+      const uint32_t off = c < nc ? (uint32_t)((c * Rmax + row) * 2) * 4u : kOob;
+      const float m = ld_b32_coh(rpm, off);
+      mc[j] = c < nc ? m : -INFINITY;
+      lc[j] = ld_b32_coh(rpm, off == kOob ? kOob : off + 4u);
+    }
+    float Mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kAttnMaxChunks / 64; ++j) Mx = fmaxf(Mx, mc[j]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, off));
+    float Ls = 0.f;
+#pragma unroll
+    for (int j = 0; j < kAttnMaxChunks / 64; ++j) {
+      mc[j] = (mc[j] == -INFINITY) ? 0.f : expf(mc[j] - Mx);
+      Ls += lc[j] * mc[j];
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) Ls += __shfl_xor(Ls, off);
+    const float inv = 1.0f / Ls;
+#pragma unroll
+    for (int j = 0; j < kAttnMaxChunks / 64; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nc) ms.sc[c][row] = mc[j] * inv;
+    }
   }
   __syncthreads();
-  if (tid < R) attn_merge_weights(ms.ml, ms.sc, NC, R, tid);
-  __syncthreads();
-  if (tid < nout) out(tid, attn_merged(rpo, ms, NC, Rmax, R, tid, v0));
-  if (tid + 512 < nout) out(tid + 512, attn_merged(rpo, ms, NC, Rmax, R, tid + 512, v1));
-  for (int o = tid + 1024; o < nout; o += 512) {
-    float v[8];
-    attn_load8(rpo, NC, Rmax, o, true, v);
-    out(o, attn_merged(rpo, ms, NC, Rmax, R, o, v));
+  attn_merge_pair(rpo, ms, nc, Rmax, nout, tid, va, vb, out);
+  for (int oa = tid + 1024; oa < nout; oa += 1024) {
+    attn_load16(rpo, 0, nc, Rmax, oa, true, va);
+    attn_load16(rpo, 0, nc, Rmax, oa + 512, oa + 512 < nout, vb);
+    attn_merge_pair(rpo, ms, nc, Rmax, nout, oa, va, vb, out);
   }
 }
 

@@ -543,36 +543,30 @@ __global__ void __launch_bounds__(256) attn_combine_kernel(AttnParams p) {
   }
 }
 
-// bf16 cache, head_dim 128: chunks of kAttnChunkB keys, one 8-wave workgroup
-// per (chunk, head, request) (device_attn.h); the last chunk of a (request,
-// head) to finish merges them into the O-projection operand.
-template <bool ABF16>
-__global__ void __launch_bounds__(512) attn_b_kernel(AttnParams p) {
-  __shared__ AttnSmemB sm;
+// bf16 cache, head_dim 128: chunks of CK keys, one 8-wave workgroup per
+// (chunk, head, request) (device_attn.h); chunks past a request's last key
+// exit at once, and the last chunk of a (request, head) to finish merges them
+// into the O-projection operand.
+template <bool ABF16, int CK>
+__global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(4)))
+attn_b_kernel(AttnParams p) {
+  __shared__ AttnSmem<CK> sm;
   __shared__ AttnMergeSmem ms;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  AttnItemB it;
-  it.active = true;
-  it.c = blockIdx.x;
-  it.h = blockIdx.y;
-  it.bl = blockIdx.z;
-  const int bg = p.b0 + it.bl;
-  it.L = p.lens[bg];
-  it.k_lo = it.c * kAttnChunkB;
-  it.k_hi = min(it.k_lo + kAttnChunkB, it.L + p.R);
-  const size_t base = ((size_t)bg * p.H + it.h) * p.kv_stride * kAttnHd;
-  it.kc = (const uint16_t*)p.kc + base;
-  it.vc = (const uint16_t*)p.vc + base;
-  AttnRegsB r;
+  const int bl = blockIdx.z, h = blockIdx.y, bg = p.b0 + bl;
+  const AttnItem it = attn_item<CK>(true, bl, h, blockIdx.x, p.lens[bg], p.R, p.kc, p.vc,
+                                    ((size_t)bg * p.H + h) * p.kv_stride * kAttnHd);
+  if (!it.active) return;  // past the request's last key: uniform, before any barrier
+  float4 qr[8];
+  attn_load_q(it, p.q + (size_t)(bl * p.R) * p.d + h * kAttnHd, p.d, p.R, lane, qr);
+  AttnRegs<CK> r;
   attn_zero_regs(r);
-  if (it.k_lo < it.k_hi) {
-    attn_load_plain(it, p.kv_stride, it.k_lo, (it.k_hi + 7) & ~7, wave, lane, r);
-    attn_mask_tail(it, wave, lane, r);
-  }
-  attn_chunk(it, p.q + (size_t)(it.bl * p.R) * p.d + it.h * kAttnHd, p.d, p.R, p.scale, r, sm);
-  attn_publish_merge(it, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int o, float O) {
-    const int row = o / kAttnHd, dd = o - row * kAttnHd;
-    store_act<ABF16>(p.act_out, p.act_split, (size_t)(it.bl * p.R + row) * p.d + it.h * kAttnHd + dd, O);
+  attn_load_plain(it, p.kv_stride, it.k_lo, (it.k_hi + 7) & ~7, wave, lane, r);
+  attn_mask_tail(it, lane, r);
+  const floatx4 o = attn_chunk(it, qr, p.R, p.scale, r, sm);
+  attn_publish_merge(it, o, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
+    const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
+    store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
   });
 }
 
@@ -838,12 +832,12 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->stride * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
 
-  // attention chunks over the longest request: kAttnChunkB keys for a bf16
-  // cache with head_dim 128 (8-wave MFMA kernel), else kAttnChunk
+  // attention chunks over the longest request: for a bf16 cache with
+  // head_dim 128 the 8-wave MFMA kernel, else kAttnChunk
   int max_keys = 0;
   for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) max_keys = std::max(max_keys, kv->lens_ub[b] + fc.R);
   const bool attn_b = D.kvdt == SPADE_BF16 && D.hd == kAttnHd && fc.R <= kAttnRows;
-  const int CK = attn_b ? kAttnChunkB : kAttnChunk;
+  const int CK = attn_b ? kAttnChunkKeys : kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
 
@@ -871,8 +865,8 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     const dim3 agrid(NC, D.H, fc.nb);
     const bool kvb = D.kvdt == SPADE_BF16;
     if (attn_b) {
-      if (wb) hipLaunchKernelGGL(attn_b_kernel<true>, agrid, dim3(512), 0, st, ap);
-      else hipLaunchKernelGGL(attn_b_kernel<false>, agrid, dim3(512), 0, st, ap);
+      if (wb) hipLaunchKernelGGL((attn_b_kernel<true, kAttnChunkKeys>), agrid, dim3(kAttnThreads), 0, st, ap);
+      else hipLaunchKernelGGL((attn_b_kernel<false, kAttnChunkKeys>), agrid, dim3(kAttnThreads), 0, st, ap);
       e = hipGetLastError();
     } else if (D.hd == 64) {
       e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);

@@ -24,6 +24,12 @@ constexpr size_t kBarBytes = 4096;               // its grid-barrier words
 constexpr int kMaxStatGroups = 2048;             // LM-head statistics entries per row (workgroups)
 inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
 
+// Keys per chunk of the bf16 / head_dim-128 verify attention.  A constant:
+// a request's attention (and so its logits) must not depend on the other
+// requests of the batch.  256 keys: about 110 VGPRs and 25 KB of LDS per
+// 8-wave workgroup, two workgroups per compute unit.
+constexpr int kAttnChunkKeys = 256;
+
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 
 inline int kblock_of(int weight_dtype) { return weight_dtype == SPADE_BF16 ? 256 : 128; }

@@ -288,49 +288,47 @@ __device__ __forceinline__ bool fused_gemm(const FusedParams& P, int layer, Grid
 // it with sc1 loads.  Each chunk writes its partial (sc1), then arrives on the
 // counter of its (request, head); the last arrival merges the chunks.
 // ---------------------------------------------------------------------------
+template <int CK>
 struct FusedAttnSmem {
-  AttnSmemB a;
+  AttnSmem<CK> a;
   AttnMergeSmem ms;
 };
 
-__device__ __forceinline__ AttnItemB fused_attn_item(const FusedParams& P, int layer, int item) {
-  AttnItemB it{};
+template <int CK>
+__device__ __forceinline__ AttnItem fused_attn_item(const FusedParams& P, int layer, int item) {
   const int total = P.nb * P.H * P.NC;
-  it.active = item < total;
-  const int x = it.active ? item : 0;
-  it.c = x % P.NC;
-  const int bh = x / P.NC;
-  it.h = bh % P.H;
-  it.bl = bh / P.H;
-  it.L = P.lens[it.bl];
-  it.k_lo = it.c * kAttnChunkB;
-  it.k_hi = it.active ? min(it.k_lo + kAttnChunkB, it.L + P.R) : it.k_lo;
-  const size_t base = ((size_t)it.bl * P.H + it.h) * P.kv_stride * kAttnHd;
-  it.kc = (const uint16_t*)(P.kc + (size_t)layer * P.kv_layer_bytes) + base;
-  it.vc = (const uint16_t*)(P.vc + (size_t)layer * P.kv_layer_bytes) + base;
-  return it;
+  const bool valid = item < total;
+  const int x = valid ? item : 0;
+  const int c = x % P.NC, bh = x / P.NC;
+  const int h = bh % P.H, bl = bh / P.H;
+  return attn_item<CK>(valid, bl, h, c, P.lens[bl], P.R, P.kc + (size_t)layer * P.kv_layer_bytes,
+                       P.vc + (size_t)layer * P.kv_layer_bytes, ((size_t)bl * P.H + h) * P.kv_stride * kAttnHd);
 }
 
 // keys older than this call: plain loads (may run before the barrier)
-__device__ __forceinline__ void fused_attn_prefetch(const FusedParams& P, const AttnItemB& it, int wave, int lane,
-                                                    AttnRegsB& r) {
+template <int CK>
+__device__ __forceinline__ void fused_attn_prefetch(const FusedParams& P, const AttnItem& it, int wave, int lane,
+                                                    AttnRegs<CK>& r) {
   attn_zero_regs(r);
   if (it.active) attn_load_plain(it, P.kv_stride, it.k_lo, min(it.k_hi, it.L), wave, lane, r);
 }
 
-__device__ __forceinline__ void fused_attn_run(const FusedParams& P, int layer, const AttnItemB& it, AttnRegsB& r,
-                                               FusedAttnSmem& sm, int wave, int lane) {
+template <int CK>
+__device__ __forceinline__ void fused_attn_run(const FusedParams& P, int layer, const AttnItem& it, AttnRegs<CK>& r,
+                                               FusedAttnSmem<CK>& sm, int wave, int lane) {
   const int R = P.R;
-  if (it.active) attn_load_new(it, wave_rsrc(it.kc), wave_rsrc(it.vc), P.kv_stride, wave, lane, r);
-  attn_mask_tail(it, wave, lane, r);
   const float* q = (const float*)(P.arena + (size_t)layer * P.fa.layer_bytes + P.fa.q) +
                    (size_t)(it.bl * R) * P.d + it.h * kAttnHd;
-  attn_chunk(it, q, P.d, R, P.scale, r, sm.a);
+  float4 qr[8];
+  attn_load_q(it, q, P.d, R, lane, qr);
+  if (it.active) attn_load_new(it, wave_rsrc(it.kc), wave_rsrc(it.vc), P.kv_stride, wave, lane, r);
+  attn_mask_tail(it, lane, r);
+  const floatx4 o = attn_chunk(it, qr, R, P.scale, r, sm.a);
   // publish, arrive, and merge in the last arrival into this layer's O operand
   uint16_t* act = (uint16_t*)(P.arena + (size_t)layer * P.fa.layer_bytes + P.fa.act_o);
   const size_t split = (size_t)kFusedRows * P.d;
-  attn_publish_merge(it, sm.a, sm.ms, P.part_o, P.part_ml, P.attn_cnt, P.H, P.NC, P.Rmax, R, [&](int o, float O) {
-    const int row = o / kAttnHd, dd = o - row * kAttnHd;
+  attn_publish_merge(it, o, sm.a, sm.ms, P.part_o, P.part_ml, P.attn_cnt, P.H, P.NC, P.Rmax, R, [&](int oi, float O) {
+    const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
     const size_t e = (size_t)(it.bl * R + row) * P.d + it.h * kAttnHd + dd;
     float rem = O;
 #pragma unroll
@@ -342,20 +340,21 @@ __device__ __forceinline__ void fused_attn_run(const FusedParams& P, int layer, 
   });
 }
 
+template <int CK>
 __device__ __forceinline__ bool fused_attention(const FusedParams& P, int layer, GridSync& gs, uint8_t* lds,
                                                 int* flag) {
-  FusedAttnSmem& sm = *(FusedAttnSmem*)lds;
+  FusedAttnSmem<CK>& sm = *(FusedAttnSmem<CK>*)lds;
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = (int)threadIdx.x & 63;
   const int total = P.nb * P.H * P.NC;
   const int rounds = (total + gs.G - 1) / gs.G;
-  AttnRegsB r;
-  AttnItemB it = fused_attn_item(P, layer, gs.bid);
+  AttnRegs<CK> r;
+  AttnItem it = fused_attn_item<CK>(P, layer, gs.bid);
   sync_arrive(gs);
   fused_attn_prefetch(P, it, wave, lane, r);
   if (!sync_wait(gs, P.err, flag)) return false;
   for (int k = 0; k < rounds; ++k) {
     if (k > 0) {
-      it = fused_attn_item(P, layer, k * gs.G + gs.bid);
+      it = fused_attn_item<CK>(P, layer, k * gs.G + gs.bid);
       fused_attn_prefetch(P, it, wave, lane, r);
     }
     fused_attn_run(P, layer, it, r, sm, wave, lane);
@@ -367,7 +366,7 @@ __device__ __forceinline__ bool fused_attention(const FusedParams& P, int layer,
 // ---------------------------------------------------------------------------
 // The kernel.
 // ---------------------------------------------------------------------------
-template <bool LDS_D, bool LDS_F>
+template <bool LDS_D, bool LDS_F, int CK>
 __global__ void __launch_bounds__(kFusedThreads) verify_fused_kernel(FusedParams P) {
   extern __shared__ uint4 lds_raw[];
   uint8_t* lds = (uint8_t*)lds_raw;
@@ -378,7 +377,7 @@ __global__ void __launch_bounds__(kFusedThreads) verify_fused_kernel(FusedParams
   fused_embed(P, gs.bid, gs.G);
   for (int l = 0; l < P.L && ok; ++l) {
     ok = fused_gemm<GEMM_QKV, LDS_D>(P, l, gs, lds, &flag);
-    if (ok) ok = fused_attention(P, l, gs, lds, &flag);
+    if (ok) ok = fused_attention<CK>(P, l, gs, lds, &flag);
     if (ok) ok = fused_gemm<GEMM_O, LDS_D>(P, l, gs, lds, &flag);
     if (ok) ok = fused_gemm<GEMM_GU, LDS_D>(P, l, gs, lds, &flag);
     if (ok) ok = fused_gemm<GEMM_DOWN, LDS_F>(P, l, gs, lds, &flag);
@@ -414,9 +413,9 @@ __global__ void __launch_bounds__(kFusedThreads) verify_fused_kernel(FusedParams
 // ---------------------------------------------------------------------------
 namespace {
 
-template <bool LDS_D, bool LDS_F>
+template <bool LDS_D, bool LDS_F, int CK>
 hipError_t launch_fused_t(const FusedParams& p, int grid, uint32_t lds, hipStream_t st) {
-  const void* fn = reinterpret_cast<const void*>(&verify_fused_kernel<LDS_D, LDS_F>);
+  const void* fn = reinterpret_cast<const void*>(&verify_fused_kernel<LDS_D, LDS_F, CK>);
   static hipError_t attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFusedLdsBytes);
   if (attr != hipSuccess) return attr;
   FusedParams arg = p;
@@ -444,7 +443,8 @@ hipError_t launch_verify_fused(spade_model md, spade_kv kv, const ForwardCall& f
   const Workspace& W = md->ws;
   int max_keys = 0;
   for (int b = 0; b < fc.nb; ++b) max_keys = std::max(max_keys, kv->lens_ub[b] + fc.R);
-  const int NC = (max_keys + kAttnChunkB - 1) / kAttnChunkB;
+  constexpr int CK = kAttnChunkKeys;  // as the per-stage path
+  const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
 
   FusedParams p{};
@@ -504,16 +504,16 @@ hipError_t launch_verify_fused(spade_model md, spade_kv kv, const ForwardCall& f
   const uint32_t lds_f = gsm + gemm_lds_a_bytes(p.M, D.F, 1);
   const bool use_d = lds_d <= kFusedLdsBytes && gemm_lds_a_ok(D.d, 1);
   const bool use_f = lds_f <= kFusedLdsBytes && gemm_lds_a_ok(D.F, 1);
-  uint32_t lds = (uint32_t)std::max(sizeof(FusedAttnSmem), sizeof(AcceptSmem));
+  uint32_t lds = (uint32_t)std::max(sizeof(FusedAttnSmem<CK>), sizeof(AcceptSmem));
   lds = std::max(lds, gsm);
   if (use_d) lds = std::max(lds, lds_d);
   if (use_f) lds = std::max(lds, lds_f);
   lds = (lds + 15) / 16 * 16;
   const int grid = md->n_cu;
-  if (use_d && use_f) return launch_fused_t<true, true>(p, grid, lds, st);
-  if (use_d) return launch_fused_t<true, false>(p, grid, lds, st);
-  if (use_f) return launch_fused_t<false, true>(p, grid, lds, st);
-  return launch_fused_t<false, false>(p, grid, lds, st);
+  if (use_d && use_f) return launch_fused_t<true, true, CK>(p, grid, lds, st);
+  if (use_d) return launch_fused_t<true, false, CK>(p, grid, lds, st);
+  if (use_f) return launch_fused_t<false, true, CK>(p, grid, lds, st);
+  return launch_fused_t<false, false, CK>(p, grid, lds, st);
 }
 
 }  // namespace spade
