@@ -183,6 +183,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   // one 8-wave GEMM workgroup per compute unit (the kernel needs two waves per
   // SIMD); SPADE_GEMM_WGS overrides for experiments
   m->gemm_wgs = m->n_cu;
+  m->wide_rt = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -429,6 +430,13 @@ spade_status spade_model_set_fused(spade_model m, int enable) {
   if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, m->device) != hipSuccess || !coop)
     return fail(SPADE_EUNSUPPORTED, "device has no cooperative launch");
   m->fused_ok = true;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_wide_tiles(spade_model m, int tiles) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (tiles < -1 || tiles > 3) return fail(SPADE_EINVAL, "tiles must be -1, 0, 1, 2 or 3");
+  m->wide_rt = tiles;
   return SPADE_OK;
 }
 

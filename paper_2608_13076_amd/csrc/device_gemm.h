@@ -92,6 +92,114 @@ struct EpiIn {
   float a, b;
 };
 
+// Epilogue inputs of output (row ml of the launch, column n of unit u) for
+// the projection kinds: QKV the RoPE (cos, sin) at position pos, O / down the
+// residual x and the next RMSNorm gain.  ok == false reads nothing (zeros).
+template <int KIND, bool COH>
+__device__ __forceinline__ EpiIn gemm_epi_load(const GemmParams& a, int u, int ml, int n, bool ok, int pos) {
+  EpiIn e{0.f, 0.f};
+  if constexpr (KIND == GEMM_QKV) {
+    const int pps = a.d >> 4, pph = a.hd >> 4;
+    const int pw = u % pps;
+    const int pair = (pw % pph) * 8 + (n & 7);
+    const Rsrc rr = make_rsrc(a.rope, 0x7ffffff0u);
+    const float2 cs = ld_f32x2<false>(rr, ok ? (uint32_t)((pos * (a.hd >> 1) + pair) * 2) * 4u : kOob);
+    e.a = cs.x;
+    e.b = cs.y;
+  } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
+    const int col = u * 16 + n;
+    const Rsrc rx = make_rsrc(a.x + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
+    const Rsrc rg = make_rsrc(a.g_next, (uint32_t)(a.d * 4));
+    e.a = ld_f32<COH>(rx, ok ? (uint32_t)(ml * a.d + col) * 4u : kOob);
+    e.b = ld_f32<false>(rg, ok ? (uint32_t)col * 4u : kOob);
+  }
+  return e;
+}
+
+// Epilogue of output (row ml of the launch, column n of unit u) for the
+// projection kinds QKV, O, gate/up and down: val is the full dot product,
+// rinv the row's 1/rms, e its gemm_epi_load inputs; rok == false stores
+// nothing.  D[i][j] of a 16x16 MFMA sits in lane j + 16*(i/4), register i%4,
+// so the 16 columns of a row are 16 consecutive lanes: every lane of the wave
+// calls it (RoPE and SwiGLU partners are lanes n and n^8, the row's sum of
+// squares runs over the 16 lanes).
+template <int KIND, bool WBF16, bool COH>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int u, int ml, int n, bool rok, int pos, int bg,
+                                              float rinv, float val, const EpiIn& e) {
+  constexpr uint32_t ELT = WBF16 ? 2u : 4u;
+  constexpr int S = WBF16 ? kActSplits : 1;
+  if constexpr (KIND == GEMM_QKV) {
+    const int pps = a.d >> 4, pph = a.hd >> 4;
+    const int sec = u / pps, pw = u - sec * pps;
+    const int h = pw / pph, wg = pw - h * pph;
+    const int pair = wg * 8 + (n & 7);
+    const bool hi = n >= 8;
+    const int f = pair + (hi ? (a.hd >> 1) : 0);
+    float v = val * rinv;
+    const float pv = __shfl_xor(v, 8);  // the RoPE partner
+    const bool rot = sec < 2;
+    const float c = rot ? e.a : 1.f, sn = rot ? e.b : 0.f;
+    v = hi ? (pv * sn + v * c) : (v * c - pv * sn);
+    const Rsrc rq = make_rsrc(a.q_out + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
+    st_f32<COH>(rq, (rok && sec == 0) ? (uint32_t)(ml * a.d + h * a.hd + f) * 4u : kOob, v);
+    // K rows [pos][hd]; V transposed, rows [feature][stride]
+    const uint32_t head = (uint32_t)(bg * a.H + h) * (uint32_t)a.kv_stride * (uint32_t)a.hd;
+    const uint32_t elem = sec == 1 ? head + (uint32_t)(pos * a.hd + f) : head + (uint32_t)(f * a.kv_stride + pos);
+    const Rsrc rkv = make_rsrc(sec == 1 ? a.kc : a.vc, a.kv_bytes);
+    const bool kok = rok && sec > 0;
+    if (a.kv_bf16) st_b16<COH>(rkv, kok ? elem * 2u : kOob, f2bf(v));
+    else st_f32<COH>(rkv, kok ? elem * 4u : kOob, v);
+  } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
+    const int col = u * 16 + n;
+    const float xv = e.a + val;
+    const Rsrc rx = make_rsrc(a.x + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
+    st_f32<COH>(rx, rok ? (uint32_t)(ml * a.d + col) * 4u : kOob, xv);
+    const uint32_t split_b = (uint32_t)(a.act_out_split * ELT);
+    const Rsrc ro = make_rsrc((const uint8_t*)a.act_out + (size_t)a.m0 * a.act_out_stride * ELT,
+                              (uint32_t)((S - 1) * (size_t)split_b + (size_t)a.M * a.act_out_stride * ELT));
+    st_act<WBF16, COH>(ro, split_b, (uint32_t)(ml * a.act_out_stride + col), rok, xv * e.b);
+    float sq = rok ? xv * xv : 0.f;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off);
+    const Rsrc rs = make_rsrc(a.ssq_out + (size_t)a.m0 * a.n_ssq_out, (uint32_t)((size_t)a.M * a.n_ssq_out * 4));
+    st_f32<COH>(rs, (rok && n == 0) ? (uint32_t)(ml * a.n_ssq_out + u) * 4u : kOob, sq);
+  } else if constexpr (KIND == GEMM_GU) {
+    const float v = val * rinv;
+    const float up = __shfl_xor(v, 8);
+    const float act = v / (1.0f + expf(-v)) * up;
+    const uint32_t split_b = (uint32_t)(a.act_out_split * ELT);
+    const Rsrc ro = make_rsrc((const uint8_t*)a.act_out + (size_t)a.m0 * a.act_out_stride * ELT,
+                              (uint32_t)((S - 1) * (size_t)split_b + (size_t)a.M * a.act_out_stride * ELT));
+    st_act<WBF16, COH>(ro, split_b, (uint32_t)(ml * a.act_out_stride + u * 8 + n), rok && n < 8, act);
+  }
+}
+
+// 1/rms of launch row `row` from the producer's per-16-column sums of
+// squares: the sixteen threads sub = 0..15 of a row sum partials sub, sub + 16,
+// ... in that order, then combine in a butterfly (all sixteen get the
+// result).  Rows past M and launches without partials get 1.
+__device__ __forceinline__ float gemm_row_rinv(const GemmParams& a, int row, int sub) {
+  float s = 0.f;
+  if (a.ssq_in != nullptr) {
+    const Rsrc rs = make_rsrc(a.ssq_in + (size_t)a.m0 * a.n_ssq, (uint32_t)((size_t)a.M * a.n_ssq * 4));
+    const uint32_t base = (uint32_t)(row * a.n_ssq) * 4u;
+    const bool rok = row < a.M;
+    for (int q0 = sub; q0 < a.n_ssq; q0 += 256) {
+      float v[16];
+#pragma unroll
+      for (int f = 0; f < 16; ++f) {
+        const int q = q0 + f * 16;
+        v[f] = ld_f32<false>(rs, (rok && q < a.n_ssq) ? base + (uint32_t)q * 4u : kOob);
+      }
+#pragma unroll
+      for (int f = 0; f < 16; ++f) s += v[f];
+    }
+  }
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+  return (a.ssq_in != nullptr && row < a.M) ? 1.0f / sqrtf(s * a.inv_din + a.eps) : 1.0f;
+}
+
 // WBF16: bf16 weights (else f32); MT: 16-row tiles of activations (1 or 2);
 // ALDS: activation operand copied to LDS once (MT == 1); COH: every output is
 // a write-through (sc1) store and the residual stream is read with sc1 loads.
@@ -242,25 +350,7 @@ struct Gemm {
 
   // epilogue inputs of the unit of item t
   __device__ __forceinline__ EpiIn epi_load(int t) const {
-    EpiIn e{0.f, 0.f};
-    const int u = bid + (t / nkw) * G;
-    const bool ok = rok && t < T;
-    if constexpr (KIND == GEMM_QKV) {
-      const int pps = a.d >> 4, pph = a.hd >> 4;
-      const int pw = u % pps;
-      const int pair = (pw % pph) * 8 + (n & 7);
-      const Rsrc rr = make_rsrc(a.rope, 0x7ffffff0u);
-      const float2 cs = ld_f32x2<false>(rr, ok ? (uint32_t)((pos * (a.hd >> 1) + pair) * 2) * 4u : kOob);
-      e.a = cs.x;
-      e.b = cs.y;
-    } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
-      const int col = u * 16 + n;
-      const Rsrc rx = make_rsrc(a.x + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
-      const Rsrc rg = make_rsrc(a.g_next, (uint32_t)(a.d * 4));
-      e.a = ld_f32<COH>(rx, ok ? (uint32_t)(ml * a.d + col) * 4u : kOob);
-      e.b = ld_f32<false>(rg, ok ? (uint32_t)col * 4u : kOob);
-    }
-    return e;
+    return gemm_epi_load<KIND, COH>(a, bid + (t / nkw) * G, ml, n, rok && t < T, pos);
   }
 
   __device__ __forceinline__ void mma(const uint4 (&w)[8], const uint4 (&x)[MT][S][8]) {
@@ -289,49 +379,8 @@ struct Gemm {
   // register i%4.
   __device__ __forceinline__ void epilogue(int u, float val, const EpiIn& e) {
     const float rinv = sm.rinv[ml];
-    if constexpr (KIND == GEMM_QKV) {
-      const int pps = a.d >> 4, pph = a.hd >> 4;
-      const int sec = u / pps, pw = u - sec * pps;
-      const int h = pw / pph, wg = pw - h * pph;
-      const int pair = wg * 8 + (n & 7);
-      const bool hi = n >= 8;
-      const int f = pair + (hi ? (a.hd >> 1) : 0);
-      float v = val * rinv;
-      const float pv = __shfl_xor(v, 8);  // the RoPE partner
-      const bool rot = sec < 2;
-      const float c = rot ? e.a : 1.f, sn = rot ? e.b : 0.f;
-      v = hi ? (pv * sn + v * c) : (v * c - pv * sn);
-      const Rsrc rq = make_rsrc(a.q_out + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
-      st_f32<COH>(rq, (rok && sec == 0) ? (uint32_t)(ml * a.d + h * a.hd + f) * 4u : kOob, v);
-      // K rows [pos][hd]; V transposed, rows [feature][stride]
-      const uint32_t head = (uint32_t)(bg * a.H + h) * (uint32_t)a.kv_stride * (uint32_t)a.hd;
-      const uint32_t elem = sec == 1 ? head + (uint32_t)(pos * a.hd + f) : head + (uint32_t)(f * a.kv_stride + pos);
-      const Rsrc rkv = make_rsrc(sec == 1 ? a.kc : a.vc, a.kv_bytes);
-      const bool kok = rok && sec > 0;
-      if (a.kv_bf16) st_b16<COH>(rkv, kok ? elem * 2u : kOob, f2bf(v));
-      else st_f32<COH>(rkv, kok ? elem * 4u : kOob, v);
-    } else if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
-      const int col = u * 16 + n;
-      const float xv = e.a + val;
-      const Rsrc rx = make_rsrc(a.x + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
-      st_f32<COH>(rx, rok ? (uint32_t)(ml * a.d + col) * 4u : kOob, xv);
-      const uint32_t split_b = (uint32_t)(a.act_out_split * ELT);
-      const Rsrc ro = make_rsrc((const uint8_t*)a.act_out + (size_t)a.m0 * a.act_out_stride * ELT,
-                                (uint32_t)((S - 1) * (size_t)split_b + (size_t)a.M * a.act_out_stride * ELT));
-      st_act<WBF16, COH>(ro, split_b, (uint32_t)(ml * a.act_out_stride + col), rok, xv * e.b);
-      float sq = rok ? xv * xv : 0.f;
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) sq += __shfl_xor(sq, off);
-      const Rsrc rs = make_rsrc(a.ssq_out + (size_t)a.m0 * a.n_ssq_out, (uint32_t)((size_t)a.M * a.n_ssq_out * 4));
-      st_f32<COH>(rs, (rok && n == 0) ? (uint32_t)(ml * a.n_ssq_out + u) * 4u : kOob, sq);
-    } else if constexpr (KIND == GEMM_GU) {
-      const float v = val * rinv;
-      const float up = __shfl_xor(v, 8);
-      const float act = v / (1.0f + expf(-v)) * up;
-      const uint32_t split_b = (uint32_t)(a.act_out_split * ELT);
-      const Rsrc ro = make_rsrc((const uint8_t*)a.act_out + (size_t)a.m0 * a.act_out_stride * ELT,
-                                (uint32_t)((S - 1) * (size_t)split_b + (size_t)a.M * a.act_out_stride * ELT));
-      st_act<WBF16, COH>(ro, split_b, (uint32_t)(ml * a.act_out_stride + u * 8 + n), rok && n < 8, act);
+    if constexpr (KIND != GEMM_LM) {
+      gemm_epilogue<KIND, WBF16, COH>(a, u, ml, n, rok, pos, bg, rinv, val, e);
     } else {  // GEMM_LM: logits and the panel's (max, sum exp, argmax) of z = logit / T
       const int col = u * 16 + n;
       const bool valid = rok && col < a.V;

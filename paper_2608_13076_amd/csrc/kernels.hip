@@ -26,6 +26,7 @@
 #include "device_accept.h"
 #include "device_attn.h"
 #include "device_gemm.h"
+#include "device_gemm_wide.h"
 
 #include <float.h>
 #include <math.h>
@@ -111,6 +112,19 @@ __global__ void __launch_bounds__(kGemmWaves * 64) gemm_kernel(GemmParams a) {
   extern __shared__ uint4 lds_dyn[];
   Gemm<WBF16, MT, ALDS, KIND, false> g(a, sm, (uint8_t*)lds_dyn, (int)blockIdx.x, (int)gridDim.x);
   g.prefetch();
+  g.run();
+}
+
+// Wide-row projection GEMM (device_gemm_wide.h): workgroup b runs on XCD
+// b % 8 and takes unit group b % 8 + 8 (q / NRG), row group q % NRG with
+// q = b / 8, so the row groups of a unit group share that XCD's L2.
+template <int RT, int KIND>
+__global__ void __launch_bounds__(kGemmWaves * 64) gemm_wide_kernel(GemmParams a, int NRG, int NUG) {
+  extern __shared__ uint4 lds_dyn[];
+  const int b = (int)blockIdx.x, q = b >> 3;
+  const int ug = (b & 7) + 8 * (q / NRG), rg = q % NRG;
+  if (ug >= NUG) return;  // uniform, before any barrier
+  GemmWide<RT, KIND> g(a, *(GemmWideSmem<RT>*)lds_dyn, ug, rg);
   g.run();
 }
 
@@ -679,6 +693,43 @@ hipError_t launch_gemm(int kind, const GemmParams& gp, int grid, int mt, hipStre
   }
 }
 
+template <int RT, int KIND>
+hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, hipStream_t st) {
+  const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, KIND>);
+  const uint32_t lds = gemm_wide_lds_bytes(RT);
+  static hipError_t attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr != hipSuccess) return attr;
+  const int grid = 8 * ((nug + 7) / 8) * nrg;
+  hipLaunchKernelGGL((gemm_wide_kernel<RT, KIND>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp, nrg, nug);
+  return hipGetLastError();
+}
+
+template <int KIND>
+hipError_t launch_wide_kind(const GemmParams& gp, int rt, int nrg, int nug, hipStream_t st) {
+  if (rt == 3) return launch_wide_rt<3, KIND>(gp, nrg, nug, st);
+  if (rt == 2) return launch_wide_rt<2, KIND>(gp, nrg, nug, st);
+  return launch_wide_rt<1, KIND>(gp, nrg, nug, st);
+}
+
+// All rows of a bf16 projection in one launch: row tiles per workgroup, the
+// largest of 3, 2, 1 that still gives a workgroup per compute unit (else 1).
+hipError_t launch_wide(int kind, const GemmParams& gp, int n_cu, int fixed_rt, hipStream_t st) {
+  const int nug = (gp.n_units + kGemmWaves - 1) / kGemmWaves;
+  int rt = fixed_rt > 0 ? fixed_rt : 1;
+  for (int c = 3; c >= 2 && fixed_rt <= 0; --c)
+    if ((long)nug * gemm_wide_row_groups(gp.M, c) >= n_cu) {
+      rt = c;
+      break;
+    }
+  const int nrg = gemm_wide_row_groups(gp.M, rt);
+  switch (kind) {
+    case GEMM_QKV: return launch_wide_kind<GEMM_QKV>(gp, rt, nrg, nug, st);
+    case GEMM_O: return launch_wide_kind<GEMM_O>(gp, rt, nrg, nug, st);
+    case GEMM_GU: return launch_wide_kind<GEMM_GU>(gp, rt, nrg, nug, st);
+    default: return launch_wide_kind<GEMM_DOWN>(gp, rt, nrg, nug, st);
+  }
+}
+
 template <int HD, int RMAX>
 hipError_t launch_attn_r(const AttnParams& ap, bool kvbf16, bool abf16, dim3 grid, hipStream_t st) {
   if (kvbf16 && abf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, true, true>), grid, dim3(256), 0, st, ap);
@@ -784,6 +835,19 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   }
   const int grid = std::min(units, md->gemm_wgs);
   g.NU = grid;  // LM head: one statistics entry per workgroup and row
+  if (wb && kind != GEMM_LM && M > kWideMinRows && md->wide_rt >= 0) {
+    // batched rows: every row in one launch, weights streamed once
+    GemmParams gp = g;
+    gp.w = wmat;
+    gp.NKB = K / KBd;
+    gp.n_units = units;
+    gp.M = M;
+    gp.m0 = 0;
+    gp.act = act;
+    gp.act_split = act_split;
+    gp.act_stride = K;
+    return launch_wide(kind, gp, md->n_cu, md->wide_rt, st);
+  }
   for (int m0 = 0; m0 < M; m0 += kMaxRowsPerGemm) {
     GemmParams gp = g;
     gp.w = wmat;

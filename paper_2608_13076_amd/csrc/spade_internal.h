@@ -12,7 +12,8 @@ namespace spade {
 
 constexpr int kPanel = 16;           // weight rows per MFMA tile (one panel)
 constexpr int kTileBytes = 8192;     // one panel x one k-block, in the arena
-constexpr int kMaxRowsPerGemm = 32;  // rows handled by one GEMM launch
+constexpr int kMaxRowsPerGemm = 32;  // rows handled by one skinny-GEMM launch
+constexpr int kWideMinRows = 16;     // bf16 projections with more rows use the wide-row GEMM
 constexpr int kPrefillRows = 16;     // tokens per prefill forward
 constexpr int kMaxR = 16;            // rows per request in one forward (gamma <= 15)
 constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
@@ -145,6 +146,7 @@ struct spade_model_s {
   int n_cu;      // compute units of the device
   int gemm_wgs;  // persistent GEMM workgroups
   bool fused_ok; // cooperative launches available and the single-launch verify pass enabled
+  int wide_rt;   // 16-row tiles per workgroup of the wide-row GEMM: 0 chosen per launch, 1..3 fixed, -1 off
 };
 
 struct spade_kv_s {

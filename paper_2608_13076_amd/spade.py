@@ -30,7 +30,7 @@ EXPORTED = (
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
     "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
-    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused",
+    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles",
 )
 
 
@@ -86,6 +86,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_profile_gemm": (I, [P, P, I, I, I, I, P]),
         "spade_get_device_error": (I, [P, P, P]),
         "spade_model_set_fused": (I, [P, I]),
+        "spade_model_set_wide_tiles": (I, [P, I]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
         "spade_kv_destroy": (None, [P]),
@@ -168,6 +169,11 @@ class Model:
         """Single persistent launch per verify call where the shape allows it
         (default), or one kernel per stage."""
         _check(self.lib.spade_model_set_fused(self.handle, 1 if enable else 0))
+
+    def set_wide_tiles(self, tiles: int) -> None:
+        """16-row tiles per workgroup of the batched projections: 0 chosen per
+        launch, 1..3 fixed, -1 skinny engine once per 32 rows."""
+        _check(self.lib.spade_model_set_wide_tiles(self.handle, int(tiles)))
 
     def device_error(self) -> int:
         v = ctypes.c_uint32()

@@ -1,0 +1,53 @@
+"""Batched verification on the wide-row GEMM (more than 16 rows, bf16).
+
+Every row tiling of the wide-row engine (1, 2 or 3 sixteen-row tiles per
+workgroup, and the per-launch choice) must give bit-for-bit the logits,
+n_accepted and corrections of the skinny engine run once per 32 rows: both sum
+each dot product over the same eight k-ranges in the same order.  The
+per-launch choice is also compared with the oracle to the usual bar, at 35
+rows (B=5, gamma 6) and at 144 rows (B=16, gamma 8, the batched-serving
+shape).
+"""
+
+import numpy as np
+import pytest
+
+from synth import ModelWeights, make_inputs, mini_workloads
+from tests.helpers import LOGIT_TOL, compare, gpu_prefill, gpu_setup, gpu_verify, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _wide_workloads():
+    base = {w.name: w for w in mini_workloads()}["mini_bf16_wide_b5"]
+    return [base, base.with_(name="mini_bf16_wide_b16", batch=16, gamma=8, ctx=(20, 600), seed=2016)]
+
+
+@pytest.mark.parametrize("w", _wide_workloads(), ids=lambda w: w.name)
+def test_wide_tilings_bit_identical_and_match_oracle(w):
+    weights = ModelWeights(w.model, w.seed)
+    inp = make_inputs(w)
+    orun = oracle_run(w, inp, weights=weights)  # also completes the chain drafts
+    model, kv = gpu_setup(w, weights)
+    gpu_prefill(kv, inp)
+    runs = {}
+    for tiles in (-1, 1, 2, 3, 0):
+        print(f"[{w.name}] M={w.batch * (w.gamma + 1)} wide tiles {tiles}", flush=True)
+        model.set_wide_tiles(tiles)
+        runs[tiles] = gpu_verify(model, kv, inp)[:3]
+    ref = runs[-1]
+    for tiles, (lg, n, c) in runs.items():
+        assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), tiles
+        assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), tiles
+    p = compare(orun, *runs[0])
+    print(f"[{w.name}] logit err {p.logit_err:.2e}, n {runs[0][1].tolist()}", flush=True)
+    assert p.logit_err < LOGIT_TOL[w.model.weight_dtype]
+    assert not p.stable_n_fail and not p.stable_corr_fail, p
+    assert model.device_error() == 0
