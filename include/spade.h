@@ -217,19 +217,22 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma,
  * early. */
 spade_status spade_model_set_fused(spade_model m, int enable);
 
-/* Row tiling of the batched projections.  A verify call with more than 16
- * rows (B * (gamma + 1) > 16) and bf16 weights runs the QKV, O, gate/up and
- * down projections on the wide-row GEMM: each weight tile is read once per
- * launch and multiplied with `tiles` 16-row tiles of the activations held in
- * LDS, the row groups of one set of panels running on one XCD so that they
- * share its L2.  tiles = 0 (the default) picks 3, 2 or 1 per launch, the
- * largest that still gives every compute unit a workgroup; 1..3 fixes it;
- * -1 turns the wide-row GEMM off (the skinny engine then runs once per 32
- * rows and streams the weights once per launch).  Results are bit-for-bit
- * the same under every setting: a row's dot products are summed over the same
- * k-ranges in the same order whatever the tiling.  Other values return
- * SPADE_EINVAL. */
-spade_status spade_model_set_wide_tiles(spade_model m, int tiles);
+/* Tiling of the batched projections.  A verify call with more than 16 rows
+ * (B * (gamma + 1) > 16) and bf16 weights runs the QKV, O, gate/up and down
+ * projections on the wide-row GEMM: each weight tile is read once per launch
+ * and multiplied with `row_tiles` 16-row tiles of the activations held in
+ * LDS; each wave owns `panels` 16-column weight panels, so that every
+ * activation fragment read from LDS feeds that many matrix instructions.  The
+ * row groups of one set of panels run on one XCD and share its L2.
+ * row_tiles = 0 and panels = 0 (the defaults) are chosen per launch from the
+ * shape and the compute-unit count; row_tiles 1..3 and panels 1..2 fix them
+ * (two panels per wave with at most two row tiles);
+ * row_tiles = -1 turns the wide-row GEMM off (the skinny engine then runs
+ * once per 32 rows and streams the weights once per launch).  Results are
+ * bit-for-bit the same under every setting: a row's dot products are summed
+ * over the same k-ranges in the same order whatever the tiling.  Other values
+ * return SPADE_EINVAL. */
+spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels);
 
 /* Context update after spade_verify (Algorithm 1: append the k accepted
  * tokens and the correction, m <- m + k + 1): lens[b] += n_accepted[b] + 1 and

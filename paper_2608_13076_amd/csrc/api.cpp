@@ -184,6 +184,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   // SIMD); SPADE_GEMM_WGS overrides for experiments
   m->gemm_wgs = m->n_cu;
   m->wide_rt = 0;
+  m->wide_p = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -433,10 +434,13 @@ spade_status spade_model_set_fused(spade_model m, int enable) {
   return SPADE_OK;
 }
 
-spade_status spade_model_set_wide_tiles(spade_model m, int tiles) {
+spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels) {
   if (!m) return fail(SPADE_EINVAL, "null model");
-  if (tiles < -1 || tiles > 3) return fail(SPADE_EINVAL, "tiles must be -1, 0, 1, 2 or 3");
-  m->wide_rt = tiles;
+  if (row_tiles < -1 || row_tiles > 3) return fail(SPADE_EINVAL, "row_tiles must be -1, 0, 1, 2 or 3");
+  if (panels < 0 || panels > 2) return fail(SPADE_EINVAL, "panels must be 0, 1 or 2");
+  if (panels == 2 && row_tiles == 3) return fail(SPADE_EINVAL, "two panels per wave take at most two row tiles");
+  m->wide_rt = row_tiles;
+  m->wide_p = panels;
   return SPADE_OK;
 }
 

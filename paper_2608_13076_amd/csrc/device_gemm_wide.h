@@ -2,17 +2,25 @@
 // activation operand has more rows than the skinny engine (device_gemm.h)
 // keeps resident: batched verification, M = B (gamma + 1) up to 256 rows.
 //
-// A workgroup of 8 waves owns 8 consecutive panels ("units"), one per wave,
-// and a group of RT 16-row tiles.  Each wave streams its panel's k-blocks
-// (8 KB weight tiles) through the same three-deep register pipeline as the
-// skinny engine and multiplies every tile with all RT row tiles.  The
-// activation k-block (RT * 16 rows x 256 k, two bf16 terms) is shared by the
-// eight waves through a two-slot LDS ring: each thread loads its share of
-// k-block kb + 3 into registers (two staging sets), writes k-block kb + 1
-// into the free slot after the MFMAs of kb, and one barrier per k-block
-// publishes it.  The loads of a step are issued activation first, weights
-// second, so the wait for the activation block never waits for a weight tile
-// issued after it.
+// A workgroup of 8 waves owns 8P consecutive panels ("units"), P per wave,
+// and a group of RT 16-row tiles.  Each wave streams its panels' k-blocks
+// (8 KB weight tiles each) through a register pipeline (3 k-blocks deep for
+// one panel, 2 for two) and multiplies every tile with all RT row tiles; each
+// activation fragment read from LDS feeds P MFMAs.  The activation k-blocks
+// (RT * 16 rows x 256 k, two bf16 terms) pass through a three-slot LDS ring
+// filled by direct buffer->LDS loads, two k-blocks ahead: right after the
+// barrier that ends every wave's reads of the slot k-block kb - 1 used,
+// k-block kb + 2 is requested into it, so a fill has two k-blocks of MFMAs to
+// land.  Rows of the ring are 512 bytes with their 16-byte chunks
+// XOR-swizzled by the row (chunk c of row r holds k-chunk c ^ (r % 16)), so
+// the 16 rows of a fragment read hit distinct banks.
+//
+// The ring is read with inline-asm ds_read_b128 and explicit lgkmcnt waits
+// tied to the fragment registers: the compiler, seeing LDS reads while a
+// direct-to-LDS load is outstanding, would otherwise wait for every such load
+// before the first read and expose each fill's latency.  Each wave instead
+// waits (vmcnt) for its own share of k-block kb, then the barrier publishes
+// the whole block.
 //
 // Row groups of the same panels run on the same XCD (workgroup b goes to XCD
 // b % 8 and takes unit group b % 8 + 8 j), so a weight tile read by the first
@@ -22,37 +30,53 @@
 // of a panel are summed over the same eight k-ranges (range w: k-blocks
 // [NKB w / 8, NKB (w + 1) / 8)), each range with a fresh MFMA accumulator in
 // the same instruction order, and the range partials are added in range
-// order.  A row's result does not depend on the engine or on the other rows.
+// order.  A row's result does not depend on the engine, the tiling or the
+// other rows.
 #pragma once
 
 #include "device_gemm.h"
 
+#include <utility>
+
 namespace spade {
 
-constexpr int kWideRowBytes = 256 * 2 + 16;  // one row of one split of a k-block in LDS (+16 B pad)
+constexpr int kWideSlots = 3;  // activation ring slots (k-blocks)
 
 template <int RT>
 struct GemmWideSmem {
-  uint8_t ring[2][kActSplits][RT * 16][kWideRowBytes];
+  uint8_t ring[kWideSlots][kActSplits][RT * 16][512];
   float rinv[RT * 16];
 };
 
-template <int RT, int KIND>
+// s_waitcnt that waits for vector memory counts <= n only (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt and lgkmcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int RT, int P, int KIND>
 struct GemmWide {
   static constexpr int S = kActSplits;
-  static constexpr int NST = 2 * RT;  // 16-byte activation chunks per thread and k-block
+  static constexpr int D = P == 1 ? 4 : 2;  // weight pipeline depth in k-blocks
+  static constexpr int PERIOD = D == 4 ? 12 : 6;  // lcm(D, kWideSlots): steps per loop iteration
+  static constexpr int NFILL = 2 * RT;      // direct LDS loads per wave and k-block
+  static_assert(S == 2, "the ring fill gives splits to waves 0-3 and 4-7");
 
   const GemmParams& a;
   GemmWideSmem<RT>& sm;
   int tid, lane, wave, g, kl;
-  int u;        // this wave's unit
-  bool uok;     // the unit exists
-  int row0;     // first launch row of the row group
-  int NKB, Tpad;
-  Rsrc ra[S];
-  uint4 w0[8], w1[8], w2[8];
-  uint4 st0[NST], st1[NST];
-  floatx4 acc[RT], tot[RT];
+  int ubase;  // first unit of this wave
+  int row0;   // first launch row of the row group
+  int NKB;
+  Rsrc rfill;  // this wave's split of the operand
+  uint32_t lds_ring;  // LDS byte address of the ring
+  uint32_t aoff[4];   // this lane's fragment offsets within a slot (slice j: aoff[j % 4] + 256 (j / 4))
+  uint4 wset[D][P][8];
+  floatx4 acc[RT][P], tot[RT][P];
   int rnext, bnd;  // next k-range index and the k-block its range starts at
 
   __device__ __forceinline__ GemmWide(const GemmParams& a_, GemmWideSmem<RT>& sm_, int ug, int rg)
@@ -62,79 +86,141 @@ struct GemmWide {
     wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     g = lane >> 4;
     kl = lane & 15;
-    u = ug * kGemmWaves + wave;
-    uok = u < a.n_units;
+    ubase = (ug * kGemmWaves + wave) * P;
     row0 = rg * RT * 16;
     NKB = a.NKB;
-    Tpad = (NKB + 5) / 6 * 6;
+    lds_ring = (uint32_t)(size_t)(__attribute__((address_space(3))) void*)&sm.ring[0][0][0][0];
 #pragma unroll
-    for (int s = 0; s < S; ++s)
-      ra[s] = make_rsrc((const uint8_t*)a.act + ((size_t)s * a.act_split + (size_t)a.m0 * a.act_stride) * 2,
-                        (uint32_t)((size_t)a.M * a.act_stride * 2));
+    for (int t = 0; t < 4; ++t) aoff[t] = (uint32_t)(kl * 512 + 64 * (t ^ (kl >> 2)) + 16 * (g ^ (kl & 3)));
+    const int s = wave >> 2;
+    rfill = make_rsrc((const uint8_t*)a.act + ((size_t)s * a.act_split + (size_t)a.m0 * a.act_stride) * 2,
+                      (uint32_t)((size_t)a.M * a.act_stride * 2));
 #pragma unroll
-    for (int mt = 0; mt < RT; ++mt) {
-      acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      tot[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int mt = 0; mt < RT; ++mt)
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        acc[mt][p] = floatx4{0.f, 0.f, 0.f, 0.f};
+        tot[mt][p] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
     rnext = 1;
     bnd = NKB / kGemmWaves;
     while (bnd == 0 && rnext < kGemmWaves) bnd = (NKB * ++rnext) / kGemmWaves;
   }
 
-  // weight tile of k-block kb of this wave's unit (zeros past the panel or
+  // weight tiles of k-block kb of this wave's units (zeros past the panel or
   // for a missing unit)
-  __device__ __forceinline__ void issue_w(int kb, uint4 (&w)[8]) const {
-    const bool ok = uok && kb < NKB;
-    const uint8_t* tile = a.w + ((size_t)(ok ? u : 0) * NKB + (ok ? kb : 0)) * kTileBytes;
-    const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
+  __device__ __forceinline__ void issue_w(int kb, uint4 (&w)[P][8]) const {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) w[j] = ld_b128<false>(r, (uint32_t)(lane * 16 + j * 1024));
-  }
-
-  // this thread's chunks of activation k-block kb: chunk c = tid + 512 i is
-  // (split s, row r, 16-byte column kc); rows past M and k-blocks past NKB
-  // read zeros
-  __device__ __forceinline__ void issue_a(int kb, uint4 (&st)[NST]) const {
+    for (int p = 0; p < P; ++p) {
+      const int u = ubase + p;
+      const bool ok = u < a.n_units && kb < NKB;
+      const uint8_t* tile = a.w + ((size_t)(ok ? u : 0) * NKB + (ok ? kb : 0)) * kTileBytes;
+      const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
 #pragma unroll
-    for (int i = 0; i < NST; ++i) {
-      const int c = tid + 512 * i;
-      const int s = c / (RT * 512), rem = c - s * (RT * 512);
-      const int r = rem >> 5, kc = rem & 31;
-      const int row = row0 + r;
-      const bool ok = row < a.M && kb < NKB;
-      const uint32_t off = ok ? (uint32_t)(row * a.act_stride + kb * 256 + kc * 8) * 2u : kOob;
-      st[i] = ld_b128<false>(s == 0 ? ra[0] : ra[S - 1], off);
+      for (int j = 0; j < 8; ++j) w[p][j] = ld_b128<false>(r, (uint32_t)(lane * 16 + j * 1024));
     }
   }
 
-  __device__ __forceinline__ void store_a(int slot, const uint4 (&st)[NST]) {
+  // Request activation k-block kb into ring slot `slot`.  Waves 0-3 move
+  // split 0 and waves 4-7 split 1; one load instruction moves two rows (lane
+  // l: row 2 rp + l / 32, LDS chunk l % 32).  Rows past M repeat row M - 1
+  // and k-blocks past the panel repeat the last one: finite values whose
+  // products are never stored (rows) or meet zero weights (k-blocks).
+  __device__ __forceinline__ void fill(int kb, int slot) const {
+    const int s = wave >> 2;
+    const int kbc = kb < NKB ? kb : NKB - 1;
+    const int c = lane & 31;
 #pragma unroll
-    for (int i = 0; i < NST; ++i) {
-      const int c = tid + 512 * i;
-      const int s = c / (RT * 512), rem = c - s * (RT * 512);
-      const int r = rem >> 5, kc = rem & 31;
-      *(uint4*)&sm.ring[slot][s][r][kc * 16] = st[i];
+    for (int i = 0; i < NFILL; ++i) {
+      const int rp = (wave & 3) + 4 * i;
+      const int row = 2 * rp + (lane >> 5);
+      const int grow = row0 + row < a.M ? row0 + row : a.M - 1;
+      const int gc = c ^ (row & 15);
+      const uint32_t off = (uint32_t)(grow * a.act_stride + kbc * 256 + gc * 8) * 2u;
+      __attribute__((address_space(3))) void* dst =
+          (__attribute__((address_space(3))) void*)&sm.ring[slot][s][2 * rp][0];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rfill, dst, 16, off, 0, 0, 0);
     }
   }
 
-  // MFMAs of one k-block: weights w, activations from ring slot `slot`, in the
-  // skinny engine's order (slice j, row tile, split hi before lo... as there:
-  // split S-1 first)
-  __device__ __forceinline__ void mma(int slot, const uint4 (&w)[8]) {
+  // 16-byte ring read at LDS byte address addr + OFF (inline asm: the
+  // compiler neither sees the LDS access nor waits for it)
+  template <int OFF>
+  __device__ __forceinline__ static u32x4 ds_read16(uint32_t addr) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+    return v;
+  }
+
+  // wait until at most N LDS reads are outstanding, ordered before every use
+  // of the fragments x
+  template <int N>
+  __device__ __forceinline__ static void lds_wait(u32x4 (&x)[RT][S]) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      uint4 x[RT][S];
+    for (int mt = 0; mt < RT; ++mt)
 #pragma unroll
-      for (int mt = 0; mt < RT; ++mt)
+      for (int s = 0; s < S; ++s) asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x[mt][s]) : "n"(N));
+  }
+
+  // fragments of slice j (row tile mt, split s) from the ring slot whose
+  // per-lane base addresses are ab[t], t = j % 4
+  template <int J, int... I>
+  __device__ __forceinline__ static void read_slice_i(const uint32_t (&ab)[4], u32x4 (&x)[RT][S],
+                                                      std::integer_sequence<int, I...>) {
+    // I = s * RT + mt
+    ((x[I % RT][I / RT] = ds_read16<I * 16 * 512 + 256 * (J >> 2)>(ab[J & 3])), ...);
+  }
+  template <int J>
+  __device__ __forceinline__ static void read_slice(const uint32_t (&ab)[4], u32x4 (&x)[RT][S]) {
+    read_slice_i<J>(ab, x, std::make_integer_sequence<int, RT * S>{});
+  }
+
+  template <int J>
+  __device__ __forceinline__ void mma_slice(const u32x4 (&x)[RT][S], const uint4 (&w)[P][8]) {
 #pragma unroll
-        for (int s = 0; s < S; ++s) x[mt][s] = *(const uint4*)&sm.ring[slot][s][mt * 16 + kl][(32 * j + 8 * g) * 2];
+    for (int p = 0; p < P; ++p)
 #pragma unroll
       for (int mt = 0; mt < RT; ++mt)
 #pragma unroll
         for (int s = S - 1; s >= 0; --s)
-          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, x[mt][s]),
-                                                            __builtin_bit_cast(bf16x8, w[j]), acc[mt], 0, 0, 0);
-    }
+          acc[mt][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, x[mt][s]),
+                                                               __builtin_bit_cast(bf16x8, w[p][J]), acc[mt][p], 0, 0, 0);
+  }
+
+  // MFMAs of one k-block: weights w, activations from ring slot `slot`, for
+  // every accumulator in the skinny engine's order (slice j, split S-1 first).
+  // Fragment reads run one slice ahead of the MFMAs.  Chunk (4j + g) ^ kl of
+  // row kl sits at byte 256 (j / 4) + 64 ((j % 4) ^ (kl / 4)) + 16 (g ^ kl % 4).
+  __device__ __forceinline__ void mma(int slot, const uint4 (&w)[P][8]) {
+    const uint32_t sb = lds_ring + (uint32_t)slot * (uint32_t)(kActSplits * RT * 16 * 512);
+    uint32_t ab[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) ab[t] = sb + aoff[t];
+    u32x4 xa[RT][S], xb[RT][S];
+    read_slice<0>(ab, xa);
+    read_slice<1>(ab, xb);
+    lds_wait<RT * S>(xa);
+    mma_slice<0>(xa, w);
+    read_slice<2>(ab, xa);
+    lds_wait<RT * S>(xb);
+    mma_slice<1>(xb, w);
+    read_slice<3>(ab, xb);
+    lds_wait<RT * S>(xa);
+    mma_slice<2>(xa, w);
+    read_slice<4>(ab, xa);
+    lds_wait<RT * S>(xb);
+    mma_slice<3>(xb, w);
+    read_slice<5>(ab, xb);
+    lds_wait<RT * S>(xa);
+    mma_slice<4>(xa, w);
+    read_slice<6>(ab, xa);
+    lds_wait<RT * S>(xb);
+    mma_slice<5>(xb, w);
+    read_slice<7>(ab, xb);
+    lds_wait<RT * S>(xa);
+    mma_slice<6>(xa, w);
+    lds_wait<0>(xb);
+    mma_slice<7>(xb, w);
   }
 
   // after k-block kb: at the end of a k-range add its partial to the total
@@ -142,11 +228,13 @@ struct GemmWide {
   __device__ __forceinline__ void range_end(int kb) {
     if (kb + 1 == bnd) {
 #pragma unroll
-      for (int mt = 0; mt < RT; ++mt) {
+      for (int mt = 0; mt < RT; ++mt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) tot[mt][i] += acc[mt][i];
-        acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      }
+        for (int p = 0; p < P; ++p) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) tot[mt][p][i] += acc[mt][p][i];
+          acc[mt][p] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
       do {
         ++rnext;
         bnd = (NKB * rnext) / kGemmWaves;
@@ -154,69 +242,95 @@ struct GemmWide {
     }
   }
 
-  // k-block kb: weights in w (refilled with kb + 3), activation block kb + 1
-  // in staging set st (written to the ring, refilled with kb + 3)
-  __device__ __forceinline__ void step(int kb, uint4 (&w)[8], uint4 (&st)[NST]) {
-    __syncthreads();  // block kb visible; the slot of kb - 1 is free
-    mma(kb & 1, w);
+  // k-block kb: weights in set WS (refilled with kb + D), activations in ring
+  // slot SLOT = kb % 3.  On entry the vector-memory operations issued after
+  // the fill of kb are at most the weights of two steps and one fill (steady
+  // state; fewer in the first steps), so waiting for that count completes this
+  // wave's share of k-block kb; the barrier then publishes every wave's share
+  // and ends the reads of slot (kb + 2) % 3, into which k-block kb + 2 is
+  // requested.  The barrier is a bare s_barrier: the ring is read with inline
+  // asm and written by direct loads whose completion each wave has just
+  // waited for, so no fence is needed (a workgroup fence would also wait for
+  // the fill of kb + 1 and everything issued before it, draining the weight
+  // pipeline).
+  template <int SLOT, int WS>
+  __device__ __forceinline__ void step(int kb) {
+    wait_vmcnt<NFILL + 16 * P>();
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    fill(kb + 2, (SLOT + 2) % kWideSlots);
+    mma(SLOT, wset[WS]);
     __builtin_amdgcn_sched_barrier(0);
     range_end(kb);
-    store_a((kb + 1) & 1, st);
-    issue_a(kb + 3, st);
-    issue_w(kb + 3, w);
+    issue_w(kb + D, wset[WS]);
+  }
+
+  template <int... I>
+  __device__ __forceinline__ void period_steps(int kb, std::integer_sequence<int, I...>) {
+    (step<I % kWideSlots, I % D>(kb + I), ...);
+  }
+
+  // the first n (< PERIOD) steps of a period, n uniform
+  template <int... I>
+  __device__ __forceinline__ void tail_steps(int kb, int n, std::integer_sequence<int, I...>) {
+    ((I < n ? step<I % kWideSlots, I % D>(kb + I) : void()), ...);
   }
 
   __device__ __forceinline__ void run() {
-    // prologue: blocks 0 and 1 of the operand and tiles 0 and 1 (operand
-    // first), block 0 into the ring, then block 2 and tile 2
-    issue_a(0, st0);
-    issue_w(0, w0);
-    issue_a(1, st1);
-    issue_w(1, w1);
+    // prologue: k-blocks 0 and 1 of the operand, the first D weight sets
+    fill(0, 0);
+    fill(1, 1);
+#pragma unroll
+    for (int i = 0; i < D; ++i) issue_w(i, wset[i]);
     // row scales of the group while those are in flight
     for (int r = tid >> 4; r < RT * 16; r += 32) {
       const float ri = gemm_row_rinv(a, row0 + r, tid & 15);
       if ((tid & 15) == 0) sm.rinv[r] = ri;
     }
-    store_a(0, st0);
-    issue_a(2, st0);
-    issue_w(2, w2);
-    // k-block kb uses weight set kb % 3 and writes staging set (kb + 1) % 2
-    for (int kb = 0; kb < Tpad; kb += 6) {
-      step(kb, w0, st1);
-      step(kb + 1, w1, st0);
-      step(kb + 2, w2, st1);
-      step(kb + 3, w0, st0);
-      step(kb + 4, w1, st1);
-      step(kb + 5, w2, st0);
-    }
-    __syncthreads();  // rinv
-    // epilogue: lane holds rows mt*16 + 4g + i, column kl of unit u
+    // whole periods in a loop (no exits inside, so the compiler's wait counts
+    // at the loop head stay exact), then the remaining k-blocks
+    const int full = NKB / PERIOD * PERIOD;
+    for (int kb = 0; kb < full; kb += PERIOD) period_steps(kb, std::make_integer_sequence<int, PERIOD>{});
+    tail_steps(full, NKB - full, std::make_integer_sequence<int, PERIOD - 1>{});
+    // the last fills (k-blocks past the end) must land before the workgroup
+    // can exit; then rinv is visible
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    // epilogue: lane holds rows mt*16 + 4g + i, column kl of each unit
 #pragma unroll
-    for (int mt = 0; mt < RT; ++mt) {
+    for (int p = 0; p < P; ++p) {
+      const int u = ubase + p;
+      const bool uok = u < a.n_units;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = mt * 16 + 4 * g + i;
-        const int ml = row0 + r;
-        const bool rok = uok && ml < a.M;
-        int pos = 0, bg = 0;
-        if constexpr (KIND == GEMM_QKV) {
-          const int m = a.m0 + ml;
-          const int bl = m / a.R, ir = m - bl * a.R;
-          bg = a.b0 + bl;
-          if (rok) pos = a.lens[bg] + ir;
+      for (int mt = 0; mt < RT; ++mt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = mt * 16 + 4 * g + i;
+          const int ml = row0 + r;
+          const bool rok = uok && ml < a.M;
+          int pos = 0, bg = 0;
+          if constexpr (KIND == GEMM_QKV) {
+            const int m = a.m0 + ml;
+            const int bl = m / a.R, ir = m - bl * a.R;
+            bg = a.b0 + bl;
+            if (rok) pos = a.lens[bg] + ir;
+          }
+          const EpiIn e = gemm_epi_load<KIND, false>(a, uok ? u : 0, ml, kl, rok, pos);
+          gemm_epilogue<KIND, true, false>(a, uok ? u : 0, ml, kl, rok, pos, bg, sm.rinv[r], tot[mt][p][i], e);
         }
-        const EpiIn e = gemm_epi_load<KIND, false>(a, uok ? u : 0, ml, kl, rok, pos);
-        gemm_epilogue<KIND, true, false>(a, uok ? u : 0, ml, kl, rok, pos, bg, sm.rinv[r], tot[mt][i], e);
       }
     }
   }
 };
 
-// Host-side shape of a wide launch: row tiles per workgroup and row groups.
+// Host-side shape of a wide launch.
 inline __host__ __device__ int gemm_wide_row_groups(int M, int rt) { return ((M + 15) / 16 + rt - 1) / rt; }
+inline __host__ __device__ int gemm_wide_unit_groups(int n_units, int p) {
+  return (n_units + kGemmWaves * p - 1) / (kGemmWaves * p);
+}
 inline __host__ __device__ uint32_t gemm_wide_lds_bytes(int rt) {
-  return (uint32_t)(2 * kActSplits * rt * 16 * kWideRowBytes + rt * 16 * 4);
+  return (uint32_t)(kWideSlots * kActSplits * rt * 16 * 512 + rt * 16 * 4);
 }
 
 }  // namespace spade

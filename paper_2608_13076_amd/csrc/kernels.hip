@@ -118,13 +118,13 @@ __global__ void __launch_bounds__(kGemmWaves * 64) gemm_kernel(GemmParams a) {
 // Wide-row projection GEMM (device_gemm_wide.h): workgroup b runs on XCD
 // b % 8 and takes unit group b % 8 + 8 (q / NRG), row group q % NRG with
 // q = b / 8, so the row groups of a unit group share that XCD's L2.
-template <int RT, int KIND>
+template <int RT, int P, int KIND>
 __global__ void __launch_bounds__(kGemmWaves * 64) gemm_wide_kernel(GemmParams a, int NRG, int NUG) {
   extern __shared__ uint4 lds_dyn[];
   const int b = (int)blockIdx.x, q = b >> 3;
   const int ug = (b & 7) + 8 * (q / NRG), rg = q % NRG;
   if (ug >= NUG) return;  // uniform, before any barrier
-  GemmWide<RT, KIND> g(a, *(GemmWideSmem<RT>*)lds_dyn, ug, rg);
+  GemmWide<RT, P, KIND> g(a, *(GemmWideSmem<RT>*)lds_dyn, ug, rg);
   g.run();
 }
 
@@ -693,40 +693,61 @@ hipError_t launch_gemm(int kind, const GemmParams& gp, int grid, int mt, hipStre
   }
 }
 
-template <int RT, int KIND>
+template <int RT, int P, int KIND>
 hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, hipStream_t st) {
-  const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, KIND>);
+  const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, P, KIND>);
   const uint32_t lds = gemm_wide_lds_bytes(RT);
   static hipError_t attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return attr;
   const int grid = 8 * ((nug + 7) / 8) * nrg;
-  hipLaunchKernelGGL((gemm_wide_kernel<RT, KIND>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp, nrg, nug);
+  hipLaunchKernelGGL((gemm_wide_kernel<RT, P, KIND>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp, nrg, nug);
   return hipGetLastError();
 }
 
 template <int KIND>
-hipError_t launch_wide_kind(const GemmParams& gp, int rt, int nrg, int nug, hipStream_t st) {
-  if (rt == 3) return launch_wide_rt<3, KIND>(gp, nrg, nug, st);
-  if (rt == 2) return launch_wide_rt<2, KIND>(gp, nrg, nug, st);
-  return launch_wide_rt<1, KIND>(gp, nrg, nug, st);
+hipError_t launch_wide_kind(const GemmParams& gp, int rt, int p, int nrg, int nug, hipStream_t st) {
+  if (p == 2) {  // two panels per wave: at most two row tiles (register budget)
+    if (rt == 2) return launch_wide_rt<2, 2, KIND>(gp, nrg, nug, st);
+    return launch_wide_rt<1, 2, KIND>(gp, nrg, nug, st);
+  }
+  if (rt == 3) return launch_wide_rt<3, 1, KIND>(gp, nrg, nug, st);
+  if (rt == 2) return launch_wide_rt<2, 1, KIND>(gp, nrg, nug, st);
+  return launch_wide_rt<1, 1, KIND>(gp, nrg, nug, st);
 }
 
-// All rows of a bf16 projection in one launch: row tiles per workgroup, the
-// largest of 3, 2, 1 that still gives a workgroup per compute unit (else 1).
-hipError_t launch_wide(int kind, const GemmParams& gp, int n_cu, int fixed_rt, hipStream_t st) {
-  const int nug = (gp.n_units + kGemmWaves - 1) / kGemmWaves;
-  int rt = fixed_rt > 0 ? fixed_rt : 1;
-  for (int c = 3; c >= 2 && fixed_rt <= 0; --c)
-    if ((long)nug * gemm_wide_row_groups(gp.M, c) >= n_cu) {
-      rt = c;
-      break;
+// All rows of a bf16 projection in one launch.  Row tiles per workgroup and
+// panels per wave are fixed by the caller (> 0) or chosen here.  A compute
+// unit streams about the same number of bytes per second whether they come
+// from HBM or L2, so the time is close to the rounds of workgroups (one per
+// compute unit at a time) times the bytes each moves per k-block: 64 KB of
+// weights per panel per wave and 16 KB of operand per row tile.
+hipError_t launch_wide(int kind, const GemmParams& gp, int n_cu, int fixed_rt, int fixed_p, hipStream_t st) {
+  const int tiles = (gp.M + 15) / 16;
+  int best_rt = 1, best_p = 1;
+  long best = -1;
+  for (int p = 2; p >= 1; --p) {
+    if (fixed_p > 0 && p != fixed_p) continue;
+    for (int rt = 3; rt >= 1; --rt) {
+      if (p == 2 && rt == 3) continue;
+      if (fixed_rt > 0 && rt != fixed_rt) continue;
+      if (fixed_rt <= 0 && rt > tiles) continue;
+      const long wgs = (long)gemm_wide_unit_groups(gp.n_units, p) * gemm_wide_row_groups(gp.M, rt);
+      const long rounds = (wgs + n_cu - 1) / n_cu;
+      const long cost = rounds * (64 * p + 16 * rt);
+      if (best < 0 || cost < best) {
+        best = cost;
+        best_rt = rt;
+        best_p = p;
+      }
     }
-  const int nrg = gemm_wide_row_groups(gp.M, rt);
+  }
+  const int nug = gemm_wide_unit_groups(gp.n_units, best_p);
+  const int nrg = gemm_wide_row_groups(gp.M, best_rt);
   switch (kind) {
-    case GEMM_QKV: return launch_wide_kind<GEMM_QKV>(gp, rt, nrg, nug, st);
-    case GEMM_O: return launch_wide_kind<GEMM_O>(gp, rt, nrg, nug, st);
-    case GEMM_GU: return launch_wide_kind<GEMM_GU>(gp, rt, nrg, nug, st);
-    default: return launch_wide_kind<GEMM_DOWN>(gp, rt, nrg, nug, st);
+    case GEMM_QKV: return launch_wide_kind<GEMM_QKV>(gp, best_rt, best_p, nrg, nug, st);
+    case GEMM_O: return launch_wide_kind<GEMM_O>(gp, best_rt, best_p, nrg, nug, st);
+    case GEMM_GU: return launch_wide_kind<GEMM_GU>(gp, best_rt, best_p, nrg, nug, st);
+    default: return launch_wide_kind<GEMM_DOWN>(gp, best_rt, best_p, nrg, nug, st);
   }
 }
 
@@ -846,7 +867,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
     gp.act = act;
     gp.act_split = act_split;
     gp.act_stride = K;
-    return launch_wide(kind, gp, md->n_cu, md->wide_rt, st);
+    return launch_wide(kind, gp, md->n_cu, md->wide_rt, md->wide_p, st);
   }
   for (int m0 = 0; m0 < M; m0 += kMaxRowsPerGemm) {
     GemmParams gp = g;

@@ -147,6 +147,7 @@ struct spade_model_s {
   int gemm_wgs;  // persistent GEMM workgroups
   bool fused_ok; // cooperative launches available and the single-launch verify pass enabled
   int wide_rt;   // 16-row tiles per workgroup of the wide-row GEMM: 0 chosen per launch, 1..3 fixed, -1 off
+  int wide_p;    // panels per wave of the wide-row GEMM: 0 chosen per launch, 1..2 fixed
 };
 
 struct spade_kv_s {

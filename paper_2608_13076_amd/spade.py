@@ -86,7 +86,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_profile_gemm": (I, [P, P, I, I, I, I, P]),
         "spade_get_device_error": (I, [P, P, P]),
         "spade_model_set_fused": (I, [P, I]),
-        "spade_model_set_wide_tiles": (I, [P, I]),
+        "spade_model_set_wide_tiles": (I, [P, I, I]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
         "spade_kv_destroy": (None, [P]),
@@ -170,10 +170,11 @@ class Model:
         (default), or one kernel per stage."""
         _check(self.lib.spade_model_set_fused(self.handle, 1 if enable else 0))
 
-    def set_wide_tiles(self, tiles: int) -> None:
-        """16-row tiles per workgroup of the batched projections: 0 chosen per
-        launch, 1..3 fixed, -1 skinny engine once per 32 rows."""
-        _check(self.lib.spade_model_set_wide_tiles(self.handle, int(tiles)))
+    def set_wide_tiles(self, row_tiles: int, panels: int = 0) -> None:
+        """Tiling of the batched projections: 16-row tiles per workgroup (0
+        chosen per launch, 1..3 fixed, -1 skinny engine once per 32 rows) and
+        weight panels per wave (0 chosen per launch, 1..2 fixed)."""
+        _check(self.lib.spade_model_set_wide_tiles(self.handle, int(row_tiles), int(panels)))
 
     def device_error(self) -> int:
         v = ctypes.c_uint32()

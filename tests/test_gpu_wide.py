@@ -1,7 +1,8 @@
 """Batched verification on the wide-row GEMM (more than 16 rows, bf16).
 
-Every row tiling of the wide-row engine (1, 2 or 3 sixteen-row tiles per
-workgroup, and the per-launch choice) must give bit-for-bit the logits,
+Every tiling of the wide-row engine (1, 2 or 3 sixteen-row tiles per
+workgroup with 1 weight panel per wave, 1 or 2 with 2 panels, and the per-launch choice)
+must give bit-for-bit the logits,
 n_accepted and corrections of the skinny engine run once per 32 rows: both sum
 each dot product over the same eight k-ranges in the same order.  The
 per-launch choice is also compared with the oracle to the usual bar, at 35
@@ -38,16 +39,16 @@ def test_wide_tilings_bit_identical_and_match_oracle(w):
     model, kv = gpu_setup(w, weights)
     gpu_prefill(kv, inp)
     runs = {}
-    for tiles in (-1, 1, 2, 3, 0):
-        print(f"[{w.name}] M={w.batch * (w.gamma + 1)} wide tiles {tiles}", flush=True)
-        model.set_wide_tiles(tiles)
+    for tiles in ((-1, 0), (1, 1), (2, 1), (3, 1), (1, 2), (2, 2), (0, 0)):
+        print(f"[{w.name}] M={w.batch * (w.gamma + 1)} wide (row tiles, panels) {tiles}", flush=True)
+        model.set_wide_tiles(*tiles)
         runs[tiles] = gpu_verify(model, kv, inp)[:3]
-    ref = runs[-1]
+    ref = runs[(-1, 0)]
     for tiles, (lg, n, c) in runs.items():
         assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), tiles
         assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), tiles
-    p = compare(orun, *runs[0])
-    print(f"[{w.name}] logit err {p.logit_err:.2e}, n {runs[0][1].tolist()}", flush=True)
+    p = compare(orun, *runs[(0, 0)])
+    print(f"[{w.name}] logit err {p.logit_err:.2e}, n {runs[(0, 0)][1].tolist()}", flush=True)
     assert p.logit_err < LOGIT_TOL[w.model.weight_dtype]
     assert not p.stable_n_fail and not p.stable_corr_fail, p
     assert model.device_error() == 0
