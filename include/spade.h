@@ -234,6 +234,20 @@ spade_status spade_model_set_fused(spade_model m, int enable);
  * return SPADE_EINVAL. */
 spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels);
 
+/* K splitting of the small-batch projections.  A verify call with at most 16
+ * rows and bf16 weights whose activation operand is too long for one LDS copy
+ * (the 7B-shaped down projection, every projection of the 13B shape) runs the
+ * QKV, O, gate/up or down projection split along K into `splits` parts: a
+ * workgroup copies only its part of the operand into LDS and streams one
+ * k-range of each of its panels; the last workgroup of a panel group to finish
+ * completes the sums and runs the epilogue.  splits = 0 (the default) picks 2
+ * or 4, the fewest whose part fits; 2 or 4 fix it (also where the whole
+ * operand would fit) where the part fits; -1 turns it off (the operand is then
+ * fetched from L2 with every weight tile).  Results are bit-for-bit the same
+ * under every setting: each dot product is summed over the same eight k-ranges
+ * in the same order.  Other values return SPADE_EINVAL. */
+spade_status spade_model_set_split_k(spade_model m, int splits);
+
 /* Context update after spade_verify (Algorithm 1: append the k accepted
  * tokens and the correction, m <- m + k + 1): lens[b] += n_accepted[b] + 1 and
  * pending[b] = correction[b], on the device.  KV rows past the new length are

@@ -86,9 +86,11 @@ ArenaLayout layout_of(const Dims& D) {
 }
 
 struct WsPlan {
-  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, bar, fused, total;
+  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, bar, fused, split_cnt,
+      split_part, total;
   FusedArena fa;
   bool has_fused;
+  int max_units;
   size_t act_split, actf_split;
   int Mmax, NCmax, Rmax;
 };
@@ -123,6 +125,9 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.rope = take((size_t)max_len * (D.hd / 2) * 2 * 4);
   p.err = take(4);
   p.bar = take(kBarBytes);
+  p.max_units = std::max(3 * D.d, 2 * D.F) / 16;
+  p.split_cnt = take((size_t)p.max_units * 4);
+  p.split_part = take((size_t)p.max_units * 8 * 256 * 4);
   // the single-launch pass handles bf16 weights and cache with head_dim 128
   p.has_fused = wb && D.kvdt == SPADE_BF16 && D.hd == 128;
   if (p.has_fused) {
@@ -185,6 +190,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->gemm_wgs = m->n_cu;
   m->wide_rt = 0;
   m->wide_p = 0;
+  m->split_ks = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -209,6 +215,8 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.attn_o = (float*)(b + p.attn_o);
   w.attn_ml = (float*)(b + p.attn_ml);
   w.attn_cnt = (uint32_t*)(b + p.attn_cnt);
+  w.split_cnt = (uint32_t*)(b + p.split_cnt);
+  w.split_part = (float*)(b + p.split_part);
   w.logits = (float*)(b + p.logits);
   w.stats = (float*)(b + p.stats);
   w.rope = (float*)(b + p.rope);
@@ -234,6 +242,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
     }
   hipError_t e = hipMemcpy(w.rope, rope.data(), rope.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemset(w.attn_cnt, 0, (size_t)max_batch * m->dims.H * 4);
+  if (e == hipSuccess) e = hipMemset(w.split_cnt, 0, (size_t)p.max_units * 4);
   if (e == hipSuccess) e = hipMemset(w.err, 0, 4);
   if (e == hipSuccess) e = hipMemset(w.bar, 0, kBarBytes);
   // activation buffers start at zero so rows past M never feed NaNs
@@ -441,6 +450,13 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
   if (panels == 2 && row_tiles == 3) return fail(SPADE_EINVAL, "two panels per wave take at most two row tiles");
   m->wide_rt = row_tiles;
   m->wide_p = panels;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_split_k(spade_model m, int splits) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (splits != -1 && splits != 0 && splits != 2 && splits != 4) return fail(SPADE_EINVAL, "splits must be -1, 0, 2 or 4");
+  m->split_ks = splits;
   return SPADE_OK;
 }
 

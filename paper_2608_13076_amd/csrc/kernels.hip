@@ -26,6 +26,7 @@
 #include "device_accept.h"
 #include "device_attn.h"
 #include "device_gemm.h"
+#include "device_gemm_split.h"
 #include "device_gemm_wide.h"
 
 #include <float.h>
@@ -111,6 +112,18 @@ __global__ void __launch_bounds__(kGemmWaves * 64) gemm_kernel(GemmParams a) {
   __shared__ GemmSmem<MT> sm;
   extern __shared__ uint4 lds_dyn[];
   Gemm<WBF16, MT, ALDS, KIND, false> g(a, sm, (uint8_t*)lds_dyn, (int)blockIdx.x, (int)gridDim.x);
+  g.prefetch();
+  g.run();
+}
+
+// Split-K skinny projection GEMM (device_gemm_split.h): G workgroups per
+// k-split, workgroup b in split b / G.
+constexpr uint32_t kSplitSmemBytes = (uint32_t)((sizeof(GemmSplitSmem) + 15) / 16 * 16);
+
+template <int KS, int KIND>
+__global__ void __launch_bounds__(kGemmWaves * 64) gemm_split_kernel(GemmParams a, uint32_t* cnt, float* part, int G) {
+  extern __shared__ uint4 lds_dyn[];
+  GemmSplit<KS, KIND> g(a, *(GemmSplitSmem*)lds_dyn, (uint8_t*)lds_dyn + kSplitSmemBytes, cnt, part, G);
   g.prefetch();
   g.run();
 }
@@ -693,6 +706,55 @@ hipError_t launch_gemm(int kind, const GemmParams& gp, int grid, int mt, hipStre
   }
 }
 
+template <int KS, int KIND>
+hipError_t launch_split_ks(const GemmParams& gp, uint32_t* cnt, float* part, int G, hipStream_t st) {
+  const void* fn = reinterpret_cast<const void*>(&gemm_split_kernel<KS, KIND>);
+  static hipError_t attr =
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)(kSplitSmemBytes + kGemmLdsABytes));
+  if (attr != hipSuccess) return attr;
+  const uint32_t lds = kSplitSmemBytes + gemm_split_lds_bytes(gp.M, gp.NKB, KS);
+  hipLaunchKernelGGL((gemm_split_kernel<KS, KIND>), dim3(G * KS), dim3(kGemmWaves * 64), lds, st, gp, cnt, part, G);
+  return hipGetLastError();
+}
+
+// k-splits for a bf16 projection with <= 16 rows whose whole operand does
+// not fit in LDS: the fewest (2 or 4) whose split fits, with at most
+// kSplitMaxGroups panel groups per workgroup; 0 when none qualifies (or the
+// whole operand fits).  fixed > 0 forces that count where it qualifies.
+int split_k_choice(const GemmParams& gp, int n_cu, int fixed) {
+  if (gp.M > 16) return 0;
+  const uint32_t whole = gemm_lds_a_bytes(gp.M, gp.act_stride, 1);
+  const bool whole_fits = whole <= kGemmLdsABytes && gemm_lds_a_ok(gp.act_stride, 1);
+  if (whole_fits && fixed <= 0) return 0;
+  for (int ks = 2; ks <= 4; ks *= 2) {
+    if (fixed > 0 && ks != fixed) continue;
+    const int G = n_cu / ks;
+    if (G < 1) continue;
+    const int groups = (gp.n_units + ks - 1) / ks;
+    if ((groups + G - 1) / G > kSplitMaxGroups) continue;
+    if (gemm_split_lds_bytes(gp.M, gp.NKB, ks) <= kGemmLdsABytes) return ks;
+  }
+  return 0;
+}
+
+hipError_t launch_split(int kind, const GemmParams& gp, int ks, int n_cu, uint32_t* cnt, float* part, hipStream_t st) {
+  const int G = n_cu / ks;
+  if (ks == 2) {
+    switch (kind) {
+      case GEMM_QKV: return launch_split_ks<2, GEMM_QKV>(gp, cnt, part, G, st);
+      case GEMM_O: return launch_split_ks<2, GEMM_O>(gp, cnt, part, G, st);
+      case GEMM_GU: return launch_split_ks<2, GEMM_GU>(gp, cnt, part, G, st);
+      default: return launch_split_ks<2, GEMM_DOWN>(gp, cnt, part, G, st);
+    }
+  }
+  switch (kind) {
+    case GEMM_QKV: return launch_split_ks<4, GEMM_QKV>(gp, cnt, part, G, st);
+    case GEMM_O: return launch_split_ks<4, GEMM_O>(gp, cnt, part, G, st);
+    case GEMM_GU: return launch_split_ks<4, GEMM_GU>(gp, cnt, part, G, st);
+    default: return launch_split_ks<4, GEMM_DOWN>(gp, cnt, part, G, st);
+  }
+}
+
 template <int RT, int P, int KIND>
 hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, hipStream_t st) {
   const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, P, KIND>);
@@ -880,6 +942,14 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
     gp.act_split = act_split;
     gp.act_stride = K;
     const int mt = gp.M > 16 ? 2 : 1;
+    if (wb && kind != GEMM_LM && md->split_ks >= 0) {
+      const int ks = split_k_choice(gp, md->n_cu, md->split_ks);
+      if (ks > 0) {
+        hipError_t r = launch_split(kind, gp, ks, md->n_cu, W.split_cnt, W.split_part, st);
+        if (r != hipSuccess) return r;
+        continue;
+      }
+    }
     hipError_t r = wb ? launch_gemm<true>(kind, gp, grid, mt, st) : launch_gemm<false>(kind, gp, grid, mt, st);
     if (r != hipSuccess) return r;
   }

@@ -126,6 +126,8 @@ struct Workspace {
   uint32_t* err;      // device error word
   uint32_t* bar;      // grid-barrier words of the single-launch verify pass (kept at zero between calls)
   uint8_t* fused;     // activation arena of the single-launch verify pass (NULL if the model cannot use it)
+  uint32_t* split_cnt;  // [max units / 2] arrival counters of the split-K GEMM (kept at zero between calls)
+  float* split_part;    // [max units][8][256] published sums and range partials of the split-K GEMM
   FusedArena fa;
   size_t act_split;   // elements between splits of act_n / act_o
   size_t actf_split;  // elements between splits of act_f
@@ -148,6 +150,7 @@ struct spade_model_s {
   bool fused_ok; // cooperative launches available and the single-launch verify pass enabled
   int wide_rt;   // 16-row tiles per workgroup of the wide-row GEMM: 0 chosen per launch, 1..3 fixed, -1 off
   int wide_p;    // panels per wave of the wide-row GEMM: 0 chosen per launch, 1..2 fixed
+  int split_ks;  // k-splits of the split-K GEMM: 0 chosen per launch, 2 or 4 where it qualifies, -1 off
 };
 
 struct spade_kv_s {

@@ -30,7 +30,7 @@ EXPORTED = (
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
     "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
-    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles",
+    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles", "spade_model_set_split_k",
 )
 
 
@@ -87,6 +87,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_get_device_error": (I, [P, P, P]),
         "spade_model_set_fused": (I, [P, I]),
         "spade_model_set_wide_tiles": (I, [P, I, I]),
+        "spade_model_set_split_k": (I, [P, I]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
         "spade_kv_destroy": (None, [P]),
@@ -175,6 +176,11 @@ class Model:
         chosen per launch, 1..3 fixed, -1 skinny engine once per 32 rows) and
         weight panels per wave (0 chosen per launch, 1..2 fixed)."""
         _check(self.lib.spade_model_set_wide_tiles(self.handle, int(row_tiles), int(panels)))
+
+    def set_split_k(self, splits: int) -> None:
+        """K splits of the small-batch projections whose operand does not fit
+        in LDS: 0 chosen per launch, 2 or 4 fixed, -1 off."""
+        _check(self.lib.spade_model_set_split_k(self.handle, int(splits)))
 
     def device_error(self) -> int:
         v = ctypes.c_uint32()
