@@ -77,12 +77,13 @@ struct GemmSmem {
   float rinv[MT * 16];
 };
 
-// LDS copy of the activation operand: per split, rows 0..M-1 and a zero row
-// at index M, each K elements plus 16 bytes of padding (rows start 4 banks
-// apart, so the 16 rows of a fragment read hit distinct banks).
+// LDS copy of the activation operand: per split, rows 0..M-1, each K elements
+// plus 16 bytes of padding (rows start 4 banks apart, so the 16 rows of a
+// fragment read hit distinct banks).  MFMA rows past M read row M - 1: their
+// outputs are never stored and do not mix with other rows.
 inline __host__ __device__ uint32_t gemm_lds_row_bytes(int K, int wbf16) { return (uint32_t)K * (wbf16 ? 2u : 4u) + 16u; }
 inline __host__ __device__ uint32_t gemm_lds_a_bytes(int M, int K, int wbf16) {
-  return (uint32_t)(wbf16 ? kActSplits : 1) * (uint32_t)(M + 1) * gemm_lds_row_bytes(K, wbf16);
+  return (uint32_t)(wbf16 ? kActSplits : 1) * (uint32_t)M * gemm_lds_row_bytes(K, wbf16);
 }
 // the LDS copy moves whole 1 KB blocks of a row
 inline __host__ __device__ bool gemm_lds_a_ok(int K, int wbf16) { return ((K * (wbf16 ? 2 : 4)) & 1023) == 0; }
@@ -309,8 +310,9 @@ struct Gemm {
 
   // ALDS: copy rows [0, M) of every split into LDS with direct buffer->LDS
   // loads (no registers: each wave instruction moves 64 consecutive 16-byte
-  // chunks of one row; rows are a multiple of 1 KB, gemm_lds_a_ok) and write
-  // the zero rows with LDS stores.
+  // chunks of one row; rows are a multiple of 1 KB, gemm_lds_a_ok).  Nothing
+  // else is written to LDS before the first wait, so the compiler's wait for
+  // the copy (before any LDS access) leaves later loads in flight.
   __device__ __forceinline__ void fill_lds_a() {
     const uint32_t rowb = gemm_lds_row_bytes(a.act_stride, WBF16);
     const int row_bytes = a.act_stride * (int)ELT;
@@ -321,13 +323,8 @@ struct Gemm {
       const int row = rem / per_row, blk = rem - row * per_row;
       const Rsrc rs = (S == 1 || s == 0) ? ra[0] : ra[S - 1];  // no dynamic index into ra
       __attribute__((address_space(3))) void* dst =
-          (__attribute__((address_space(3))) void*)(lds_a + (uint32_t)(s * (a.M + 1) + row) * rowb + (uint32_t)blk * 1024u);
+          (__attribute__((address_space(3))) void*)(lds_a + (uint32_t)(s * a.M + row) * rowb + (uint32_t)blk * 1024u);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 16, (uint32_t)(row * row_bytes + blk * 1024 + lane * 16), 0, 0, 0);
-    }
-    const int cpr = row_bytes >> 4;
-    for (int c = tid; c < S * cpr; c += NW * 64) {
-      const int s = c / cpr, cc = c - s * cpr;
-      *(uint4*)(lds_a + (uint32_t)(s * (a.M + 1) + a.M) * rowb + (uint32_t)cc * 16u) = make_uint4(0, 0, 0, 0);
     }
   }
 
@@ -336,7 +333,7 @@ struct Gemm {
   __device__ __forceinline__ void read_a_lds(int k) {
     const uint32_t rowb = gemm_lds_row_bytes(a.act_stride, WBF16);
     const int r = lane & 15;
-    const int rr = r < a.M ? r : a.M;
+    const int rr = r < a.M ? r : a.M - 1;
     const int kb = kbl + (k < cnt ? k : 0);
     uint32_t off;
     if constexpr (WBF16) off = (uint32_t)rr * rowb + (uint32_t)(kb * 256 + (lane >> 4) * 8) * 2u;
@@ -345,7 +342,7 @@ struct Gemm {
     for (int s = 0; s < S; ++s)
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        av[0][s][j] = *(const uint4*)(lds_a + (uint32_t)(s * (a.M + 1)) * rowb + off + (uint32_t)j * 64u);
+        av[0][s][j] = *(const uint4*)(lds_a + (uint32_t)(s * a.M) * rowb + off + (uint32_t)j * 64u);
   }
 
   // epilogue inputs of the unit of item t
@@ -432,32 +429,35 @@ struct Gemm {
 
   // 1/rms of every row from the producer's per-16-column sums of squares:
   // thread (row, sub) sums partials sub, sub + 16, ... in that order, then the
-  // sixteen subs combine in a butterfly.  The first sixteen partials of each
-  // thread are requested with the other prologue loads (ssq_issue).
+  // sixteen subs combine in a butterfly.  The first 32 partials of each thread
+  // (d <= 8192; 16 with two row tiles, for registers) are requested with the
+  // other prologue loads (ssq_issue).
+  static constexpr int kSsqFirst = MT == 1 ? 32 : 16;
+
   __device__ __forceinline__ Rsrc ssq_rsrc() const {
     return make_rsrc(a.ssq_in + (size_t)a.m0 * a.n_ssq, (uint32_t)((size_t)a.M * a.n_ssq * 4));
   }
 
-  __device__ __forceinline__ void ssq_issue(float (&v)[16]) const {
+  __device__ __forceinline__ void ssq_issue(float (&v)[kSsqFirst]) const {
     const int row = tid >> 4, sub = tid & 15;
     const Rsrc rs = ssq_rsrc();
     const uint32_t base = (uint32_t)(row * a.n_ssq) * 4u;
 #pragma unroll
-    for (int f = 0; f < 16; ++f) {
+    for (int f = 0; f < kSsqFirst; ++f) {
       const int q = sub + f * 16;
       v[f] = ld_f32<false>(rs, (a.ssq_in != nullptr && q < a.n_ssq) ? base + (uint32_t)q * 4u : kOob);
     }
   }
 
-  __device__ __forceinline__ void row_scales(const float (&v0)[16]) {
+  __device__ __forceinline__ void row_scales(const float (&v0)[kSsqFirst]) {
     const int row = tid >> 4, sub = tid & 15;
     float s = 0.f;
 #pragma unroll
-    for (int f = 0; f < 16; ++f) s += v0[f];
+    for (int f = 0; f < kSsqFirst; ++f) s += v0[f];
     if (a.ssq_in != nullptr) {
       const Rsrc rs = ssq_rsrc();
       const uint32_t base = (uint32_t)(row * a.n_ssq) * 4u;
-      for (int q0 = sub + 256; q0 < a.n_ssq; q0 += 256) {
+      for (int q0 = sub + 16 * kSsqFirst; q0 < a.n_ssq; q0 += 256) {
         float v[16];
 #pragma unroll
         for (int f = 0; f < 16; ++f) {
@@ -503,29 +503,37 @@ struct Gemm {
     if (k == nkw - 1) unit_end(t, ecur);
   }
 
-  // Everything after prefetch(): operands, row scales, the item loop.
-  __device__ __forceinline__ void run() {
-    // prologue: operand copy, epilogue inputs and row partials in one round trip
-    if constexpr (ALDS) fill_lds_a();
-    else issue_a_t(0, av);
-    e0 = epi_load(0);
-    e1 = epi_load(1);
-    float sv[16];
-    ssq_issue(sv);
-    row_scales(sv);
-    // the first item needs all of the above; starting the loop with nothing in
-    // flight lets the loop head take its wait counts from the loop body
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    // the item count is padded to a multiple of 3 (padding items load zeros
-    // and store nothing): a loop body without exits keeps the wait counts
-    // at the loop head exact
+  // The item loop (no exits inside; the item count is padded to a multiple of
+  // 3 with padding items that load zeros and store nothing, so the wait
+  // counts at the loop head stay exact).
+  __device__ __forceinline__ void items() {
     const int Tpad = (T + 2) / 3 * 3;
     for (int t = 0; t < Tpad; t += 3) {
       step<0>(t);
       step<1>(t + 1);
       step<2>(t + 2);
     }
+  }
+
+  // Everything after prefetch(): operands, row scales, the item loop.  The
+  // first item needs all of the prologue; starting the loop with nothing in
+  // flight lets the loop head take its wait counts from the loop body.
+  __device__ __forceinline__ void run() {
+    // prologue: operand copy, epilogue inputs and row partials in one round trip
+    if constexpr (ALDS) fill_lds_a();
+    else issue_a_t(0, av);
+    e0 = epi_load(0);
+    e1 = epi_load(1);
+    float sv[kSsqFirst];
+    ssq_issue(sv);
+    row_scales(sv);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    items();
+    finish();
+  }
+
+  __device__ __forceinline__ void finish() {
     if constexpr (KIND == GEMM_LM) {
       // one (max, sum exp, argmax) per (row, workgroup): stats[m][bid], NU = grid size
       const Rsrc rst = make_rsrc(a.stats + (size_t)a.m0 * a.NU * 3, (uint32_t)((size_t)a.M * a.NU * 12));

@@ -249,6 +249,8 @@ struct GemmSplit {
     }
   }
 
+  // Everything after prefetch() (the first three weight tiles, requested
+  // first so that HBM starts streaming at once).
   __device__ __forceinline__ void run() {
     fill_lds_a();
     for (int r = tid >> 4; r < 16; r += 32) {

@@ -48,14 +48,6 @@ struct GemmWideSmem {
   float rinv[RT * 16];
 };
 
-// s_waitcnt that waits for vector memory counts <= n only (gfx9 encoding:
-// vmcnt bits [3:0] and [15:14], expcnt and lgkmcnt left at their maxima)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 template <int RT, int P, int KIND>
@@ -281,21 +273,22 @@ struct GemmWide {
     // prologue: k-blocks 0 and 1 of the operand, the first D weight sets
     fill(0, 0);
     fill(1, 1);
+    // the fills stay older than every weight load (the waits count on it)
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < D; ++i) issue_w(i, wset[i]);
-    // row scales of the group while those are in flight
-    for (int r = tid >> 4; r < RT * 16; r += 32) {
-      const float ri = gemm_row_rinv(a, row0 + r, tid & 15);
-      if ((tid & 15) == 0) sm.rinv[r] = ri;
-    }
     // whole periods in a loop (no exits inside, so the compiler's wait counts
     // at the loop head stay exact), then the remaining k-blocks
     const int full = NKB / PERIOD * PERIOD;
     for (int kb = 0; kb < full; kb += PERIOD) period_steps(kb, std::make_integer_sequence<int, PERIOD>{});
     tail_steps(full, NKB - full, std::make_integer_sequence<int, PERIOD - 1>{});
-    // the last fills (k-blocks past the end) must land before the workgroup
-    // can exit; then rinv is visible
+    // the last fills (k-blocks past the end) must land before the ring is
+    // reused; the row scales are only needed by the epilogue
     __builtin_amdgcn_s_waitcnt(0);
+    for (int r = tid >> 4; r < RT * 16; r += 32) {
+      const float ri = gemm_row_rinv(a, row0 + r, tid & 15);
+      if ((tid & 15) == 0) sm.rinv[r] = ri;
+    }
     __syncthreads();
     // epilogue: lane holds rows mt*16 + 4g + i, column kl of each unit
 #pragma unroll

@@ -21,6 +21,17 @@ constexpr int kAuxCoh = 16;
 // are dropped.  Masks a lane's access without a branch.
 constexpr uint32_t kOob = 0x80000000u;
 
+// s_waitcnt that waits until at most N vector-memory operations of this wave
+// are outstanding (gfx9 encoding: vmcnt bits [3:0] and [15:14]; expcnt and
+// lgkmcnt left at their maxima).  Vector-memory operations complete in issue
+// order, so this completes everything issued before the last N.  Direct
+// buffer->LDS loads count here; a barrier alone does not wait for them.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 // round to nearest even; NaN stays NaN
