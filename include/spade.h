@@ -83,12 +83,15 @@ enum {
  * x_{l+1} = x_l + f_l(x_l) with f_l = attention then feed-forward, LM head,
  * softmax).  Attention is multi-head with rotary position embedding
  * (rotate-half pairing of feature i with i + head_dim/2, angle
- * pos * rope_theta^(-2i/head_dim)); the feed-forward is SwiGLU
+ * pos * rope_theta^(-2i/head_dim)), grouped-query when n_kv_heads <
+ * n_heads: query head h attends with K/V head h / (n_heads / n_kv_heads),
+ * and Wk, Wv have n_kv_heads * head_dim rows; the feed-forward is SwiGLU
  * (silu(h W_gate^T) * (h W_up^T)) W_down^T; RMSNorm(x) = x / sqrt(mean(x^2)
  * + rms_eps) * g; no biases; the LM head is untied.
  *
  * weight_dtype: SPADE_BF16 or SPADE_F32 for every matrix (gains are float32).
  * kv_dtype: storage type of K and V (RoPE is applied before storing).
+ * n_kv_heads: 0 (the default: n_heads) or a divisor of n_heads.
  * Supported: head_dim 64 or 128; d_model = n_heads * head_dim; d_model and
  * d_ffn multiples of 256 (bf16 weights) or 128 (f32); any vocab >= 2; at most
  * 15 drafts per request (gamma + 1 <= 16 rows).
@@ -97,6 +100,7 @@ typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab;
   int32_t weight_dtype, kv_dtype;
   float rms_eps, rope_theta;
+  int32_t n_kv_heads;
 } spade_config;
 
 /* Bytes of the library's weight arena (its own tiled layout; filled by

@@ -5,8 +5,11 @@ updates the residual stream x_{l+1} = x_l + f_l(x_l) with f_l = self-attention
 then feed-forward, the LM head g maps the last hidden state to logits o_L, and
 P(y_{t+1} | y_{1:t}) = softmax(o_L^t).  The paper does not fix the block; the
 verifier here is the Llama-style instance: pre-RMSNorm, rotary position
-embedding (rotate-half pairing, base 10000), multi-head causal attention with
-scale 1/sqrt(head_dim), a SwiGLU feed-forward, no biases, untied LM head.
+embedding (rotate-half pairing, base rope_theta), multi-head causal attention
+with scale 1/sqrt(head_dim), a SwiGLU feed-forward, no biases, untied LM head.
+The paper's own cloud verifier is LLaMA-3.1-8B (Experiments, "Models"), whose
+attention is grouped-query: with n_kv_heads < n_heads, query head h attends
+with the K/V head floor(h / (n_heads / n_kv_heads)).
 
 Readings the paper leaves open (each listed in the design notes):
 * RMSNorm(x) = x / sqrt(mean(x^2) + eps) * g with eps = 1e-5;
@@ -83,7 +86,7 @@ def softmax(z: np.ndarray, axis: int = -1) -> np.ndarray:
 
 @dataclass
 class KVCache:
-    """One request's cache: per layer K and V of shape [H, capacity, hd]."""
+    """One request's cache: per layer K and V of shape [KV heads, capacity, hd]."""
 
     n_layers: int
     n_heads: int
@@ -127,7 +130,7 @@ class Decoder:
 
     def new_cache(self, capacity: int) -> KVCache:
         s = self.shape
-        return KVCache(s.n_layers, s.n_heads, s.head_dim, capacity)
+        return KVCache(s.n_layers, s.kv_heads, s.head_dim, capacity)
 
     def _store(self, x: np.ndarray) -> np.ndarray:
         return bf16_round(x) if self.shape.kv_dtype == "bf16" else x.astype(np.float32).astype(np.float64)
@@ -142,6 +145,8 @@ class Decoder:
         if L + R > cache.capacity:
             raise ValueError("cache capacity exceeded")
         H, hd = s.n_heads, s.head_dim
+        KVH = s.kv_heads
+        G = H // KVH  # query heads per K/V head
         pos = np.arange(L, L + R)
         cos, sin = rope_tables(pos, hd, s.rope_theta)
         x = self.w("embed")[tokens]  # x_0
@@ -150,14 +155,15 @@ class Decoder:
             # attention sub-block
             h = rms_norm(x, self.w("g_attn", l), s.rms_eps)
             q = (h @ self.w("wq", l).T).reshape(R, H, hd)
-            k = (h @ self.w("wk", l).T).reshape(R, H, hd)
-            v = (h @ self.w("wv", l).T).reshape(R, H, hd)
+            k = (h @ self.w("wk", l).T).reshape(R, KVH, hd)
+            v = (h @ self.w("wv", l).T).reshape(R, KVH, hd)
             q = apply_rope(q, cos, sin)
             k = apply_rope(k, cos, sin)
             cache.k[l][:, L:L + R, :] = self._store(k).transpose(1, 0, 2)
             cache.v[l][:, L:L + R, :] = self._store(v).transpose(1, 0, 2)
-            K = cache.k[l][:, :L + R, :]  # [H, L+R, hd]
-            Vv = cache.v[l][:, :L + R, :]
+            # query head h reads K/V head h // G
+            K = np.repeat(cache.k[l][:, :L + R, :], G, axis=0)  # [H, L+R, hd]
+            Vv = np.repeat(cache.v[l][:, :L + R, :], G, axis=0)
             scores = np.matmul(q.transpose(1, 0, 2), K.transpose(0, 2, 1)) * scale  # [H, R, L+R]
             key_pos = np.arange(L + R)
             mask = key_pos[None, :] <= pos[:, None]  # row i sees keys <= L+i

@@ -42,6 +42,8 @@ spade_status check_config(const spade_config* c) {
   if (c->kv_dtype != SPADE_BF16 && c->kv_dtype != SPADE_F32)
     return fail(SPADE_EINVAL, "kv_dtype must be SPADE_BF16 or SPADE_F32");
   if (c->d_model != c->n_heads * c->head_dim) return fail(SPADE_EINVAL, "d_model != n_heads * head_dim");
+  if (c->n_kv_heads < 0 || (c->n_kv_heads > 0 && c->n_heads % c->n_kv_heads != 0))
+    return fail(SPADE_EINVAL, "n_kv_heads must be 0 or a divisor of n_heads");
   if (c->head_dim != 64 && c->head_dim != 128) return fail(SPADE_EUNSUPPORTED, "head_dim must be 64 or 128");
   const int kb = kblock_of(c->weight_dtype);
   if (c->d_model % kb || c->d_ffn % kb)
@@ -56,6 +58,8 @@ Dims dims_of(const spade_config* c) {
   d.d = c->d_model;
   d.H = c->n_heads;
   d.hd = c->head_dim;
+  d.KVH = c->n_kv_heads > 0 ? c->n_kv_heads : c->n_heads;
+  d.dkv = d.KVH * c->head_dim;
   d.F = c->d_ffn;
   d.V = c->vocab;
   d.Vpad = (c->vocab + 15) / 16 * 16;
@@ -70,7 +74,7 @@ ArenaLayout layout_of(const Dims& D) {
   const size_t e = D.wdt == SPADE_BF16 ? 2 : 4;
   ArenaLayout a{};
   size_t off = 0;
-  a.qkv = off;  off += align256((size_t)3 * D.d * D.d * e);
+  a.qkv = off;  off += align256((size_t)(D.d + 2 * D.dkv) * D.d * e);
   a.o = off;    off += align256((size_t)D.d * D.d * e);
   a.gu = off;   off += align256((size_t)2 * D.F * D.d * e);
   a.down = off; off += align256((size_t)D.d * D.F * e);
@@ -158,7 +162,8 @@ size_t spade_workspace_bytes(const spade_config* cfg, int max_batch, int max_gam
 size_t spade_kv_bytes(const spade_config* cfg, int max_batch, int max_len) {
   if (check_config(cfg) != SPADE_OK || max_batch < 1 || max_len < 1) return 0;
   const size_t e = cfg->kv_dtype == SPADE_BF16 ? 2 : 4;
-  return 2 * align256((size_t)cfg->n_layers * max_batch * cfg->n_heads * kv_stride_of(max_len) * cfg->head_dim * e);
+  const int kvh = cfg->n_kv_heads > 0 ? cfg->n_kv_heads : cfg->n_heads;
+  return 2 * align256((size_t)cfg->n_layers * max_batch * kvh * kv_stride_of(max_len) * cfg->head_dim * e);
 }
 
 spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* d_workspace, int max_batch,

@@ -47,6 +47,7 @@ struct GemmParams {
   void* vc;
   uint32_t kv_bytes;  // bytes of one layer's K (or V) cache
   int H, hd, d, kv_stride, kv_bf16;
+  int Hkv;  // K/V heads (the cache's head count; H for multi-head attention)
   const float* rope;
   // O / DOWN
   float* x;
@@ -100,9 +101,8 @@ template <int KIND, bool COH>
 __device__ __forceinline__ EpiIn gemm_epi_load(const GemmParams& a, int u, int ml, int n, bool ok, int pos) {
   EpiIn e{0.f, 0.f};
   if constexpr (KIND == GEMM_QKV) {
-    const int pps = a.d >> 4, pph = a.hd >> 4;
-    const int pw = u % pps;
-    const int pair = (pw % pph) * 8 + (n & 7);
+    const int pph = a.hd >> 4;  // sections start at multiples of pph panels
+    const int pair = (u % pph) * 8 + (n & 7);
     const Rsrc rr = make_rsrc(a.rope, 0x7ffffff0u);
     const float2 cs = ld_f32x2<false>(rr, ok ? (uint32_t)((pos * (a.hd >> 1) + pair) * 2) * 4u : kOob);
     e.a = cs.x;
@@ -130,9 +130,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int u, int ml
   constexpr uint32_t ELT = WBF16 ? 2u : 4u;
   constexpr int S = WBF16 ? kActSplits : 1;
   if constexpr (KIND == GEMM_QKV) {
-    const int pps = a.d >> 4, pph = a.hd >> 4;
-    const int sec = u / pps, pw = u - sec * pps;
-    const int h = pw / pph, wg = pw - h * pph;
+    const int pph = a.hd >> 4;
+    int pw;
+    const int sec = qkv_section(u, a.d, a.Hkv * a.hd, &pw);
+    const int h = pw / pph, wg = pw - h * pph;  // query head (sec 0) or K/V head
     const int pair = wg * 8 + (n & 7);
     const bool hi = n >= 8;
     const int f = pair + (hi ? (a.hd >> 1) : 0);
@@ -144,7 +145,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int u, int ml
     const Rsrc rq = make_rsrc(a.q_out + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
     st_f32<COH>(rq, (rok && sec == 0) ? (uint32_t)(ml * a.d + h * a.hd + f) * 4u : kOob, v);
     // K rows [pos][hd]; V transposed, rows [feature][stride]
-    const uint32_t head = (uint32_t)(bg * a.H + h) * (uint32_t)a.kv_stride * (uint32_t)a.hd;
+    const uint32_t head = (uint32_t)(bg * a.Hkv + h) * (uint32_t)a.kv_stride * (uint32_t)a.hd;
     const uint32_t elem = sec == 1 ? head + (uint32_t)(pos * a.hd + f) : head + (uint32_t)(f * a.kv_stride + pos);
     const Rsrc rkv = make_rsrc(sec == 1 ? a.kc : a.vc, a.kv_bytes);
     const bool kok = rok && sec > 0;

@@ -157,6 +157,7 @@ struct AttnParams {
   const void* vc;
   const int32_t* lens;
   int b0, R, H, d, kv_stride;
+  int Hkv, G;  // K/V heads of the cache; query head h reads K/V head h / G
   int CK, NC;
   float scale;
   float* part_o;
@@ -242,7 +243,7 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   const size_t bh = (size_t)bl * p.H + h;
   float* po = p.part_o + ((bh * p.NC + c) * p.Rmax) * HD;
   float* pml = p.part_ml + ((bh * p.NC + c) * p.Rmax) * 2;
-  const size_t kbase = ((size_t)bg * p.H + h) * p.kv_stride * HD;  // K rows [key][HD]
+  const size_t kbase = ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * HD;  // K rows [key][HD]
   const size_t vbase = kbase;                                       // V^T rows [feature][kv_stride]
 
   if (k_lo < k_hi) {
@@ -582,7 +583,7 @@ attn_b_kernel(AttnParams p) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int bl = blockIdx.z, h = blockIdx.y, bg = p.b0 + bl;
   const AttnItem it = attn_item<CK>(true, bl, h, blockIdx.x, p.lens[bg], p.R, p.kc, p.vc,
-                                    ((size_t)bg * p.H + h) * p.kv_stride * kAttnHd);
+                                    ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * kAttnHd);
   if (!it.active) return;  // past the request's last key: uniform, before any barrier
   float4 qr[8];
   attn_load_q(it, p.q + (size_t)(bl * p.R) * p.d + h * kAttnHd, p.d, p.R, lane, qr);
@@ -640,7 +641,7 @@ struct PackParams {
   uint8_t* dst;
   int kind, wbf16;
   int N_src, row_off, K, NKB, n_units, pad_from, N_logical;
-  int d, hd, F;
+  int d, hd, F, dkv;
 };
 
 __global__ void pack_kernel(PackParams p) {
@@ -652,7 +653,7 @@ __global__ void pack_kernel(PackParams p) {
   const size_t t = chunk >> 9;
   const int kb = (int)(t % p.NKB);
   const int u = (int)(t / p.NKB);
-  const int row = panel_row(p.kind, u, lane & 15, p.d, p.hd, p.F);
+  const int row = panel_row(p.kind, u, lane & 15, p.d, p.hd, p.F, p.dkv);
   const int g = lane >> 4;
   const int k = p.wbf16 ? kb * 256 + 32 * j + 8 * g : kb * 128 + 16 * j + 4 * g;
   const int srow = row - p.row_off;
@@ -842,7 +843,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   const Workspace& W = md->ws;
   const bool wb = D.wdt == SPADE_BF16;
   const int KBd = kblock_of(D.wdt);
-  const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->stride * D.hd;  // elements
+  const size_t kv_layer = (size_t)kv->max_batch * D.KVH * kv->stride * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
   const uint8_t* lb = md->weights + (size_t)layer * md->lay.layer_bytes;
   const int M = fc.nb * fc.R;
@@ -855,6 +856,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   g.eps = D.eps;
   g.n_ssq = D.d / 16;
   g.H = D.H;
+  g.Hkv = D.KVH;
   g.hd = D.hd;
   g.d = D.d;
   g.F = D.F;
@@ -871,7 +873,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   size_t act_split;
   switch (kind) {
     case GEMM_QKV:
-      wmat = lb + md->lay.qkv; K = D.d; units = 3 * D.d / 16; act = W.act_n; act_split = W.act_split;
+      wmat = lb + md->lay.qkv; K = D.d; units = (D.d + 2 * D.dkv) / 16; act = W.act_n; act_split = W.act_split;
       g.ssq_in = W.ssq;
       g.q_out = W.q;
       g.kc = kv->k + (size_t)layer * kv_layer * kv_elt;
@@ -984,7 +986,7 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   else hipLaunchKernelGGL(embed_kernel<false>, egrid, dim3(256), 0, st, ep);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
-  const size_t kv_layer = (size_t)kv->max_batch * D.H * kv->stride * D.hd;  // elements
+  const size_t kv_layer = (size_t)kv->max_batch * D.KVH * kv->stride * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
 
   // attention chunks over the longest request: for a bf16 cache with
@@ -1006,6 +1008,8 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     ap.b0 = fc.b0;
     ap.R = fc.R;
     ap.H = D.H;
+    ap.Hkv = D.KVH;
+    ap.G = D.H / D.KVH;
     ap.d = D.d;
     ap.kv_stride = kv->stride;
     ap.CK = CK;
@@ -1070,10 +1074,13 @@ hipError_t launch_pack(spade_model md, int kind, int layer, const void* src, hip
   pp.d = D.d;
   pp.hd = D.hd;
   pp.F = D.F;
+  pp.dkv = D.dkv;
   switch (kind) {
     case SPADE_WQ: case SPADE_WK: case SPADE_WV:
-      pp.kind = GEMM_QKV; pp.K = D.d; pp.N_src = D.d; pp.row_off = (kind - SPADE_WQ) * D.d;
-      pp.N_logical = 3 * D.d; pp.n_units = 3 * D.d / 16; dst = (uint8_t*)lb + md->lay.qkv; break;
+      pp.kind = GEMM_QKV; pp.K = D.d;
+      pp.N_src = kind == SPADE_WQ ? D.d : D.dkv;
+      pp.row_off = kind == SPADE_WQ ? 0 : (kind == SPADE_WK ? D.d : D.d + D.dkv);
+      pp.N_logical = D.d + 2 * D.dkv; pp.n_units = pp.N_logical / 16; dst = (uint8_t*)lb + md->lay.qkv; break;
     case SPADE_WO:
       pp.kind = GEMM_O; pp.K = D.d; pp.N_src = D.d; pp.row_off = 0; pp.N_logical = D.d;
       pp.n_units = D.d / 16; dst = (uint8_t*)lb + md->lay.o; break;

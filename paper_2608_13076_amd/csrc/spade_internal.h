@@ -35,22 +35,32 @@ enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 
 
 inline int kblock_of(int weight_dtype) { return weight_dtype == SPADE_BF16 ? 256 : 128; }
 
+// QKV section of arena panel p: 0 (queries, d_model / 16 panels), 1 (keys) or
+// 2 (values, dkv / 16 panels each), and the panel's index within it.
+__host__ __device__ inline int qkv_section(int p, int d_model, int dkv, int* pw) {
+  const int pq = d_model / 16, pk = dkv / 16;
+  const int s = p < pq ? 0 : (p < pq + pk ? 1 : 2);
+  *pw = p - (s == 0 ? 0 : (s == 1 ? pq : pq + pk));
+  return s;
+}
+
 // Row of the logical [N, K] weight matrix held by row r (0..15) of arena
 // panel p.  Panels are stored in order, each as its k-blocks in order.
-//   QKV (N = 3d, rows of Wq, Wk, Wv): panel p of section s holds, for head h
-//     and group w, features w*8 .. w*8+7 in rows 0..7 and their rotary
-//     partners w*8+hd/2 .. w*8+7+hd/2 in rows 8..15, so lanes n and n^8 of an
-//     MFMA output hold a RoPE pair.
+//   QKV (N = d + 2 dkv, rows of Wq, Wk, Wv; dkv = kv heads * hd): panel p of
+//     section s holds, for head h and group w, features w*8 .. w*8+7 in rows
+//     0..7 and their rotary partners w*8+hd/2 .. w*8+7+hd/2 in rows 8..15, so
+//     lanes n and n^8 of an MFMA output hold a RoPE pair.
 //   GU (N = 2F, gate rows then up rows): panel p holds gate rows p*8 .. p*8+7
 //     in rows 0..7 and the matching up rows in rows 8..15.
 //   O, DOWN, LM: panel p holds rows p*16 .. p*16+15.
-__host__ __device__ inline int panel_row(int kind, int p, int r, int d_model, int head_dim, int d_ffn) {
+__host__ __device__ inline int panel_row(int kind, int p, int r, int d_model, int head_dim, int d_ffn, int dkv) {
   if (kind == GEMM_QKV) {
-    const int pps = d_model / 16, pph = head_dim / 16;
-    const int s = p / pps, pw = p % pps;
+    const int pph = head_dim / 16;
+    int pw;
+    const int s = qkv_section(p, d_model, dkv, &pw);
     const int h = pw / pph, w = pw % pph;
     const int f = w * 8 + (r & 7) + (r >= 8 ? head_dim / 2 : 0);
-    return s * d_model + h * head_dim + f;
+    return (s == 0 ? 0 : (s == 1 ? d_model : d_model + dkv)) + h * head_dim + f;
   }
   if (kind == GEMM_GU) return (r < 8) ? p * 8 + r : d_ffn + p * 8 + (r - 8);
   return p * 16 + r;
@@ -99,6 +109,7 @@ inline FusedArena fused_arena_of(int L, int d, int F) {
 
 struct Dims {
   int L, d, H, hd, F, V, Vpad, wdt, kvdt;
+  int KVH, dkv;  // K/V heads (grouped-query attention: H / KVH query heads each) and their width KVH * hd
   float eps, theta;
 };
 

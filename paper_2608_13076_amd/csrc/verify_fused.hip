@@ -207,6 +207,7 @@ __device__ __forceinline__ GemmParams fused_gemm_params(const FusedParams& P, in
   g.eps = P.eps;
   g.n_ssq = P.d >> 4;
   g.H = P.H;
+  g.Hkv = P.H;
   g.hd = kHd;
   g.d = P.d;
   g.F = P.F;
@@ -429,6 +430,7 @@ bool fused_eligible(spade_model md, spade_kv kv, const ForwardCall& fc) {
   const Dims& D = md->dims;
   if (!md->fused_ok || md->ws.fused == nullptr) return false;
   if (D.wdt != SPADE_BF16 || D.kvdt != SPADE_BF16 || D.hd != kHd) return false;
+  if (D.KVH != D.H) return false;  // multi-head attention only
   if (fc.tokens != nullptr || fc.b0 != 0 || !fc.want_logits) return false;
   const int M = fc.nb * fc.R;
   if (M > kFusedRows || fc.R > kAttnRows) return false;

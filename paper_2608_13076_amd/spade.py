@@ -45,14 +45,16 @@ class SpadeConfig(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("weight_dtype", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
-                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float),
+                ("n_kv_heads", ctypes.c_int32)]
 
 
 def config_from(shape) -> SpadeConfig:
     """spade_config from any object with the ModelShape attributes."""
     return SpadeConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.d_ffn,
                        shape.vocab, BF16 if shape.weight_dtype == "bf16" else F32,
-                       BF16 if shape.kv_dtype == "bf16" else F32, shape.rms_eps, shape.rope_theta)
+                       BF16 if shape.kv_dtype == "bf16" else F32, shape.rms_eps, shape.rope_theta,
+                       getattr(shape, "n_kv_heads", 0))
 
 
 _LIB = None

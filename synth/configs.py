@@ -16,7 +16,8 @@ from typing import List, Optional, Tuple
 
 @dataclass(frozen=True)
 class ModelShape:
-    """Pre-RMSNorm decoder with RoPE, multi-head attention and a SwiGLU FFN."""
+    """Pre-RMSNorm decoder with RoPE, multi-head (or grouped-query) attention
+    and a SwiGLU FFN."""
 
     name: str
     n_layers: int
@@ -33,11 +34,18 @@ class ModelShape:
     # Gains of the three RMSNorms.  1.0 everywhere for the full-size shapes;
     # the mini shapes draw them from N(1, gain_std) so a dropped gain shows.
     gain_std: float = 0.0
+    # K/V heads; 0 means one per query head (multi-head attention).
+    n_kv_heads: int = 0
+
+    @property
+    def kv_heads(self) -> int:
+        return self.n_kv_heads or self.n_heads
 
     def weight_bytes(self) -> int:
         elt = 2 if self.weight_dtype == "bf16" else 4
         d, f, v = self.d_model, self.d_ffn, self.vocab
-        per_layer = (4 * d * d + 3 * d * f) * elt + 2 * d * 4
+        dkv = self.kv_heads * self.head_dim
+        per_layer = (2 * d * d + 2 * d * dkv + 3 * d * f) * elt + 2 * d * 4
         return self.n_layers * per_layer + 2 * v * d * elt + d * 4
 
 
@@ -80,6 +88,12 @@ LLAMA_13B = ModelShape("llama-13b-shape", n_layers=40, d_model=5120, n_heads=40,
                        head_dim=128, d_ffn=13824, vocab=32000)
 LLAMA_33B = ModelShape("llama-33b-shape", n_layers=60, d_model=6656, n_heads=52,
                        head_dim=128, d_ffn=17920, vocab=32000)
+# The paper's cloud verifier's shape (LLaMA-3.1-8B: grouped-query attention
+# with 8 K/V heads for 32 query heads, a 128256-token vocabulary, RoPE base
+# 500000); random weights as for the other shapes.
+LLAMA3_8B = ModelShape("llama3-8b-gqa-shape", n_layers=32, d_model=4096, n_heads=32,
+                       head_dim=128, d_ffn=14336, vocab=128256, n_kv_heads=8,
+                       rope_theta=500000.0)
 
 WORKLOADS = {
     "c1_tiny_greedy": Workload(
@@ -110,6 +124,16 @@ WORKLOADS = {
         draft_recipe="chain_half", rounds=2, seed=1005,
         description="33B-shaped bf16 verifier, 4 requests x 1536 cached tokens, "
                     "gamma=6, greedy, kv_commit then a second verify round"),
+    "gqa_8b_greedy": Workload(
+        "gqa_8b_greedy", LLAMA3_8B, batch=1, gamma=5, ctx=(1024, 1024), mode="greedy",
+        draft_recipe="random", seed=1006,
+        description="8B-shaped bf16 verifier with grouped-query attention (8 K/V heads) and a "
+                    "128256-token vocabulary, 1024 cached tokens, gamma=5, greedy"),
+    "gqa_8b_batched": Workload(
+        "gqa_8b_batched", LLAMA3_8B, batch=16, gamma=8, ctx=(256, 4096), mode="mixed",
+        draft_recipe="chain_half", seed=1007,
+        description="8B-shaped GQA verifier, 16 requests, contexts U[256,4096], gamma=8, "
+                    "mixed greedy/sampling (sampling rows: q = softmax(N(0,1)))"),
 }
 
 
@@ -124,6 +148,9 @@ MINI_BF16 = ModelShape("mini-bf16", n_layers=2, d_model=512, n_heads=4, head_dim
                        d_ffn=1536, vocab=4001, init_std=0.06, gain_std=0.1)
 MINI_BF16_WIDE = ModelShape("mini-bf16-wide", n_layers=3, d_model=1024, n_heads=8,
                             head_dim=128, d_ffn=2816, vocab=8011, init_std=0.05, gain_std=0.1)
+MINI_GQA = ModelShape("mini-gqa", n_layers=2, d_model=1024, n_heads=8, head_dim=128,
+                      d_ffn=2816, vocab=12007, n_kv_heads=2, rope_theta=500000.0,
+                      init_std=0.05, gain_std=0.1)
 MINI_F32 = ModelShape("mini-f32", n_layers=2, d_model=256, n_heads=4, head_dim=64,
                       d_ffn=768, vocab=1999, weight_dtype="f32", kv_dtype="f32", init_std=0.06,
                       gain_std=0.1)
@@ -141,4 +168,8 @@ def mini_workloads() -> List[Workload]:
                  mode="mixed", draft_recipe="chain_half", seed=2004),
         Workload("mini_bf16_wide_b5", MINI_BF16_WIDE, batch=5, gamma=6, ctx=(60, 700),
                  mode="mixed", draft_recipe="chain_half", seed=2005),
+        Workload("mini_gqa_greedy", MINI_GQA, batch=1, gamma=5, ctx=(300, 300),
+                 mode="greedy", draft_recipe="chain_half", seed=2006),
+        Workload("mini_gqa_mixed_b5", MINI_GQA, batch=5, gamma=6, ctx=(40, 650),
+                 mode="mixed", draft_recipe="chain_half", seed=2007),
     ]

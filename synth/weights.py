@@ -70,8 +70,9 @@ def normal_table_bf16(std: float) -> np.ndarray:
 
 def tensor_shape(shape: ModelShape, kind: str) -> Tuple[int, ...]:
     d, f, v = shape.d_model, shape.d_ffn, shape.vocab
+    dkv = shape.kv_heads * shape.head_dim
     return {
-        "wq": (d, d), "wk": (d, d), "wv": (d, d), "wo": (d, d),
+        "wq": (d, d), "wk": (dkv, d), "wv": (dkv, d), "wo": (d, d),
         "wg": (f, d), "wu": (f, d), "wd": (d, f),
         "g_attn": (d,), "g_ffn": (d,), "g_final": (d,),
         "embed": (v, d), "lm_head": (v, d),

@@ -49,6 +49,24 @@ def test_buffer_sizes(lib):
         assert lib.spade_workspace_bytes(ctypes.byref(cfg), 4, 16, 1000) == 0  # gamma + 1 > 16
 
 
+def test_gqa_buffer_sizes(lib):
+    m = workload("gqa_8b_greedy").model
+    cfg = spade.config_from(m)
+    assert cfg.n_kv_heads == 8
+    wb = lib.spade_weight_bytes(ctypes.byref(cfg))
+    d, f, v, dkv = m.d_model, m.d_ffn, m.vocab, m.kv_heads * m.head_dim
+    vpad = (v + 15) // 16 * 16
+    mats = m.n_layers * (2 * d * d + 2 * d * dkv + 3 * d * f) + (v + vpad) * d
+    assert mats * 2 <= wb <= mats * 2 + (6 * m.n_layers + 8) * 256 + (2 * m.n_layers + 1) * d * 4
+    # the cache holds the 8 K/V heads only
+    kvb = lib.spade_kv_bytes(ctypes.byref(cfg), 2, 1024)
+    assert 2 * m.n_layers * 2 * 8 * 1024 * m.head_dim * 2 <= kvb < 2 * m.n_layers * 2 * 9 * 1024 * m.head_dim * 2
+    # 0 means one K/V head per query head; a non-divisor is rejected
+    for kvh, ok in ((0, True), (32, True), (1, True), (3, False), (-1, False)):
+        bad = m.__class__(**{**m.__dict__, "n_kv_heads": kvh})
+        assert (lib.spade_weight_bytes(ctypes.byref(spade.config_from(bad))) > 0) == ok, kvh
+
+
 def test_unsupported_configs(lib):
     base = workload("c2_7b_greedy").model
     for kw in (dict(head_dim=96, n_heads=32, d_model=3072), dict(d_model=4000, n_heads=40, head_dim=100),

@@ -92,14 +92,14 @@ def _greedy_consistent(lg_b, drafts_b, n_b, c_b):
     return n_b == n_exp and c_b == am[n_exp]
 
 
-def test_c4_7b_batched_properties():
-    w = workload("c4_7b_batched")
+def _batched_properties(name):
+    w = workload(name)
     inp = make_inputs(w)
     max_len = int(inp.lens.max()) + 2 * (w.gamma + 1) + 8
-    print(f"[c4] weights + prefill of {int(inp.lens.sum())} tokens", flush=True)
+    print(f"[{name}] weights + prefill of {int(inp.lens.sum())} tokens", flush=True)
     model, kv = gpu_setup_streaming(w, max_len)
     gpu_prefill(kv, inp)
-    print("[c4] verify B=16", flush=True)
+    print(f"[{name}] verify B={w.batch}", flush=True)
     lg, n, c, _ = gpu_verify(model, kv, inp)
     assert model.device_error() == 0
     # batch independence: the first k requests alone give bit-identical rows
@@ -110,7 +110,7 @@ def test_c4_7b_batched_properties():
         sub.modes = inp.modes[:k].copy()
         sub.draft_probs = None if inp.draft_probs is None else inp.draft_probs[:k].copy()
         sub.workload = w.with_(batch=k)
-        print(f"[c4] verify B={k}", flush=True)
+        print(f"[{name}] verify B={k}", flush=True)
         lgk, nk, ck, _ = gpu_verify(model, kv, sub)
         np.testing.assert_array_equal(lgk, lg[:k])
         np.testing.assert_array_equal(nk, n[:k])
@@ -134,6 +134,17 @@ def test_c4_7b_batched_properties():
     _check_layer0_keys(w, inp, kv, max_len)
 
 
+def test_c4_7b_batched_properties():
+    _batched_properties("c4_7b_batched")
+
+
+def test_gqa_8b_batched_properties():
+    """The LLaMA-3.1-8B-shaped verifier (grouped-query attention, 8 K/V
+    heads; 128256-token vocabulary) under the same properties; its layer-0 K
+    rows (8 heads per request) match the oracle's."""
+    _batched_properties("gqa_8b_batched")
+
+
 def _check_layer0_keys(w, inp, kv, max_len, n_samples=24):
     import torch
     from oracle.decoder import Decoder, apply_rope, bf16_round, rms_norm, rope_tables
@@ -145,6 +156,7 @@ def _check_layer0_keys(w, inp, kv, max_len, n_samples=24):
     from oracle.decoder import bf16_bits_to_f64
     E = bf16_bits_to_f64(emb) if emb.dtype == np.uint16 else emb.astype(np.float64)
     Wk = bf16_bits_to_f64(wk) if wk.dtype == np.uint16 else wk.astype(np.float64)
+    KVH = m.kv_heads
     stride = (max_len + 31) // 32 * 32
     kcache = kv.buf[: kv.buf.numel() // 2].view(torch.int16 if m.kv_dtype == "bf16" else torch.float32)
     rng = np.random.default_rng(5)
@@ -153,11 +165,11 @@ def _check_layer0_keys(w, inp, kv, max_len, n_samples=24):
         pos = int(rng.integers(0, int(inp.lens[b])))
         tok = int(inp.prompts[b][pos])
         h = rms_norm(E[tok][None], g.astype(np.float64), m.rms_eps)
-        k = (h @ Wk.T).reshape(1, m.n_heads, m.head_dim)
+        k = (h @ Wk.T).reshape(1, KVH, m.head_dim)
         cs, sn = rope_tables(np.array([pos]), m.head_dim, m.rope_theta)
         k = bf16_round(apply_rope(k, cs, sn))[0]
-        for hh in (0, m.n_heads - 1):
-            off = ((b * m.n_heads + hh) * stride + pos) * m.head_dim
+        for hh in (0, KVH - 1):
+            off = ((b * KVH + hh) * stride + pos) * m.head_dim
             row = kcache[off: off + m.head_dim].cpu().numpy()
             got = (row.view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
             # equal up to one bf16 rounding step of float32 differences

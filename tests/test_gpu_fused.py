@@ -1,8 +1,8 @@
 """The single-launch verify pass against the oracle and against the
 one-kernel-per-stage path, through the C ABI.
 
-Eligible workloads (bf16 weights and cache, head_dim 128, B * (gamma+1) <=
-16) run both paths on the same model, cache and inputs:
+Eligible workloads (bf16 weights and cache, head_dim 128, multi-head
+attention, B * (gamma+1) <= 16) run both paths on the same model, cache and inputs:
 * each path meets the parity bar of test_gpu_parity.py against the oracle;
 * the two paths agree bit for bit (logits, n_accepted, correction): they run
   the same GEMM engine, attention arithmetic and accept code;
@@ -29,7 +29,7 @@ def need_gpu():
 def _eligible(w):
     m = w.model
     return m.weight_dtype == "bf16" and m.kv_dtype == "bf16" and m.head_dim == 128 and \
-        w.batch * (w.gamma + 1) <= 16
+        m.kv_heads == m.n_heads and w.batch * (w.gamma + 1) <= 16
 
 
 FUSED_CASES = [w for w in mini_workloads() if _eligible(w)]

@@ -6,7 +6,10 @@
 * the paper's statement that one verify pass over d+1 positions yields the
   autoregressive conditionals (Sec. III-B, Algorithm 1): verify logits equal
   d+1 sequential single-token decodes and a from-scratch recompute;
-* RoPE invariants: norm preservation and dependence on relative position only.
+* RoPE invariants: norm preservation and dependence on relative position only;
+* grouped-query attention: the library decoder with fewer K/V heads, and the
+  special case it reduces to -- multi-head attention whose K/V projections
+  repeat each K/V head's rows for every query head of its group.
 """
 
 import numpy as np
@@ -27,6 +30,9 @@ def _model(shape, seed=7, keep=True):
 
 SMALL_F32 = ModelShape("t-f32", n_layers=2, d_model=64, n_heads=2, head_dim=32, d_ffn=96,
                        vocab=97, weight_dtype="f32", kv_dtype="f32", init_std=0.08, gain_std=0.2)
+SMALL_GQA = ModelShape("t-gqa", n_layers=2, d_model=128, n_heads=4, head_dim=32, d_ffn=96,
+                       vocab=97, weight_dtype="f32", kv_dtype="f32", init_std=0.08, gain_std=0.2,
+                       n_kv_heads=2, rope_theta=500000.0)
 SMALL_BF16 = ModelShape("t-bf16", n_layers=2, d_model=128, n_heads=2, head_dim=64, d_ffn=256,
                         vocab=211, weight_dtype="bf16", kv_dtype="bf16", init_std=0.05, gain_std=0.2)
 
@@ -80,7 +86,7 @@ def _hf_model(shape, mw):
     from transformers import LlamaConfig, LlamaForCausalLM
     cfg = LlamaConfig(vocab_size=shape.vocab, hidden_size=shape.d_model,
                       intermediate_size=shape.d_ffn, num_hidden_layers=shape.n_layers,
-                      num_attention_heads=shape.n_heads, num_key_value_heads=shape.n_heads,
+                      num_attention_heads=shape.n_heads, num_key_value_heads=shape.kv_heads,
                       head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps,
                       rope_theta=shape.rope_theta, max_position_embeddings=512,
                       tie_word_embeddings=False, attention_bias=False, mlp_bias=False)
@@ -101,11 +107,12 @@ def _hf_model(shape, mw):
     return m
 
 
-def test_decoder_matches_hf_llama():
-    dec, mw = _model(SMALL_F32)
-    hf = _hf_model(SMALL_F32, mw)
+@pytest.mark.parametrize("shape", [SMALL_F32, SMALL_GQA], ids=lambda s: s.name)
+def test_decoder_matches_hf_llama(shape):
+    dec, mw = _model(shape)
+    hf = _hf_model(shape, mw)
     rng = np.random.default_rng(3)
-    toks = rng.integers(0, SMALL_F32.vocab, 40)
+    toks = rng.integers(0, shape.vocab, 40)
     with torch.no_grad():
         ref = hf(torch.from_numpy(toks)[None]).logits[0].numpy()
     cache = dec.new_cache(64)
@@ -116,7 +123,41 @@ def test_decoder_matches_hf_llama():
     assert np.abs(ref).max() > 0.5  # the comparison is not trivially small
 
 
-@pytest.mark.parametrize("shape", [SMALL_F32, SMALL_BF16])
+def test_gqa_equals_mha_with_repeated_kv_heads():
+    from dataclasses import replace
+    gqa, mw = _model(SMALL_GQA)
+    G = SMALL_GQA.n_heads // SMALL_GQA.kv_heads
+    hd = SMALL_GQA.head_dim
+
+    def get_mha(kind, layer=None):
+        t = mw.get(kind, layer)
+        if kind in ("wk", "wv"):  # [KVH*hd, d] -> [H*hd, d], K/V head j serves query heads jG..jG+G-1
+            t = np.repeat(t.reshape(SMALL_GQA.kv_heads, hd, -1), G, axis=0).reshape(SMALL_GQA.n_heads * hd, -1)
+        return t
+
+    mha_shape = replace(SMALL_GQA, n_kv_heads=0)
+    mha = Decoder(mha_shape, get_mha, keep_f64=True)
+    rng = np.random.default_rng(8)
+    toks = rng.integers(0, SMALL_GQA.vocab, 36)
+    c1, c2 = gqa.new_cache(48), mha.new_cache(48)
+    gqa.prefill(c1, toks[:30])
+    mha.prefill(c2, toks[:30])
+    a, b = gqa.forward(c1, toks[30:]), mha.forward(c2, toks[30:])
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+    assert c1.k[0].shape[0] == SMALL_GQA.kv_heads and c2.k[0].shape[0] == SMALL_GQA.n_heads
+    # a genuinely different model if the K/V heads are paired with the wrong query heads
+    def get_wrong(kind, layer=None):
+        t = get_mha(kind, layer)
+        if kind in ("wk", "wv"):
+            t = t.reshape(SMALL_GQA.n_heads, hd, -1)[::-1].reshape(SMALL_GQA.n_heads * hd, -1)
+        return t
+    wrong = Decoder(mha_shape, get_wrong, keep_f64=True)
+    c3 = wrong.new_cache(48)
+    wrong.prefill(c3, toks[:30])
+    assert np.abs(wrong.forward(c3, toks[30:]) - a).max() > 1e-3
+
+
+@pytest.mark.parametrize("shape", [SMALL_F32, SMALL_BF16, SMALL_GQA], ids=lambda s: s.name)
 def test_verify_block_equals_sequential_decodes(shape):
     dec, _ = _model(shape)
     rng = np.random.default_rng(4)
