@@ -125,11 +125,11 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.attn_ml = take((size_t)max_batch * D.H * p.NCmax * p.Rmax * 2 * 4);
   p.attn_cnt = take((size_t)max_batch * D.H * 4);
   p.logits = take((size_t)p.Mmax * D.V * 4);
-  p.stats = take((size_t)p.Mmax * std::max(NU, kMaxStatGroups) * 3 * 4);
+  p.stats = take((size_t)p.Mmax * std::max(NU, kMaxStatGroups) * 3 * 4);  // NU = panels of the LM head
   p.rope = take((size_t)max_len * (D.hd / 2) * 2 * 4);
   p.err = take(4);
   p.bar = take(kBarBytes);
-  p.max_units = std::max(3 * D.d, 2 * D.F) / 16;
+  p.max_units = std::max(std::max(D.d + 2 * D.dkv, 2 * D.F), D.Vpad) / 16;
   p.split_cnt = take((size_t)p.max_units * 4);
   p.split_part = take((size_t)p.max_units * 8 * 256 * 4);
   // the single-launch pass handles bf16 weights and cache with head_dim 128
@@ -417,6 +417,7 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
   ac.logits = fc.logits_out;
   ac.stats = m->ws.stats;
   ac.NU = std::min(m->dims.Vpad / 16, m->gemm_wgs);  // LM-head workgroups (fused: n_cu, set there)
+  ac.panels = lm_stats_panels(m, B * (gamma + 1));
   ac.drafts = d_draft_tokens;
   ac.q = d_draft_probs;
   ac.u = d_uniforms;

@@ -13,6 +13,7 @@ struct AcceptParams {
   const float* logits;
   const float* stats;
   int NU;
+  int panels;  // 0: stats holds NU workgroup entries per row; > 0: one entry per panel
   int V, gamma, R;
   const int32_t* drafts;
   const float* q;
@@ -97,7 +98,21 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
   // fixed order
   for (int r = wave; r < R; r += NWV) {
     RowStat st{-INFINITY, 0.f, 0x7fffffff};
-    if (p.stats != nullptr) {
+    if (p.stats != nullptr && p.panels > 0) {
+      // per-panel statistics: rebuild the NU workgroup entries of the skinny
+      // LM head (workgroup q folds panels q, q + NU, ... in order), then merge
+      // them exactly as below
+      const float* sp = p.stats + (size_t)(b * R + r) * p.panels * 3;
+      for (int q = lane; q < p.NU; q += 64) {
+        RowStat one{-INFINITY, 0.f, 0x7fffffff};
+        for (int u = q; u < p.panels; u += p.NU) {
+          const RowStat ps{ld_any<COH>(sp + u * 3), ld_any<COH>(sp + u * 3 + 1),
+                           __float_as_int(ld_any<COH>(sp + u * 3 + 2))};
+          if (ps.m != -INFINITY) one = merge_stat(one, ps);
+        }
+        if (one.m != -INFINITY) st = merge_stat(st, one);
+      }
+    } else if (p.stats != nullptr) {
       const float* sp = p.stats + (size_t)(b * R + r) * p.NU * 3;
 #pragma unroll 8
       for (int q = lane; q < p.NU; q += 64) {

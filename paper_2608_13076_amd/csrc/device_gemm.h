@@ -64,6 +64,7 @@ struct GemmParams {
   int V;
   float* stats;  // [M][NU][3]: (max, sum exp, argmax) of z = logit (/T) per row and workgroup
   int NU;        // workgroups of the LM-head launch
+  float* pstats; // [M][n_units][3]: the same per row and panel (wide-row and split-K LM heads)
   const uint8_t* mode;
   float inv_T;
   int have_q;
@@ -174,6 +175,56 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int u, int ml
                               (uint32_t)((S - 1) * (size_t)split_b + (size_t)a.M * a.act_out_stride * ELT));
     st_act<WBF16, COH>(ro, split_b, (uint32_t)(ml * a.act_out_stride + u * 8 + n), rok && n < 8, act);
   }
+}
+
+// LM head: store the logit of (launch row ml, column n of panel u) and return
+// the panel's (max, sum exp, argmax) of z = logit (/T for sampling rows) over
+// its 16 columns (every lane of the 16 gets it; ties keep the lower id).
+// Every lane of the wave calls it.
+template <bool COH>
+__device__ __forceinline__ RowStat gemm_lm_panel(const GemmParams& a, int u, int ml, int n, bool rok, bool samp,
+                                                 float rinv, float val, bool& nan_seen) {
+  const int col = u * 16 + n;
+  const bool valid = rok && col < a.V;
+  const float lg = val * rinv;
+  const Rsrc rl = make_rsrc(a.logits + (size_t)a.m0 * a.V, (uint32_t)((size_t)a.M * a.V * 4));
+  st_f32<COH>(rl, valid ? (uint32_t)(ml * a.V + col) * 4u : kOob, lg);
+  const bool isnan = lg != lg;
+  nan_seen = nan_seen || (valid && isnan);
+  const bool use = valid && !isnan;
+  const float z = use ? (samp ? lg * a.inv_T : lg) : -INFINITY;
+  const int id = use ? col : 0x7fffffff;
+  float zm = z;
+  int am = id;
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) {
+    const float oz = __shfl_xor(zm, off);
+    const int oa = __shfl_xor(am, off);
+    const bool take = oz > zm || (oz == zm && oa < am);
+    zm = take ? oz : zm;
+    am = take ? oa : am;
+  }
+  float ex = (z == -INFINITY) ? 0.f : expf(z - zm);
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) ex += __shfl_xor(ex, off);
+  return RowStat{zm, ex, am};
+}
+
+// Store a panel's statistics at pstats[m0 + ml][u] (lane n == 0 of the 16).
+__device__ __forceinline__ void gemm_lm_store_panel(const GemmParams& a, int u, int ml, int n, bool rok,
+                                                    const RowStat& ps) {
+  const Rsrc rs = make_rsrc(a.pstats + (size_t)a.m0 * a.n_units * 3, (uint32_t)((size_t)a.M * a.n_units * 12));
+  const uint32_t so = (rok && n == 0) ? (uint32_t)((ml * a.n_units + u) * 3) * 4u : kOob;
+  st_f32<false>(rs, so, ps.m);
+  st_f32<false>(rs, so == kOob ? kOob : so + 4u, ps.s);
+  st_f32<false>(rs, so == kOob ? kOob : so + 8u, __int_as_float(ps.a));
+}
+
+// Sampling row?  (launch row ml of request (m0 + ml) / R)
+__device__ __forceinline__ bool gemm_lm_samp(const GemmParams& a, int ml, bool rok) {
+  if (!rok || a.mode == nullptr) return false;
+  const int bl = (a.m0 + ml) / a.R;
+  return a.mode[bl] == SPADE_SAMPLE && a.have_q;
 }
 
 // 1/rms of launch row `row` from the producer's per-16-column sums of
@@ -380,32 +431,10 @@ struct Gemm {
     if constexpr (KIND != GEMM_LM) {
       gemm_epilogue<KIND, WBF16, COH>(a, u, ml, n, rok, pos, bg, rinv, val, e);
     } else {  // GEMM_LM: logits and the panel's (max, sum exp, argmax) of z = logit / T
-      const int col = u * 16 + n;
-      const bool valid = rok && col < a.V;
-      const float lg = val * rinv;
-      const Rsrc rl = make_rsrc(a.logits + (size_t)a.m0 * a.V, (uint32_t)((size_t)a.M * a.V * 4));
-      st_f32<COH>(rl, valid ? (uint32_t)(ml * a.V + col) * 4u : kOob, lg);
-      const bool isnan = lg != lg;
-      nan_seen = nan_seen || (valid && isnan);
-      const bool use = valid && !isnan;
-      const float z = use ? (samp ? lg * a.inv_T : lg) : -INFINITY;
-      const int id = use ? col : 0x7fffffff;
-      float zm = z;
-      int am = id;
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) {
-        const float oz = __shfl_xor(zm, off);
-        const int oa = __shfl_xor(am, off);
-        const bool take = oz > zm || (oz == zm && oa < am);
-        zm = take ? oz : zm;
-        am = take ? oa : am;
-      }
-      float ex = (z == -INFINITY) ? 0.f : expf(z - zm);
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) ex += __shfl_xor(ex, off);
       // fold the panel into this workgroup's running statistics of the row
       // (panels in the workgroup's unit order); stored once after the loop
-      if (zm != -INFINITY) lmrun = merge_stat(lmrun, RowStat{zm, ex, am});
+      const RowStat ps = gemm_lm_panel<COH>(a, u, ml, n, rok, samp, rinv, val, nan_seen);
+      if (ps.m != -INFINITY) lmrun = merge_stat(lmrun, ps);
     }
   }
 

@@ -1,7 +1,8 @@
-// Split-K skinny GEMM for the projection kinds (QKV, O, gate/up, down) when
-// the activation operand (<= 16 rows) is too long for one LDS copy: the
-// down projection at 7B (6 rows x 11008 x two bf16 terms = 264 KB) and every
-// projection at 13B.  The skinny engine (device_gemm.h) then has to fetch the
+// Split-K skinny GEMM for the projections (QKV, O, gate/up, down) and the LM
+// head when the activation operand (<= 16 rows) is too long for one LDS copy:
+// the down projection at 7B (6 rows x 11008 x two bf16 terms = 264 KB) and
+// every projection at 13B.  The LM head stores per-panel statistics, as in
+// the wide-row engine.  The skinny engine (device_gemm.h) then has to fetch the
 // operand from L2 with every weight tile, one tile ahead, and waits on that
 // round trip at every step.
 //
@@ -29,7 +30,7 @@
 
 namespace spade {
 
-constexpr int kSplitMaxGroups = 16;  // panel groups per workgroup (host-checked)
+constexpr int kSplitMaxGroups = 64;  // panel groups per workgroup (host-checked)
 
 struct GemmSplitSmem {
   float red[kGemmWaves][4][64];
@@ -237,20 +238,26 @@ struct GemmSplit {
       float val = v[0];
 #pragma unroll
       for (int r = RPS; r < 8; ++r) val += v[r];
-      int pos = 0, bg = 0;
-      if constexpr (KIND == GEMM_QKV) {
-        const int m = a.m0 + ml;
-        const int bl = m / a.R, ir = m - bl * a.R;
-        bg = a.b0 + bl;
-        if (rok) pos = a.lens[bg] + ir;
+      if constexpr (KIND == GEMM_LM) {
+        const bool samp = gemm_lm_samp(a, ml, rok);
+        bool nan_seen = false;
+        const RowStat ps = gemm_lm_panel<false>(a, uok ? u : 0, ml, n, rok, samp, sm.rinv[ml], val, nan_seen);
+        gemm_lm_store_panel(a, uok ? u : 0, ml, n, rok, ps);
+        if (nan_seen) flag_error(a.err, SPADE_DERR_NAN);
+      } else {
+        int pos = 0, bg = 0;
+        if constexpr (KIND == GEMM_QKV) {
+          const int m = a.m0 + ml;
+          const int bl = m / a.R, ir = m - bl * a.R;
+          bg = a.b0 + bl;
+          if (rok) pos = a.lens[bg] + ir;
+        }
+        const EpiIn e = gemm_epi_load<KIND, false>(a, uok ? u : 0, ml, n, rok, pos);
+        gemm_epilogue<KIND, true, false>(a, uok ? u : 0, ml, n, rok, pos, bg, sm.rinv[ml], val, e);
       }
-      const EpiIn e = gemm_epi_load<KIND, false>(a, uok ? u : 0, ml, n, rok, pos);
-      gemm_epilogue<KIND, true, false>(a, uok ? u : 0, ml, n, rok, pos, bg, sm.rinv[ml], val, e);
     }
   }
 
-  // Everything after prefetch() (the first three weight tiles, requested
-  // first so that HBM starts streaming at once).
   __device__ __forceinline__ void run() {
     fill_lds_a();
     for (int r = tid >> 4; r < 16; r += 32) {

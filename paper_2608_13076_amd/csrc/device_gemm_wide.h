@@ -1,6 +1,9 @@
-// Wide-row GEMM for the projection kinds (QKV, O, gate/up, down) when the
-// activation operand has more rows than the skinny engine (device_gemm.h)
-// keeps resident: batched verification, M = B (gamma + 1) up to 256 rows.
+// Wide-row GEMM for the projections (QKV, O, gate/up, down) and the LM head
+// when the activation operand has more rows than the skinny engine
+// (device_gemm.h) keeps resident: batched verification, M = B (gamma + 1) up
+// to 256 rows.  The LM head stores its logits and, per row and panel, the
+// panel's (max, sum exp, argmax); the accept step folds them in the skinny
+// engine's order.
 //
 // A workgroup of 8 waves owns 8P consecutive panels ("units"), P per wave,
 // and a group of RT 16-row tiles.  Each wave streams its panels' k-blocks
@@ -291,6 +294,7 @@ struct GemmWide {
     }
     __syncthreads();
     // epilogue: lane holds rows mt*16 + 4g + i, column kl of each unit
+    bool nan_seen = false;
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       const int u = ubase + p;
@@ -302,18 +306,28 @@ struct GemmWide {
           const int r = mt * 16 + 4 * g + i;
           const int ml = row0 + r;
           const bool rok = uok && ml < a.M;
-          int pos = 0, bg = 0;
-          if constexpr (KIND == GEMM_QKV) {
-            const int m = a.m0 + ml;
-            const int bl = m / a.R, ir = m - bl * a.R;
-            bg = a.b0 + bl;
-            if (rok) pos = a.lens[bg] + ir;
+          if constexpr (KIND == GEMM_LM) {
+            // logits and the panel's statistics (the accept step folds the
+            // panels in the skinny engine's workgroup order)
+            const bool samp = gemm_lm_samp(a, ml, rok);
+            const RowStat ps =
+                gemm_lm_panel<false>(a, uok ? u : 0, ml, kl, rok, samp, sm.rinv[r], tot[mt][p][i], nan_seen);
+            gemm_lm_store_panel(a, uok ? u : 0, ml, kl, rok, ps);
+          } else {
+            int pos = 0, bg = 0;
+            if constexpr (KIND == GEMM_QKV) {
+              const int m = a.m0 + ml;
+              const int bl = m / a.R, ir = m - bl * a.R;
+              bg = a.b0 + bl;
+              if (rok) pos = a.lens[bg] + ir;
+            }
+            const EpiIn e = gemm_epi_load<KIND, false>(a, uok ? u : 0, ml, kl, rok, pos);
+            gemm_epilogue<KIND, true, false>(a, uok ? u : 0, ml, kl, rok, pos, bg, sm.rinv[r], tot[mt][p][i], e);
           }
-          const EpiIn e = gemm_epi_load<KIND, false>(a, uok ? u : 0, ml, kl, rok, pos);
-          gemm_epilogue<KIND, true, false>(a, uok ? u : 0, ml, kl, rok, pos, bg, sm.rinv[r], tot[mt][p][i], e);
         }
       }
     }
+    if (nan_seen) flag_error(a.err, SPADE_DERR_NAN);
   }
 };
 

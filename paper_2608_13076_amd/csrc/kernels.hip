@@ -738,6 +738,27 @@ int split_k_choice(const GemmParams& gp, int n_cu, int fixed) {
   return 0;
 }
 
+}  // namespace
+
+// Whether the LM head of a call with M rows leaves one statistics entry per
+// row and panel (wide-row or split-K engine; the accept step then folds the
+// panels in the skinny engine's workgroup order): the number of panels, else
+// 0 (one entry per workgroup).  The same conditions as launch_layer_gemm.
+int lm_stats_panels(spade_model md, int M) {
+  const Dims& D = md->dims;
+  if (D.wdt != SPADE_BF16) return 0;
+  if (M > kWideMinRows) return md->wide_rt >= 0 ? D.Vpad / 16 : 0;
+  if (md->split_ks < 0) return 0;
+  GemmParams gp{};
+  gp.M = M;
+  gp.act_stride = D.d;
+  gp.NKB = D.d / kblock_of(D.wdt);
+  gp.n_units = D.Vpad / 16;
+  return split_k_choice(gp, md->n_cu, md->split_ks) > 0 ? D.Vpad / 16 : 0;
+}
+
+namespace {
+
 hipError_t launch_split(int kind, const GemmParams& gp, int ks, int n_cu, uint32_t* cnt, float* part, hipStream_t st) {
   const int G = n_cu / ks;
   if (ks == 2) {
@@ -745,14 +766,16 @@ hipError_t launch_split(int kind, const GemmParams& gp, int ks, int n_cu, uint32
       case GEMM_QKV: return launch_split_ks<2, GEMM_QKV>(gp, cnt, part, G, st);
       case GEMM_O: return launch_split_ks<2, GEMM_O>(gp, cnt, part, G, st);
       case GEMM_GU: return launch_split_ks<2, GEMM_GU>(gp, cnt, part, G, st);
-      default: return launch_split_ks<2, GEMM_DOWN>(gp, cnt, part, G, st);
+      case GEMM_DOWN: return launch_split_ks<2, GEMM_DOWN>(gp, cnt, part, G, st);
+      default: return launch_split_ks<2, GEMM_LM>(gp, cnt, part, G, st);
     }
   }
   switch (kind) {
     case GEMM_QKV: return launch_split_ks<4, GEMM_QKV>(gp, cnt, part, G, st);
     case GEMM_O: return launch_split_ks<4, GEMM_O>(gp, cnt, part, G, st);
     case GEMM_GU: return launch_split_ks<4, GEMM_GU>(gp, cnt, part, G, st);
-    default: return launch_split_ks<4, GEMM_DOWN>(gp, cnt, part, G, st);
+    case GEMM_DOWN: return launch_split_ks<4, GEMM_DOWN>(gp, cnt, part, G, st);
+    default: return launch_split_ks<4, GEMM_LM>(gp, cnt, part, G, st);
   }
 }
 
@@ -810,7 +833,8 @@ hipError_t launch_wide(int kind, const GemmParams& gp, int n_cu, int fixed_rt, i
     case GEMM_QKV: return launch_wide_kind<GEMM_QKV>(gp, best_rt, best_p, nrg, nug, st);
     case GEMM_O: return launch_wide_kind<GEMM_O>(gp, best_rt, best_p, nrg, nug, st);
     case GEMM_GU: return launch_wide_kind<GEMM_GU>(gp, best_rt, best_p, nrg, nug, st);
-    default: return launch_wide_kind<GEMM_DOWN>(gp, best_rt, best_p, nrg, nug, st);
+    case GEMM_DOWN: return launch_wide_kind<GEMM_DOWN>(gp, best_rt, best_p, nrg, nug, st);
+    default: return launch_wide_kind<GEMM_LM>(gp, best_rt, best_p, nrg, nug, st);
   }
 }
 
@@ -913,6 +937,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
       g.ssq_in = W.ssq;
       g.logits = fc.logits_out;
       g.stats = W.stats;
+      g.pstats = W.stats;  // per-panel layout when the wide-row or split-K engine runs it
       g.mode = fc.mode;
       g.inv_T = fc.inv_T;
       g.have_q = fc.have_q;
@@ -920,7 +945,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   }
   const int grid = std::min(units, md->gemm_wgs);
   g.NU = grid;  // LM head: one statistics entry per workgroup and row
-  if (wb && kind != GEMM_LM && M > kWideMinRows && md->wide_rt >= 0) {
+  if (wb && M > kWideMinRows && md->wide_rt >= 0) {
     // batched rows: every row in one launch, weights streamed once
     GemmParams gp = g;
     gp.w = wmat;
@@ -944,7 +969,8 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
     gp.act_split = act_split;
     gp.act_stride = K;
     const int mt = gp.M > 16 ? 2 : 1;
-    if (wb && kind != GEMM_LM && md->split_ks >= 0) {
+    // (the LM head only for a call of <= 16 rows in all: lm_stats_panels)
+    if (wb && md->split_ks >= 0 && (kind != GEMM_LM || M <= kWideMinRows)) {
       const int ks = split_k_choice(gp, md->n_cu, md->split_ks);
       if (ks > 0) {
         hipError_t r = launch_split(kind, gp, ks, md->n_cu, W.split_cnt, W.split_part, st);
@@ -1047,6 +1073,7 @@ hipError_t launch_accept(spade_model md, const AcceptCall& ac, hipStream_t st) {
   p.logits = ac.logits;
   p.stats = ac.stats;
   p.NU = ac.NU;
+  p.panels = ac.panels;
   p.V = ac.V;
   p.gamma = ac.gamma;
   p.R = ac.gamma + 1;

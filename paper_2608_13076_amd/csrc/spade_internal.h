@@ -194,6 +194,7 @@ struct AcceptCall {
   const float* logits;     // [B][gamma+1][V]
   const float* stats;      // [B*(gamma+1)][NU][3] from the LM head, or NULL
   int NU;
+  int panels;              // > 0: stats is [B*(gamma+1)][panels][3], one entry per panel
   const int32_t* drafts;
   const float* q;
   const float* u;
@@ -204,6 +205,7 @@ struct AcceptCall {
 };
 
 hipError_t launch_forward(spade_model m, spade_kv kv, const ForwardCall& fc, hipStream_t st);
+int lm_stats_panels(spade_model m, int M);
 // single-launch verify pass (verify_fused.hip): eligibility and launch
 bool fused_eligible(spade_model m, spade_kv kv, const ForwardCall& fc);
 hipError_t launch_verify_fused(spade_model m, spade_kv kv, const ForwardCall& fc, const AcceptCall& ac,
