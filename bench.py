@@ -46,12 +46,13 @@ def algorithmic_bytes(w, lens) -> dict:
     elt = 2 if m.weight_dtype == "bf16" else 4
     kvelt = 2 if m.kv_dtype == "bf16" else 4
     d, f, v, L = m.d_model, m.d_ffn, m.vocab, m.n_layers
+    dkv = m.kv_heads * m.head_dim  # K/V width (grouped-query attention: fewer K/V heads)
     R = w.gamma + 1
     M = w.batch * R
-    weights = L * (4 * d * d + 3 * d * f) * elt + L * 2 * d * 4 + v * d * elt + d * 4
+    weights = L * (2 * d * d + 2 * d * dkv + 3 * d * f) * elt + L * 2 * d * 4 + v * d * elt + d * 4
     embed = M * d * elt
-    kv_read = sum(int(l) + R for l in lens) * L * 2 * d * kvelt
-    kv_write = M * L * 2 * d * kvelt
+    kv_read = sum(int(l) + R for l in lens) * L * 2 * dkv * kvelt
+    kv_write = M * L * 2 * dkv * kvelt
     return {"weights": weights, "embed": embed, "kv_read": kv_read, "kv_write": kv_write,
             "total": weights + embed + kv_read + kv_write}
 

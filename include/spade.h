@@ -252,10 +252,24 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
  * in the same order.  Other values return SPADE_EINVAL. */
 spade_status spade_model_set_split_k(spade_model m, int splits);
 
+/* Probabilities softmax(logits / temperature) of `rows` rows of V logits,
+ * float32, row-major [rows][V] in and out (device pointers, caller-owned; out
+ * may not alias in).  The edge side of Algorithm 1 keeps, for every draft
+ * token, the distribution q it was drawn from (Sec. III-C: the acceptance
+ * test and the residual need q); with the draft model run through
+ * spade_verify with gamma = 0, this turns that call's logits into q.
+ * Stream-ordered; SPADE_EINVAL for null pointers, rows < 1, V < 2 or a
+ * temperature that is not finite and > 0. */
+spade_status spade_softmax(const float* d_logits, int rows, int V, float temperature, float* d_probs,
+                           void* stream);
+
 /* Context update after spade_verify (Algorithm 1: append the k accepted
  * tokens and the correction, m <- m + k + 1): lens[b] += n_accepted[b] + 1 and
  * pending[b] = correction[b], on the device.  KV rows past the new length are
- * the rolled-back drafts; they are overwritten by the next round. */
+ * the rolled-back drafts; they are overwritten by the next round.  The
+ * host-side upper bound of lens (the capacity check of spade_verify) grows by
+ * gamma + 1 of the last spade_verify on this cache; spade_kv_set_state makes
+ * it exact again. */
 spade_status spade_kv_commit(spade_kv kv, int B, const int32_t* d_n_accepted,
                              const int32_t* d_correction, void* stream);
 

@@ -179,3 +179,96 @@ def commit(cache: KVCache, res: VerifyResult) -> int:
     the k accepted drafts, drop the rest; returns the new pending token."""
     cache.length = res.start_len + res.n_accepted + 1
     return res.correction
+
+
+@dataclass
+class LoopResult:
+    """Output of an Algorithm 1 run: the emitted tokens (after the prompt), the
+    number of cloud verify calls, and the accepted drafts per call."""
+
+    tokens: List[int]
+    calls: int
+    accepted: List[int]
+    margins: List[float] = field(default_factory=list)  # greedy: top-2 margin behind each emitted token
+
+
+def decode_step(model: Decoder, cache: KVCache, pending: int, u: float, mode: int,
+                temperature: float = 1.0):
+    """One autoregressive step (a verify call with no drafts): append
+    ``pending``, draw the next token from the row's distribution (greedy: its
+    argmax; sampling: the Gumbel-max draw keyed by ``u``).  Returns (token,
+    logits row, margin of the draw)."""
+    res = verify(model, cache, pending, np.zeros(0, dtype=np.int64), None, np.array([u]), mode, temperature)
+    cache.length = res.start_len + 1
+    return res.correction, res.logits[0], res.draw_margin
+
+
+def algorithm1(target: Decoder, draft: Decoder, prompt: np.ndarray, gamma: int, max_new: int,
+               mode: int, uniforms, temperature: float = 1.0, capacity: Optional[int] = None) -> LoopResult:
+    """Algorithm 1 of the paper with both sides on one machine.
+
+    Edge: the draft model continues the context autoregressively for
+    ``gamma`` tokens, keeping the distribution q_j each token was drawn from.
+    Cloud: one verify call scores them (``verify``: accept/reject, correction
+    or bonus token).  Both sides keep the accepted prefix plus the correction
+    (m <- m + k + 1); the draft's cache is cut back to the same length, and
+    when every draft was accepted the draft first appends its last draft,
+    which it never ran.  Stops after ``max_new`` emitted tokens.
+
+    ``uniforms`` yields float32 values in [0, 1): one per draft step (its
+    draw), then gamma + 1 per cloud call, in that order (greedy ignores them).
+    The prompt's last id is the first pending token."""
+    prompt = np.asarray(prompt, dtype=np.int64)
+    cap = capacity or (len(prompt) + max_new + gamma + 2)
+    tc, dc = target.new_cache(cap), draft.new_cache(cap)
+    target.prefill(tc, prompt[:-1])
+    draft.prefill(dc, prompt[:-1])
+    pending = int(prompt[-1])
+    out: List[int] = []
+    accepted: List[int] = []
+    margins: List[float] = []
+    calls = 0
+    while len(out) < max_new:
+        start = tc.length
+        # edge: gamma draft tokens and their distributions
+        drafts = np.zeros(gamma, dtype=np.int64)
+        q = np.zeros((gamma, target.shape.vocab))
+        dp = pending
+        for j in range(gamma):
+            tok, row, _ = decode_step(draft, dc, dp, next(uniforms), mode, temperature)
+            z = row / temperature if mode == SAMPLE else row
+            q[j] = np.exp(_log_softmax(z)).astype(np.float32)
+            drafts[j] = tok
+            dp = tok
+        # cloud: one verify call
+        u = np.array([next(uniforms) for _ in range(gamma + 1)])
+        res = verify(target, tc, pending, drafts, q if mode == SAMPLE else None, u, mode, temperature)
+        calls += 1
+        n = res.n_accepted
+        new_pending = commit(tc, res)
+        if mode == GREEDY:
+            margins += [r.margin for r in res.rows[:n]] + [res.draw_margin]
+        # edge: keep [pending, d_1 .. d_n]; with all accepted, run d_gamma first
+        if n == gamma:
+            draft.forward(dc, drafts[gamma - 1:], want_logits=False)
+        dc.length = start + n + 1
+        out += [int(t) for t in drafts[:n]] + [new_pending]
+        accepted.append(n)
+        pending = new_pending
+    return LoopResult(out[:max_new], calls, accepted, margins[:max_new])
+
+
+def target_only(target: Decoder, prompt: np.ndarray, max_new: int, mode: int, uniforms,
+                temperature: float = 1.0) -> LoopResult:
+    """Plain autoregressive decoding with the verifier (one call per token):
+    the baseline Algorithm 1 is measured against."""
+    prompt = np.asarray(prompt, dtype=np.int64)
+    tc = target.new_cache(len(prompt) + max_new + 1)
+    target.prefill(tc, prompt[:-1])
+    pending = int(prompt[-1])
+    out, margins = [], []
+    for _ in range(max_new):
+        pending, _, m = decode_step(target, tc, pending, next(uniforms), mode, temperature)
+        out.append(pending)
+        margins.append(m)
+    return LoopResult(out, max_new, [0] * max_new, margins)

@@ -291,6 +291,7 @@ spade_status spade_kv_create(spade_model m, void* d_kv, int max_batch, int max_l
   kv->max_len = max_len;
   kv->stride = kv_stride_of(max_len);
   kv->lens_ub = new (std::nothrow) int[max_batch]();
+  kv->last_rows = m->max_gamma + 1;
   kv->snap_ub = new (std::nothrow) int[max_batch]();
   if (!kv->lens_ub || !kv->snap_ub) {
     delete[] kv->lens_ub;
@@ -400,6 +401,7 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
       return fail(SPADE_ECAPACITY, "request %d: %d cached + %d rows exceed max_len %d", b, kv->lens_ub[b],
                   gamma + 1, kv->max_len);
   hipStream_t st = (hipStream_t)stream;
+  kv->last_rows = gamma + 1;
   ForwardCall fc{};
   fc.b0 = 0;
   fc.nb = B;
@@ -459,6 +461,17 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
   return SPADE_OK;
 }
 
+spade_status spade_softmax(const float* d_logits, int rows, int V, float temperature, float* d_probs,
+                           void* stream) {
+  if (!d_logits || !d_probs) return fail(SPADE_EINVAL, "null pointer");
+  if (rows < 1 || V < 2) return fail(SPADE_EINVAL, "rows must be >= 1 and V >= 2");
+  if (!(temperature > 0.f && std::isfinite(temperature)))
+    return fail(SPADE_EINVAL, "temperature must be finite and > 0");
+  hipError_t e = launch_softmax(d_logits, rows, V, 1.0f / temperature, d_probs, (hipStream_t)stream);
+  if (e != hipSuccess) return hipfail(e, "softmax");
+  return SPADE_OK;
+}
+
 spade_status spade_model_set_split_k(spade_model m, int splits) {
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (splits != -1 && splits != 0 && splits != 2 && splits != 4) return fail(SPADE_EINVAL, "splits must be -1, 0, 2 or 4");
@@ -473,7 +486,7 @@ spade_status spade_kv_commit(spade_kv kv, int B, const int32_t* d_n_accepted, co
   hipError_t e = launch_commit(kv, B, d_n_accepted, d_correction, (hipStream_t)stream);
   if (e != hipSuccess) return hipfail(e, "kv_commit");
   // n_accepted <= max_gamma, so the bound grows by at most max_gamma + 1
-  for (int b = 0; b < B; ++b) kv->lens_ub[b] += kv->model->max_gamma + 1;
+  for (int b = 0; b < B; ++b) kv->lens_ub[b] += kv->last_rows;
   return SPADE_OK;
 }
 

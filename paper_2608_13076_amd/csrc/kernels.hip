@@ -610,6 +610,41 @@ __global__ void __launch_bounds__(kAcceptThreads) accept_kernel(AcceptParams p) 
 }
 
 // ---------------------------------------------------------------------------
+// Row softmax of logits / T (the draft side of Algorithm 1 keeps the
+// distribution each of its tokens was drawn from): one workgroup per row,
+// max then sum of exp in a fixed order, float32.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float block_reduce_256(float v, bool is_max, float* red) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float o = __shfl_xor(v, off);
+    v = is_max ? fmaxf(v, o) : v + o;
+  }
+  const int wave = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[wave] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int w = 1; w < 4; ++w) r = is_max ? fmaxf(r, red[w]) : r + red[w];
+  return r;
+}
+
+__global__ void __launch_bounds__(256) softmax_rows_kernel(const float* logits, int V, float invT, float* out) {
+  __shared__ float red[4];
+  const float* z = logits + (size_t)blockIdx.x * V;
+  float* o = out + (size_t)blockIdx.x * V;
+  float m = -INFINITY;
+  for (int v = threadIdx.x; v < V; v += 256) m = fmaxf(m, z[v] * invT);
+  m = block_reduce_256(m, true, red);
+  float s = 0.f;
+  for (int v = threadIdx.x; v < V; v += 256) s += expf(z[v] * invT - m);
+  s = block_reduce_256(s, false, red);
+  const float inv = 1.0f / s;
+  for (int v = threadIdx.x; v < V; v += 256) o[v] = expf(z[v] * invT - m) * inv;
+}
+
+// ---------------------------------------------------------------------------
 // Small kernels: commit, lens advance, packing.
 // ---------------------------------------------------------------------------
 __global__ void commit_kernel(int B, int32_t* lens, int32_t* pending, const int32_t* n, const int32_t* corr) {
@@ -1137,6 +1172,11 @@ hipError_t launch_pack(spade_model md, int kind, int layer, const void* src, hip
   const size_t total = (size_t)pp.n_units * pp.NKB * 512;
   const unsigned blocks = (unsigned)((total + 255) / 256);
   hipLaunchKernelGGL(pack_kernel, dim3(blocks), dim3(256), 0, st, pp);
+  return hipGetLastError();
+}
+
+hipError_t launch_softmax(const float* logits, int rows, int V, float invT, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(softmax_rows_kernel, dim3(rows), dim3(256), 0, st, logits, V, invT, out);
   return hipGetLastError();
 }
 

@@ -173,6 +173,7 @@ struct spade_kv_s {
   int max_batch, max_len;
   int stride;    // positions per (request, head) row of the cache: max_len rounded up to 32
   int* lens_ub;  // host upper bound of lens per request
+  int last_rows; // rows (gamma + 1) of the last spade_verify on this cache: what a commit can add at most
   int* snap_ub;  // lens_ub at the last snapshot
 };
 
@@ -206,6 +207,7 @@ struct AcceptCall {
 
 hipError_t launch_forward(spade_model m, spade_kv kv, const ForwardCall& fc, hipStream_t st);
 int lm_stats_panels(spade_model m, int M);
+hipError_t launch_softmax(const float* logits, int rows, int V, float invT, float* out, hipStream_t st);
 // single-launch verify pass (verify_fused.hip): eligibility and launch
 bool fused_eligible(spade_model m, spade_kv kv, const ForwardCall& fc);
 hipError_t launch_verify_fused(spade_model m, spade_kv kv, const ForwardCall& fc, const AcceptCall& ac,

@@ -30,7 +30,7 @@ EXPORTED = (
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
     "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
-    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles", "spade_model_set_split_k",
+    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles", "spade_model_set_split_k", "spade_softmax",
 )
 
 
@@ -90,6 +90,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_model_set_fused": (I, [P, I]),
         "spade_model_set_wide_tiles": (I, [P, I, I]),
         "spade_model_set_split_k": (I, [P, I]),
+        "spade_softmax": (I, [P, I, I, F, P, P]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
         "spade_kv_destroy": (None, [P]),
@@ -295,6 +296,14 @@ def verify(model: Model, kv: KVCache, buf: VerifyBuffers, temperature: float = 1
                                   _ptr(buf.corr), _ptr(buf.logits), _stream()))
 
 
+def softmax_into(logits: torch.Tensor, out: torch.Tensor, temperature: float = 1.0) -> None:
+    """out = softmax(logits / temperature) row by row (float32, last dim V),
+    on the current stream."""
+    V = logits.shape[-1]
+    rows = logits.numel() // V
+    _check(load_library().spade_softmax(_ptr(logits), rows, V, float(temperature), _ptr(out), _stream()))
+
+
 GEMM_KINDS = {"qkv": 0, "o": 1, "gu": 2, "down": 3, "lm": 4}
 
 
@@ -302,7 +311,8 @@ def gemm_weight_bytes(shape, kind: str) -> int:
     """Weight bytes one launch of a projection GEMM streams."""
     elt = 2 if shape.weight_dtype == "bf16" else 4
     d, f, v = shape.d_model, shape.d_ffn, shape.vocab
-    n_k = {"qkv": (3 * d, d), "o": (d, d), "gu": (2 * f, d), "down": (d, f), "lm": (v, d)}[kind]
+    dkv = getattr(shape, "kv_heads", shape.n_heads) * shape.head_dim
+    n_k = {"qkv": (d + 2 * dkv, d), "o": (d, d), "gu": (2 * f, d), "down": (d, f), "lm": (v, d)}[kind]
     return n_k[0] * n_k[1] * elt
 
 
