@@ -141,14 +141,16 @@ def run_target_only(target: spade.Model, prompt, max_new: int, mode: int, unifor
     return LoopStats(toks.cpu().tolist(), max_new, [], secs)
 
 
-def load_model(shape, seed: int, max_len: int, gamma: int, n_layers: Optional[int] = None) -> spade.Model:
+def load_model(shape, seed: int, max_len: int, gamma: int, n_layers: Optional[int] = None,
+               sigma: float = 0.0, noise_seed: int = 7) -> spade.Model:
     """A model of ``shape`` (or its first ``n_layers`` layers with the same
     embedding, final norm and LM head: an early-exit draft) with the seeded
-    synthetic weights."""
-    from synth import iter_weights
+    synthetic weights, every matrix perturbed by ``sigma`` (relative to the
+    weights' scale; 0: none) for a draft of controlled agreement."""
+    from synth import iter_weights_perturbed
     sh = shape if n_layers is None else replace(shape, n_layers=n_layers)
     m = spade.Model(sh, 1, gamma, max_len)
-    for kind, layer, arr in iter_weights(sh, seed):
+    for kind, layer, arr in iter_weights_perturbed(sh, seed, sigma, noise_seed):
         m.load_numpy(kind, layer, arr)
     return m
 
@@ -160,14 +162,16 @@ def main() -> int:
     ap.add_argument("--prompt", type=int, default=1024)
     ap.add_argument("--tokens", type=int, default=96)
     ap.add_argument("--gammas", default="3,5,8")
-    ap.add_argument("--draft-layers", default="2,8,16")
+    ap.add_argument("--draft-layers", default="2,8,16", help="early-exit drafts (comma list; empty: none)")
+    ap.add_argument("--draft-noise", default="", help="full-depth drafts with perturbed weights: sigmas")
     ap.add_argument("--mode", default="greedy", choices=["greedy", "sample"])
     ap.add_argument("--temperature", type=float, default=1.0)
     a = ap.parse_args()
     w = workload(a.workload)
     mode = GREEDY if a.mode == "greedy" else SAMPLE
     gammas = [int(x) for x in a.gammas.split(",")]
-    layers = [int(x) for x in a.draft_layers.split(",")]
+    layers = [int(x) for x in a.draft_layers.split(",") if x]
+    sigmas = [float(x) for x in a.draft_noise.split(",") if x]
     max_len = a.prompt + a.tokens + 2 * max(gammas) + 8
     prompt = np.random.default_rng(w.seed).integers(0, w.model.vocab, a.prompt + 1).astype(np.int32)
     uniforms = np.random.default_rng(w.seed + 1).random(8 * a.tokens * (max(gammas) + 2), dtype=np.float32)
@@ -176,12 +180,14 @@ def main() -> int:
     rows = [{"draft_layers": None, "gamma": 0, "calls": base.calls, "tokens": a.tokens,
              "calls_per_token": 1.0, "ms_per_token": round(base.seconds * 1e3 / a.tokens, 3)}]
     print(json.dumps(rows[0]), flush=True)
-    for k in layers:
-        draft = load_model(w.model, w.seed, max_len, max(gammas), n_layers=k)
+    drafts = [("draft_layers", k, dict(n_layers=k)) for k in layers] + \
+             [("draft_noise", sg, dict(sigma=sg)) for sg in sigmas]
+    for key, val, kw in drafts:
+        draft = load_model(w.model, w.seed, max_len, max(gammas), **kw)
         for g in gammas:
             r = run_algorithm1(target, draft, prompt, g, a.tokens, mode, uniforms, a.temperature)
             same = r.tokens == base.tokens if mode == GREEDY else None
-            row = {"draft_layers": k, "gamma": g, "calls": r.calls, "tokens": a.tokens,
+            row = {key: val, "gamma": g, "calls": r.calls, "tokens": a.tokens,
                    "calls_per_token": round(r.calls / a.tokens, 4),
                    "accepted_per_call": round(float(np.mean(r.accepted)), 3),
                    "ms_per_token": round(r.seconds * 1e3 / a.tokens, 3), "same_as_target_only": same}

@@ -20,6 +20,8 @@ from .weights import (  # noqa: F401
     tensor_shape,
     make_tensor,
     iter_weights,
+    iter_weights_perturbed,
+    perturb_tensor,
     ModelWeights,
 )
 from .inputs import make_inputs, VerifyInputs  # noqa: F401

@@ -135,6 +135,45 @@ def iter_weights(shape: ModelShape, seed: int) -> Iterator[Tuple[str, Optional[i
             yield kind, None, make_tensor(shape, kind, None, seed, pool)
 
 
+def perturb_tensor(shape: ModelShape, kind: str, layer: Optional[int], t: np.ndarray, sigma: float,
+                   noise_seed: int) -> np.ndarray:
+    """A weight matrix plus sigma * init_std * N(0, 1) noise of its own seeded
+    stream (normal quantiles, as for the weights), rounded back to the
+    tensor's type; gains are returned unchanged.  A model built from these is
+    a draft whose agreement with the unperturbed model falls as sigma grows."""
+    if kind.startswith("g_") or sigma == 0.0:
+        return t
+    lay = _GLOBAL_LAYER if layer is None else int(layer)
+    n = t.size
+    table = normal_table_f32()
+    out = np.empty(n, dtype=np.float32)
+    base = bf16_bits_to_f32(t.ravel()) if t.dtype == np.uint16 else t.ravel().astype(np.float32)
+    scale = np.float32(sigma * shape.init_std)
+    for c in range((n + CHUNK - 1) // CHUNK):
+        lo, hi = c * CHUNK, min(n, (c + 1) * CHUNK)
+        r = _rng(noise_seed, lay, kind, c)
+        out[lo:hi] = base[lo:hi] + scale * table[r.integers(0, 65536, size=hi - lo, dtype=np.uint16)]
+    out = out.reshape(t.shape)
+    return f32_to_bf16_bits(out) if t.dtype == np.uint16 else out
+
+
+def normal_table_f32() -> np.ndarray:
+    """65536 N(0, 1) quantiles at (i + 0.5) / 65536, float32."""
+    t = _TABLES.get("f32")
+    if t is None:
+        p = (np.arange(65536, dtype=np.float64) + 0.5) / 65536.0
+        t = ndtri(p).astype(np.float32)
+        _TABLES["f32"] = t
+    return t
+
+
+def iter_weights_perturbed(shape: ModelShape, seed: int, sigma: float,
+                           noise_seed: int) -> Iterator[Tuple[str, Optional[int], np.ndarray]]:
+    """iter_weights with every matrix perturbed (perturb_tensor)."""
+    for kind, layer, t in iter_weights(shape, seed):
+        yield kind, layer, perturb_tensor(shape, kind, layer, t, sigma, noise_seed)
+
+
 class ModelWeights:
     """All tensors of one model, generated on first use and kept."""
 

@@ -65,3 +65,19 @@ def test_sampling_loop_with_the_verifier_as_draft_accepts_everything():
     assert res.accepted == [4] * res.calls
     assert res.calls == 5
     assert len(res.tokens) == 25 and all(0 <= t < SHAPE.vocab for t in res.tokens)
+
+
+def test_agreement_falls_with_draft_noise():
+    """A draft built from the verifier's weights plus noise: the more noise,
+    the fewer drafts accepted (the alignment knob of the gamma sweep)."""
+    from synth import perturb_tensor
+    mw = ModelWeights(SHAPE, 11)
+    target = Decoder(SHAPE, mw.get, keep_f64=True)
+    prompt = np.random.default_rng(4).integers(0, SHAPE.vocab, 9)
+    acc = []
+    for sigma in (0.0, 0.05, 3.0):
+        get = (lambda s: (lambda k, l=None: perturb_tensor(SHAPE, k, l, mw.get(k, l), s, 99)))(sigma)
+        draft = Decoder(SHAPE, get, keep_f64=True)
+        r = algorithm1(target, draft, prompt, 4, 40, GREEDY, _uniforms(0))
+        acc.append(np.mean(r.accepted))
+    assert acc[0] == 4 and acc[0] > acc[1] > acc[2]

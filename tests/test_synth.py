@@ -35,3 +35,20 @@ def test_inputs_shapes():
             for b in range(B):
                 if inp.recipe[b] == "noise_q":
                     np.testing.assert_allclose(s[b], 1.0, atol=1e-5)
+
+
+def test_perturbed_weights():
+    from synth import make_tensor, perturb_tensor
+    from synth.configs import ModelShape
+    sh = ModelShape("p", n_layers=1, d_model=256, n_heads=2, head_dim=128, d_ffn=512, vocab=300)
+    t = make_tensor(sh, "wq", 0, 5)
+    assert perturb_tensor(sh, "wq", 0, t, 0.0, 1) is t
+    g = make_tensor(sh, "g_attn", 0, 5)
+    assert perturb_tensor(sh, "g_attn", 0, g, 0.5, 1) is g
+    from synth import bf16_bits_to_f32
+    p1 = perturb_tensor(sh, "wq", 0, t, 0.25, 1)
+    assert p1.dtype == np.uint16 and p1.shape == t.shape
+    np.testing.assert_array_equal(p1, perturb_tensor(sh, "wq", 0, t, 0.25, 1))  # seeded
+    diff = bf16_bits_to_f32(p1).astype(np.float64) - bf16_bits_to_f32(t)
+    assert abs(diff.std() / (0.25 * sh.init_std) - 1) < 0.05 and abs(diff.mean()) < 1e-4
+    assert not np.array_equal(p1, perturb_tensor(sh, "wq", 0, t, 0.25, 2))
