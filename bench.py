@@ -231,8 +231,7 @@ def main() -> int:
         log("counter run done: 1 calibration copy, 4 gate/up launches")
         return 0
     t0 = time.perf_counter()
-    for b in range(w.batch):
-        kv.prefill(b, inp.prompts[b])
+    kv.prefill_batch(inp.prompts)  # all requests' chunks in one forward each
     log(f"prefill of {inp.lens.tolist()} tokens in {time.perf_counter() - t0:.1f}s")
     lens0, pend0 = kv.snapshot(w.batch)
     buf = spade.VerifyBuffers(model, inp.drafts, inp.draft_probs, inp.uniforms, inp.modes, want_logits=False)

@@ -252,6 +252,19 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
  * in the same order.  Other values return SPADE_EINVAL. */
 spade_status spade_model_set_split_k(spade_model m, int splits);
 
+/* Prefill of B requests at once: request b caches h_n_tokens[b] - 1 prompt
+ * tokens (row b of d_tokens, device int32 [B][ld], ld >= every count) after
+ * its current length, and its last prompt token becomes pending -- the same
+ * cache contents and state as spade_prefill of each request.  Every forward
+ * takes the next R = 16 tokens of every request (the GEMMs read each weight
+ * once for all B * R rows; the workspace holds max_batch * 16 rows); a request
+ * whose prompt is used up contributes placeholder rows, written past its
+ * length, so each request needs R free positions beyond its prompt
+ * (lens + h_n_tokens[b] - 1 + R <= max_len, else SPADE_ECAPACITY).  Counts
+ * are read from host memory (h_n_tokens) before the call returns. */
+spade_status spade_prefill_batch(spade_model m, spade_kv kv, int B, const int32_t* d_tokens, int ld,
+                                 const int32_t* h_n_tokens, void* stream);
+
 /* Probabilities softmax(logits / temperature) of `rows` rows of V logits,
  * float32, row-major [rows][V] in and out (device pointers, caller-owned; out
  * may not alias in).  The edge side of Algorithm 1 keeps, for every draft

@@ -91,7 +91,7 @@ ArenaLayout layout_of(const Dims& D) {
 
 struct WsPlan {
   size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, bar, fused, split_cnt,
-      split_part, total;
+      split_part, prefill_tok, prefill_cnt, total;
   FusedArena fa;
   bool has_fused;
   int max_units;
@@ -102,7 +102,8 @@ struct WsPlan {
 WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   WsPlan p{};
   p.Rmax = std::max(max_gamma + 1, kPrefillRows);
-  p.Mmax = std::max(max_batch * (max_gamma + 1), kPrefillRows);
+  // rows of one forward: a verify call, or a batched prefill of 16 tokens per request
+  p.Mmax = std::max(max_batch * (max_gamma + 1), max_batch * kPrefillRows);
   p.NCmax = std::min(kAttnMaxChunks, (max_len + kAttnChunk - 1) / kAttnChunk);
   const bool wb = D.wdt == SPADE_BF16;
   const size_t ae = wb ? 2 * kActSplits : 4;  // bf16 terms or one float
@@ -132,6 +133,8 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.max_units = std::max(std::max(D.d + 2 * D.dkv, 2 * D.F), D.Vpad) / 16;
   p.split_cnt = take((size_t)p.max_units * 4);
   p.split_part = take((size_t)p.max_units * 8 * 256 * 4);
+  p.prefill_tok = take((size_t)p.Mmax * 4);
+  p.prefill_cnt = take((size_t)max_batch * 4);
   // the single-launch pass handles bf16 weights and cache with head_dim 128
   p.has_fused = wb && D.kvdt == SPADE_BF16 && D.hd == 128;
   if (p.has_fused) {
@@ -222,6 +225,8 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.attn_cnt = (uint32_t*)(b + p.attn_cnt);
   w.split_cnt = (uint32_t*)(b + p.split_cnt);
   w.split_part = (float*)(b + p.split_part);
+  w.prefill_tok = (int32_t*)(b + p.prefill_tok);
+  w.prefill_cnt = (int32_t*)(b + p.prefill_cnt);
   w.logits = (float*)(b + p.logits);
   w.stats = (float*)(b + p.stats);
   w.rope = (float*)(b + p.rope);
@@ -458,6 +463,25 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
   if (panels == 2 && row_tiles == 3) return fail(SPADE_EINVAL, "two panels per wave take at most two row tiles");
   m->wide_rt = row_tiles;
   m->wide_p = panels;
+  return SPADE_OK;
+}
+
+spade_status spade_prefill_batch(spade_model m, spade_kv kv, int B, const int32_t* d_tokens, int ld,
+                                 const int32_t* h_n_tokens, void* stream) {
+  if (!m || !kv || !d_tokens || !h_n_tokens) return fail(SPADE_EINVAL, "null pointer");
+  if (kv->model != m) return fail(SPADE_EINVAL, "kv belongs to another model");
+  if (B < 1 || B > kv->max_batch || B > m->max_batch) return fail(SPADE_ECAPACITY, "B=%d out of range", B);
+  const int R = prefill_batch_rows(m, B);
+  std::vector<int> n_cache(B);
+  for (int b = 0; b < B; ++b) {
+    if (h_n_tokens[b] < 1 || h_n_tokens[b] > ld) return fail(SPADE_EINVAL, "request %d: n_tokens must be in [1, ld]", b);
+    n_cache[b] = h_n_tokens[b] - 1;
+    if (kv->lens_ub[b] + n_cache[b] + R > kv->max_len)
+      return fail(SPADE_ECAPACITY, "request %d: %d cached + %d prompt tokens + %d rows of slack exceed max_len %d", b,
+                  kv->lens_ub[b], n_cache[b], R, kv->max_len);
+  }
+  hipError_t e = launch_prefill_batch(m, kv, B, d_tokens, ld, n_cache.data(), (hipStream_t)stream);
+  if (e != hipSuccess) return hipfail(e, "prefill_batch");
   return SPADE_OK;
 }
 

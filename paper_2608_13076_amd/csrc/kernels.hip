@@ -61,7 +61,7 @@ __device__ __forceinline__ void store_act(void* base, size_t split, size_t idx, 
 struct EmbedParams {
   const void* E;
   const float* g;
-  const int32_t* tokens;   // prefill ids [R] or NULL
+  const int32_t* tokens;   // prefill ids [nb][R] or NULL
   const int32_t* drafts;   // [nb][R-1]
   const int32_t* pending;  // global [Bmax]
   int b0, R, d, V;
@@ -77,7 +77,7 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedParams p) {
   const int m = blockIdx.x;
   const int bl = m / p.R, i = m % p.R;
   int t;
-  if (p.tokens) t = p.tokens[i];
+  if (p.tokens) t = p.tokens[m];
   else t = (i == 0) ? p.pending[p.b0 + bl] : p.drafts[bl * (p.R - 1) + i - 1];
   if (t < 0 || t >= p.V) {
     if (threadIdx.x == 0 && blockIdx.y == 0) flag_error(p.err, SPADE_DERR_TOKEN);
@@ -671,6 +671,39 @@ __global__ void advance_kernel(int b, int count, int32_t* lens, int32_t* pending
   }
 }
 
+// Batched prefill: the next R prompt tokens of every request (0 past a
+// request's end: a placeholder row, written past its length), each
+// request's length advanced by its real tokens, and the pending tokens.
+struct PrefillCounts {
+  int n[64];
+};
+
+__global__ void prefill_counts_kernel(PrefillCounts c, int b0, int nb, int32_t* dst) {
+  const int i = threadIdx.x;
+  if (i < nb) dst[b0 + i] = c.n[i];
+}
+
+__global__ void prefill_gather_kernel(const int32_t* tokens, int ld, const int32_t* n_cache, int B, int R, int c0,
+                                      int32_t* out) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= B * R) return;
+  const int b = m / R, pos = c0 + m % R;
+  out[m] = pos < n_cache[b] ? tokens[(size_t)b * ld + pos] : 0;
+}
+
+__global__ void prefill_advance_kernel(int B, int R, int c0, const int32_t* n_cache, int32_t* lens) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) {
+    const int rem = n_cache[b] - c0;
+    lens[b] += rem <= 0 ? 0 : (rem < R ? rem : R);
+  }
+}
+
+__global__ void prefill_pending_kernel(int B, const int32_t* tokens, int ld, const int32_t* n_cache, int32_t* pending) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) pending[b] = tokens[(size_t)b * ld + n_cache[b]];
+}
+
 struct PackParams {
   const uint8_t* src;
   uint8_t* dst;
@@ -1191,6 +1224,45 @@ hipError_t launch_copy_state(int B, int32_t* lens, int32_t* pending, const int32
                      src_pending);
   return hipGetLastError();
 }
+
+hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_t* tokens, int ld,
+                                const int* n_cache, hipStream_t st) {
+  const Workspace& W = md->ws;
+  for (int b0 = 0; b0 < B; b0 += 64) {
+    PrefillCounts c{};
+    const int nb = std::min(64, B - b0);
+    for (int i = 0; i < nb; ++i) c.n[i] = n_cache[b0 + i];
+    hipLaunchKernelGGL(prefill_counts_kernel, dim3(1), dim3(64), 0, st, c, b0, nb, W.prefill_cnt);
+  }
+  int mx = 0;
+  for (int b = 0; b < B; ++b) mx = std::max(mx, n_cache[b]);
+  const int R = std::max(1, std::min(kPrefillRows, W.Mmax / B));
+  hipError_t e = hipGetLastError();
+  for (int c0 = 0; c0 < mx && e == hipSuccess; c0 += R) {
+    hipLaunchKernelGGL(prefill_gather_kernel, dim3((B * R + 255) / 256), dim3(256), 0, st, tokens, ld, W.prefill_cnt,
+                       B, R, c0, W.prefill_tok);
+    ForwardCall fc{};
+    fc.b0 = 0;
+    fc.nb = B;
+    fc.R = R;
+    fc.tokens = W.prefill_tok;
+    fc.want_logits = false;
+    e = launch_forward(md, kv, fc, st);
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(prefill_advance_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, R, c0, W.prefill_cnt, kv->lens);
+      e = hipGetLastError();
+    }
+    // the host bound of lens follows the device lengths (the next forward
+    // sizes its attention grid from it)
+    for (int b = 0; b < B; ++b) kv->lens_ub[b] += std::max(0, std::min(R, n_cache[b] - c0));
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(prefill_pending_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, tokens, ld, W.prefill_cnt,
+                     kv->pending);
+  return hipGetLastError();
+}
+
+int prefill_batch_rows(spade_model md, int B) { return std::max(1, std::min(kPrefillRows, md->ws.Mmax / B)); }
 
 hipError_t launch_advance(spade_kv kv, int b, int count, const int32_t* pending_src, hipStream_t st) {
   hipLaunchKernelGGL(advance_kernel, dim3(1), dim3(64), 0, st, b, count, kv->lens, kv->pending, pending_src);

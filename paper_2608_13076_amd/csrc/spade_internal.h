@@ -139,6 +139,8 @@ struct Workspace {
   uint8_t* fused;     // activation arena of the single-launch verify pass (NULL if the model cannot use it)
   uint32_t* split_cnt;  // [max units / 2] arrival counters of the split-K GEMM (kept at zero between calls)
   float* split_part;    // [max units][8][256] published sums and range partials of the split-K GEMM
+  int32_t* prefill_tok; // [Mmax] token ids of one batched-prefill forward
+  int32_t* prefill_cnt; // [Bmax] prompt tokens to cache per request (batched prefill)
   FusedArena fa;
   size_t act_split;   // elements between splits of act_n / act_o
   size_t actf_split;  // elements between splits of act_f
@@ -208,6 +210,9 @@ struct AcceptCall {
 hipError_t launch_forward(spade_model m, spade_kv kv, const ForwardCall& fc, hipStream_t st);
 int lm_stats_panels(spade_model m, int M);
 hipError_t launch_softmax(const float* logits, int rows, int V, float invT, float* out, hipStream_t st);
+hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_t* tokens, int ld,
+                                const int* n_cache, hipStream_t st);
+int prefill_batch_rows(spade_model md, int B);
 // single-launch verify pass (verify_fused.hip): eligibility and launch
 bool fused_eligible(spade_model m, spade_kv kv, const ForwardCall& fc);
 hipError_t launch_verify_fused(spade_model m, spade_kv kv, const ForwardCall& fc, const AcceptCall& ac,

@@ -30,7 +30,7 @@ EXPORTED = (
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
     "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
-    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles", "spade_model_set_split_k", "spade_softmax",
+    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles", "spade_model_set_split_k", "spade_softmax", "spade_prefill_batch",
 )
 
 
@@ -91,6 +91,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_model_set_wide_tiles": (I, [P, I, I]),
         "spade_model_set_split_k": (I, [P, I]),
         "spade_softmax": (I, [P, I, I, F, P, P]),
+        "spade_prefill_batch": (I, [P, P, I, P, I, P, P]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
         "spade_kv_destroy": (None, [P]),
@@ -253,6 +254,19 @@ class KVCache:
     def prefill(self, b: int, tokens) -> None:
         t = torch.as_tensor(np.asarray(tokens, dtype=np.int32)).to(self.model.device)
         _check(self.lib.spade_prefill(self.model.handle, self.handle, b, _ptr(t), t.numel(), _stream()))
+        torch.cuda.current_stream(self.model.device).synchronize()
+
+    def prefill_batch(self, prompts) -> None:
+        """Prefill requests 0..len(prompts)-1 at once (spade_prefill_batch)."""
+        B = len(prompts)
+        ld = max(len(p) for p in prompts)
+        arr = np.zeros((B, ld), dtype=np.int32)
+        for b, p in enumerate(prompts):
+            arr[b, :len(p)] = np.asarray(p, dtype=np.int32)
+        counts = np.array([len(p) for p in prompts], dtype=np.int32)
+        t = torch.from_numpy(arr).to(self.model.device)
+        _check(self.lib.spade_prefill_batch(self.model.handle, self.handle, B, _ptr(t), ld,
+                                            counts.ctypes.data_as(P), _stream()))
         torch.cuda.current_stream(self.model.device).synchronize()
 
     def commit(self, n: torch.Tensor, corr: torch.Tensor) -> None:
