@@ -238,6 +238,19 @@ spade_status spade_model_set_fused(spade_model m, int enable);
  * return SPADE_EINVAL. */
 spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels);
 
+/* K splitting of the batched O and down projections on the wide-row GEMM.
+ * Their weights have few panels (d_model / 16), so one workgroup per panel
+ * group leaves most compute units idle; with `splits` = 2 or 4 each
+ * workgroup streams only 1/splits of the k-blocks (whole k-ranges of the
+ * engine's eight), publishes its partial sums to the workspace, and the
+ * last workgroup of a panel group to finish adds them in range order and
+ * runs the epilogue.  splits = 0 (the default) chooses per launch from the
+ * shape, 1 turns k-splitting off, 2 or 4 fix it (falling back to 1 where the
+ * workspace's published-value buffers are too small).  Results are
+ * bit-for-bit the same under every setting.  Other values return
+ * SPADE_EINVAL. */
+spade_status spade_model_set_wide_k_splits(spade_model m, int splits);
+
 /* K splitting of the small-batch projections.  A verify call with at most 16
  * rows and bf16 weights whose activation operand is too long for one LDS copy
  * (the 7B-shaped down projection, every projection of the 13B shape) runs the
@@ -303,6 +316,16 @@ spade_status spade_accept_from_logits(spade_model m, int B, int gamma, int V, co
  * cache rows past lens, so run it between verify calls, not inside a round. */
 spade_status spade_profile_gemm(spade_model m, spade_kv kv, int kind, int B, int gamma, int launches,
                                 void* stream);
+
+/* Inspection hook (host only, no device): the tiling the wide-row GEMM picks
+ * for a bf16 projection launch of `rows` rows (> 16), `n_units` 16-row weight
+ * panels and `k` inputs (a multiple of 256) on `n_cu` compute units, with
+ * every setting at its default and buffers large enough for any k-split.
+ * kind as for spade_profile_gemm.  Writes the 16-row tiles per workgroup,
+ * the panels per wave and the k-splits; SPADE_EINVAL on a null pointer or
+ * a shape out of range. */
+spade_status spade_wide_tiling(int kind, int rows, int n_units, int k, int n_cu, int* row_tiles, int* panels,
+                               int* k_splits);
 
 /* Read and clear the device error word.  Synchronises the stream. */
 spade_status spade_get_device_error(spade_model m, uint32_t* h_flags, void* stream);

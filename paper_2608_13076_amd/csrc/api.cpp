@@ -91,7 +91,8 @@ ArenaLayout layout_of(const Dims& D) {
 
 struct WsPlan {
   size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, bar, fused, split_cnt,
-      split_part, prefill_tok, prefill_cnt, total;
+      split_part, wide_cnt, wide_part, prefill_tok, prefill_cnt, total;
+  size_t wide_items, wide_floats;
   FusedArena fa;
   bool has_fused;
   int max_units;
@@ -133,6 +134,18 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.max_units = std::max(std::max(D.d + 2 * D.dkv, 2 * D.F), D.Vpad) / 16;
   p.split_cnt = take((size_t)p.max_units * 4);
   p.split_part = take((size_t)p.max_units * 8 * 256 * 4);
+  // k-split wide-row O and down projections (d / 16 panels, up to Mmax rows):
+  // the most (unit group, row group) items and published floats any tiling needs
+  if (wb) {
+    const int nu = D.d / 16;
+    // unit groups of 8 panels (one per wave) x row groups of one 16-row tile
+    p.wide_items = (size_t)((nu + 7) / 8) * (size_t)((p.Mmax + 15) / 16);
+    for (int rt = 1; rt <= 3; ++rt)
+      for (int pp = 1; pp <= 2; ++pp)
+        if (!(pp == 2 && rt == 3)) p.wide_floats = std::max(p.wide_floats, wide_split_floats(nu, p.Mmax, rt, pp));
+  }
+  p.wide_cnt = take(p.wide_items * 4);
+  p.wide_part = take(p.wide_floats * 4);
   p.prefill_tok = take((size_t)p.Mmax * 4);
   p.prefill_cnt = take((size_t)max_batch * 4);
   // the single-launch pass handles bf16 weights and cache with head_dim 128
@@ -198,6 +211,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->gemm_wgs = m->n_cu;
   m->wide_rt = 0;
   m->wide_p = 0;
+  m->wide_ks = 0;
   m->split_ks = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
@@ -225,6 +239,10 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.attn_cnt = (uint32_t*)(b + p.attn_cnt);
   w.split_cnt = (uint32_t*)(b + p.split_cnt);
   w.split_part = (float*)(b + p.split_part);
+  w.wide_cnt = (uint32_t*)(b + p.wide_cnt);
+  w.wide_part = (float*)(b + p.wide_part);
+  w.wide_items = p.wide_items;
+  w.wide_floats = p.wide_floats;
   w.prefill_tok = (int32_t*)(b + p.prefill_tok);
   w.prefill_cnt = (int32_t*)(b + p.prefill_cnt);
   w.logits = (float*)(b + p.logits);
@@ -253,6 +271,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   hipError_t e = hipMemcpy(w.rope, rope.data(), rope.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemset(w.attn_cnt, 0, (size_t)max_batch * m->dims.H * 4);
   if (e == hipSuccess) e = hipMemset(w.split_cnt, 0, (size_t)p.max_units * 4);
+  if (e == hipSuccess && p.wide_items > 0) e = hipMemset(w.wide_cnt, 0, p.wide_items * 4);
   if (e == hipSuccess) e = hipMemset(w.err, 0, 4);
   if (e == hipSuccess) e = hipMemset(w.bar, 0, kBarBytes);
   // activation buffers start at zero so rows past M never feed NaNs
@@ -466,6 +485,13 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
   return SPADE_OK;
 }
 
+spade_status spade_model_set_wide_k_splits(spade_model m, int splits) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (splits != 0 && splits != 1 && splits != 2 && splits != 4) return fail(SPADE_EINVAL, "splits must be 0, 1, 2 or 4");
+  m->wide_ks = splits;
+  return SPADE_OK;
+}
+
 spade_status spade_prefill_batch(spade_model m, spade_kv kv, int B, const int32_t* d_tokens, int ld,
                                  const int32_t* h_n_tokens, void* stream) {
   if (!m || !kv || !d_tokens || !h_n_tokens) return fail(SPADE_EINVAL, "null pointer");
@@ -565,6 +591,19 @@ spade_status spade_profile_gemm(spade_model m, spade_kv kv, int kind, int B, int
     hipError_t e = launch_layer_gemm(m, kv, kind, i % m->dims.L, fc, (hipStream_t)stream);
     if (e != hipSuccess) return hipfail(e, "profile_gemm");
   }
+  return SPADE_OK;
+}
+
+spade_status spade_wide_tiling(int kind, int rows, int n_units, int k, int n_cu, int* row_tiles, int* panels,
+                               int* k_splits) {
+  if (!row_tiles || !panels || !k_splits) return fail(SPADE_EINVAL, "null pointer");
+  if (kind < GEMM_QKV || kind > GEMM_LM || rows <= kWideMinRows || n_units < 1 || k < 256 || k % 256 != 0 ||
+      n_cu < 1)
+    return fail(SPADE_EINVAL, "shape out of range");
+  const WideChoice c = wide_choice(kind, rows, n_units, k / 256, k, n_cu, 0, 0, 0, (size_t)-1, (size_t)-1);
+  *row_tiles = c.rt;
+  *panels = c.p;
+  *k_splits = c.ks;
   return SPADE_OK;
 }
 

@@ -29,6 +29,14 @@
 // b % 8 and takes unit group b % 8 + 8 j), so a weight tile read by the first
 // row group is an L2 hit for the others.
 //
+// K-splits (KS = 2 or 4; the O and down projections, whose few panels give
+// too few workgroups to fill the chip): workgroup split s streams only the
+// k-blocks of ranges [8s/KS, 8(s+1)/KS).  Split 0 publishes its running sum
+// over its ranges, the other splits each range partial (write-through stores);
+// every workgroup then arrives on the counter of its (unit group, row group),
+// and the last to arrive continues split 0's sum over the other ranges in
+// range order and runs the epilogue.
+//
 // Arithmetic is the skinny engine's, operation for operation: the k-blocks
 // of a panel are summed over the same eight k-ranges (range w: k-blocks
 // [NKB w / 8, NKB (w + 1) / 8)), each range with a fresh MFMA accumulator in
@@ -49,12 +57,21 @@ template <int RT>
 struct GemmWideSmem {
   uint8_t ring[kWideSlots][kActSplits][RT * 16][512];
   float rinv[RT * 16];
+  int last;  // k-splits: this workgroup arrived last
 };
+
+// Published values of one (unit group, row group) of a k-split launch: slot
+// r (0: split 0's running sum, r >= 8/KS: range r), then per wave, panel, row
+// tile, accumulator register and lane one float.
+template <int RT, int P>
+constexpr int kWideItemFloats = 8 * kGemmWaves * P * RT * 256;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <int RT, int P, int KIND>
+template <int RT, int P, int KIND, int KS = 1>
 struct GemmWide {
+  static_assert(KS == 1 || KS == 2 || KS == 4, "k-splits");
+  static constexpr int NPR = KS == 2 ? 3 : 1;  // range partials a split > 0 holds besides tot
   static constexpr int S = kActSplits;
   static constexpr int D = P == 1 ? 4 : 2;  // weight pipeline depth in k-blocks
   static constexpr int PERIOD = D == 4 ? 12 : 6;  // lcm(D, kWideSlots): steps per loop iteration
@@ -67,15 +84,20 @@ struct GemmWide {
   int ubase;  // first unit of this wave
   int row0;   // first launch row of the row group
   int NKB;
+  int ks, kb0, kb1;  // k-split and its k-blocks [kb0, kb1)
+  uint32_t* cnt;     // k-splits: arrival counter of this (unit group, row group)
+  float* part;       // k-splits: its published values (kWideItemFloats)
   Rsrc rfill;  // this wave's split of the operand
   uint32_t lds_ring;  // LDS byte address of the ring
   uint32_t aoff[4];   // this lane's fragment offsets within a slot (slice j: aoff[j % 4] + 256 (j / 4))
   uint4 wset[D][P][8];
   floatx4 acc[RT][P], tot[RT][P];
+  floatx4 pr[NPR][RT][P];  // split > 0: earlier range partials, latest first
   int rnext, bnd;  // next k-range index and the k-block its range starts at
 
-  __device__ __forceinline__ GemmWide(const GemmParams& a_, GemmWideSmem<RT>& sm_, int ug, int rg)
-      : a(a_), sm(sm_) {
+  __device__ __forceinline__ GemmWide(const GemmParams& a_, GemmWideSmem<RT>& sm_, int ug, int rg, int ks_ = 0,
+                                      uint32_t* cnt_ = nullptr, float* part_ = nullptr)
+      : a(a_), sm(sm_), ks(ks_), cnt(cnt_), part(part_) {
     tid = threadIdx.x;
     lane = tid & 63;
     wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -96,10 +118,16 @@ struct GemmWide {
       for (int p = 0; p < P; ++p) {
         acc[mt][p] = floatx4{0.f, 0.f, 0.f, 0.f};
         tot[mt][p] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < NPR; ++q) pr[q][mt][p] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
-    rnext = 1;
-    bnd = NKB / kGemmWaves;
-    while (bnd == 0 && rnext < kGemmWaves) bnd = (NKB * ++rnext) / kGemmWaves;
+    // ranges [r_lo, r_hi) of this split; rnext / bnd: the first non-empty one
+    const int r_lo = kGemmWaves * ks / KS, r_hi = kGemmWaves * (ks + 1) / KS;
+    kb0 = NKB * r_lo / kGemmWaves;
+    kb1 = NKB * r_hi / kGemmWaves;
+    rnext = r_lo + 1;
+    bnd = NKB * rnext / kGemmWaves;
+    while (bnd == kb0 && rnext < r_hi) bnd = (NKB * ++rnext) / kGemmWaves;
   }
 
   // weight tiles of k-block kb of this wave's units (zeros past the panel or
@@ -108,7 +136,7 @@ struct GemmWide {
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       const int u = ubase + p;
-      const bool ok = u < a.n_units && kb < NKB;
+      const bool ok = u < a.n_units && kb < kb1;
       const uint8_t* tile = a.w + ((size_t)(ok ? u : 0) * NKB + (ok ? kb : 0)) * kTileBytes;
       const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
 #pragma unroll
@@ -118,12 +146,12 @@ struct GemmWide {
 
   // Request activation k-block kb into ring slot `slot`.  Waves 0-3 move
   // split 0 and waves 4-7 split 1; one load instruction moves two rows (lane
-  // l: row 2 rp + l / 32, LDS chunk l % 32).  Rows past M repeat row M - 1
-  // and k-blocks past the panel repeat the last one: finite values whose
-  // products are never stored (rows) or meet zero weights (k-blocks).
+  // l: row 2 rp + l / 32, LDS chunk l % 32).  Rows past M repeat row M - 1:
+  // finite values whose products are never stored.  K-blocks past this
+  // split's end read nothing (the loop never reaches them).
   __device__ __forceinline__ void fill(int kb, int slot) const {
     const int s = wave >> 2;
-    const int kbc = kb < NKB ? kb : NKB - 1;
+    const bool kok = kb < kb1;
     const int c = lane & 31;
 #pragma unroll
     for (int i = 0; i < NFILL; ++i) {
@@ -131,7 +159,7 @@ struct GemmWide {
       const int row = 2 * rp + (lane >> 5);
       const int grow = row0 + row < a.M ? row0 + row : a.M - 1;
       const int gc = c ^ (row & 15);
-      const uint32_t off = (uint32_t)(grow * a.act_stride + kbc * 256 + gc * 8) * 2u;
+      const uint32_t off = kok ? (uint32_t)(grow * a.act_stride + kb * 256 + gc * 8) * 2u : kOob;
       __attribute__((address_space(3))) void* dst =
           (__attribute__((address_space(3))) void*)&sm.ring[slot][s][2 * rp][0];
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rfill, dst, 16, off, 0, 0, 0);
@@ -219,15 +247,24 @@ struct GemmWide {
   }
 
   // after k-block kb: at the end of a k-range add its partial to the total
-  // (ranges in order; an empty range adds nothing, as a zero partial would)
+  // (ranges in order; an empty range adds nothing, as a zero partial would).
+  // A k-split other than the first keeps each range partial instead: the
+  // latest in tot, the earlier ones in pr (latest first).
   __device__ __forceinline__ void range_end(int kb) {
     if (kb + 1 == bnd) {
 #pragma unroll
       for (int mt = 0; mt < RT; ++mt)
 #pragma unroll
         for (int p = 0; p < P; ++p) {
+          if (KS == 1 || ks == 0) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) tot[mt][p][i] += acc[mt][p][i];
+            for (int i = 0; i < 4; ++i) tot[mt][p][i] += acc[mt][p][i];
+          } else {
+#pragma unroll
+            for (int q = NPR - 1; q > 0; --q) pr[q][mt][p] = pr[q - 1][mt][p];
+            pr[0][mt][p] = tot[mt][p];
+            tot[mt][p] = acc[mt][p];
+          }
           acc[mt][p] = floatx4{0.f, 0.f, 0.f, 0.f};
         }
       do {
@@ -272,19 +309,98 @@ struct GemmWide {
     ((I < n ? step<I % kWideSlots, I % D>(kb + I) : void()), ...);
   }
 
+  // Byte offset of (slot, panel p, row tile mt, register i) of this lane in
+  // the published values of a k-split launch.
+  __device__ __forceinline__ uint32_t part_off(int slot, int p, int mt, int i) const {
+    return (uint32_t)(((((slot * kGemmWaves + wave) * P + p) * RT + mt) * 4 + i) * 64 + lane) * 4u;
+  }
+
+  // K-splits: publish this split's values, arrive, and in the last workgroup
+  // to arrive leave in tot the full sums (split 0's running sum, then the
+  // non-empty ranges of the other splits in range order).  Returns whether
+  // this workgroup runs the epilogue (uniform).
+  __device__ __forceinline__ bool combine_splits() {
+    const Rsrc rp = make_rsrc(part, (uint32_t)kWideItemFloats<RT, P> * 4u);
+    const int r_lo = kGemmWaves * ks / KS, r_hi = kGemmWaves * (ks + 1) / KS;
+    auto nonempty = [&](int r) { return NKB * (r + 1) / kGemmWaves > NKB * r / kGemmWaves; };
+    // value q (tot, then pr[q - 1]) holds the q-th non-empty range from the
+    // top of this split; split 0 stores only its running sum, in slot 0
+    int slot[NPR + 1];
+    {
+      int q = 0;
+#pragma unroll
+      for (int i = 0; i <= NPR; ++i) slot[i] = -1;
+      for (int r = r_hi - 1; r >= r_lo; --r)
+        if (nonempty(r)) {
+#pragma unroll
+          for (int i = 0; i <= NPR; ++i)
+            if (i == q) slot[i] = r;
+          ++q;
+        }
+      if (ks == 0) {
+        slot[0] = 0;
+#pragma unroll
+        for (int i = 1; i <= NPR; ++i) slot[i] = -1;
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+#pragma unroll
+      for (int mt = 0; mt < RT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          st_f32<true>(rp, slot[0] >= 0 ? part_off(slot[0], p, mt, i) : kOob, tot[mt][p][i]);
+#pragma unroll
+          for (int q = 1; q <= NPR; ++q)
+            st_f32<true>(rp, slot[q] >= 0 ? part_off(slot[q], p, mt, i) : kOob, pr[q - 1][mt][p][i]);
+        }
+    // every published value has landed: arrive
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int last = old == (uint32_t)KS - 1u;
+      if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      sm.last = last;
+    }
+    __syncthreads();
+    if (!sm.last) return false;
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+#pragma unroll
+      for (int mt = 0; mt < RT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v[kGemmWaves];
+#pragma unroll
+          for (int r = 0; r < kGemmWaves; ++r) {
+            const bool use = r == 0 || (r >= kGemmWaves / KS && nonempty(r));
+            v[r] = ld_b32_coh(rp, use ? part_off(r, p, mt, i) : kOob);
+          }
+          float t = v[0];
+#pragma unroll
+          for (int r = kGemmWaves / KS; r < kGemmWaves; ++r)
+            if (nonempty(r)) t += v[r];
+          tot[mt][p][i] = t;
+        }
+    return true;
+  }
+
   __device__ __forceinline__ void run() {
-    // prologue: k-blocks 0 and 1 of the operand, the first D weight sets
-    fill(0, 0);
-    fill(1, 1);
+    // prologue: the split's first two k-blocks of the operand, the first D
+    // weight sets
+    fill(kb0, 0);
+    fill(kb0 + 1, 1);
     // the fills stay older than every weight load (the waits count on it)
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 0; i < D; ++i) issue_w(i, wset[i]);
+    for (int i = 0; i < D; ++i) issue_w(kb0 + i, wset[i]);
     // whole periods in a loop (no exits inside, so the compiler's wait counts
     // at the loop head stay exact), then the remaining k-blocks
-    const int full = NKB / PERIOD * PERIOD;
-    for (int kb = 0; kb < full; kb += PERIOD) period_steps(kb, std::make_integer_sequence<int, PERIOD>{});
-    tail_steps(full, NKB - full, std::make_integer_sequence<int, PERIOD - 1>{});
+    const int n = kb1 - kb0;
+    const int full = n / PERIOD * PERIOD;
+    for (int t = 0; t < full; t += PERIOD) period_steps(kb0 + t, std::make_integer_sequence<int, PERIOD>{});
+    tail_steps(kb0 + full, n - full, std::make_integer_sequence<int, PERIOD - 1>{});
     // the last fills (k-blocks past the end) must land before the ring is
     // reused; the row scales are only needed by the epilogue
     __builtin_amdgcn_s_waitcnt(0);
@@ -293,6 +409,8 @@ struct GemmWide {
       if ((tid & 15) == 0) sm.rinv[r] = ri;
     }
     __syncthreads();
+    if constexpr (KS > 1)
+      if (!combine_splits()) return;
     // epilogue: lane holds rows mt*16 + 4g + i, column kl of each unit
     bool nan_seen = false;
 #pragma unroll
@@ -337,7 +455,7 @@ inline __host__ __device__ int gemm_wide_unit_groups(int n_units, int p) {
   return (n_units + kGemmWaves * p - 1) / (kGemmWaves * p);
 }
 inline __host__ __device__ uint32_t gemm_wide_lds_bytes(int rt) {
-  return (uint32_t)(kWideSlots * kActSplits * rt * 16 * 512 + rt * 16 * 4);
+  return (uint32_t)(kWideSlots * kActSplits * rt * 16 * 512 + rt * 16 * 4 + 16);
 }
 
 }  // namespace spade

@@ -129,15 +129,23 @@ __global__ void __launch_bounds__(kGemmWaves * 64) gemm_split_kernel(GemmParams 
 }
 
 // Wide-row projection GEMM (device_gemm_wide.h): workgroup b runs on XCD
-// b % 8 and takes unit group b % 8 + 8 (q / NRG), row group q % NRG with
-// q = b / 8, so the row groups of a unit group share that XCD's L2.
-template <int RT, int P, int KIND>
-__global__ void __launch_bounds__(kGemmWaves * 64) gemm_wide_kernel(GemmParams a, int NRG, int NUG) {
+// b % 8 and takes unit group b % 8 + 8 (q / (NRG KS)), then k-split and row
+// group from q % (NRG KS) (row group fastest), q = b / 8, so the row groups
+// and k-splits of a unit group share that XCD's L2.  K-splits: cnt / part
+// hold one arrival counter / kWideItemFloats published values per (unit
+// group, row group).
+template <int RT, int P, int KIND, int KS>
+__global__ void __launch_bounds__(kGemmWaves * 64)
+    gemm_wide_kernel(GemmParams a, int NRG, int NUG, uint32_t* cnt, float* part) {
   extern __shared__ uint4 lds_dyn[];
   const int b = (int)blockIdx.x, q = b >> 3;
-  const int ug = (b & 7) + 8 * (q / NRG), rg = q % NRG;
+  const int j = q / (NRG * KS), rem = q - j * (NRG * KS);
+  const int ks = rem / NRG, rg = rem - ks * NRG;
+  const int ug = (b & 7) + 8 * j;
   if (ug >= NUG) return;  // uniform, before any barrier
-  GemmWide<RT, P, KIND> g(a, *(GemmWideSmem<RT>*)lds_dyn, ug, rg);
+  const int item = ug * NRG + rg;
+  GemmWide<RT, P, KIND, KS> g(a, *(GemmWideSmem<RT>*)lds_dyn, ug, rg, ks, KS > 1 ? cnt + item : nullptr,
+                              KS > 1 ? part + (size_t)item * kWideItemFloats<RT, P> : nullptr);
   g.run();
 }
 
@@ -847,62 +855,134 @@ hipError_t launch_split(int kind, const GemmParams& gp, int ks, int n_cu, uint32
   }
 }
 
-template <int RT, int P, int KIND>
-hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, hipStream_t st) {
-  const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, P, KIND>);
+template <int RT, int P, int KIND, int KS>
+hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, uint32_t* cnt, float* part, hipStream_t st) {
+  const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, P, KIND, KS>);
   const uint32_t lds = gemm_wide_lds_bytes(RT);
   static hipError_t attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return attr;
-  const int grid = 8 * ((nug + 7) / 8) * nrg;
-  hipLaunchKernelGGL((gemm_wide_kernel<RT, P, KIND>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp, nrg, nug);
+  const int grid = 8 * ((nug + 7) / 8) * nrg * KS;
+  hipLaunchKernelGGL((gemm_wide_kernel<RT, P, KIND, KS>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp, nrg, nug,
+                     cnt, part);
   return hipGetLastError();
 }
 
-template <int KIND>
-hipError_t launch_wide_kind(const GemmParams& gp, int rt, int p, int nrg, int nug, hipStream_t st) {
-  if (p == 2) {  // two panels per wave: at most two row tiles (register budget)
-    if (rt == 2) return launch_wide_rt<2, 2, KIND>(gp, nrg, nug, st);
-    return launch_wide_rt<1, 2, KIND>(gp, nrg, nug, st);
+template <int KIND, int KS>
+hipError_t launch_wide_ks(const GemmParams& gp, int rt, int p, int nrg, int nug, uint32_t* cnt, float* part,
+                          hipStream_t st) {
+  if constexpr (KS != 2) {
+    if (p == 2 && rt == 2) return launch_wide_rt<2, 2, KIND, KS>(gp, nrg, nug, cnt, part, st);
+    if (rt == 3) return launch_wide_rt<3, 1, KIND, KS>(gp, nrg, nug, cnt, part, st);
+  } else if (rt * p > 2) {
+    return hipErrorInvalidValue;  // wide_choice gives two k-splits at most two accumulators
   }
-  if (rt == 3) return launch_wide_rt<3, 1, KIND>(gp, nrg, nug, st);
-  if (rt == 2) return launch_wide_rt<2, 1, KIND>(gp, nrg, nug, st);
-  return launch_wide_rt<1, 1, KIND>(gp, nrg, nug, st);
+  if (p == 2) return launch_wide_rt<1, 2, KIND, KS>(gp, nrg, nug, cnt, part, st);
+  if (rt == 2) return launch_wide_rt<2, 1, KIND, KS>(gp, nrg, nug, cnt, part, st);
+  return launch_wide_rt<1, 1, KIND, KS>(gp, nrg, nug, cnt, part, st);
 }
 
-// All rows of a bf16 projection in one launch.  Row tiles per workgroup and
-// panels per wave are fixed by the caller (> 0) or chosen here.  A compute
-// unit streams about the same number of bytes per second whether they come
-// from HBM or L2, so the time is close to the rounds of workgroups (one per
-// compute unit at a time) times the bytes each moves per k-block: 64 KB of
-// weights per panel per wave and 16 KB of operand per row tile.
-hipError_t launch_wide(int kind, const GemmParams& gp, int n_cu, int fixed_rt, int fixed_p, hipStream_t st) {
-  const int tiles = (gp.M + 15) / 16;
-  int best_rt = 1, best_p = 1;
-  long best = -1;
+template <int KIND>
+hipError_t launch_wide_kind(const GemmParams& gp, int rt, int p, int ks, int nrg, int nug, uint32_t* cnt, float* part,
+                            hipStream_t st) {
+  if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
+    if (ks == 4) return launch_wide_ks<KIND, 4>(gp, rt, p, nrg, nug, cnt, part, st);
+    if (ks == 2) return launch_wide_ks<KIND, 2>(gp, rt, p, nrg, nug, cnt, part, st);
+  }
+  return launch_wide_ks<KIND, 1>(gp, rt, p, nrg, nug, cnt, part, st);
+}
+
+}  // namespace
+
+// Published floats of a k-split wide launch of M rows and n_units panels
+// with (rt, p): one block of kWideItemFloats per (unit group, row group).
+size_t wide_split_floats(int n_units, int M, int rt, int p) {
+  const size_t items = (size_t)gemm_wide_unit_groups(n_units, p) * gemm_wide_row_groups(M, rt);
+  return items * (size_t)8 * kGemmWaves * p * rt * 256;
+}
+
+WideChoice wide_choice(int kind, int M, int n_units, int NKB, int K, int n_cu, int fixed_rt, int fixed_p, int fixed_ks,
+                       size_t cap_items, size_t cap_floats) {
+  const int tiles = (M + 15) / 16;
+  const bool splittable = kind == GEMM_O || kind == GEMM_DOWN;
+  const bool can_split = splittable && fixed_ks != 1;
+  WideChoice best{1, 1, 1};
+  double best_cost = -1.0, best_cu = 0.0;
   for (int p = 2; p >= 1; --p) {
     if (fixed_p > 0 && p != fixed_p) continue;
     for (int rt = 3; rt >= 1; --rt) {
       if (p == 2 && rt == 3) continue;
       if (fixed_rt > 0 && rt != fixed_rt) continue;
       if (fixed_rt <= 0 && rt > tiles) continue;
-      const long wgs = (long)gemm_wide_unit_groups(gp.n_units, p) * gemm_wide_row_groups(gp.M, rt);
-      const long rounds = (wgs + n_cu - 1) / n_cu;
-      const long cost = rounds * (64 * p + 16 * rt);
-      if (best < 0 || cost < best) {
-        best = cost;
-        best_rt = rt;
-        best_p = p;
+      for (int ks = 1; ks <= 4; ks *= 2) {
+        if (ks > 1 && !can_split) continue;
+        if (fixed_ks > 1 && ks != fixed_ks && (can_split || ks != 1)) continue;
+        // two k-splits hold three more range partials per accumulator: at most
+        // two accumulators per lane (register budget)
+        if (ks == 2 && rt * p > 2) continue;
+        const int nug = gemm_wide_unit_groups(n_units, p), nrg = gemm_wide_row_groups(M, rt);
+        const size_t items = (size_t)nug * nrg;
+        if (ks > 1 && (items > cap_items || wide_split_floats(n_units, M, rt, p) > cap_floats)) continue;
+        const long wgs = (long)items * ks;
+        const long rounds = (wgs + n_cu - 1) / n_cu;
+        const int nkbs = (NKB + ks - 1) / ks;
+        double cost, cu = 0.0;
+        if (!splittable) {
+          // KB each workgroup moves per k-block, times rounds of workgroups
+          cost = (double)rounds * (64 * p + 16 * rt);
+        } else {
+          // Fitted to stand-alone launches of the 7B and 33B O and down
+          // projections at 144 and 28 rows over every tiling: per round a
+          // workgroup streams its weight tiles at about 86 KB/us (75 with two
+          // panels per wave), its operand k-blocks and published values at
+          // 37 KB/us and pays 1.8 us of latency; all workgroups together stay
+          // under 6 TB/s of HBM; the k-split combine (publish, arrive, the
+          // last workgroup's reads and epilogue) adds about 10 us.
+          const double slot_kb = 8.0 * rt * p;  // one published slot
+          const double part_kb = ks > 1 ? (8.0 / ks + (9.0 - 8.0 / ks) / ks) * slot_kb : 0.0;
+          const double w_kb = (double)nkbs * 64 * p, a_kb = (double)nkbs * 16 * rt + part_kb;
+          const double per_round = w_kb / (p == 1 ? 86.0 : 75.0) + a_kb / 37.0 + 1.8;
+          const double uniq_kb = (double)n_units * NKB * 8 + (double)M * K * 4 / 1024.0 +
+                                 (ks > 1 ? items * (9.0 - 8.0 / ks) * slot_kb * 2 : 0.0);
+          cu = rounds * per_round;
+          cost = std::max(cu, uniq_kb / 6000.0 + 1.8) + (ks > 1 ? 10.0 : 0.0);
+        }
+        // ties (HBM-bound tilings) go to the least compute-unit time
+        if (best_cost < 0 || cost < best_cost - 1e-9 || (cost <= best_cost + 1e-9 && cu < best_cu - 1e-9)) {
+          best_cost = cost;
+          best_cu = cu;
+          best = WideChoice{rt, p, ks};
+        }
       }
     }
   }
-  const int nug = gemm_wide_unit_groups(gp.n_units, best_p);
-  const int nrg = gemm_wide_row_groups(gp.M, best_rt);
+  // a fixed k-split that does not fit the published-value buffers: none
+  if (best_cost < 0 && fixed_ks > 1)
+    return wide_choice(kind, M, n_units, NKB, K, n_cu, fixed_rt, fixed_p, 1, cap_items, cap_floats);
+  return best;
+}
+
+namespace {
+
+// All rows of a bf16 projection in one launch.  Row tiles per workgroup,
+// panels per wave and k-splits are fixed by the caller (> 0) or chosen by
+// wide_choice: a compute unit streams about the same number of bytes per
+// second whether they come from HBM or L2, so the time is close to the rounds
+// of workgroups (one per compute unit at a time) times the bytes each moves
+// per k-block, 64 KB of weights per panel per wave and 16 KB of operand per
+// row tile; the O and down projections, which can also be k-split, use a
+// model fitted to measured launches.
+hipError_t launch_wide(spade_model md, int kind, const GemmParams& gp, hipStream_t st) {
+  const Workspace& W = md->ws;
+  const WideChoice c = wide_choice(kind, gp.M, gp.n_units, gp.NKB, gp.NKB * 256, md->n_cu, md->wide_rt, md->wide_p,
+                                   md->wide_ks, W.wide_items, W.wide_floats);
+  const int nug = gemm_wide_unit_groups(gp.n_units, c.p);
+  const int nrg = gemm_wide_row_groups(gp.M, c.rt);
   switch (kind) {
-    case GEMM_QKV: return launch_wide_kind<GEMM_QKV>(gp, best_rt, best_p, nrg, nug, st);
-    case GEMM_O: return launch_wide_kind<GEMM_O>(gp, best_rt, best_p, nrg, nug, st);
-    case GEMM_GU: return launch_wide_kind<GEMM_GU>(gp, best_rt, best_p, nrg, nug, st);
-    case GEMM_DOWN: return launch_wide_kind<GEMM_DOWN>(gp, best_rt, best_p, nrg, nug, st);
-    default: return launch_wide_kind<GEMM_LM>(gp, best_rt, best_p, nrg, nug, st);
+    case GEMM_QKV: return launch_wide_kind<GEMM_QKV>(gp, c.rt, c.p, 1, nrg, nug, nullptr, nullptr, st);
+    case GEMM_O: return launch_wide_kind<GEMM_O>(gp, c.rt, c.p, c.ks, nrg, nug, W.wide_cnt, W.wide_part, st);
+    case GEMM_GU: return launch_wide_kind<GEMM_GU>(gp, c.rt, c.p, 1, nrg, nug, nullptr, nullptr, st);
+    case GEMM_DOWN: return launch_wide_kind<GEMM_DOWN>(gp, c.rt, c.p, c.ks, nrg, nug, W.wide_cnt, W.wide_part, st);
+    default: return launch_wide_kind<GEMM_LM>(gp, c.rt, c.p, 1, nrg, nug, nullptr, nullptr, st);
   }
 }
 
@@ -1024,7 +1104,7 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
     gp.act = act;
     gp.act_split = act_split;
     gp.act_stride = K;
-    return launch_wide(kind, gp, md->n_cu, md->wide_rt, md->wide_p, st);
+    return launch_wide(md, kind, gp, st);
   }
   for (int m0 = 0; m0 < M; m0 += kMaxRowsPerGemm) {
     GemmParams gp = g;

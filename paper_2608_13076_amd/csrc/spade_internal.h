@@ -139,6 +139,9 @@ struct Workspace {
   uint8_t* fused;     // activation arena of the single-launch verify pass (NULL if the model cannot use it)
   uint32_t* split_cnt;  // [max units / 2] arrival counters of the split-K GEMM (kept at zero between calls)
   float* split_part;    // [max units][8][256] published sums and range partials of the split-K GEMM
+  uint32_t* wide_cnt;   // [wide_items] arrival counters of the k-split wide-row GEMM (kept at zero between calls)
+  float* wide_part;     // [wide_floats] its published sums and range partials
+  size_t wide_items, wide_floats;
   int32_t* prefill_tok; // [Mmax] token ids of one batched-prefill forward
   int32_t* prefill_cnt; // [Bmax] prompt tokens to cache per request (batched prefill)
   FusedArena fa;
@@ -163,6 +166,7 @@ struct spade_model_s {
   bool fused_ok; // cooperative launches available and the single-launch verify pass enabled
   int wide_rt;   // 16-row tiles per workgroup of the wide-row GEMM: 0 chosen per launch, 1..3 fixed, -1 off
   int wide_p;    // panels per wave of the wide-row GEMM: 0 chosen per launch, 1..2 fixed
+  int wide_ks;   // k-splits of its O and down projections: 0 chosen per launch, 1 off, 2 or 4 fixed
   int split_ks;  // k-splits of the split-K GEMM: 0 chosen per launch, 2 or 4 where it qualifies, -1 off
 };
 
@@ -208,6 +212,13 @@ struct AcceptCall {
 };
 
 hipError_t launch_forward(spade_model m, spade_kv kv, const ForwardCall& fc, hipStream_t st);
+// tiling of a wide-row launch: row tiles per workgroup, panels per wave, k-splits
+struct WideChoice {
+  int rt, p, ks;
+};
+WideChoice wide_choice(int kind, int M, int n_units, int NKB, int K, int n_cu, int fixed_rt, int fixed_p, int fixed_ks,
+                       size_t cap_items, size_t cap_floats);
+size_t wide_split_floats(int n_units, int M, int rt, int p);
 int lm_stats_panels(spade_model m, int M);
 hipError_t launch_softmax(const float* logits, int rows, int V, float invT, float* out, hipStream_t st);
 hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_t* tokens, int ld,

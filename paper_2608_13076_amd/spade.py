@@ -30,7 +30,9 @@ EXPORTED = (
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
     "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
-    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles", "spade_model_set_split_k", "spade_softmax", "spade_prefill_batch",
+    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles",
+    "spade_model_set_wide_k_splits", "spade_model_set_split_k", "spade_softmax", "spade_prefill_batch",
+    "spade_wide_tiling",
 )
 
 
@@ -89,9 +91,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_get_device_error": (I, [P, P, P]),
         "spade_model_set_fused": (I, [P, I]),
         "spade_model_set_wide_tiles": (I, [P, I, I]),
+        "spade_model_set_wide_k_splits": (I, [P, I]),
         "spade_model_set_split_k": (I, [P, I]),
         "spade_softmax": (I, [P, I, I, F, P, P]),
         "spade_prefill_batch": (I, [P, P, I, P, I, P, P]),
+        "spade_wide_tiling": (I, [I, I, I, I, I, P, P, P]),
         "spade_last_error": (ctypes.c_char_p, []),
         "spade_model_destroy": (None, [P]),
         "spade_kv_destroy": (None, [P]),
@@ -180,6 +184,11 @@ class Model:
         chosen per launch, 1..3 fixed, -1 skinny engine once per 32 rows) and
         weight panels per wave (0 chosen per launch, 1..2 fixed)."""
         _check(self.lib.spade_model_set_wide_tiles(self.handle, int(row_tiles), int(panels)))
+
+    def set_wide_k_splits(self, splits: int) -> None:
+        """K splits of the batched O and down projections on the wide-row
+        GEMM: 0 chosen per launch, 1 off, 2 or 4 fixed."""
+        _check(self.lib.spade_model_set_wide_k_splits(self.handle, int(splits)))
 
     def set_split_k(self, splits: int) -> None:
         """K splits of the small-batch projections whose operand does not fit
@@ -328,6 +337,16 @@ def gemm_weight_bytes(shape, kind: str) -> int:
     dkv = getattr(shape, "kv_heads", shape.n_heads) * shape.head_dim
     n_k = {"qkv": (d + 2 * dkv, d), "o": (d, d), "gu": (2 * f, d), "down": (d, f), "lm": (v, d)}[kind]
     return n_k[0] * n_k[1] * elt
+
+
+def wide_tiling(kind: str, rows: int, n_units: int, k: int, n_cu: int = 256) -> tuple:
+    """(row tiles, panels per wave, k-splits) the wide-row GEMM picks for a
+    projection of `rows` rows, `n_units` weight panels and `k` inputs."""
+    lib = load_library()
+    rt, p, ks = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(lib.spade_wide_tiling(GEMM_KINDS[kind], rows, n_units, k, n_cu, ctypes.byref(rt), ctypes.byref(p),
+                                 ctypes.byref(ks)))
+    return rt.value, p.value, ks.value
 
 
 def gemm_roofline(model: Model, kv: KVCache, kind: str, B: int, gamma: int, reps: int, peak_gbs: float) -> dict:

@@ -89,3 +89,31 @@ def test_host_validation_without_device(lib):
     assert lib.spade_prefill(None, None, 0, None, 3, None) == -1
     assert lib.spade_kv_create(None, None, 1, 8, None, None, ctypes.byref(out)) == -1
     assert "null" in lib.spade_last_error().decode()
+
+
+def test_wide_tiling_splits_narrow_projections(lib):
+    """The wide-row tiling model cuts the down projection of the batched 7B
+    shape (144 rows) and the O and down projections of the 33B shape (28
+    rows) into k-splits -- their few panel groups would leave most compute
+    units idle -- and never splits QKV, gate/up or the LM head.  The picks
+    are the fastest tilings measured for those launches (7B O: 2 row tiles,
+    no split; 7B down: 3 row tiles, 4 splits; 33B O and down: 2 row tiles,
+    4 splits)."""
+    want = {(144, "o"): (2, 1, 1), (144, "down"): (3, 1, 4), (28, "o"): (2, 1, 4), (28, "down"): (2, 1, 4)}
+    for (M, d, F) in ((144, 4096, 11008), (28, 6656, 17920)):
+        for kind, nu, K in (("o", d // 16, d), ("down", d // 16, F), ("qkv", 3 * d // 16, d),
+                            ("gu", 2 * F // 16, d), ("lm", 2000, d)):
+            rt, p, ks = spade.wide_tiling(kind, M, nu, K)
+            assert 1 <= rt <= 3 and 1 <= p <= 2 and not (rt == 3 and p == 2)
+            if kind in ("o", "down"):
+                assert (rt, p, ks) == want[(M, kind)], (M, kind, rt, p, ks)
+            else:
+                assert ks == 1, (M, kind, rt, p, ks)
+    # two k-splits only with at most two accumulators per lane
+    for M in range(17, 257, 7):
+        rt, p, ks = spade.wide_tiling("down", M, 256, 11008)
+        assert ks != 2 or rt * p <= 2
+    with pytest.raises(spade.SpadeError):
+        spade.wide_tiling("o", 16, 256, 4096)
+    with pytest.raises(spade.SpadeError):
+        spade.wide_tiling("o", 64, 256, 4000)

@@ -1,13 +1,15 @@
 """Batched verification on the wide-row GEMM (more than 16 rows, bf16).
 
 Every tiling of the wide-row engine (1, 2 or 3 sixteen-row tiles per
-workgroup with 1 weight panel per wave, 1 or 2 with 2 panels, and the per-launch choice)
-must give bit-for-bit the logits,
-n_accepted and corrections of the skinny engine run once per 32 rows: both sum
-each dot product over the same eight k-ranges in the same order.  The
-per-launch choice is also compared with the oracle to the usual bar, at 35
-rows (B=5, gamma 6) and at 144 rows (B=16, gamma 8, the batched-serving
-shape).
+workgroup with 1 weight panel per wave, 1 or 2 with 2 panels, and the
+per-launch choice), each with the O and down projections unsplit or cut
+into 2 or 4 k-splits, must give bit-for-bit the logits, n_accepted and
+corrections of the skinny engine run once per 32 rows: all sum each dot
+product over the same eight k-ranges in the same order.  The mini shape's O
+projection has 4 k-blocks (empty k-ranges, splits without k-blocks) and its
+down projection 11.  The per-launch choice is also compared with the oracle
+to the usual bar, at 35 rows (B=5, gamma 6) and at 144 rows (B=16, gamma 8,
+the batched-serving shape).
 """
 
 import numpy as np
@@ -40,15 +42,19 @@ def test_wide_tilings_bit_identical_and_match_oracle(w):
     gpu_prefill(kv, inp)
     runs = {}
     for tiles in ((-1, 0), (1, 1), (2, 1), (3, 1), (1, 2), (2, 2), (0, 0)):
-        print(f"[{w.name}] M={w.batch * (w.gamma + 1)} wide (row tiles, panels) {tiles}", flush=True)
-        model.set_wide_tiles(*tiles)
-        runs[tiles] = gpu_verify(model, kv, inp)[:3]
-    ref = runs[(-1, 0)]
-    for tiles, (lg, n, c) in runs.items():
-        assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), tiles
-        assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), tiles
-    p = compare(orun, *runs[(0, 0)])
-    print(f"[{w.name}] logit err {p.logit_err:.2e}, n {runs[(0, 0)][1].tolist()}", flush=True)
+        for ks in ((0,) if tiles[0] < 0 else (1, 2, 4, 0)):
+            print(f"[{w.name}] M={w.batch * (w.gamma + 1)} wide (row tiles, panels) {tiles} k-splits {ks}",
+                  flush=True)
+            model.set_wide_tiles(*tiles)
+            model.set_wide_k_splits(ks)
+            runs[tiles + (ks,)] = gpu_verify(model, kv, inp)[:3]
+    ref = runs[(-1, 0, 0)]
+    for cfg, (lg, n, c) in runs.items():
+        assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), cfg
+        assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), cfg
+    p = compare(orun, *runs[(0, 0, 0)])
+    print(f"[{w.name}] logit err {p.logit_err:.2e}, n {runs[(0, 0, 0)][1].tolist()}", flush=True)
     assert p.logit_err < LOGIT_TOL[w.model.weight_dtype]
     assert not p.stable_n_fail and not p.stable_corr_fail, p
     assert model.device_error() == 0
+
