@@ -238,6 +238,18 @@ spade_status spade_model_set_fused(spade_model m, int enable);
  * return SPADE_EINVAL. */
 spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels);
 
+/* Work per workgroup of the verify attention (bf16 cache, head_dim 128).
+ * The attention is computed in chunks of 256 keys per (request, head), each
+ * giving a partial (row max, row sum, unnormalised output) that is merged in
+ * chunk order.  With `chunks` = 1 every chunk is one workgroup; with n > 1 a
+ * workgroup computes up to n consecutive chunks of one (request, head),
+ * fetching the next chunk's keys and values while it computes the current
+ * one, which keeps HBM busy when a call has many chunks (batched requests
+ * with long caches).  chunks = 0 (the default) chooses per call from the
+ * number of chunks and compute units.  Results are bit-for-bit the same
+ * under every setting.  Values outside [0, 128] return SPADE_EINVAL. */
+spade_status spade_model_set_attn_chunks(spade_model m, int chunks);
+
 /* K splitting of the batched O and down projections on the wide-row GEMM.
  * Their weights have few panels (d_model / 16), so one workgroup per panel
  * group leaves most compute units idle; with `splits` = 2 or 4 each

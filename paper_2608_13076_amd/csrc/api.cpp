@@ -213,6 +213,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->wide_p = 0;
   m->wide_ks = 0;
   m->split_ks = 0;
+  m->attn_cpw = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -482,6 +483,13 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
   if (panels == 2 && row_tiles == 3) return fail(SPADE_EINVAL, "two panels per wave take at most two row tiles");
   m->wide_rt = row_tiles;
   m->wide_p = panels;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_attn_chunks(spade_model m, int chunks) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (chunks < 0 || chunks > kAttnMaxChunks) return fail(SPADE_EINVAL, "chunks must be in [0, %d]", kAttnMaxChunks);
+  m->attn_cpw = chunks;
   return SPADE_OK;
 }
 

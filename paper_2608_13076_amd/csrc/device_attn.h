@@ -198,6 +198,20 @@ __device__ __forceinline__ void attn_load_q(const AttnItem& it, const float* q, 
   }
 }
 
+// Workgroup barrier.  LDSBAR: orders LDS accesses only, so loads and stores
+// to global memory stay in flight across it (a full __syncthreads waits for
+// pending global stores, and so for every older load as well).
+template <bool LDSBAR>
+__device__ __forceinline__ void attn_bar() {
+  if constexpr (LDSBAR) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  } else {
+    __syncthreads();
+  }
+}
+
 // One chunk with K/V fragments in r and query slices in qr (attn_load_q).
 // Returns this lane's unnormalised chunk outputs: rows 4g + i (i = 0..3),
 // feature 16 wave + kl.  Threads tid < R also set sm.m[tid] / sm.l[tid], the
@@ -209,7 +223,7 @@ __device__ __forceinline__ void attn_load_q(const AttnItem& it, const float* q, 
 // the eight waves (LDS, in wave order).  Probabilities (exp2 of the
 // log2(e)-scaled difference) go to LDS once, as two bf16 terms, and every
 // wave reads them as the A operand of O = P V.
-template <int CK>
+template <int CK, bool LDSBAR = false>
 __device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (&qr)[8], int R, float scale,
                                               const AttnRegs<CK>& r, AttnSmem<CK>& sm) {
   constexpr int NG = CK / 128;
@@ -250,7 +264,7 @@ __device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (
     mx = row16_max(mx);
     if (kl == 0) sm.pm[4 * g + i][wave] = mx;
   }
-  __syncthreads();
+  attn_bar<LDSBAR>();
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = 4 * g + i;
@@ -271,7 +285,7 @@ __device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (
     sum = row16_sum(sum);
     if (kl == 0) sm.ps[row][wave] = sum;
   }
-  __syncthreads();
+  attn_bar<LDSBAR>();
   if (tid < R) {
     float l = 0.f, M = -INFINITY;
 #pragma unroll
@@ -355,10 +369,11 @@ __device__ __forceinline__ void attn_merge_pair(Rsrc rpo, const AttnMergeSmem& m
 // resets the counter.  part_o / part_ml: [bh][NC][Rmax][kAttnHd] /
 // [bh][NC][Rmax][2].  All 512 threads call it; inactive items only
 // synchronise.
-template <int CK, class Out>
-__device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o, const AttnSmem<CK>& sa,
-                                                   AttnMergeSmem& ms, float* part_o, float* part_ml,
-                                                   uint32_t* attn_cnt, int H, int NC, int Rmax, int R, Out&& out) {
+// Store this chunk's partial (o: attn_chunk's result; m / l from sa) with
+// write-through stores, without waiting for them.
+template <int CK>
+__device__ __forceinline__ void attn_publish(const AttnItem& it, floatx4 o, const AttnSmem<CK>& sa, float* part_o,
+                                             float* part_ml, int H, int NC, int Rmax, int R) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, kl = lane & 15;
   const size_t bh = (size_t)it.bl * H + it.h;
@@ -375,14 +390,28 @@ __device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o
       __hip_atomic_store(pml + tid * 2 + 1, sa.l[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
+}
+
+// Once this workgroup's published partials (n_mine chunks of the (request,
+// head) of it) have landed, arrive on the counter of that (request, head)
+// with n_mine, and, in the workgroup whose arrival completes the request's
+// chunks, merge them and pass each merged output o = row * kAttnHd + dd to
+// out(o, value).  The completing arrival resets the counter.  All 512 threads
+// call it.
+template <class Out>
+__device__ __forceinline__ void attn_arrive_merge(const AttnItem& it, int n_mine, AttnMergeSmem& ms, float* part_o,
+                                                  float* part_ml, uint32_t* attn_cnt, int H, int NC, int Rmax, int R,
+                                                  Out&& out) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const size_t bh = (size_t)it.bl * H + it.h;
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (tid == 0) {
     int last = 0;
-    if (it.active) {
+    if (n_mine > 0) {
       uint32_t* cnt = attn_cnt + bh;
-      const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (old == (uint32_t)it.nc - 1u) {
+      const uint32_t old = __hip_atomic_fetch_add(cnt, (uint32_t)n_mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (old + (uint32_t)n_mine == (uint32_t)it.nc) {
         __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         last = 1;
       }
@@ -436,6 +465,16 @@ __device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o
     attn_load16(rpo, 0, nc, Rmax, oa + 512, oa + 512 < nout, vb);
     attn_merge_pair(rpo, ms, nc, Rmax, nout, oa, va, vb, out);
   }
+}
+
+// attn_publish and attn_arrive_merge for a workgroup that computed the one
+// chunk it.
+template <int CK, class Out>
+__device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o, const AttnSmem<CK>& sa,
+                                                   AttnMergeSmem& ms, float* part_o, float* part_ml,
+                                                   uint32_t* attn_cnt, int H, int NC, int Rmax, int R, Out&& out) {
+  attn_publish<CK>(it, o, sa, part_o, part_ml, H, NC, Rmax, R);
+  attn_arrive_merge(it, it.active ? 1 : 0, ms, part_o, part_ml, attn_cnt, H, NC, Rmax, R, out);
 }
 
 }  // namespace spade

@@ -167,6 +167,7 @@ struct AttnParams {
   int b0, R, H, d, kv_stride;
   int Hkv, G;  // K/V heads of the cache; query head h reads K/V head h / G
   int CK, NC;
+  int nb;  // requests of the call (bf16 kernels: the grid is one-dimensional)
   float scale;
   float* part_o;
   float* part_ml;
@@ -579,6 +580,25 @@ __global__ void __launch_bounds__(256) attn_combine_kernel(AttnParams p) {
   }
 }
 
+// Work of workgroup i of a bf16 attention launch over n_runs runs of chunks
+// (one chunk each, or cpw) per (request, K/V head): run r, query head h,
+// request bl.  The G query heads that share a K/V head get workgroups 8
+// apart, which run on one XCD, so the second to fourth reads of the same
+// keys and values are L2 hits.  ok == false: past the last item.
+struct AttnWork {
+  bool ok;
+  int r, h, bl;
+};
+__device__ __forceinline__ AttnWork attn_work(int i, int n_runs, int Hkv, int G, int nb) {
+  const int x = i & 7, j = i >> 3;     // XCD, slot on it
+  const int t = j / G, g = j - t * G;  // group of 8 items, query head within the K/V head
+  const int k = 8 * t + x;             // item: (run, K/V head, request), run fastest
+  const int r = k % n_runs, q = k / n_runs;
+  const int kvh = q % Hkv, bl = q / Hkv;
+  return AttnWork{bl < nb, r, kvh * G + g, bl};
+}
+inline int attn_grid(int n_runs, int Hkv, int G, int nb) { return 8 * G * ((n_runs * Hkv * nb + 7) / 8); }
+
 // bf16 cache, head_dim 128: chunks of CK keys, one 8-wave workgroup per
 // (chunk, head, request) (device_attn.h); chunks past a request's last key
 // exit at once, and the last chunk of a (request, head) to finish merges them
@@ -589,8 +609,10 @@ attn_b_kernel(AttnParams p) {
   __shared__ AttnSmem<CK> sm;
   __shared__ AttnMergeSmem ms;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int bl = blockIdx.z, h = blockIdx.y, bg = p.b0 + bl;
-  const AttnItem it = attn_item<CK>(true, bl, h, blockIdx.x, p.lens[bg], p.R, p.kc, p.vc,
+  const AttnWork wk = attn_work((int)blockIdx.x, p.NC, p.Hkv, p.G, p.nb);
+  if (!wk.ok) return;
+  const int bl = wk.bl, h = wk.h, bg = p.b0 + bl;
+  const AttnItem it = attn_item<CK>(true, bl, h, wk.r, p.lens[bg], p.R, p.kc, p.vc,
                                     ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * kAttnHd);
   if (!it.active) return;  // past the request's last key: uniform, before any barrier
   float4 qr[8];
@@ -601,6 +623,68 @@ attn_b_kernel(AttnParams p) {
   attn_mask_tail(it, lane, r);
   const floatx4 o = attn_chunk(it, qr, p.R, p.scale, r, sm);
   attn_publish_merge(it, o, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
+    const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
+    store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
+  });
+}
+
+// The same over runs of chunks: workgroup (run g, head h, request b) computes
+// chunks [g cpw, min((g + 1) cpw, nc_b)) of (b, h) in order, requesting the
+// K/V of the next chunk before it computes the current one, so its loads stay
+// in flight through the chunk's products, softmax and partial stores (the
+// barriers inside order LDS only).  Each chunk's partial and the merge are
+// exactly those of the one-chunk kernel; the workgroup arrives once with the
+// number of chunks it published.
+template <bool ABF16, int CK>
+__device__ __forceinline__ void attn_run_chunk(const AttnParams& p, const AttnItem& it0, int c, int c1,
+                                               const float4 (&qr)[8], AttnRegs<CK>& cur, AttnRegs<CK>& nxt,
+                                               AttnSmem<CK>& sm) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  // chunk c's K/V (and the previous chunk's stores) have landed; every wave
+  // is done with the previous chunk's LDS
+  __builtin_amdgcn_s_waitcnt(0);
+  attn_bar<true>();
+  AttnItem it = it0;
+  it.c = c;
+  it.k_lo = c * CK;
+  it.k_hi = min(it.k_lo + CK, it0.L + p.R);
+  if (c + 1 < c1) {
+    AttnItem in = it0;
+    in.c = c + 1;
+    in.k_lo = (c + 1) * CK;
+    in.k_hi = min(in.k_lo + CK, it0.L + p.R);
+    attn_zero_regs(nxt);
+    attn_load_plain(in, p.kv_stride, in.k_lo, (in.k_hi + 7) & ~7, wave, lane, nxt);
+  }
+  attn_mask_tail(it, lane, cur);
+  const floatx4 o = attn_chunk<CK, true>(it, qr, p.R, p.scale, cur, sm);
+  attn_publish<CK>(it, o, sm, p.part_o, p.part_ml, p.H, p.NC, p.Rmax, p.R);
+}
+
+template <bool ABF16, int CK>
+__global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
+attn_bp_kernel(AttnParams p, int cpw) {
+  __shared__ AttnSmem<CK> sm;
+  __shared__ AttnMergeSmem ms;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const AttnWork wk = attn_work((int)blockIdx.x, (p.NC + cpw - 1) / cpw, p.Hkv, p.G, p.nb);
+  if (!wk.ok) return;
+  const int bl = wk.bl, h = wk.h, bg = p.b0 + bl;
+  const int c0 = wk.r * cpw;
+  const AttnItem it0 = attn_item<CK>(true, bl, h, c0, p.lens[bg], p.R, p.kc, p.vc,
+                                     ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * kAttnHd);
+  if (!it0.active) return;  // past the request's last key: uniform, before any barrier
+  const int c1 = min(c0 + cpw, it0.nc);
+  float4 qr[8];
+  attn_load_q(it0, p.q + (size_t)(bl * p.R) * p.d + h * kAttnHd, p.d, p.R, lane, qr);
+  AttnRegs<CK> ra, rb;
+  attn_zero_regs(ra);
+  attn_load_plain(it0, p.kv_stride, it0.k_lo, (it0.k_hi + 7) & ~7, wave, lane, ra);
+  for (int c = c0; c < c1; c += 2) {
+    attn_run_chunk<ABF16, CK>(p, it0, c, c1, qr, ra, rb, sm);
+    if (c + 1 < c1) attn_run_chunk<ABF16, CK>(p, it0, c + 1, c1, qr, rb, ra, sm);
+  }
+  attn_arrive_merge(it0, c1 - c0, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
     const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
     store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
   });
@@ -1171,6 +1255,20 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   const int CK = attn_b ? kAttnChunkKeys : kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
+  // chunks per workgroup of the bf16 attention: fixed (> 0), else all the
+  // chunks of a (request, head) in one workgroup when query heads share K/V
+  // heads and the call has at least four chunks per compute unit (the K/V
+  // reads are then mostly L2 hits and the run's prefetch hides their
+  // latency), else one (with distinct K/V per head the one-chunk kernel's two
+  // workgroups per compute unit keep HBM busier: measured on the batched 7B
+  // and 8B shapes)
+  int cpw = md->attn_cpw;
+  if (attn_b && cpw <= 0) {
+    long chunks = 0;
+    for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) chunks += (kv->lens_ub[b] + fc.R + CK - 1) / CK;
+    chunks *= D.H;
+    cpw = (D.KVH < D.H && chunks >= 4L * md->n_cu) ? NC : 1;
+  }
 
   for (int l = 0; l < D.L; ++l) {
     if ((e = launch_layer_gemm(md, kv, GEMM_QKV, l, fc, st)) != hipSuccess) return e;
@@ -1197,9 +1295,16 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     ap.act_split = W.act_split;
     const dim3 agrid(NC, D.H, fc.nb);
     const bool kvb = D.kvdt == SPADE_BF16;
-    if (attn_b) {
-      if (wb) hipLaunchKernelGGL((attn_b_kernel<true, kAttnChunkKeys>), agrid, dim3(kAttnThreads), 0, st, ap);
-      else hipLaunchKernelGGL((attn_b_kernel<false, kAttnChunkKeys>), agrid, dim3(kAttnThreads), 0, st, ap);
+    ap.nb = fc.nb;
+    if (attn_b && cpw > 1) {
+      const dim3 rgrid(attn_grid((NC + cpw - 1) / cpw, D.KVH, D.H / D.KVH, fc.nb));
+      if (wb) hipLaunchKernelGGL((attn_bp_kernel<true, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
+      else hipLaunchKernelGGL((attn_bp_kernel<false, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
+      e = hipGetLastError();
+    } else if (attn_b) {
+      const dim3 bgrid(attn_grid(NC, D.KVH, D.H / D.KVH, fc.nb));
+      if (wb) hipLaunchKernelGGL((attn_b_kernel<true, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
+      else hipLaunchKernelGGL((attn_b_kernel<false, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
       e = hipGetLastError();
     } else if (D.hd == 64) {
       e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);

@@ -58,3 +58,33 @@ def test_wide_tilings_bit_identical_and_match_oracle(w):
     assert not p.stable_n_fail and not p.stable_corr_fail, p
     assert model.device_error() == 0
 
+
+
+@pytest.mark.parametrize("batch", [1, 6])
+def test_attention_runs_bit_identical(batch):
+    """The verify attention with one 256-key chunk per workgroup and with runs
+    of 2, 3, 4 or 9 chunks per workgroup (the next chunk's keys and values
+    fetched while the current one is computed), and the per-call choice, give
+    bit-for-bit the same logits, n_accepted and corrections: every chunk's
+    partial and the merge in chunk order are the same whichever workgroup
+    computes them.  Contexts up to 2100 keys (9 chunks); batch 1 runs the
+    skinny projections, batch 6 the wide-row ones."""
+    base = {w.name: w for w in mini_workloads()}["mini_bf16_wide_b5"]
+    w = base.with_(name=f"mini_bf16_long_b{batch}", batch=batch, gamma=4,
+                   ctx=(2000, 2100) if batch == 1 else (90, 2100), mode="greedy", draft_recipe="random",
+                   seed=2018 + batch)
+    weights = ModelWeights(w.model, w.seed)
+    inp = make_inputs(w)
+    model, kv = gpu_setup(w, weights)
+    kv.prefill_batch(inp.prompts)
+    runs = {}
+    for cpw in (1, 2, 3, 4, 9, 0):
+        print(f"[{w.name}] lens {inp.lens.tolist()} attention chunks per workgroup {cpw}", flush=True)
+        model.set_attn_chunks(cpw)
+        runs[cpw] = gpu_verify(model, kv, inp)[:3]
+    ref = runs[1]
+    assert np.isfinite(ref[0]).all()
+    for cpw, (lg, n, c) in runs.items():
+        assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), cpw
+        assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), cpw
+    assert model.device_error() == 0
