@@ -77,6 +77,13 @@ def test_attention_runs_bit_identical(batch):
     inp = make_inputs(w)
     model, kv = gpu_setup(w, weights)
     kv.prefill_batch(inp.prompts)
+    from paper_2608_13076_amd import spade
+    for bad in (-1, 129):
+        with pytest.raises(spade.SpadeError):
+            model.set_attn_chunks(bad)
+    for bad in (-1, 3, 8):
+        with pytest.raises(spade.SpadeError):
+            model.set_wide_k_splits(bad)
     runs = {}
     for cpw in (1, 2, 3, 4, 9, 0):
         print(f"[{w.name}] lens {inp.lens.tolist()} attention chunks per workgroup {cpw}", flush=True)
