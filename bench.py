@@ -192,9 +192,9 @@ def main() -> int:
     if args.summarize_counters:
         return summarize_counters(*args.summarize_counters)
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "this benchmark measures one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
-        print("bench.py: only --gpus 1 is supported (single-GPU build)", file=sys.stderr)
+        print("bench.py: only --gpus 1 is supported (one GPU)", file=sys.stderr)
         return 2
 
     import torch
@@ -302,7 +302,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16 weights+KV, f32 activations" if m.weight_dtype == "bf16" else "f32",
         "data": "synthetic (seeded N(0,0.02) weights, uniform prompt ids; no trained weights)",
-        "config": {"workload": w.name, "model": m.name, "batch": w.batch, "gamma": w.gamma,
+        "config": {"workload": w.name, "shape": m.name, "batch": w.batch, "gamma": w.gamma,
                    "cached_tokens": inp.lens.tolist(), "mode": w.mode, "drafts": drafts_src},
         "algorithmic_bytes_per_step": ab["total"],
         "achieved_GBps_whole_pass": round(gbs, 1),

@@ -1,6 +1,6 @@
 """Model shapes and verify workloads.
 
-The five full-size workloads follow the configurations this build is measured
+The five full-size workloads are the configurations the verify path is measured
 on: a tiny fp32 verifier and Llama-7B/13B/33B-shaped bf16 verifiers.  The paper
 itself runs LLaMA-3.1-8B as the cloud verifier (Experiments, "Models"); the
 synthetic shapes stand in for it.  ``mini_workloads`` are scaled-down variants

@@ -6,7 +6,7 @@ correction) that has not been run through the verifier yet.  The call scores
 the rows [pending, d_1 .. d_gamma] at positions lens[b] .. lens[b] + gamma.
 A prompt therefore has lens[b] + 1 ids.
 
-Draft recipes (the draft model itself is not part of this build):
+Draft recipes (no trained draft model exists here):
   random       uniform ids;
   chain_half   the first ceil(gamma/2) drafts are placeholders that the caller
                replaces with the verifier's own argmax chain, the rest uniform;

@@ -185,7 +185,7 @@ def test_c5_33b_commit_round_two_equals_fresh_prefill():
     print("[c5] weights + prefill", flush=True)
     model, kv = gpu_setup_streaming(w, max_len)
     gpu_prefill(kv, inp)
-    print("[c5] round 1", flush=True)
+    print("[c5] first verify call", flush=True)
     lg1, n1, c1, buf = gpu_verify(model, kv, inp)
     for b in range(w.batch):
         assert _greedy_consistent(lg1[b], inp.drafts[b], n1[b], c1[b]), b
@@ -195,7 +195,7 @@ def test_c5_33b_commit_round_two_equals_fresh_prefill():
     np.testing.assert_array_equal(lens2, inp.lens + n1 + 1)
     np.testing.assert_array_equal(pend2, c1)
     inp2 = make_inputs(w, round_index=1)
-    print("[c5] round 2", flush=True)
+    print("[c5] second verify call, after the commit", flush=True)
     lg2, n2, c2, _ = gpu_verify(model, kv, inp2)
     # fresh cache holding the committed sequences
     from paper_2608_13076_amd import spade
@@ -203,7 +203,7 @@ def test_c5_33b_commit_round_two_equals_fresh_prefill():
     for b in range(w.batch):
         seq = np.concatenate([inp.prompts[b], inp.drafts[b, : n1[b]], [c1[b]]]).astype(np.int32)
         kv2.prefill(b, seq)
-    print("[c5] round 2 on a fresh prefill", flush=True)
+    print("[c5] second verify call on a fresh prefill", flush=True)
     lg2f, n2f, c2f, _ = gpu_verify(model, kv2, inp2)
     np.testing.assert_array_equal(lg2, lg2f)
     np.testing.assert_array_equal(n2, n2f)
