@@ -583,8 +583,9 @@ __global__ void __launch_bounds__(256) attn_combine_kernel(AttnParams p) {
 // Work of workgroup i of a bf16 attention launch over n_runs runs of chunks
 // (one chunk each, or cpw) per (request, K/V head): run r, query head h,
 // request bl.  The G query heads that share a K/V head get workgroups 8
-// apart, which run on one XCD, so the second to fourth reads of the same
-// keys and values are L2 hits.  ok == false: past the last item.
+// apart, which run on one XCD, so all but the first of their reads of the
+// same keys and values can hit that XCD's L2.  ok == false: past the last
+// item.
 struct AttnWork {
   bool ok;
   int r, h, bl;
@@ -628,8 +629,8 @@ attn_b_kernel(AttnParams p) {
   });
 }
 
-// The same over runs of chunks: workgroup (run g, head h, request b) computes
-// chunks [g cpw, min((g + 1) cpw, nc_b)) of (b, h) in order, requesting the
+// The same over runs of chunks: the workgroup of run r of (request b, head h)
+// (attn_work) computes chunks [r cpw, min((r + 1) cpw, nc_b)) in order, requesting the
 // K/V of the next chunk before it computes the current one, so its loads stay
 // in flight through the chunk's products, softmax and partial stores (the
 // barriers inside order LDS only).  Each chunk's partial and the merge are
