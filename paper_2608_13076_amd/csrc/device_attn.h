@@ -310,6 +310,124 @@ __device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (
   return o;
 }
 
+// Low-register variant of attn_chunk for launches with many chunks per
+// compute unit: the K fragments come from attn_load_k, the queries from LDS
+// (sq, staged by the caller: row i, feature f at sq[i][f], rows past R zero),
+// and the V^T fragments are requested only after the score products, into the
+// registers the K fragments held, so a wave holds one of the two at a time.
+// Scores, softmax, P V and the returned partial are computed by the same
+// instructions in the same order as attn_chunk with attn_load_plain's
+// fragments.
+template <int CK>
+__device__ __forceinline__ void attn_load_k(const AttnItem& it, int wave, int lane, uint4 (&kf)[CK / 128][4]) {
+  const int g = lane >> 4, kl = lane & 15;
+#pragma unroll
+  for (int grp = 0; grp < CK / 128; ++grp) {
+    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = make_uint4(0, 0, 0, 0);
+    if (key < it.k_hi) {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = *(const uint4*)(it.kc + (size_t)key * kAttnHd + 32 * ks + 8 * g);
+    }
+  }
+}
+
+template <int CK>
+__device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
+                                                 const float (*sq)[kAttnHd + 4], int R, float scale, int stride,
+                                                 AttnSmem<CK>& sm) {
+  constexpr int NG = CK / 128;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, kl = lane & 15;
+  const int ke = (it.k_hi + 7) & ~7;
+  float sv[NG][4];
+#pragma unroll
+  for (int grp = 0; grp < NG; ++grp) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const float4 x0 = *(const float4*)&sq[kl][32 * ks + 8 * g];
+      const float4 x1 = *(const float4*)&sq[kl][32 * ks + 8 * g + 4];
+      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      uint4 qh, ql;
+      attn_split2(xs, qh, ql);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql),
+                                                    __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh),
+                                                    __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+    }
+    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * g + i;
+      sv[grp][i] = (key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
+    }
+  }
+  // the V^T fragments, after the score products (the K registers are free)
+  __builtin_amdgcn_sched_barrier(0);
+  AttnRegs<CK> r;
+  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
+#pragma unroll
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const int kv0 = it.k_lo + 32 * ks + 8 * g;
+    r.vf[ks] = make_uint4(0, 0, 0, 0);
+    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float mx = sv[0][i];
+#pragma unroll
+    for (int grp = 1; grp < NG; ++grp) mx = fmaxf(mx, sv[grp][i]);
+    mx = row16_max(mx);
+    if (kl == 0) sm.pm[4 * g + i][wave] = mx;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * g + i;
+    const float4 a = *(const float4*)&sm.pm[row][0];
+    const float4 b = *(const float4*)&sm.pm[row][4];
+    const float M = fmaxf(fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)), fmaxf(fmaxf(b.x, b.y), fmaxf(b.z, b.w)));
+    float sum = 0.f;
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp) {
+      const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[grp][i] - M) * 1.44269504088896341f);
+      sum += e;
+      const uint16_t h = f2bf(e);
+      const int kc = (CK / 8) * wave + 16 * grp + kl;
+      sm.ph[row][kc] = h;
+      sm.pl[row][kc] = f2bf(e - bf2f(h));
+    }
+    sum = row16_sum(sum);
+    if (kl == 0) sm.ps[row][wave] = sum;
+  }
+  __syncthreads();
+  if (tid < R) {
+    float l = 0.f, M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      l += sm.ps[tid][w];
+      M = fmaxf(M, sm.pm[tid][w]);
+    }
+    sm.m[tid] = M;
+    sm.l[tid] = l;
+  }
+  attn_mask_tail(it, lane, r);
+  floatx4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const uint4 ph = *(const uint4*)&sm.ph[kl][32 * ks + 8 * g];
+    const uint4 pl = *(const uint4*)&sm.pl[kl][32 * ks + 8 * g];
+    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
+                                                0, 0, 0);
+    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
+                                                0, 0, 0);
+  }
+  return o;
+}
+
 // Last-arrival merge of the chunks of one (request, head).
 struct AttnMergeSmem {
   float sc[kAttnMaxChunks][kAttnRows];  // merge weights

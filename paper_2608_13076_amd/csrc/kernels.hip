@@ -601,14 +601,18 @@ __device__ __forceinline__ AttnWork attn_work(int i, int n_runs, int Hkv, int G,
 inline int attn_grid(int n_runs, int Hkv, int G, int nb) { return 8 * G * ((n_runs * Hkv * nb + 7) / 8); }
 
 // bf16 cache, head_dim 128: chunks of CK keys, one 8-wave workgroup per
-// (chunk, head, request) (device_attn.h); chunks past a request's last key
-// exit at once, and the last chunk of a (request, head) to finish merges them
-// into the O-projection operand.
+// (chunk, head, request) (device_attn.h; attn_work orders them); chunks past a
+// request's last key exit at once, and the last chunk of a (request, head) to
+// finish merges them into the O-projection operand.  The queries are staged in
+// LDS and the V^T fragments loaded after the score products into the
+// registers K held (attn_chunk_lr): 78 VGPRs, three workgroups per compute
+// unit (keeping K, V and the queries in registers at once took 120: two).
 template <bool ABF16, int CK>
-__global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(4)))
-attn_b_kernel(AttnParams p) {
+__global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(6)))
+attn_lr_kernel(AttnParams p) {
   __shared__ AttnSmem<CK> sm;
   __shared__ AttnMergeSmem ms;
+  __shared__ float sq[kAttnRows][kAttnHd + 4];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const AttnWork wk = attn_work((int)blockIdx.x, p.NC, p.Hkv, p.G, p.nb);
   if (!wk.ok) return;
@@ -616,13 +620,15 @@ attn_b_kernel(AttnParams p) {
   const AttnItem it = attn_item<CK>(true, bl, h, wk.r, p.lens[bg], p.R, p.kc, p.vc,
                                     ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * kAttnHd);
   if (!it.active) return;  // past the request's last key: uniform, before any barrier
-  float4 qr[8];
-  attn_load_q(it, p.q + (size_t)(bl * p.R) * p.d + h * kAttnHd, p.d, p.R, lane, qr);
-  AttnRegs<CK> r;
-  attn_zero_regs(r);
-  attn_load_plain(it, p.kv_stride, it.k_lo, (it.k_hi + 7) & ~7, wave, lane, r);
-  attn_mask_tail(it, lane, r);
-  const floatx4 o = attn_chunk(it, qr, p.R, p.scale, r, sm);
+  // thread t stages features 4 (t % 32) .. + 3 of query row t / 32 (rows past R: zeros)
+  const int qrow = tid >> 5, f4 = tid & 31;
+  float4 qv = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (qrow < p.R) qv = *(const float4*)(p.q + (size_t)(bl * p.R + qrow) * p.d + h * kAttnHd + 4 * f4);
+  uint4 kf[CK / 128][4];
+  attn_load_k<CK>(it, wave, lane, kf);
+  *(float4*)&sq[qrow][4 * f4] = qv;
+  __syncthreads();
+  const floatx4 o = attn_chunk_lr<CK>(it, kf, sq, p.R, p.scale, p.kv_stride, sm);
   attn_publish_merge(it, o, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
     const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
     store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
@@ -1260,9 +1266,9 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   // chunks of a (request, head) in one workgroup when query heads share K/V
   // heads and the call has at least four chunks per compute unit (the K/V
   // reads are then mostly L2 hits and the run's prefetch hides their
-  // latency), else one (with distinct K/V per head the one-chunk kernel's two
-  // workgroups per compute unit keep HBM busier: measured on the batched 7B
-  // and 8B shapes)
+  // latency), else one (with distinct K/V per head the one-chunk kernel's
+  // three workgroups per compute unit keep HBM busier: measured on the
+  // batched 7B and 8B shapes)
   int cpw = md->attn_cpw;
   if (attn_b && cpw <= 0) {
     long chunks = 0;
@@ -1304,8 +1310,8 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
       e = hipGetLastError();
     } else if (attn_b) {
       const dim3 bgrid(attn_grid(NC, D.KVH, D.H / D.KVH, fc.nb));
-      if (wb) hipLaunchKernelGGL((attn_b_kernel<true, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
-      else hipLaunchKernelGGL((attn_b_kernel<false, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
+      if (wb) hipLaunchKernelGGL((attn_lr_kernel<true, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
+      else hipLaunchKernelGGL((attn_lr_kernel<false, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
       e = hipGetLastError();
     } else if (D.hd == 64) {
       e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);
