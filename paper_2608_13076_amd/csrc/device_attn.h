@@ -435,13 +435,14 @@ struct AttnMergeSmem {
 };
 
 // partials of output o (= row * kAttnHd + dd) for chunks c0 .. c0 + 15
-// (sc1 loads; chunks past nc and ok == false read 0)
+// (COH: sc1 loads; chunks past nc and ok == false read 0)
+template <bool COH>
 __device__ __forceinline__ void attn_load16(Rsrc rpo, int c0, int nc, int Rmax, int o, bool ok, float (&v)[16]) {
   const int row = o / kAttnHd, dd = o - row * kAttnHd;
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     const int c = c0 + j;
-    v[j] = ld_b32_coh(rpo, (ok && c < nc) ? (uint32_t)((c * Rmax + row) * kAttnHd + dd) * 4u : kOob);
+    v[j] = ld_f32<COH>(rpo, (ok && c < nc) ? (uint32_t)((c * Rmax + row) * kAttnHd + dd) * 4u : kOob);
   }
 }
 
@@ -461,7 +462,7 @@ __device__ __forceinline__ void attn_acc16(const AttnMergeSmem& ms, int c0, int 
 
 // merged outputs oa and oa + 512 (each where < nout); va / vb hold their
 // chunks 0..15 on entry
-template <class Out>
+template <bool COH, class Out>
 __device__ __forceinline__ void attn_merge_pair(Rsrc rpo, const AttnMergeSmem& ms, int nc, int Rmax, int nout,
                                                 int oa, float (&va)[16], float (&vb)[16], Out&& out) {
   const int ob = oa + 512;
@@ -469,8 +470,8 @@ __device__ __forceinline__ void attn_merge_pair(Rsrc rpo, const AttnMergeSmem& m
   attn_acc16(ms, 0, nc, oa, va, Oa);
   attn_acc16(ms, 0, nc, ob, vb, Ob);
   for (int c0 = 16; c0 < nc; c0 += 16) {
-    attn_load16(rpo, c0, nc, Rmax, oa, oa < nout, va);
-    attn_load16(rpo, c0, nc, Rmax, ob, ob < nout, vb);
+    attn_load16<COH>(rpo, c0, nc, Rmax, oa, oa < nout, va);
+    attn_load16<COH>(rpo, c0, nc, Rmax, ob, ob < nout, vb);
     attn_acc16(ms, c0, nc, oa, va, Oa);
     attn_acc16(ms, c0, nc, ob, vb, Ob);
   }
@@ -515,8 +516,12 @@ __device__ __forceinline__ void attn_publish(const AttnItem& it, floatx4 o, cons
 // with n_mine, and, in the workgroup whose arrival completes the request's
 // chunks, merge them and pass each merged output o = row * kAttnHd + dd to
 // out(o, value).  The completing arrival resets the counter.  All 512 threads
-// call it.
-template <class Out>
+// call it.  COH: read the partials with sc1 loads (the single-launch pass,
+// where an earlier stage of the same launch may have cached their lines); a
+// per-stage launch reads them with plain loads (no workgroup of the launch
+// reads a partial before its write-through store has landed, and the launch
+// starts with the L2 invalidated).
+template <bool COH = true, class Out>
 __device__ __forceinline__ void attn_arrive_merge(const AttnItem& it, int n_mine, AttnMergeSmem& ms, float* part_o,
                                                   float* part_ml, uint32_t* attn_cnt, int H, int NC, int Rmax, int R,
                                                   Out&& out) {
@@ -539,60 +544,71 @@ __device__ __forceinline__ void attn_arrive_merge(const AttnItem& it, int n_mine
   __syncthreads();
   if (!ms.last) return;  // uniform across the workgroup
   const int nc = it.nc;
-  // this thread's first partials, and each row's (m, l) pairs, in one round trip
+  // this thread's first partials, and the (m, l) pairs of the wave's rows
+  // (wave and wave + 8: R <= 16), in one round trip
   const Rsrc rpo = wave_rsrc(part_o + (bh * NC * Rmax) * kAttnHd);
   const Rsrc rpm = wave_rsrc(part_ml + (bh * NC * Rmax) * 2);
   const int nout = R * kAttnHd;
   float va[16], vb[16];
-  attn_load16(rpo, 0, nc, Rmax, tid, tid < nout, va);
-  attn_load16(rpo, 0, nc, Rmax, tid + 512, tid + 512 < nout, vb);
-  for (int row = wave; row < R; row += 8) {
-    float mc[kAttnMaxChunks / 64], lc[kAttnMaxChunks / 64];
+  attn_load16<COH>(rpo, 0, nc, Rmax, tid, tid < nout, va);
+  attn_load16<COH>(rpo, 0, nc, Rmax, tid + 512, tid + 512 < nout, vb);
+  constexpr int NJ = kAttnMaxChunks / 64;
+  float mc[2][NJ], lc[2][NJ];
 #pragma unroll
-    for (int j = 0; j < kAttnMaxChunks / 64; ++j) {
+  for (int k = 0; k < 2; ++k) {
+    const int row = wave + 8 * k;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
       const int c = lane + 64 * j;
-      const uint32_t off = c < nc ? (uint32_t)((c * Rmax + row) * 2) * 4u : kOob;
-      const float m = ld_b32_coh(rpm, off);
-      mc[j] = c < nc ? m : -INFINITY;
-      lc[j] = ld_b32_coh(rpm, off == kOob ? kOob : off + 4u);
+      const bool ok = row < R && c < nc;
+      const uint32_t off = ok ? (uint32_t)((c * Rmax + row) * 2) * 4u : kOob;
+      const float m = ld_f32<COH>(rpm, off);
+      mc[k][j] = ok ? m : -INFINITY;
+      lc[k][j] = ld_f32<COH>(rpm, off == kOob ? kOob : off + 4u);
     }
-    float Mx = -INFINITY;
+  }
 #pragma unroll
-    for (int j = 0; j < kAttnMaxChunks / 64; ++j) Mx = fmaxf(Mx, mc[j]);
+  for (int k = 0; k < 2; ++k) {
+    const int row = wave + 8 * k;
+    if (row < R) {  // uniform across the wave
+      float Mx = -INFINITY;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, off));
-    float Ls = 0.f;
+      for (int j = 0; j < NJ; ++j) Mx = fmaxf(Mx, mc[k][j]);
 #pragma unroll
-    for (int j = 0; j < kAttnMaxChunks / 64; ++j) {
-      mc[j] = (mc[j] == -INFINITY) ? 0.f : expf(mc[j] - Mx);
-      Ls += lc[j] * mc[j];
-    }
+      for (int off = 32; off >= 1; off >>= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, off));
+      float Ls = 0.f;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) Ls += __shfl_xor(Ls, off);
-    const float inv = 1.0f / Ls;
+      for (int j = 0; j < NJ; ++j) {
+        mc[k][j] = (mc[k][j] == -INFINITY) ? 0.f : expf(mc[k][j] - Mx);
+        Ls += lc[k][j] * mc[k][j];
+      }
 #pragma unroll
-    for (int j = 0; j < kAttnMaxChunks / 64; ++j) {
-      const int c = lane + 64 * j;
-      if (c < nc) ms.sc[c][row] = mc[j] * inv;
+      for (int off = 32; off >= 1; off >>= 1) Ls += __shfl_xor(Ls, off);
+      const float inv = 1.0f / Ls;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int c = lane + 64 * j;
+        if (c < nc) ms.sc[c][row] = mc[k][j] * inv;
+      }
     }
   }
   __syncthreads();
-  attn_merge_pair(rpo, ms, nc, Rmax, nout, tid, va, vb, out);
+  attn_merge_pair<COH>(rpo, ms, nc, Rmax, nout, tid, va, vb, out);
   for (int oa = tid + 1024; oa < nout; oa += 1024) {
-    attn_load16(rpo, 0, nc, Rmax, oa, true, va);
-    attn_load16(rpo, 0, nc, Rmax, oa + 512, oa + 512 < nout, vb);
-    attn_merge_pair(rpo, ms, nc, Rmax, nout, oa, va, vb, out);
+    attn_load16<COH>(rpo, 0, nc, Rmax, oa, true, va);
+    attn_load16<COH>(rpo, 0, nc, Rmax, oa + 512, oa + 512 < nout, vb);
+    attn_merge_pair<COH>(rpo, ms, nc, Rmax, nout, oa, va, vb, out);
   }
 }
 
 // attn_publish and attn_arrive_merge for a workgroup that computed the one
 // chunk it.
-template <int CK, class Out>
+template <int CK, bool COH = true, class Out>
 __device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o, const AttnSmem<CK>& sa,
                                                    AttnMergeSmem& ms, float* part_o, float* part_ml,
                                                    uint32_t* attn_cnt, int H, int NC, int Rmax, int R, Out&& out) {
   attn_publish<CK>(it, o, sa, part_o, part_ml, H, NC, Rmax, R);
-  attn_arrive_merge(it, it.active ? 1 : 0, ms, part_o, part_ml, attn_cnt, H, NC, Rmax, R, out);
+  attn_arrive_merge<COH>(it, it.active ? 1 : 0, ms, part_o, part_ml, attn_cnt, H, NC, Rmax, R, out);
 }
 
 }  // namespace spade

@@ -629,7 +629,7 @@ attn_lr_kernel(AttnParams p) {
   *(float4*)&sq[qrow][4 * f4] = qv;
   __syncthreads();
   const floatx4 o = attn_chunk_lr<CK>(it, kf, sq, p.R, p.scale, p.kv_stride, sm);
-  attn_publish_merge(it, o, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
+  attn_publish_merge<CK, false>(it, o, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
     const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
     store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
   });
@@ -691,7 +691,7 @@ attn_bp_kernel(AttnParams p, int cpw) {
     attn_run_chunk<ABF16, CK>(p, it0, c, c1, qr, ra, rb, sm);
     if (c + 1 < c1) attn_run_chunk<ABF16, CK>(p, it0, c + 1, c1, qr, rb, ra, sm);
   }
-  attn_arrive_merge(it0, c1 - c0, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
+  attn_arrive_merge<false>(it0, c1 - c0, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
     const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
     store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
   });
