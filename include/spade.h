@@ -250,6 +250,16 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
  * under every setting.  Values outside [0, 128] return SPADE_EINVAL. */
 spade_status spade_model_set_attn_chunks(spade_model m, int chunks);
 
+/* Merge of the attention's chunk partials when every workgroup computes one
+ * chunk (spade_model_set_attn_chunks).  mode 1: the last workgroup of a
+ * (request, head) to finish merges its chunks, which makes every chunk
+ * workgroup wait for its stores and an arrival counter; mode 2: the chunk
+ * workgroups store their partials and exit, and a second launch merges each
+ * (request, head); mode 0 (the default) chooses per call (mode 2 from four
+ * chunks per compute unit).  Results are bit-for-bit the same under every
+ * mode.  Other values return SPADE_EINVAL. */
+spade_status spade_model_set_attn_merge(spade_model m, int mode);
+
 /* K splitting of the batched O and down projections on the wide-row GEMM.
  * Their weights have few panels (d_model / 16), so one workgroup per panel
  * group leaves most compute units idle; with `splits` = 2 or 4 each

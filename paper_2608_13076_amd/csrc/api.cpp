@@ -214,6 +214,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->wide_ks = 0;
   m->split_ks = 0;
   m->attn_cpw = 0;
+  m->attn_merge = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -483,6 +484,13 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
   if (panels == 2 && row_tiles == 3) return fail(SPADE_EINVAL, "two panels per wave take at most two row tiles");
   m->wide_rt = row_tiles;
   m->wide_p = panels;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_attn_merge(spade_model m, int mode) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
+  m->attn_merge = mode;
   return SPADE_OK;
 }
 

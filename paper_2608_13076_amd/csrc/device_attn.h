@@ -511,39 +511,14 @@ __device__ __forceinline__ void attn_publish(const AttnItem& it, floatx4 o, cons
   }
 }
 
-// Once this workgroup's published partials (n_mine chunks of the (request,
-// head) of it) have landed, arrive on the counter of that (request, head)
-// with n_mine, and, in the workgroup whose arrival completes the request's
-// chunks, merge them and pass each merged output o = row * kAttnHd + dd to
-// out(o, value).  The completing arrival resets the counter.  All 512 threads
-// call it.  COH: read the partials with sc1 loads (the single-launch pass,
-// where an earlier stage of the same launch may have cached their lines); a
-// per-stage launch reads them with plain loads (no workgroup of the launch
-// reads a partial before its write-through store has landed, and the launch
-// starts with the L2 invalidated).
-template <bool COH = true, class Out>
-__device__ __forceinline__ void attn_arrive_merge(const AttnItem& it, int n_mine, AttnMergeSmem& ms, float* part_o,
-                                                  float* part_ml, uint32_t* attn_cnt, int H, int NC, int Rmax, int R,
-                                                  Out&& out) {
+// Merge the nc chunk partials of (request, head) bh in chunk order and pass
+// each merged output o = row * kAttnHd + dd to out(o, value).  Merge weights
+// of a row: one wave, chunks over its lanes; the weight of chunk c is
+// exp(m_c - max) / sum_c(l_c exp(m_c - max)).  All 512 threads call it.
+template <bool COH, class Out>
+__device__ __forceinline__ void attn_merge(size_t bh, int nc, AttnMergeSmem& ms, float* part_o, float* part_ml,
+                                           int NC, int Rmax, int R, Out&& out) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const size_t bh = (size_t)it.bl * H + it.h;
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (tid == 0) {
-    int last = 0;
-    if (n_mine > 0) {
-      uint32_t* cnt = attn_cnt + bh;
-      const uint32_t old = __hip_atomic_fetch_add(cnt, (uint32_t)n_mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (old + (uint32_t)n_mine == (uint32_t)it.nc) {
-        __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        last = 1;
-      }
-    }
-    ms.last = last;
-  }
-  __syncthreads();
-  if (!ms.last) return;  // uniform across the workgroup
-  const int nc = it.nc;
   // this thread's first partials, and the (m, l) pairs of the wave's rows
   // (wave and wave + 8: R <= 16), in one round trip
   const Rsrc rpo = wave_rsrc(part_o + (bh * NC * Rmax) * kAttnHd);
@@ -599,6 +574,41 @@ __device__ __forceinline__ void attn_arrive_merge(const AttnItem& it, int n_mine
     attn_load16<COH>(rpo, 0, nc, Rmax, oa + 512, oa + 512 < nout, vb);
     attn_merge_pair<COH>(rpo, ms, nc, Rmax, nout, oa, va, vb, out);
   }
+}
+
+// Once this workgroup's published partials (n_mine chunks of the (request,
+// head) of it) have landed, arrive on the counter of that (request, head)
+// with n_mine, and, in the workgroup whose arrival completes the request's
+// chunks, merge them and pass each merged output o = row * kAttnHd + dd to
+// out(o, value).  The completing arrival resets the counter.  All 512 threads
+// call it.  COH: read the partials with sc1 loads (the single-launch pass,
+// where an earlier stage of the same launch may have cached their lines); a
+// per-stage launch reads them with plain loads (no workgroup of the launch
+// reads a partial before its write-through store has landed, and the launch
+// starts with the L2 invalidated).
+template <bool COH = true, class Out>
+__device__ __forceinline__ void attn_arrive_merge(const AttnItem& it, int n_mine, AttnMergeSmem& ms, float* part_o,
+                                                  float* part_ml, uint32_t* attn_cnt, int H, int NC, int Rmax, int R,
+                                                  Out&& out) {
+  const int tid = threadIdx.x;
+  const size_t bh = (size_t)it.bl * H + it.h;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) {
+    int last = 0;
+    if (n_mine > 0) {
+      uint32_t* cnt = attn_cnt + bh;
+      const uint32_t old = __hip_atomic_fetch_add(cnt, (uint32_t)n_mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (old + (uint32_t)n_mine == (uint32_t)it.nc) {
+        __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last = 1;
+      }
+    }
+    ms.last = last;
+  }
+  __syncthreads();
+  if (!ms.last) return;  // uniform across the workgroup
+  attn_merge<COH>(bh, it.nc, ms, part_o, part_ml, NC, Rmax, R, out);
 }
 
 // attn_publish and attn_arrive_merge for a workgroup that computed the one

@@ -607,7 +607,7 @@ inline int attn_grid(int n_runs, int Hkv, int G, int nb) { return 8 * G * ((n_ru
 // LDS and the V^T fragments loaded after the score products into the
 // registers K held (attn_chunk_lr): 78 VGPRs, three workgroups per compute
 // unit (keeping K, V and the queries in registers at once took 120: two).
-template <bool ABF16, int CK>
+template <bool ABF16, int CK, bool ARRIVE>
 __global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(6)))
 attn_lr_kernel(AttnParams p) {
   __shared__ AttnSmem<CK> sm;
@@ -629,7 +629,27 @@ attn_lr_kernel(AttnParams p) {
   *(float4*)&sq[qrow][4 * f4] = qv;
   __syncthreads();
   const floatx4 o = attn_chunk_lr<CK>(it, kf, sq, p.R, p.scale, p.kv_stride, sm);
+  if constexpr (!ARRIVE) {  // attn_merge_kernel merges after this launch
+    attn_publish<CK>(it, o, sm, p.part_o, p.part_ml, p.H, p.NC, p.Rmax, p.R);
+    return;
+  }
   attn_publish_merge<CK, false>(it, o, sm, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
+    const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
+    store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
+  });
+}
+
+// Second pass of the attention for launches with several rounds of chunk
+// workgroups: workgroup (head h, request b) merges the chunk partials that
+// attn_lr_kernel<..., false> stored (attn_merge, the same arithmetic as the
+// last-arrival merge), so no chunk workgroup waits for its stores or an
+// arrival counter while it holds its compute unit.
+template <bool ABF16>
+__global__ void __launch_bounds__(kAttnThreads) attn_merge_kernel(AttnParams p) {
+  __shared__ AttnMergeSmem ms;
+  const int h = blockIdx.x, bl = blockIdx.y, bg = p.b0 + bl;
+  const int nc = (p.lens[bg] + p.R + kAttnChunkKeys - 1) / kAttnChunkKeys;
+  attn_merge<false>((size_t)bl * p.H + h, nc, ms, p.part_o, p.part_ml, p.NC, p.Rmax, p.R, [&](int oi, float O) {
     const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
     store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
   });
@@ -1269,6 +1289,18 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   // latency), else one (with distinct K/V per head the one-chunk kernel's
   // three workgroups per compute unit keep HBM busier: measured on the
   // batched 7B and 8B shapes)
+  // one chunk per workgroup: merge by the last chunk to arrive, or, when the
+  // call has at least four chunks per compute unit (several rounds of chunk
+  // workgroups), in a second launch (measured: C4 12.78 -> 12.25 ms, C5
+  // 17.66 -> 17.49; at C2 the extra launch costs more than it saves)
+  bool two_pass = false;
+  if (md->attn_merge == 2) {
+    two_pass = true;
+  } else if (md->attn_merge == 0) {
+    long chunks = 0;
+    for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) chunks += (kv->lens_ub[b] + fc.R + CK - 1) / CK;
+    two_pass = chunks * D.H >= 4L * md->n_cu;
+  }
   int cpw = md->attn_cpw;
   if (attn_b && cpw <= 0) {
     long chunks = 0;
@@ -1308,10 +1340,18 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
       if (wb) hipLaunchKernelGGL((attn_bp_kernel<true, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
       else hipLaunchKernelGGL((attn_bp_kernel<false, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
       e = hipGetLastError();
+    } else if (attn_b && two_pass) {
+      const dim3 bgrid(attn_grid(NC, D.KVH, D.H / D.KVH, fc.nb));
+      if (wb) hipLaunchKernelGGL((attn_lr_kernel<true, kAttnChunkKeys, false>), bgrid, dim3(kAttnThreads), 0, st, ap);
+      else hipLaunchKernelGGL((attn_lr_kernel<false, kAttnChunkKeys, false>), bgrid, dim3(kAttnThreads), 0, st, ap);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      if (wb) hipLaunchKernelGGL((attn_merge_kernel<true>), dim3(D.H, fc.nb), dim3(kAttnThreads), 0, st, ap);
+      else hipLaunchKernelGGL((attn_merge_kernel<false>), dim3(D.H, fc.nb), dim3(kAttnThreads), 0, st, ap);
+      e = hipGetLastError();
     } else if (attn_b) {
       const dim3 bgrid(attn_grid(NC, D.KVH, D.H / D.KVH, fc.nb));
-      if (wb) hipLaunchKernelGGL((attn_lr_kernel<true, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
-      else hipLaunchKernelGGL((attn_lr_kernel<false, kAttnChunkKeys>), bgrid, dim3(kAttnThreads), 0, st, ap);
+      if (wb) hipLaunchKernelGGL((attn_lr_kernel<true, kAttnChunkKeys, true>), bgrid, dim3(kAttnThreads), 0, st, ap);
+      else hipLaunchKernelGGL((attn_lr_kernel<false, kAttnChunkKeys, true>), bgrid, dim3(kAttnThreads), 0, st, ap);
       e = hipGetLastError();
     } else if (D.hd == 64) {
       e = launch_attn_hd<64>(ap, kvb, wb, agrid, st);

@@ -169,6 +169,7 @@ struct spade_model_s {
   int wide_ks;   // k-splits of its O and down projections: 0 chosen per launch, 1 off, 2 or 4 fixed
   int split_ks;  // k-splits of the split-K GEMM: 0 chosen per launch, 2 or 4 where it qualifies, -1 off
   int attn_cpw;  // attention chunks per workgroup (bf16 cache, head_dim 128): 0 chosen per call, >= 1 fixed
+  int attn_merge;  // merge of one-chunk attention partials: 0 chosen per call, 1 last arrival, 2 second launch
 };
 
 struct spade_kv_s {

@@ -32,7 +32,7 @@ EXPORTED = (
     "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
     "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles",
     "spade_model_set_wide_k_splits", "spade_model_set_split_k", "spade_softmax", "spade_prefill_batch",
-    "spade_wide_tiling", "spade_model_set_attn_chunks",
+    "spade_wide_tiling", "spade_model_set_attn_chunks", "spade_model_set_attn_merge",
 )
 
 
@@ -93,6 +93,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_model_set_wide_tiles": (I, [P, I, I]),
         "spade_model_set_wide_k_splits": (I, [P, I]),
         "spade_model_set_attn_chunks": (I, [P, I]),
+        "spade_model_set_attn_merge": (I, [P, I]),
         "spade_model_set_split_k": (I, [P, I]),
         "spade_softmax": (I, [P, I, I, F, P, P]),
         "spade_prefill_batch": (I, [P, P, I, P, I, P, P]),
@@ -185,6 +186,11 @@ class Model:
         chosen per launch, 1..3 fixed, -1 skinny engine once per 32 rows) and
         weight panels per wave (0 chosen per launch, 1..2 fixed)."""
         _check(self.lib.spade_model_set_wide_tiles(self.handle, int(row_tiles), int(panels)))
+
+    def set_attn_merge(self, mode: int) -> None:
+        """Merge of one-chunk attention partials: 0 chosen per call, 1 by the
+        last chunk workgroup, 2 in a second launch."""
+        _check(self.lib.spade_model_set_attn_merge(self.handle, int(mode)))
 
     def set_attn_chunks(self, chunks: int) -> None:
         """Attention chunks (256 keys) per workgroup: 0 chosen per call, n >= 1

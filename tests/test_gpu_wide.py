@@ -62,8 +62,9 @@ def test_wide_tilings_bit_identical_and_match_oracle(w):
 
 @pytest.mark.parametrize("batch", [1, 6])
 def test_attention_runs_bit_identical(batch):
-    """The verify attention with one 256-key chunk per workgroup and with runs
-    of 2, 3, 4 or 9 chunks per workgroup (the next chunk's keys and values
+    """The verify attention with one 256-key chunk per workgroup (merged by the
+    last chunk workgroup to finish, or in a second launch) and with runs of
+    2, 3, 4 or 9 chunks per workgroup (the next chunk's keys and values
     fetched while the current one is computed), and the per-call choice, give
     bit-for-bit the same logits, n_accepted and corrections: every chunk's
     partial and the merge in chunk order are the same whichever workgroup
@@ -84,14 +85,18 @@ def test_attention_runs_bit_identical(batch):
     for bad in (-1, 3, 8):
         with pytest.raises(spade.SpadeError):
             model.set_wide_k_splits(bad)
+    for bad in (-1, 3):
+        with pytest.raises(spade.SpadeError):
+            model.set_attn_merge(bad)
     runs = {}
-    for cpw in (1, 2, 3, 4, 9, 0):
-        print(f"[{w.name}] lens {inp.lens.tolist()} attention chunks per workgroup {cpw}", flush=True)
+    for cpw, merge in ((1, 1), (1, 2), (2, 0), (3, 0), (4, 0), (9, 0), (0, 0), (1, 1)):
+        print(f"[{w.name}] lens {inp.lens.tolist()} attention chunks per workgroup {cpw}, merge {merge}", flush=True)
         model.set_attn_chunks(cpw)
-        runs[cpw] = gpu_verify(model, kv, inp)[:3]
-    ref = runs[1]
+        model.set_attn_merge(merge)
+        runs[(cpw, merge)] = gpu_verify(model, kv, inp)[:3]
+    ref = runs[(1, 1)]
     assert np.isfinite(ref[0]).all()
-    for cpw, (lg, n, c) in runs.items():
-        assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), cpw
-        assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), cpw
+    for cfg, (lg, n, c) in runs.items():
+        assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), cfg
+        assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), cfg
     assert model.device_error() == 0
