@@ -245,9 +245,9 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
  * workgroup computes up to n consecutive chunks of one (request, head),
  * fetching the next chunk's keys and values while it computes the current
  * one, which keeps HBM busy when a call has many chunks (batched requests
- * with long caches).  chunks = 0 (the default) chooses per call from the
- * number of chunks and compute units.  Results are bit-for-bit the same
- * under every setting.  Values outside [0, 128] return SPADE_EINVAL. */
+ * with long caches).  chunks = 0 (the default) is one chunk per workgroup,
+ * which measured fastest at every shape tried.  Results are bit-for-bit the
+ * same under every setting.  Values outside [0, 128] return SPADE_EINVAL. */
 spade_status spade_model_set_attn_chunks(spade_model m, int chunks);
 
 /* Merge of the attention's chunk partials when every workgroup computes one

@@ -1282,13 +1282,11 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   const int CK = attn_b ? kAttnChunkKeys : kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
-  // chunks per workgroup of the bf16 attention: fixed (> 0), else all the
-  // chunks of a (request, head) in one workgroup when query heads share K/V
-  // heads and the call has at least four chunks per compute unit (the K/V
-  // reads are then mostly L2 hits and the run's prefetch hides their
-  // latency), else one (with distinct K/V per head the one-chunk kernel's
-  // three workgroups per compute unit keep HBM busier: measured on the
-  // batched 7B and 8B shapes)
+  // chunks per workgroup of the bf16 attention: fixed (> 0), else one (the
+  // low-register one-chunk kernel with the merge below beat runs of chunks
+  // at every measured shape: C4 13.53 vs 14.2-18.0 ms, 8B-GQA batched 13.67
+  // vs 14.73)
+  const int cpw = md->attn_cpw > 0 ? md->attn_cpw : 1;
   // one chunk per workgroup: merge by the last chunk to arrive, or, when the
   // call has at least four chunks per compute unit (several rounds of chunk
   // workgroups), in a second launch (measured: C4 12.78 -> 12.25 ms, C5
@@ -1300,13 +1298,6 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     long chunks = 0;
     for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) chunks += (kv->lens_ub[b] + fc.R + CK - 1) / CK;
     two_pass = chunks * D.H >= 4L * md->n_cu;
-  }
-  int cpw = md->attn_cpw;
-  if (attn_b && cpw <= 0) {
-    long chunks = 0;
-    for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) chunks += (kv->lens_ub[b] + fc.R + CK - 1) / CK;
-    chunks *= D.H;
-    cpw = (D.KVH < D.H && chunks >= 4L * md->n_cu) ? NC : 1;
   }
 
   for (int l = 0; l < D.L; ++l) {
