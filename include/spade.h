@@ -260,6 +260,18 @@ spade_status spade_model_set_attn_chunks(spade_model m, int chunks);
  * mode.  Other values return SPADE_EINVAL. */
 spade_status spade_model_set_attn_merge(spade_model m, int mode);
 
+/* Where the correction draw of a sampling request runs (Sec. III-C: sample
+ * from norm(max(0, p - q)), or from p when every draft is accepted; the draw
+ * is a Gumbel-max pass over the vocabulary).  mode 0 (the default) or 2: when
+ * the call may sample (uniforms given, and draft_probs given or gamma = 0),
+ * spade_verify (per-stage path) and spade_accept_from_logits run it in a
+ * second launch over slices of 1024 tokens (at most 256 slices), one
+ * workgroup per (slice, request), the last slice of a request to finish
+ * taking the best of the slices; mode 1 keeps it in the request's accept
+ * workgroup.  The single-launch pass always keeps it there.  Results are bit-for-bit the same under
+ * every mode.  Other values return SPADE_EINVAL. */
+spade_status spade_model_set_correction_slices(spade_model m, int mode);
+
 /* K splitting of the batched O and down projections on the wide-row GEMM.
  * Their weights have few panels (d_model / 16), so one workgroup per panel
  * group leaves most compute units idle; with `splits` = 2 or 4 each

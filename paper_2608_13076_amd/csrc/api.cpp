@@ -91,7 +91,7 @@ ArenaLayout layout_of(const Dims& D) {
 
 struct WsPlan {
   size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, bar, fused, split_cnt,
-      split_part, wide_cnt, wide_part, prefill_tok, prefill_cnt, total;
+      split_part, wide_cnt, wide_part, corr_lse, corr_part, corr_cnt, prefill_tok, prefill_cnt, total;
   size_t wide_items, wide_floats;
   FusedArena fa;
   bool has_fused;
@@ -146,6 +146,9 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   }
   p.wide_cnt = take(p.wide_items * 4);
   p.wide_part = take(p.wide_floats * 4);
+  p.corr_lse = take((size_t)max_batch * 4);
+  p.corr_part = take((size_t)max_batch * kCorrMaxSlices * 4 * 4);
+  p.corr_cnt = take((size_t)max_batch * 4);
   p.prefill_tok = take((size_t)p.Mmax * 4);
   p.prefill_cnt = take((size_t)max_batch * 4);
   // the single-launch pass handles bf16 weights and cache with head_dim 128
@@ -215,6 +218,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->split_ks = 0;
   m->attn_cpw = 0;
   m->attn_merge = 0;
+  m->corr_split = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -245,6 +249,9 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.wide_part = (float*)(b + p.wide_part);
   w.wide_items = p.wide_items;
   w.wide_floats = p.wide_floats;
+  w.corr_lse = (float*)(b + p.corr_lse);
+  w.corr_part = (float*)(b + p.corr_part);
+  w.corr_cnt = (uint32_t*)(b + p.corr_cnt);
   w.prefill_tok = (int32_t*)(b + p.prefill_tok);
   w.prefill_cnt = (int32_t*)(b + p.prefill_cnt);
   w.logits = (float*)(b + p.logits);
@@ -274,6 +281,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   if (e == hipSuccess) e = hipMemset(w.attn_cnt, 0, (size_t)max_batch * m->dims.H * 4);
   if (e == hipSuccess) e = hipMemset(w.split_cnt, 0, (size_t)p.max_units * 4);
   if (e == hipSuccess && p.wide_items > 0) e = hipMemset(w.wide_cnt, 0, p.wide_items * 4);
+  if (e == hipSuccess) e = hipMemset(w.corr_cnt, 0, (size_t)max_batch * 4);
   if (e == hipSuccess) e = hipMemset(w.err, 0, 4);
   if (e == hipSuccess) e = hipMemset(w.bar, 0, kBarBytes);
   // activation buffers start at zero so rows past M never feed NaNs
@@ -491,6 +499,13 @@ spade_status spade_model_set_attn_merge(spade_model m, int mode) {
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
   m->attn_merge = mode;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_correction_slices(spade_model m, int mode) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
+  m->corr_split = mode;
   return SPADE_OK;
 }
 

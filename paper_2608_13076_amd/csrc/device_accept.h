@@ -14,7 +14,7 @@ struct AcceptParams {
   const float* stats;
   int NU;
   int panels;  // 0: stats holds NU workgroup entries per row; > 0: one entry per panel
-  int V, gamma, R;
+  int B, V, gamma, R;
   const int32_t* drafts;
   const float* q;
   const float* u;
@@ -23,6 +23,14 @@ struct AcceptParams {
   int32_t* n_out;
   int32_t* corr_out;
   uint32_t* err;
+  // > 0: the correction draws of sampling requests are left to
+  // correct_slices over this many vocabulary slices (accept_request stores
+  // the log-sum-exp of the draw's row in corr_lse[b]); corr_part /
+  // corr_cnt: per-slice winners and per-request arrival counters
+  int corr_slices;
+  float* corr_lse;
+  float* corr_part;
+  uint32_t* corr_cnt;
 };
 
 // SplitMix64 output v (0-based) of the stream seeded with `seed`.
@@ -55,6 +63,29 @@ __device__ __forceinline__ float ld_any(const float* p) {
   else return *p;
 }
 
+// Gumbel-max scores of token v for the correction draw: the residual
+// max(0, p - q) (log w + g, -inf where w <= 0) and p itself (z + g), with z
+// the logit over the temperature and g the token's Gumbel noise.  No
+// contraction, so every caller gets the same roundings.
+__device__ __forceinline__ float corr_score_p(float logit, float invT, float g) {
+#pragma clang fp contract(off)
+  const float z = logit * invT;
+  return z + g;
+}
+
+__device__ __forceinline__ float corr_score_res(float logit, float invT, float lse, float qv, float g) {
+#pragma clang fp contract(off)
+  const float z = logit * invT;
+  const float w = expf(z - lse) - qv;
+  return w > 0.f ? logf(w) + g : -INFINITY;
+}
+
+// Whether request b draws by sampling (else greedily); the accept step and
+// the sliced correction decide it the same way.
+__device__ __forceinline__ bool accept_samples(const AcceptParams& p, int b) {
+  return p.mode[b] == SPADE_SAMPLE && p.u != nullptr && (p.gamma == 0 || p.q != nullptr);
+}
+
 struct AcceptSmem {
   float rlse[kMaxR];
   int rarg[kMaxR];
@@ -70,11 +101,8 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int R = p.R, V = p.V, G = p.gamma;
 
-  bool sample = p.mode[b] == SPADE_SAMPLE;
-  if (sample && (p.u == nullptr || (G > 0 && p.q == nullptr))) {
-    if (tid == 0) flag_error(p.err, SPADE_DERR_NOQ);
-    sample = false;
-  }
+  const bool sample = accept_samples(p, b);
+  if (!sample && p.mode[b] == SPADE_SAMPLE && tid == 0) flag_error(p.err, SPADE_DERR_NOQ);
   const float invT = sample ? p.inv_T : 1.0f;
   const float* lg = p.logits + (size_t)b * R * V;
 
@@ -102,13 +130,25 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
       // per-panel statistics: rebuild the NU workgroup entries of the skinny
       // LM head (workgroup q folds panels q, q + NU, ... in order), then merge
       // them exactly as below
+      // (the panels of an entry are requested sixteen at a time and then
+      // folded in order, so the loads do not wait for one another)
+      constexpr int kBatch = 16;
       const float* sp = p.stats + (size_t)(b * R + r) * p.panels * 3;
       for (int q = lane; q < p.NU; q += 64) {
         RowStat one{-INFINITY, 0.f, 0x7fffffff};
-        for (int u = q; u < p.panels; u += p.NU) {
-          const RowStat ps{ld_any<COH>(sp + u * 3), ld_any<COH>(sp + u * 3 + 1),
-                           __float_as_int(ld_any<COH>(sp + u * 3 + 2))};
-          if (ps.m != -INFINITY) one = merge_stat(one, ps);
+        for (int u0 = q; u0 < p.panels; u0 += kBatch * p.NU) {
+          RowStat ps[kBatch];
+#pragma unroll
+          for (int j = 0; j < kBatch; ++j) {
+            const int u = u0 + j * p.NU;
+            ps[j] = RowStat{-INFINITY, 0.f, 0x7fffffff};
+            if (u < p.panels)
+              ps[j] = RowStat{ld_any<COH>(sp + u * 3), ld_any<COH>(sp + u * 3 + 1),
+                              __float_as_int(ld_any<COH>(sp + u * 3 + 2))};
+          }
+#pragma unroll
+          for (int j = 0; j < kBatch; ++j)
+            if (ps[j].m != -INFINITY) one = merge_stat(one, ps[j]);
         }
         if (one.m != -INFINITY) st = merge_stat(st, one);
       }
@@ -165,6 +205,13 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
   int corr = 0;
   if (!sample) {
     corr = sm.rarg[n];
+  } else if (p.corr_slices > 0) {
+    // correct_slices draws it after this launch
+    if (tid == 0) {
+      p.corr_lse[b] = sm.rlse[n];
+      p.n_out[b] = n;
+    }
+    return;
   } else {
     const uint64_t seed = (uint64_t)__float_as_uint(p.u[(size_t)b * (G + 1) + G]);
     const float* row = lg + (size_t)n * V;
@@ -176,14 +223,8 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
       Best bst{-INFINITY, 0x7fffffff};
 #pragma unroll 4
       for (int v = tid; v < V; v += NT) {
-        const float z = ld_any<COH>(row + v) * invT;
-        float sc;
-        if (use_res) {
-          const float w = expf(z - lse) - qrow[v];
-          sc = w > 0.f ? logf(w) + gumbel_at(seed, v) : -INFINITY;
-        } else {
-          sc = z + gumbel_at(seed, v);
-        }
+        const float lv = ld_any<COH>(row + v), g = gumbel_at(seed, v);
+        const float sc = use_res ? corr_score_res(lv, invT, lse, qrow[v], g) : corr_score_p(lv, invT, g);
         if (sc != sc) continue;
         bst = better(bst, Best{sc, v});
       }
@@ -206,6 +247,90 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
   }
   if (tid == 0) {
     p.n_out[b] = n;
+    p.corr_out[b] = corr;
+  }
+}
+
+__device__ __forceinline__ Best wave_best(Best x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = better(x, Best{__shfl_xor(x.s, off), __shfl_xor(x.a, off)});
+  return x;
+}
+
+// Slice s of corr_slices of the correction draw of a sampling request b,
+// after accept_request (previous launch) stored n and the row's log-sum-exp:
+// the best residual score and the best score under p over the slice's tokens
+// (NaN scores skipped, as in the one-workgroup draw), published write-through;
+// the last slice to arrive takes the best of all slices (the order of this
+// maximum does not matter: ties go to the lower token id) and stores the
+// correction, the residual's winner unless the residual had no mass.
+// NT threads, one workgroup per (slice, request).
+template <int NT>
+__device__ __forceinline__ void correct_slice(const AcceptParams& p, int b, int s) {
+  constexpr int NWV = NT / 64;
+  __shared__ Best sres[NWV], sp[NWV];
+  __shared__ int last;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  if (!accept_samples(p, b)) return;  // uniform
+  const int V = p.V, G = p.gamma, S = p.corr_slices;
+  const int n = p.n_out[b];
+  const bool residual = n < G;
+  const float invT = p.inv_T, lse = p.corr_lse[b];
+  const uint64_t seed = (uint64_t)__float_as_uint(p.u[(size_t)b * (G + 1) + G]);
+  const float* row = p.logits + ((size_t)b * (G + 1) + n) * V;
+  const float* qrow = residual ? p.q + ((size_t)b * G + n) * V : nullptr;
+  const int per = (V + S - 1) / S;
+  const int v0 = s * per, v1 = min(V, v0 + per);
+  Best br{-INFINITY, 0x7fffffff}, bp{-INFINITY, 0x7fffffff};
+#pragma unroll 4
+  for (int v = v0 + tid; v < v1; v += NT) {
+    const float lv = row[v], g = gumbel_at(seed, v);
+    const float sc = corr_score_p(lv, invT, g);
+    if (sc == sc) bp = better(bp, Best{sc, v});
+    if (residual) {
+      const float sr = corr_score_res(lv, invT, lse, qrow[v], g);
+      if (sr == sr) br = better(br, Best{sr, v});
+    }
+  }
+  br = wave_best(br);
+  bp = wave_best(bp);
+  if (lane == 0) {
+    sres[wave] = br;
+    sp[wave] = bp;
+  }
+  __syncthreads();
+  const Rsrc rp = make_rsrc(p.corr_part, (uint32_t)(p.B * kCorrMaxSlices * 4 * 4));
+  const uint32_t base = (uint32_t)((b * kCorrMaxSlices + s) * 4) * 4u;
+  if (tid == 0) {
+    for (int w = 1; w < NWV; ++w) {
+      br = better(br, sres[w]);
+      bp = better(bp, sp[w]);
+    }
+    st_f32<true>(rp, base, br.s);
+    st_f32<true>(rp, base + 4u, __int_as_float(br.a));
+    st_f32<true>(rp, base + 8u, bp.s);
+    st_f32<true>(rp, base + 12u, __int_as_float(bp.a));
+    __builtin_amdgcn_s_waitcnt(0);  // the winners have landed: arrive
+    const uint32_t old = __hip_atomic_fetch_add(p.corr_cnt + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    last = old == (uint32_t)S - 1u;
+    if (last) __hip_atomic_store(p.corr_cnt + b, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!last || wave != 0) return;
+  Best r{-INFINITY, 0x7fffffff}, q{-INFINITY, 0x7fffffff};
+  for (int i = lane; i < S; i += 64) {
+    const uint32_t off = (uint32_t)((b * kCorrMaxSlices + i) * 4) * 4u;
+    r = better(r, Best{ld_f32<true>(rp, off), __float_as_int(ld_f32<true>(rp, off + 4u))});
+    q = better(q, Best{ld_f32<true>(rp, off + 8u), __float_as_int(ld_f32<true>(rp, off + 12u))});
+  }
+  r = wave_best(r);
+  q = wave_best(q);
+  if (lane == 0) {
+    int corr = q.a;
+    if (residual) {
+      if (r.s != -INFINITY) corr = r.a;
+      else flag_error(p.err, SPADE_DERR_RESIDUAL);
+    }
     p.corr_out[b] = corr;
   }
 }

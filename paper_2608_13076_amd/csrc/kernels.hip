@@ -728,6 +728,15 @@ __global__ void __launch_bounds__(kAcceptThreads) accept_kernel(AcceptParams p) 
   accept_request<kAcceptThreads, false>(p, (int)blockIdx.x, sm);
 }
 
+// The correction draws of sampling requests over vocabulary slices: workgroup
+// (slice, request), after accept_kernel (device_accept.h: correct_slice).
+constexpr int kCorrThreads = 256;
+constexpr int kCorrSliceTokens = 1024;  // tokens per slice (up to kCorrMaxSlices slices)
+
+__global__ void __launch_bounds__(kCorrThreads) correct_kernel(AcceptParams p) {
+  correct_slice<kCorrThreads>(p, (int)blockIdx.y, (int)blockIdx.x);
+}
+
 // ---------------------------------------------------------------------------
 // Row softmax of logits / T (the draft side of Algorithm 1 keeps the
 // distribution each of its tokens was drawn from): one workgroup per row,
@@ -1365,6 +1374,7 @@ hipError_t launch_accept(spade_model md, const AcceptCall& ac, hipStream_t st) {
   p.stats = ac.stats;
   p.NU = ac.NU;
   p.panels = ac.panels;
+  p.B = ac.B;
   p.V = ac.V;
   p.gamma = ac.gamma;
   p.R = ac.gamma + 1;
@@ -1376,7 +1386,23 @@ hipError_t launch_accept(spade_model md, const AcceptCall& ac, hipStream_t st) {
   p.n_out = ac.n_out;
   p.corr_out = ac.corr_out;
   p.err = md->ws.err;
+  // a request may sample: its correction draw (a pass over the vocabulary
+  // with two logarithms per token) goes to a second launch over slices of
+  // the vocabulary, unless turned off (the accept workgroup then draws it)
+  const bool may_sample = ac.u != nullptr && (ac.q != nullptr || ac.gamma == 0);
+  const bool split = may_sample && md->corr_split != 1 && ac.B <= md->max_batch;
+  if (split) {
+    p.corr_slices = std::min(kCorrMaxSlices, (ac.V + kCorrSliceTokens - 1) / kCorrSliceTokens);
+    p.corr_lse = md->ws.corr_lse;
+    p.corr_part = md->ws.corr_part;
+    p.corr_cnt = md->ws.corr_cnt;
+  }
   hipLaunchKernelGGL(accept_kernel, dim3(ac.B), dim3(kAcceptThreads), 0, st, p);
+  if (split) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(correct_kernel, dim3(p.corr_slices, ac.B), dim3(kCorrThreads), 0, st, p);
+  }
   return hipGetLastError();
 }
 

@@ -16,6 +16,7 @@ constexpr int kMaxRowsPerGemm = 32;  // rows handled by one skinny-GEMM launch
 constexpr int kWideMinRows = 16;     // bf16 projections with more rows use the wide-row GEMM
 constexpr int kPrefillRows = 16;     // tokens per prefill forward
 constexpr int kMaxR = 16;            // rows per request in one forward (gamma <= 15)
+constexpr int kCorrMaxSlices = 256; // vocabulary slices of one correction draw
 constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
 constexpr int kAttnChunk = 128;      // keys per attention workgroup
 constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
@@ -142,6 +143,9 @@ struct Workspace {
   uint32_t* wide_cnt;   // [wide_items] arrival counters of the k-split wide-row GEMM (kept at zero between calls)
   float* wide_part;     // [wide_floats] its published sums and range partials
   size_t wide_items, wide_floats;
+  float* corr_lse;      // [Bmax] log-sum-exp of each sampling request's correction row
+  float* corr_part;     // [Bmax][kCorrMaxSlices][4] per-slice winners of the correction draw
+  uint32_t* corr_cnt;   // [Bmax] arrival counters of the correction slices (kept at zero between calls)
   int32_t* prefill_tok; // [Mmax] token ids of one batched-prefill forward
   int32_t* prefill_cnt; // [Bmax] prompt tokens to cache per request (batched prefill)
   FusedArena fa;
@@ -170,6 +174,7 @@ struct spade_model_s {
   int split_ks;  // k-splits of the split-K GEMM: 0 chosen per launch, 2 or 4 where it qualifies, -1 off
   int attn_cpw;  // attention chunks per workgroup (bf16 cache, head_dim 128): 0 chosen per call, >= 1 fixed
   int attn_merge;  // merge of one-chunk attention partials: 0 chosen per call, 1 last arrival, 2 second launch
+  int corr_split;  // correction draws of sampling requests: 0/2 over vocabulary slices, 1 in the accept workgroup
 };
 
 struct spade_kv_s {

@@ -86,3 +86,43 @@ def test_accept_error_flags(model):
     from paper_2608_13076_amd.spade import DERR_TOKEN
     assert model.device_error() & DERR_TOKEN
     assert model.device_error() == 0  # cleared by the read
+
+
+@pytest.mark.parametrize("V,G,B,scale", [(7, 3, 16, 3.0), (40000, 8, 6, 1.3), (33, 0, 5, 1.0),
+                                         (300000, 2, 3, 2.0)])
+def test_correction_slices_bit_identical(model, V, G, B, scale):
+    """The correction draw over vocabulary slices (a second launch) gives the
+    one-workgroup draw's n and correction bit for bit, every request sampling
+    (1024 tokens a slice; 300000 tokens hit the 256-slice cap), and matches
+    the oracle where the oracle pins it."""
+    import torch
+    rng = np.random.default_rng(7 * V + G)
+    dev = model.device
+    try:
+        for rep in range(4):
+            logits, drafts, q, u, modes = _case(rng, B, G, V, scale, 1.0)
+            T = 1.0 if rep % 2 == 0 else 0.7
+            print(f"correction slices V={V} G={G} B={B} rep={rep}", flush=True)
+            args = (torch.from_numpy(logits).to(dev), torch.from_numpy(drafts).to(dev),
+                    torch.from_numpy(q).to(dev), torch.from_numpy(u).to(dev), torch.from_numpy(modes).to(dev), T)
+            out = {}
+            for mode in (1, 2):
+                model.set_correction_slices(mode)
+                n, c = model.accept_from_logits(*args)
+                torch.cuda.synchronize()
+                out[mode] = (n.cpu().numpy(), c.cpu().numpy())
+            assert np.array_equal(out[1][0], out[2][0]) and np.array_equal(out[1][1], out[2][1]), (out[1], out[2])
+            n, c = out[2]
+            for b in range(B):
+                r = speculative_rows(logits[b].astype(np.float64), drafts[b], q[b].astype(np.float64), u[b],
+                                     SAMPLE, T)
+                if r.pinned_n:
+                    assert n[b] == r.n_accepted, (b, n[b], r.n_accepted)
+                if r.pinned_correction:
+                    assert c[b] == r.correction, (b, c[b], r.correction)
+        assert model.device_error() == 0
+    finally:
+        model.set_correction_slices(0)
+    from paper_2608_13076_amd.spade import SpadeError
+    with pytest.raises(SpadeError):
+        model.set_correction_slices(3)
