@@ -15,13 +15,26 @@
 //                  fused epilogues: RMSNorm scale + RoPE + KV append (QKV),
 //                  residual add + next RMS partials (O, down), SiLU gate
 //                  (gate/up), logits + per-panel softmax statistics (LM head)
-//   attn_kernel    multi-query causal attention of the gamma+1 rows over the
-//                  cache, split over key chunks of 128 keys
-//   attn_combine_kernel  merges the chunk partials of each (request, head) in
-//                  chunk order into the O-projection operand
+//   gemm_split_kernel  the same with the k-blocks of each panel split over
+//                  2 or 4 workgroups (few panels, long K: the down projection)
+//   gemm_wide_kernel   the same epilogues for more than 16 rows: row tiles
+//                  and panels per workgroup, the operand through an LDS ring,
+//                  optional k-splits for the O and down projections
+//   attn_lr_kernel the bf16 / head_dim-128 verify attention, one 256-key
+//                  chunk per workgroup; merges the chunks of a (request,
+//                  head) in the last one to finish, or leaves that to
+//   attn_merge_kernel  a second launch (several rounds of chunk workgroups)
+//   attn_bp_kernel runs of several chunks per workgroup (selectable)
+//   attn_kernel / attn_combine_kernel  f32 cache or other head sizes:
+//                  128-key chunks, then the chunk-order merge
 //   accept_kernel  per request: vocabulary-wide max / log-sum-exp / argmax
 //                  per row, the accept chain, the Gumbel-max correction draw
+//   correct_kernel that draw over vocabulary slices (calls that may sample)
 //   commit_kernel  lens += n + 1, pending = correction
+//   copy_state_kernel / advance_kernel  cache-state copies and single-request
+//                  prefill bookkeeping
+//   prefill_*_kernel   batched prefill: counts, token gather, advance, pending
+//   softmax_rows_kernel  softmax of logits / T (the draft side of Algorithm 1)
 //   pack_kernel    row-major weights -> tiled arena
 #include "device_accept.h"
 #include "device_attn.h"
@@ -1287,8 +1300,8 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   // head_dim 128 the 8-wave MFMA kernel, else kAttnChunk
   int max_keys = 0;
   for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) max_keys = std::max(max_keys, kv->lens_ub[b] + fc.R);
-  const bool attn_b = D.kvdt == SPADE_BF16 && D.hd == kAttnHd && fc.R <= kAttnRows;
-  const int CK = attn_b ? kAttnChunkKeys : kAttnChunk;
+  const bool mfma_attn = D.kvdt == SPADE_BF16 && D.hd == kAttnHd && fc.R <= kAttnRows;
+  const int CK = mfma_attn ? kAttnChunkKeys : kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
   // chunks per workgroup of the bf16 attention: fixed (> 0), else one (the
@@ -1335,12 +1348,12 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     const dim3 agrid(NC, D.H, fc.nb);
     const bool kvb = D.kvdt == SPADE_BF16;
     ap.nb = fc.nb;
-    if (attn_b && cpw > 1) {
+    if (mfma_attn && cpw > 1) {
       const dim3 rgrid(attn_grid((NC + cpw - 1) / cpw, D.KVH, D.H / D.KVH, fc.nb));
       if (wb) hipLaunchKernelGGL((attn_bp_kernel<true, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
       else hipLaunchKernelGGL((attn_bp_kernel<false, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
       e = hipGetLastError();
-    } else if (attn_b && two_pass) {
+    } else if (mfma_attn && two_pass) {
       const dim3 bgrid(attn_grid(NC, D.KVH, D.H / D.KVH, fc.nb));
       if (wb) hipLaunchKernelGGL((attn_lr_kernel<true, kAttnChunkKeys, false>), bgrid, dim3(kAttnThreads), 0, st, ap);
       else hipLaunchKernelGGL((attn_lr_kernel<false, kAttnChunkKeys, false>), bgrid, dim3(kAttnThreads), 0, st, ap);
@@ -1348,7 +1361,7 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
       if (wb) hipLaunchKernelGGL((attn_merge_kernel<true>), dim3(D.H, fc.nb), dim3(kAttnThreads), 0, st, ap);
       else hipLaunchKernelGGL((attn_merge_kernel<false>), dim3(D.H, fc.nb), dim3(kAttnThreads), 0, st, ap);
       e = hipGetLastError();
-    } else if (attn_b) {
+    } else if (mfma_attn) {
       const dim3 bgrid(attn_grid(NC, D.KVH, D.H / D.KVH, fc.nb));
       if (wb) hipLaunchKernelGGL((attn_lr_kernel<true, kAttnChunkKeys, true>), bgrid, dim3(kAttnThreads), 0, st, ap);
       else hipLaunchKernelGGL((attn_lr_kernel<false, kAttnChunkKeys, true>), bgrid, dim3(kAttnThreads), 0, st, ap);

@@ -18,7 +18,7 @@ constexpr int kPrefillRows = 16;     // tokens per prefill forward
 constexpr int kMaxR = 16;            // rows per request in one forward (gamma <= 15)
 constexpr int kCorrMaxSlices = 256; // vocabulary slices of one correction draw
 constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
-constexpr int kAttnChunk = 128;      // keys per attention workgroup
+constexpr int kAttnChunk = 128;      // keys per workgroup of the generic attention (f32 cache or head_dim != 128)
 constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
 constexpr int kMaxLen = kAttnChunk * kAttnMaxChunks;
 constexpr uint32_t kFusedLdsBytes = 159 * 1024;  // dynamic LDS of the single-launch verify kernel
@@ -28,8 +28,8 @@ inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
 
 // Keys per chunk of the bf16 / head_dim-128 verify attention.  A constant:
 // a request's attention (and so its logits) must not depend on the other
-// requests of the batch.  256 keys: about 110 VGPRs and 25 KB of LDS per
-// 8-wave workgroup, two workgroups per compute unit.
+// requests of the batch.  256 keys: 78 VGPRs and 35 KB of LDS per 8-wave
+// workgroup of the one-chunk kernel, three workgroups per compute unit.
 constexpr int kAttnChunkKeys = 256;
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
