@@ -272,6 +272,16 @@ spade_status spade_model_set_attn_merge(spade_model m, int mode);
  * every mode.  Other values return SPADE_EINVAL. */
 spade_status spade_model_set_correction_slices(spade_model m, int mode);
 
+/* Grouped-query attention chunks.  For a model with G = heads / K/V heads
+ * > 1, when the attention partials are merged in a second launch (see
+ * spade_model_set_attn_merge) and the G (gamma+1) rows of a request fit 48
+ * rows, mode 0 (the default) computes each 256-key chunk for all G query
+ * heads of a K/V head in one workgroup (the rows packed into 16-row MFMA
+ * tiles), so the chunk's keys and values pass through a compute unit once;
+ * mode 1 keeps one workgroup per query head.  Results are bit-for-bit the
+ * same under both modes.  Other values return SPADE_EINVAL. */
+spade_status spade_model_set_attn_grouped(spade_model m, int mode);
+
 /* K splitting of the batched O and down projections on the wide-row GEMM.
  * Their weights have few panels (d_model / 16), so one workgroup per panel
  * group leaves most compute units idle; with `splits` = 2 or 4 each

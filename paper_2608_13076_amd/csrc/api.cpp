@@ -219,6 +219,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->attn_cpw = 0;
   m->attn_merge = 0;
   m->corr_split = 0;
+  m->attn_grouped = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -499,6 +500,13 @@ spade_status spade_model_set_attn_merge(spade_model m, int mode) {
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
   m->attn_merge = mode;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_attn_grouped(spade_model m, int mode) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (mode < 0 || mode > 1) return fail(SPADE_EINVAL, "mode must be 0 or 1");
+  m->attn_grouped = mode;
   return SPADE_OK;
 }
 

@@ -160,6 +160,26 @@ __device__ __forceinline__ void attn_split2(const float* xs, uint4& hi, uint4& l
   lo = make_uint4(lw[0], lw[1], lw[2], lw[3]);
 }
 
+// Queries staged in LDS as their two bf16 terms (rows of kAttnQPitch
+// elements: 16-byte aligned, consecutive rows four banks apart).  Four
+// consecutive features x of row `row` go in as attn_split2 splits them.
+constexpr int kAttnQPitch = kAttnHd + 8;
+
+__device__ __forceinline__ void attn_stage_q(uint16_t (*sqh)[kAttnQPitch], uint16_t (*sql)[kAttnQPitch], int row,
+                                             int f, float4 x) {
+  const float xs[4] = {x.x, x.y, x.z, x.w};
+  uint32_t hw[2], lw[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const uint16_t h0 = f2bf(xs[2 * e]), h1 = f2bf(xs[2 * e + 1]);
+    const uint16_t l0 = f2bf(xs[2 * e] - bf2f(h0)), l1 = f2bf(xs[2 * e + 1] - bf2f(h1));
+    hw[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    lw[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+  *(uint2*)&sqh[row][f] = make_uint2(hw[0], hw[1]);
+  *(uint2*)&sql[row][f] = make_uint2(lw[0], lw[1]);
+}
+
 // Cross-lane moves within a row of 16 lanes (DPP): lane i reads lane i^1,
 // i^2, 7-i (within its half row) and 15-i; the four steps reduce the row.
 template <int CTRL>
@@ -312,7 +332,8 @@ __device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (
 
 // Low-register variant of attn_chunk for launches with many chunks per
 // compute unit: the K fragments come from attn_load_k, the queries from LDS
-// (sq, staged by the caller: row i, feature f at sq[i][f], rows past R zero),
+// (sqh / sql, their bf16 terms staged by the caller with attn_stage_q: row i,
+// feature f at [i][f], rows past R zero),
 // and the V^T fragments are requested only after the score products, into the
 // registers the K fragments held, so a wave holds one of the two at a time.
 // Scores, softmax, P V and the returned partial are computed by the same
@@ -335,7 +356,8 @@ __device__ __forceinline__ void attn_load_k(const AttnItem& it, int wave, int la
 
 template <int CK>
 __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
-                                                 const float (*sq)[kAttnHd + 4], int R, float scale, int stride,
+                                                 const uint16_t (*sqh)[kAttnQPitch],
+                                                 const uint16_t (*sql)[kAttnQPitch], int R, float scale, int stride,
                                                  AttnSmem<CK>& sm) {
   constexpr int NG = CK / 128;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -347,11 +369,8 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const float4 x0 = *(const float4*)&sq[kl][32 * ks + 8 * g];
-      const float4 x1 = *(const float4*)&sq[kl][32 * ks + 8 * g + 4];
-      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      uint4 qh, ql;
-      attn_split2(xs, qh, ql);
+      const uint4 qh = *(const uint4*)&sqh[kl][32 * ks + 8 * g];
+      const uint4 ql = *(const uint4*)&sql[kl][32 * ks + 8 * g];
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql),
                                                     __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh),
@@ -619,6 +638,153 @@ __device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o
                                                    uint32_t* attn_cnt, int H, int NC, int Rmax, int R, Out&& out) {
   attn_publish<CK>(it, o, sa, part_o, part_ml, H, NC, Rmax, R);
   attn_arrive_merge<COH>(it, it.active ? 1 : 0, ms, part_o, part_ml, attn_cnt, H, NC, Rmax, R, out);
+}
+
+// Grouped-query variant of attn_chunk_lr: one workgroup computes the chunk
+// for all G query heads of a K/V head, so the chunk's keys and values pass
+// through the compute unit once.  The G R rows are packed into T 16-row
+// tiles (packed row pr = gg R + i: query head gg of the group, request row
+// i; rows past G R are masked).  Every packed row goes through the same
+// instructions in the same order as its row in attn_chunk_lr, so its
+// partial is bit-identical.  sqh / sql: the packed query rows, staged by
+// the caller with attn_stage_q.  o[t]: rows 16 t + 4 g + i (i = 0..3), feature 16 wave + kl.
+template <int CK, int T>
+struct AttnSmemG {
+  uint16_t ph[16 * T][CK + 8], pl[16 * T][CK + 8];
+  float pm[16 * T][8], ps[16 * T][8];
+  float m[16 * T], l[16 * T];
+};
+
+template <int CK, int T>
+__device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
+                                               const uint16_t (*sqh)[kAttnQPitch],
+                                               const uint16_t (*sql)[kAttnQPitch], int R, int NR, float scale,
+                                               int stride, AttnSmemG<CK, T>& sm, floatx4 (&o)[T]) {
+  constexpr int NG = CK / 128;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, kl = lane & 15;
+  const int ke = (it.k_hi + 7) & ~7;
+  float sv[T][NG][4];
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const uint4 qh = *(const uint4*)&sqh[16 * t + kl][32 * ks + 8 * g];
+        const uint4 ql = *(const uint4*)&sql[16 * t + kl][32 * ks + 8 * g];
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql),
+                                                      __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh),
+                                                      __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+      }
+      const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int pr = 16 * t + 4 * g + i;
+        const int row = pr - (pr / R) * R;
+        sv[t][grp][i] = (pr < NR && key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
+      }
+    }
+  __builtin_amdgcn_sched_barrier(0);
+  AttnRegs<CK> r;
+  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
+#pragma unroll
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const int kv0 = it.k_lo + 32 * ks + 8 * g;
+    r.vf[ks] = make_uint4(0, 0, 0, 0);
+    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float mx = sv[t][0][i];
+#pragma unroll
+      for (int grp = 1; grp < NG; ++grp) mx = fmaxf(mx, sv[t][grp][i]);
+      mx = row16_max(mx);
+      if (kl == 0) sm.pm[16 * t + 4 * g + i][wave] = mx;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 16 * t + 4 * g + i;
+      const float4 a = *(const float4*)&sm.pm[row][0];
+      const float4 b = *(const float4*)&sm.pm[row][4];
+      const float M = fmaxf(fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)), fmaxf(fmaxf(b.x, b.y), fmaxf(b.z, b.w)));
+      float sum = 0.f;
+#pragma unroll
+      for (int grp = 0; grp < NG; ++grp) {
+        const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[t][grp][i] - M) * 1.44269504088896341f);
+        sum += e;
+        const uint16_t h = f2bf(e);
+        const int kc = (CK / 8) * wave + 16 * grp + kl;
+        sm.ph[row][kc] = h;
+        sm.pl[row][kc] = f2bf(e - bf2f(h));
+      }
+      sum = row16_sum(sum);
+      if (kl == 0) sm.ps[row][wave] = sum;
+    }
+  __syncthreads();
+  if (tid < NR) {
+    float l = 0.f, M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      l += sm.ps[tid][w];
+      M = fmaxf(M, sm.pm[tid][w]);
+    }
+    sm.m[tid] = M;
+    sm.l[tid] = l;
+  }
+  attn_mask_tail(it, lane, r);
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < CK / 32; ++ks) {
+      const uint4 ph = *(const uint4*)&sm.ph[16 * t + kl][32 * ks + 8 * g];
+      const uint4 pl = *(const uint4*)&sm.pl[16 * t + kl][32 * ks + 8 * g];
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl),
+                                                    __builtin_bit_cast(bf16x8, r.vf[ks]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph),
+                                                    __builtin_bit_cast(bf16x8, r.vf[ks]), acc, 0, 0, 0);
+    }
+    o[t] = acc;
+  }
+}
+
+// Store the grouped chunk's partials where attn_publish stores each head's:
+// packed row pr goes to query head kvh G + pr / R, row pr % R.
+template <int CK, int T>
+__device__ __forceinline__ void attn_publish_grp(const AttnItem& it, int kvh, int G, const floatx4 (&o)[T],
+                                                 const AttnSmemG<CK, T>& sa, float* part_o, float* part_ml, int H,
+                                                 int NC, int Rmax, int R) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, kl = lane & 15;
+  const int NR = G * R;
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int pr = 16 * t + 4 * g + i;
+      if (pr < NR) {
+        const int gg = pr / R, row = pr - gg * R;
+        const size_t bh = (size_t)it.bl * H + kvh * G + gg;
+        float* po = part_o + ((bh * NC + it.c) * Rmax + row) * kAttnHd + 16 * wave + kl;
+        __hip_atomic_store(po, o[t][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  if (tid < NR) {
+    const int gg = tid / R, row = tid - gg * R;
+    const size_t bh = (size_t)it.bl * H + kvh * G + gg;
+    float* pml = part_ml + ((bh * NC + it.c) * Rmax + row) * 2;
+    __hip_atomic_store(pml, sa.m[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(pml + 1, sa.l[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 }  // namespace spade

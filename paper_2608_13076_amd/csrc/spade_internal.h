@@ -174,6 +174,7 @@ struct spade_model_s {
   int split_ks;  // k-splits of the split-K GEMM: 0 chosen per launch, 2 or 4 where it qualifies, -1 off
   int attn_cpw;  // attention chunks per workgroup (bf16 cache, head_dim 128): 0 chosen per call, >= 1 fixed
   int attn_merge;  // merge of one-chunk attention partials: 0 chosen per call, 1 last arrival, 2 second launch
+  int attn_grouped;  // grouped-query chunks (one workgroup per K/V head and chunk): 0 where they apply, 1 off
   int corr_split;  // correction draws of sampling requests: 0/2 over vocabulary slices, 1 in the accept workgroup
 };
 

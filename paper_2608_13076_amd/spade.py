@@ -33,7 +33,7 @@ EXPORTED = (
     "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles",
     "spade_model_set_wide_k_splits", "spade_model_set_split_k", "spade_softmax", "spade_prefill_batch",
     "spade_wide_tiling", "spade_model_set_attn_chunks", "spade_model_set_attn_merge",
-    "spade_model_set_correction_slices",
+    "spade_model_set_correction_slices", "spade_model_set_attn_grouped",
 )
 
 
@@ -96,6 +96,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_model_set_attn_chunks": (I, [P, I]),
         "spade_model_set_attn_merge": (I, [P, I]),
         "spade_model_set_correction_slices": (I, [P, I]),
+        "spade_model_set_attn_grouped": (I, [P, I]),
         "spade_model_set_split_k": (I, [P, I]),
         "spade_softmax": (I, [P, I, I, F, P, P]),
         "spade_prefill_batch": (I, [P, P, I, P, I, P, P]),
@@ -193,6 +194,11 @@ class Model:
         """Merge of one-chunk attention partials: 0 chosen per call, 1 by the
         last chunk workgroup, 2 in a second launch."""
         _check(self.lib.spade_model_set_attn_merge(self.handle, int(mode)))
+
+    def set_attn_grouped(self, mode: int) -> None:
+        """Grouped-query attention chunks (all query heads of a K/V head in one
+        workgroup, with the second-launch merge): 0 where they apply, 1 off."""
+        _check(self.lib.spade_model_set_attn_grouped(self.handle, int(mode)))
 
     def set_correction_slices(self, mode: int) -> None:
         """Correction draw of sampling requests: 0 or 2 over vocabulary slices

@@ -92,6 +92,7 @@ def test_host_validation_without_device(lib):
     assert lib.spade_model_set_attn_chunks(None, 1) == -1
     assert lib.spade_model_set_attn_merge(None, 1) == -1
     assert lib.spade_model_set_correction_slices(None, 1) == -1
+    assert lib.spade_model_set_attn_grouped(None, 1) == -1
     assert lib.spade_model_set_wide_tiles(None, 0, 0) == -1
     assert lib.spade_model_set_split_k(None, 0) == -1
     assert "null" in lib.spade_last_error().decode()

@@ -100,3 +100,34 @@ def test_attention_runs_bit_identical(batch):
         assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), cfg
         assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), cfg
     assert model.device_error() == 0
+
+
+@pytest.mark.parametrize("gamma,kv_heads", [(6, 2), (11, 2), (2, 2), (6, 4), (15, 4)])
+def test_grouped_attention_bit_identical(gamma, kv_heads):
+    """Grouped-query chunks (one workgroup computes a chunk for all G query
+    heads of a K/V head, the G (gamma+1) rows packed into one to three 16-row
+    tiles) give the per-head chunks' logits, n_accepted and corrections bit
+    for bit, with the second-launch merge forced so both run: G = 4 and 2,
+    rows per request 3 to 16, one to three tiles."""
+    import dataclasses
+    base = {w.name: w for w in mini_workloads()}["mini_gqa_mixed_b5"]
+    w = base.with_(name=f"mini_gqa_g{gamma}_kvh{kv_heads}", model=dataclasses.replace(base.model, n_kv_heads=kv_heads),
+                   gamma=gamma, seed=3000 + gamma + kv_heads)
+    weights = ModelWeights(w.model, w.seed)
+    inp = make_inputs(w)
+    model, kv = gpu_setup(w, weights)
+    kv.prefill_batch(inp.prompts)
+    from paper_2608_13076_amd import spade
+    with pytest.raises(spade.SpadeError):
+        model.set_attn_grouped(2)
+    model.set_attn_merge(2)
+    runs = {}
+    for grouped in (1, 0):
+        print(f"[{w.name}] lens {inp.lens.tolist()} grouped attention mode {grouped}", flush=True)
+        model.set_attn_grouped(grouped)
+        runs[grouped] = gpu_verify(model, kv, inp)[:3]
+    a, b = runs[1], runs[0]
+    assert np.isfinite(a[0]).all()
+    assert np.array_equal(a[0].view(np.uint32), b[0].view(np.uint32))
+    assert np.array_equal(a[1], b[1]) and np.array_equal(a[2], b[2])
+    assert model.device_error() == 0
