@@ -230,7 +230,8 @@ spade_status spade_model_set_fused(spade_model m, int enable);
  * row groups of one set of panels run on one XCD and share its L2.
  * row_tiles = 0 and panels = 0 (the defaults) are chosen per launch from the
  * shape and the compute-unit count; row_tiles 1..3 and panels 1..2 fix them
- * (two panels per wave with at most two row tiles);
+ * (the O and down projections, which can be k-split, take two panels per
+ * wave with at most two row tiles and fall back to one tile and one panel);
  * row_tiles = -1 turns the wide-row GEMM off (the skinny engine then runs
  * once per 32 rows and streams the weights once per launch).  Results are
  * bit-for-bit the same under every setting: a row's dot products are summed

@@ -490,7 +490,6 @@ spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (row_tiles < -1 || row_tiles > 3) return fail(SPADE_EINVAL, "row_tiles must be -1, 0, 1, 2 or 3");
   if (panels < 0 || panels > 2) return fail(SPADE_EINVAL, "panels must be 0, 1 or 2");
-  if (panels == 2 && row_tiles == 3) return fail(SPADE_EINVAL, "two panels per wave take at most two row tiles");
   m->wide_rt = row_tiles;
   m->wide_p = panels;
   return SPADE_OK;

@@ -1044,6 +1044,9 @@ hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, uint32_t* cnt,
 template <int KIND, int KS>
 hipError_t launch_wide_ks(const GemmParams& gp, int rt, int p, int nrg, int nug, uint32_t* cnt, float* part,
                           hipStream_t st) {
+  if constexpr (KS == 1) {
+    if (p == 2 && rt == 3) return launch_wide_rt<3, 2, KIND, KS>(gp, nrg, nug, cnt, part, st);
+  }
   if constexpr (KS != 2) {
     if (p == 2 && rt == 2) return launch_wide_rt<2, 2, KIND, KS>(gp, nrg, nug, cnt, part, st);
     if (rt == 3) return launch_wide_rt<3, 1, KIND, KS>(gp, nrg, nug, cnt, part, st);
@@ -1084,7 +1087,7 @@ WideChoice wide_choice(int kind, int M, int n_units, int NKB, int K, int n_cu, i
   for (int p = 2; p >= 1; --p) {
     if (fixed_p > 0 && p != fixed_p) continue;
     for (int rt = 3; rt >= 1; --rt) {
-      if (p == 2 && rt == 3) continue;
+      if (p == 2 && rt == 3 && splittable) continue;  // k-splittable kinds: not instantiated
       if (fixed_rt > 0 && rt != fixed_rt) continue;
       if (fixed_rt <= 0 && rt > tiles) continue;
       for (int ks = 1; ks <= 4; ks *= 2) {

@@ -41,7 +41,7 @@ def test_wide_tilings_bit_identical_and_match_oracle(w):
     model, kv = gpu_setup(w, weights)
     gpu_prefill(kv, inp)
     runs = {}
-    for tiles in ((-1, 0), (1, 1), (2, 1), (3, 1), (1, 2), (2, 2), (0, 0)):
+    for tiles in ((-1, 0), (1, 1), (2, 1), (3, 1), (1, 2), (2, 2), (3, 2), (0, 0)):
         for ks in ((0,) if tiles[0] < 0 else (1, 2, 4, 0)):
             print(f"[{w.name}] M={w.batch * (w.gamma + 1)} wide (row tiles, panels) {tiles} k-splits {ks}",
                   flush=True)
