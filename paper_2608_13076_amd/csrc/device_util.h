@@ -34,12 +34,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// round to nearest even; NaN stays NaN
+// round to nearest even (the hardware conversion, v_cvt_pk_bf16_f32: for
+// every non-NaN float the same bits as adding 0x7fff plus the lowest kept
+// bit and truncating, checked over all 2^32 inputs); NaN becomes 0x7fc0
 __device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  if (f != f) return 0x7fc0;
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 // Raw (unswizzled) buffer resource over [p, p + bytes); bytes < 2^31.
