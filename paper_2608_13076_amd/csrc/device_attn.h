@@ -147,6 +147,10 @@ __device__ __forceinline__ void attn_mask_tail(const AttnItem& it, int lane, Att
   }
 }
 
+// f2bf without the NaN canonicalisation (the probabilities of a chunk are
+// NaN only when its scores are, and then the outputs are NaN either way).
+__device__ __forceinline__ uint16_t f2bf_num(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+
 __device__ __forceinline__ void attn_split2(const float* xs, uint4& hi, uint4& lo) {
   uint32_t hw[4], lw[4];
 #pragma unroll
@@ -297,10 +301,10 @@ __device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (
       // masked keys: exp2(-inf) = 0
       const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[grp][i] - M) * 1.44269504088896341f);
       sum += e;
-      const uint16_t h = f2bf(e);
+      const uint16_t h = f2bf_num(e);
       const int kc = (CK / 8) * wave + 16 * grp + kl;
       sm.ph[row][kc] = h;
-      sm.pl[row][kc] = f2bf(e - bf2f(h));
+      sm.pl[row][kc] = f2bf_num(e - bf2f(h));
     }
     sum = row16_sum(sum);
     if (kl == 0) sm.ps[row][wave] = sum;
@@ -414,10 +418,10 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
     for (int grp = 0; grp < NG; ++grp) {
       const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[grp][i] - M) * 1.44269504088896341f);
       sum += e;
-      const uint16_t h = f2bf(e);
+      const uint16_t h = f2bf_num(e);
       const int kc = (CK / 8) * wave + 16 * grp + kl;
       sm.ph[row][kc] = h;
-      sm.pl[row][kc] = f2bf(e - bf2f(h));
+      sm.pl[row][kc] = f2bf_num(e - bf2f(h));
     }
     sum = row16_sum(sum);
     if (kl == 0) sm.ps[row][wave] = sum;
@@ -721,10 +725,10 @@ __device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (
       for (int grp = 0; grp < NG; ++grp) {
         const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[t][grp][i] - M) * 1.44269504088896341f);
         sum += e;
-        const uint16_t h = f2bf(e);
+        const uint16_t h = f2bf_num(e);
         const int kc = (CK / 8) * wave + 16 * grp + kl;
         sm.ph[row][kc] = h;
-        sm.pl[row][kc] = f2bf(e - bf2f(h));
+        sm.pl[row][kc] = f2bf_num(e - bf2f(h));
       }
       sum = row16_sum(sum);
       if (kl == 0) sm.ps[row][wave] = sum;
