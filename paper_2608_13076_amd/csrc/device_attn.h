@@ -659,6 +659,34 @@ struct AttnSmemG {
   float m[16 * T], l[16 * T];
 };
 
+// Query head within the group (gg) and request row (rw) of packed rows
+// p0 + 16 t + i (t < T, i < NI), p0 + 16 t + i = gg R + rw: two divisions,
+// then steps (a division per row costs some twenty VALU instructions).
+template <int T, int NI>
+__device__ __forceinline__ void attn_grp_rows(int p0, int R, int (&gg)[T][NI], int (&rw)[T][NI]) {
+  const int sq = 16 / R, sr = 16 - sq * R;
+  int q = p0 / R, r = p0 - q * R;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    int qi = q, ri = r;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      gg[t][i] = qi;
+      rw[t][i] = ri;
+      if (++ri == R) {
+        ri = 0;
+        ++qi;
+      }
+    }
+    r += sr;
+    q += sq;
+    if (r >= R) {
+      r -= R;
+      ++q;
+    }
+  }
+}
+
 template <int CK, int T>
 __device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
                                                const uint16_t (*sqh)[kAttnQPitch],
@@ -668,6 +696,8 @@ __device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, kl = lane & 15;
   const int ke = (it.k_hi + 7) & ~7;
+  int gg[T][4], rw[T][4];
+  attn_grp_rows<T, 4>(4 * g, R, gg, rw);
   float sv[T][NG][4];
 #pragma unroll
   for (int t = 0; t < T; ++t)
@@ -687,8 +717,7 @@ __device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int pr = 16 * t + 4 * g + i;
-        const int row = pr - (pr / R) * R;
-        sv[t][grp][i] = (pr < NR && key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
+        sv[t][grp][i] = (pr < NR && key < it.k_hi && key <= it.L + rw[t][i]) ? acc[i] * scale : -INFINITY;
       }
     }
   __builtin_amdgcn_sched_barrier(0);
@@ -770,15 +799,16 @@ __device__ __forceinline__ void attn_publish_grp(const AttnItem& it, int kvh, in
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, kl = lane & 15;
   const int NR = G * R;
+  int gq[T][4], rw[T][4];
+  attn_grp_rows<T, 4>(4 * g, R, gq, rw);
 #pragma unroll
   for (int t = 0; t < T; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int pr = 16 * t + 4 * g + i;
       if (pr < NR) {
-        const int gg = pr / R, row = pr - gg * R;
-        const size_t bh = (size_t)it.bl * H + kvh * G + gg;
-        float* po = part_o + ((bh * NC + it.c) * Rmax + row) * kAttnHd + 16 * wave + kl;
+        const size_t bh = (size_t)it.bl * H + kvh * G + gq[t][i];
+        float* po = part_o + ((bh * NC + it.c) * Rmax + rw[t][i]) * kAttnHd + 16 * wave + kl;
         __hip_atomic_store(po, o[t][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }

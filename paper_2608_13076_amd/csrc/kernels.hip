@@ -674,14 +674,14 @@ attn_g_kernel(AttnParams p) {
   // thread t stages features 4 (t % 32) .. + 3 of packed rows t / 32 + 16 j
   const int f4 = tid & 31;
   float4 qv[T];
+  int gg[T][1], rw[T][1];
+  attn_grp_rows<T, 1>(tid >> 5, p.R, gg, rw);
 #pragma unroll
   for (int j = 0; j < T; ++j) {
     const int pr = (tid >> 5) + 16 * j;
     qv[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (pr < NR) {
-      const int gg = pr / p.R, i = pr - gg * p.R;
-      qv[j] = *(const float4*)(p.q + (size_t)(bl * p.R + i) * p.d + (kvh * p.G + gg) * kAttnHd + 4 * f4);
-    }
+    if (pr < NR)
+      qv[j] = *(const float4*)(p.q + (size_t)(bl * p.R + rw[j][0]) * p.d + (kvh * p.G + gg[j][0]) * kAttnHd + 4 * f4);
   }
   uint4 kf[CK / 128][4];
   attn_load_k<CK>(it, wave, lane, kf);
