@@ -97,14 +97,20 @@ class KVCache:
     v: List[np.ndarray] = field(default_factory=list)
 
     def __post_init__(self):
+        # Every stored value is already rounded to the cache precision (bf16
+        # or float32), so float32 arrays hold it exactly; attention reads
+        # widen it back to float64 without loss.
         if not self.k:
             shp = (self.n_heads, self.capacity, self.head_dim)
-            self.k = [np.zeros(shp) for _ in range(self.n_layers)]
-            self.v = [np.zeros(shp) for _ in range(self.n_layers)]
+            self.k = [np.zeros(shp, dtype=np.float32) for _ in range(self.n_layers)]
+            self.v = [np.zeros(shp, dtype=np.float32) for _ in range(self.n_layers)]
 
     def copy(self) -> "KVCache":
         return KVCache(self.n_layers, self.n_heads, self.head_dim, self.capacity, self.length,
                        [a.copy() for a in self.k], [a.copy() for a in self.v])
+
+
+_LAYER_KINDS = ("g_attn", "wq", "wk", "wv", "wo", "g_ffn", "wg", "wu", "wd")
 
 
 class Decoder:
@@ -135,12 +141,13 @@ class Decoder:
     def _store(self, x: np.ndarray) -> np.ndarray:
         return bf16_round(x) if self.shape.kv_dtype == "bf16" else x.astype(np.float32).astype(np.float64)
 
-    def forward(self, cache: KVCache, tokens: np.ndarray, want_logits: bool = True) -> Optional[np.ndarray]:
-        """Append ``tokens`` (R ids) at positions cache.length .. +R-1 and
-        return the R rows of next-token logits [R, V] (float64)."""
+    def block(self, l: int, W: Callable[[str], np.ndarray], cache: KVCache, x: np.ndarray) -> np.ndarray:
+        """Residual block l (self-attention, then feed-forward) for the R rows
+        x at positions cache.length .. +R-1; writes their K/V rows to the
+        cache (the length is advanced by the caller).  ``W(kind)`` returns the
+        block's weights."""
         s = self.shape
-        tokens = np.asarray(tokens, dtype=np.int64)
-        R = tokens.shape[0]
+        R = x.shape[0]
         L = cache.length
         if L + R > cache.capacity:
             raise ValueError("cache capacity exceeded")
@@ -149,37 +156,68 @@ class Decoder:
         G = H // KVH  # query heads per K/V head
         pos = np.arange(L, L + R)
         cos, sin = rope_tables(pos, hd, s.rope_theta)
-        x = self.w("embed")[tokens]  # x_0
         scale = 1.0 / np.sqrt(hd)
-        for l in range(s.n_layers):
-            # attention sub-block
-            h = rms_norm(x, self.w("g_attn", l), s.rms_eps)
-            q = (h @ self.w("wq", l).T).reshape(R, H, hd)
-            k = (h @ self.w("wk", l).T).reshape(R, KVH, hd)
-            v = (h @ self.w("wv", l).T).reshape(R, KVH, hd)
-            q = apply_rope(q, cos, sin)
-            k = apply_rope(k, cos, sin)
-            cache.k[l][:, L:L + R, :] = self._store(k).transpose(1, 0, 2)
-            cache.v[l][:, L:L + R, :] = self._store(v).transpose(1, 0, 2)
-            # query head h reads K/V head h // G
-            K = np.repeat(cache.k[l][:, :L + R, :], G, axis=0)  # [H, L+R, hd]
-            Vv = np.repeat(cache.v[l][:, :L + R, :], G, axis=0)
-            scores = np.matmul(q.transpose(1, 0, 2), K.transpose(0, 2, 1)) * scale  # [H, R, L+R]
-            key_pos = np.arange(L + R)
-            mask = key_pos[None, :] <= pos[:, None]  # row i sees keys <= L+i
-            scores = np.where(mask[None, :, :], scores, -np.inf)
-            p = softmax(scores, axis=-1)
-            o = np.matmul(p, Vv).transpose(1, 0, 2).reshape(R, H * hd)
-            x = x + o @ self.w("wo", l).T
-            # feed-forward sub-block
-            h = rms_norm(x, self.w("g_ffn", l), s.rms_eps)
-            a = silu(h @ self.w("wg", l).T) * (h @ self.w("wu", l).T)
-            x = x + a @ self.w("wd", l).T
-        cache.length = L + R
-        if not want_logits:
-            return None
-        h = rms_norm(x, self.w("g_final"), s.rms_eps)
-        return h @ self.w("lm_head").T  # o_L for each row
+        # attention sub-block
+        h = rms_norm(x, W("g_attn"), s.rms_eps)
+        q = (h @ W("wq").T).reshape(R, H, hd)
+        k = (h @ W("wk").T).reshape(R, KVH, hd)
+        v = (h @ W("wv").T).reshape(R, KVH, hd)
+        q = apply_rope(q, cos, sin)
+        k = apply_rope(k, cos, sin)
+        cache.k[l][:, L:L + R, :] = self._store(k).transpose(1, 0, 2)
+        cache.v[l][:, L:L + R, :] = self._store(v).transpose(1, 0, 2)
+        # query head h reads K/V head h // G
+        K = np.repeat(cache.k[l][:, :L + R, :], G, axis=0).astype(np.float64)  # [H, L+R, hd]
+        Vv = np.repeat(cache.v[l][:, :L + R, :], G, axis=0).astype(np.float64)
+        scores = np.matmul(q.transpose(1, 0, 2), K.transpose(0, 2, 1)) * scale  # [H, R, L+R]
+        key_pos = np.arange(L + R)
+        mask = key_pos[None, :] <= pos[:, None]  # row i sees keys <= L+i
+        scores = np.where(mask[None, :, :], scores, -np.inf)
+        p = softmax(scores, axis=-1)
+        o = np.matmul(p, Vv).transpose(1, 0, 2).reshape(R, H * hd)
+        x = x + o @ W("wo").T
+        # feed-forward sub-block
+        h = rms_norm(x, W("g_ffn"), s.rms_eps)
+        a = silu(h @ W("wg").T) * (h @ W("wu").T)
+        return x + a @ W("wd").T
+
+    def head(self, x: np.ndarray) -> np.ndarray:
+        """LM head: o_L = RMSNorm(x_L) W_lm^T for each row."""
+        h = rms_norm(x, self.w("g_final"), self.shape.rms_eps)
+        return h @ self.w("lm_head").T
+
+    def forward(self, cache: KVCache, tokens: np.ndarray, want_logits: bool = True) -> Optional[np.ndarray]:
+        """Append ``tokens`` (R ids) at positions cache.length .. +R-1 and
+        return the R rows of next-token logits [R, V] (float64)."""
+        tokens = np.asarray(tokens, dtype=np.int64)
+        if cache.length + tokens.shape[0] > cache.capacity:
+            raise ValueError("cache capacity exceeded")
+        x = self.w("embed")[tokens]  # x_0
+        for l in range(self.shape.n_layers):
+            x = self.block(l, lambda kind: self.w(kind, l), cache, x)
+        cache.length += tokens.shape[0]
+        return self.head(x) if want_logits else None
+
+    def forward_many(self, caches: List[KVCache], tokens: List[np.ndarray],
+                     want_logits: bool = True) -> Optional[List[np.ndarray]]:
+        """``forward`` for several independent requests, layer by layer: each
+        layer's weights are fetched once and applied to every request in
+        turn (the same arithmetic per request as ``forward``)."""
+        toks = [np.asarray(t, dtype=np.int64) for t in tokens]
+        for c, t in zip(caches, toks):
+            if c.length + t.shape[0] > c.capacity:
+                raise ValueError("cache capacity exceeded")
+        E = self.w("embed")
+        xs = [E[t] for t in toks]
+        del E
+        for l in range(self.shape.n_layers):
+            Wl = {kind: self.w(kind, l) for kind in _LAYER_KINDS}
+            for i, c in enumerate(caches):
+                xs[i] = self.block(l, Wl.__getitem__, c, xs[i])
+            del Wl
+        for c, t in zip(caches, toks):
+            c.length += t.shape[0]
+        return [self.head(x) for x in xs] if want_logits else None
 
     def prefill(self, cache: KVCache, tokens: np.ndarray, chunk: int = 4096) -> None:
         """Run the cached prefix through the model (no logits needed)."""

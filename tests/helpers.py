@@ -24,22 +24,32 @@ class OracleRun:
     chains: list = field(default_factory=list)
 
 
-def complete_drafts(dec: Decoder, inp, caches) -> None:
+def chain_drafts(inp, b: int, chain) -> None:
+    """chain_half recipe for request b: its first chain_slots drafts are the
+    verifier's argmax chain; the next draft (a uniform id) is moved off the
+    argmax of its row so the chain ends there."""
+    k = inp.chain_slots
+    G, V = inp.workload.gamma, inp.workload.model.vocab
+    inp.drafts[b, :k] = chain[:k]
+    if k < G and inp.drafts[b, k] == chain[k]:
+        inp.drafts[b, k] = (chain[k] + 1) % V
+
+
+def complete_drafts(dec: Decoder, inp, caches, requests=None) -> None:
     """Fill the draft slots that depend on the verifier (chain_half,
-    draft_model recipes) using the oracle, in place."""
+    draft_model recipes) using the oracle, in place.  ``caches[b]`` is
+    request b's prefilled cache; ``requests`` limits the work to some b."""
     w = inp.workload
-    G, V = w.gamma, w.model.vocab
-    for b, rec in enumerate(inp.recipe):
+    G = w.gamma
+    for b in (range(w.batch) if requests is None else requests):
+        rec = inp.recipe[b]
         if rec == "chain_half" and G > 0:
             c = caches[b].copy()
             cur, chain = int(inp.pending[b]), []
             for _ in range(min(inp.chain_slots + 1, G + 1)):
                 cur = _argmax_f32(dec.forward(c, [cur])[0])
                 chain.append(cur)
-            k = inp.chain_slots
-            inp.drafts[b, :k] = chain[:k]
-            if k < G and inp.drafts[b, k] == chain[k]:
-                inp.drafts[b, k] = (chain[k] + 1) % V
+            chain_drafts(inp, b, chain)
         elif rec == "draft_model":
             c = caches[b].copy()
             cur = int(inp.pending[b])

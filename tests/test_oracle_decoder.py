@@ -193,3 +193,44 @@ def test_bf16_kv_storage_is_what_attention_reads():
     for l in range(SMALL_BF16.n_layers):
         np.testing.assert_array_equal(bf16_round(c.k[l]), c.k[l])
         np.testing.assert_array_equal(bf16_round(c.v[l]), c.v[l])
+
+
+@pytest.mark.parametrize("shape", [SMALL_BF16, SMALL_GQA], ids=["bf16", "gqa"])
+def test_forward_many_equals_forward_per_request(shape):
+    """The layer-by-layer driver over several requests (used to generate the
+    stored oracle results of the large batched workloads) gives every request
+    exactly what ``forward`` gives it alone: prefill, a one-token step and a
+    multi-row block, with ragged lengths."""
+    dec, _ = _model(shape, seed=11)
+    rng = np.random.default_rng(12)
+    lens = [1, 17, 40]
+    prompts = [rng.integers(0, shape.vocab, size=L) for L in lens]
+    solo = [dec.new_cache(64) for _ in lens]
+    many = [dec.new_cache(64) for _ in lens]
+    for c, p in zip(solo, prompts):
+        dec.forward(c, p, want_logits=False)
+    dec.forward_many(many, prompts, want_logits=False)
+    for step in ([5], [3, 9, 11, 2]):
+        toks = [np.array(step) + b for b in range(len(lens))]
+        ref = [dec.forward(c, t) for c, t in zip(solo, toks)]
+        got = dec.forward_many(many, toks)
+        for r, g in zip(ref, got):
+            np.testing.assert_array_equal(r, g)
+    for cs, cm in zip(solo, many):
+        assert cs.length == cm.length
+        for l in range(shape.n_layers):
+            np.testing.assert_array_equal(cs.k[l], cm.k[l])
+            np.testing.assert_array_equal(cs.v[l], cm.v[l])
+
+
+def test_bf16_widening_matches_torch_for_every_pattern():
+    """bf16 -> float64 widening of all 65536 bit patterns equals torch's
+    bfloat16 -> float64 conversion (NaN patterns stay NaN)."""
+    from oracle.decoder import bf16_bits_to_f64
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    got = bf16_bits_to_f64(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    np.testing.assert_array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))

@@ -210,6 +210,85 @@ def test_monte_carlo_first_token_and_acceptance_rate():
     assert abs(rate - target) < 4 * np.sqrt(target * (1 - target) / N)
 
 
+def _block_chi_square(tm, d, N, seed, q_equals_p=False):
+    """Monte Carlo of whole verify rounds through ``speculative_rows`` (the
+    float32 acceptance test, the Gumbel-max residual and bonus draws keyed by
+    the last uniform): the emitted block drafts[:n] + (correction,) against
+    its exact distribution from ``_round_outcomes`` (chi-square, cells with
+    small expectation pooled)."""
+    V = tm.V
+    rng = np.random.default_rng(seed)
+    qf = tm.p if q_equals_p else tm.q
+    exact = {}
+    for e, pr in _round_outcomes_q(tm, qf, d).items():
+        exact[e] = exact.get(e, 0.0) + pr
+    counts = {}
+    logit_rows = {}
+    for _ in range(N):
+        drafts = []
+        for i in range(d):
+            drafts.append(int(rng.choice(V, p=qf(tuple(drafts)))))
+        rows = []
+        for i in range(d + 1):
+            ctx = tuple(drafts[:i])
+            if ctx not in logit_rows:
+                logit_rows[ctx] = _logits_from(tm.p(ctx))
+            rows.append(logit_rows[ctx])
+        q = np.stack([qf(tuple(drafts[:i])) for i in range(d)])
+        u = rng.random(d + 1).astype(np.float32)
+        res = speculative_rows(np.stack(rows), np.array(drafts), q, u, SAMPLE, 1.0)
+        e = tuple(drafts[:res.n_accepted]) + (res.correction,)
+        counts[e] = counts.get(e, 0) + 1
+    assert set(counts) <= {e for e, pr in exact.items() if pr > 0}, "emitted a block of probability 0"
+    keys = sorted(exact, key=lambda e: -exact[e])
+    obs, exp, pool_o, pool_e = [], [], 0, 0.0
+    for e in keys:
+        if exact[e] * N >= 10:
+            obs.append(counts.get(e, 0))
+            exp.append(exact[e] * N)
+        else:
+            pool_o += counts.get(e, 0)
+            pool_e += exact[e] * N
+    if pool_e > 0:
+        obs.append(pool_o)
+        exp.append(pool_e)
+    exp = np.asarray(exp) * (sum(obs) / sum(exp))
+    return chisquare(obs, exp).pvalue, counts, exact
+
+
+def _round_outcomes_q(tm, qf, d):
+    """``_round_outcomes`` with q(. | prefix) given by ``qf`` and the float32
+    acceptance threshold."""
+    class _Q:
+        V = tm.V
+        p = staticmethod(tm.p)
+        q = staticmethod(qf)
+    return _round_outcomes(_Q, (), d)
+
+
+def test_whole_block_chi_square():
+    """Every position of the emitted block -- accepted drafts, the residual
+    draw at whichever row rejects, and the bonus draw from the row after the
+    last draft when all are accepted -- has the exact distribution of a
+    verify round (Sec. III-C; Algorithm 1)."""
+    tm = TableModel(4, seed=21, mix=0.6)
+    pv, counts, exact = _block_chi_square(tm, d=2, N=40000, seed=8)
+    assert pv > 1e-3, pv
+    # each kind of ending was exercised: rejection at rows 0 and 1, and a bonus
+    lens = {len(e) for e in counts}
+    assert lens == {1, 2, 3}
+
+
+def test_q_equal_p_bonus_follows_last_row():
+    """q = p accepts every draft (Sec. III-C: min(1, p/q) = 1), so every
+    round emits the d drafts plus a bonus token drawn from p(. | prefix,
+    drafts): the block distribution is the verifier's chain probability."""
+    tm = TableModel(5, seed=33)
+    pv, counts, exact = _block_chi_square(tm, d=2, N=30000, seed=9, q_equals_p=True)
+    assert pv > 1e-3, pv
+    assert {len(e) for e in counts} == {3}
+
+
 @pytest.mark.parametrize("sampler", ["gumbel", "inverse_cdf"])
 def test_samplers_chi_square(sampler):
     rng = np.random.default_rng(11)
