@@ -186,8 +186,6 @@ def main() -> int:
                     help="counter-collection run: a calibration copy, then the gate/up GEMM launches; no timing")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH", "CMD_WRITE"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc runs of --counters")
-    ap.add_argument("--fused", type=int, default=None,
-                    help="1: single-launch verify kernel, 0: one kernel per stage (default: the library's)")
     args = ap.parse_args()
     if args.summarize_counters:
         return summarize_counters(*args.summarize_counters)
@@ -217,8 +215,6 @@ def main() -> int:
     log(f"weights generated + loaded in {time.perf_counter() - t0:.1f}s "
         f"({model.weight_bytes() / 1e9:.2f} GB arena)")
     kv = spade.KVCache(model, w.batch, max_len)
-    if args.fused is not None:
-        model.set_fused(bool(args.fused))
     if args.counters:
         src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)

@@ -26,6 +26,9 @@
  *   are clamped and flagged in the device error word (spade_get_device_error).
  * - A model and the KV handles built on it must be used from one stream at a
  *   time: calls share the workspace.
+ * - Schedule choices that do not change any result (tilings, k-splits,
+ *   attention merge, correction slices) and the measurement hooks are
+ *   declared in spade_tuning.h.
  */
 #ifndef SPADE_H
 #define SPADE_H
@@ -58,8 +61,11 @@ enum {
   SPADE_DERR_NAN = 2u,      /* a logit was NaN                                  */
   SPADE_DERR_RESIDUAL = 4u, /* max(0, p - q) had no mass; drew from p instead   */
   SPADE_DERR_NOQ = 8u,      /* a sampling request got no draft_probs; greedy    */
-  SPADE_DERR_SYNC = 16u     /* a grid barrier of the single-launch verify pass
-                               timed out; that call's outputs are invalid       */
+  SPADE_DERR_CAPACITY = 16u, /* a request's length left fewer than gamma + 1 free
+                                positions (lens written outside the library's
+                                calls); clamped, that call's outputs are invalid */
+  SPADE_DERR_COMMIT = 32u   /* spade_kv_commit read an n_accepted outside
+                               [0, gamma] of the last verify call; clamped      */
 };
 
 /* Weight tensors, row-major [out_features, in_features] unless noted. */
@@ -198,117 +204,17 @@ spade_status spade_prefill(spade_model m, spade_kv kv, int b, const int32_t* d_t
  *
  * The KV rows of all gamma+1 positions are written but lens is unchanged, so
  * the call can be repeated (idempotent) until spade_kv_commit.  Requires
- * lens[b] + gamma + 1 <= max_len (checked against the host-side upper bound
- * of lens) and B <= max_batch, gamma <= max_gamma.
+ * lens[b] + gamma + 1 <= max_len, checked against the host-side upper bound
+ * of lens (refreshed from the device, synchronising the stream, when the
+ * bound alone fails), and B <= max_batch, gamma <= max_gamma.  A device
+ * length the bound did not cover (lens written outside the library) is
+ * clamped on the device and flagged SPADE_DERR_CAPACITY.
  */
 spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma,
                           const int32_t* d_draft_tokens, const float* d_draft_probs,
                           const float* d_uniforms, const uint8_t* d_mode, float temperature,
                           int32_t* d_n_accepted, int32_t* d_correction, float* d_logits,
                           void* stream);
-
-/* Execution path of spade_verify.  After spade_model_set_fused(m, 1), a call
- * whose shape the single-launch pass handles -- bf16 weights and cache,
- * head_dim 128, B * (gamma + 1) <= 16, a device with cooperative launches --
- * runs as ONE persistent kernel over all compute units (grid barriers between
- * the stages, the next stage's weights requested before each barrier wait);
- * any other call runs as one kernel per stage.  Both paths compute bit-for-bit
- * the same results (same tiling, summation orders and merge order).  The
- * default at model creation is the per-stage path unless the environment
- * variable SPADE_FUSED is "1".  enable != 0 on a device without cooperative
- * launches returns SPADE_EUNSUPPORTED.  A persistent pass whose grid barrier
- * does not complete within about a second sets SPADE_DERR_SYNC and returns
- * early. */
-spade_status spade_model_set_fused(spade_model m, int enable);
-
-/* Tiling of the batched projections.  A verify call with more than 16 rows
- * (B * (gamma + 1) > 16) and bf16 weights runs the QKV, O, gate/up and down
- * projections on the wide-row GEMM: each weight tile is read once per launch
- * and multiplied with `row_tiles` 16-row tiles of the activations held in
- * LDS; each wave owns `panels` 16-column weight panels, so that every
- * activation fragment read from LDS feeds that many matrix instructions.  The
- * row groups of one set of panels run on one XCD and share its L2.
- * row_tiles = 0 and panels = 0 (the defaults) are chosen per launch from the
- * shape and the compute-unit count; row_tiles 1..3 and panels 1..2 fix them
- * (the O and down projections, which can be k-split, take two panels per
- * wave with at most two row tiles and fall back to one tile and one panel);
- * row_tiles = -1 turns the wide-row GEMM off (the skinny engine then runs
- * once per 32 rows and streams the weights once per launch).  Results are
- * bit-for-bit the same under every setting: a row's dot products are summed
- * over the same k-ranges in the same order whatever the tiling.  Other values
- * return SPADE_EINVAL. */
-spade_status spade_model_set_wide_tiles(spade_model m, int row_tiles, int panels);
-
-/* Work per workgroup of the verify attention (bf16 cache, head_dim 128).
- * The attention is computed in chunks of 256 keys per (request, head), each
- * giving a partial (row max, row sum, unnormalised output) that is merged in
- * chunk order.  With `chunks` = 1 every chunk is one workgroup; with n > 1 a
- * workgroup computes up to n consecutive chunks of one (request, head),
- * fetching the next chunk's keys and values while it computes the current
- * one, which keeps HBM busy when a call has many chunks (batched requests
- * with long caches).  chunks = 0 (the default) is one chunk per workgroup,
- * which measured fastest at every shape tried.  Results are bit-for-bit the
- * same under every setting.  Values outside [0, 128] return SPADE_EINVAL. */
-spade_status spade_model_set_attn_chunks(spade_model m, int chunks);
-
-/* Merge of the attention's chunk partials when every workgroup computes one
- * chunk (spade_model_set_attn_chunks).  mode 1: the last workgroup of a
- * (request, head) to finish merges its chunks, which makes every chunk
- * workgroup wait for its stores and an arrival counter; mode 2: the chunk
- * workgroups store their partials and exit, and a second launch merges each
- * (request, head); mode 0 (the default) chooses per call (mode 2 from four
- * chunks per compute unit).  Results are bit-for-bit the same under every
- * mode.  Other values return SPADE_EINVAL. */
-spade_status spade_model_set_attn_merge(spade_model m, int mode);
-
-/* Where the correction draw of a sampling request runs (Sec. III-C: sample
- * from norm(max(0, p - q)), or from p when every draft is accepted; the draw
- * is a Gumbel-max pass over the vocabulary).  mode 0 (the default) or 2: when
- * the call may sample (uniforms given, and draft_probs given or gamma = 0),
- * spade_verify (per-stage path) and spade_accept_from_logits run it in a
- * second launch over slices of 1024 tokens (at most 256 slices), one
- * workgroup per (slice, request), the last slice of a request to finish
- * taking the best of the slices; mode 1 keeps it in the request's accept
- * workgroup.  The single-launch pass always keeps it there.  Results are bit-for-bit the same under
- * every mode.  Other values return SPADE_EINVAL. */
-spade_status spade_model_set_correction_slices(spade_model m, int mode);
-
-/* Grouped-query attention chunks.  For a model with G = heads / K/V heads
- * > 1, when the attention partials are merged in a second launch (see
- * spade_model_set_attn_merge) and the G (gamma+1) rows of a request fit 48
- * rows, mode 0 (the default) computes each 256-key chunk for all G query
- * heads of a K/V head in one workgroup (the rows packed into 16-row MFMA
- * tiles), so the chunk's keys and values pass through a compute unit once;
- * mode 1 keeps one workgroup per query head.  Results are bit-for-bit the
- * same under both modes.  Other values return SPADE_EINVAL. */
-spade_status spade_model_set_attn_grouped(spade_model m, int mode);
-
-/* K splitting of the batched O and down projections on the wide-row GEMM.
- * Their weights have few panels (d_model / 16), so one workgroup per panel
- * group leaves most compute units idle; with `splits` = 2 or 4 each
- * workgroup streams only 1/splits of the k-blocks (whole k-ranges of the
- * engine's eight), publishes its partial sums to the workspace, and the
- * last workgroup of a panel group to finish adds them in range order and
- * runs the epilogue.  splits = 0 (the default) chooses per launch from the
- * shape, 1 turns k-splitting off, 2 or 4 fix it (falling back to 1 where the
- * workspace's published-value buffers are too small).  Results are
- * bit-for-bit the same under every setting.  Other values return
- * SPADE_EINVAL. */
-spade_status spade_model_set_wide_k_splits(spade_model m, int splits);
-
-/* K splitting of the small-batch projections.  A verify call with at most 16
- * rows and bf16 weights whose activation operand is too long for one LDS copy
- * (the 7B-shaped down projection, every projection of the 13B shape) runs the
- * QKV, O, gate/up or down projection split along K into `splits` parts: a
- * workgroup copies only its part of the operand into LDS and streams one
- * k-range of each of its panels; the last workgroup of a panel group to finish
- * completes the sums and runs the epilogue.  splits = 0 (the default) picks 2
- * or 4, the fewest whose part fits; 2 or 4 fix it (also where the whole
- * operand would fit) where the part fits; -1 turns it off (the operand is then
- * fetched from L2 with every weight tile).  Results are bit-for-bit the same
- * under every setting: each dot product is summed over the same eight k-ranges
- * in the same order.  Other values return SPADE_EINVAL. */
-spade_status spade_model_set_split_k(spade_model m, int splits);
 
 /* Prefill of B requests at once: request b caches h_n_tokens[b] - 1 prompt
  * tokens (row b of d_tokens, device int32 [B][ld], ld >= every count) after
@@ -336,11 +242,14 @@ spade_status spade_softmax(const float* d_logits, int rows, int V, float tempera
 
 /* Context update after spade_verify (Algorithm 1: append the k accepted
  * tokens and the correction, m <- m + k + 1): lens[b] += n_accepted[b] + 1 and
- * pending[b] = correction[b], on the device.  KV rows past the new length are
- * the rolled-back drafts; they are overwritten by the next round.  The
- * host-side upper bound of lens (the capacity check of spade_verify) grows by
- * gamma + 1 of the last spade_verify on this cache; spade_kv_set_state makes
- * it exact again. */
+ * pending[b] = correction[b] for b < B, on the device.  KV rows past the new
+ * length are the rolled-back drafts; they are overwritten by the next round.
+ * Needs a spade_verify on this cache since the last commit, prefill or state
+ * change, covering at least B requests (else SPADE_EINVAL); each n_accepted is
+ * clamped to [0, gamma] of that call (SPADE_DERR_COMMIT if it was outside).
+ * The host-side upper bound of lens grows by gamma + 1; spade_verify reads the
+ * device lengths back (one synchronisation) only when that bound would fail
+ * its capacity check, so a long verify -> commit loop needs no host sync. */
 spade_status spade_kv_commit(spade_kv kv, int B, const int32_t* d_n_accepted,
                              const int32_t* d_correction, void* stream);
 
@@ -352,25 +261,6 @@ spade_status spade_accept_from_logits(spade_model m, int B, int gamma, int V, co
                                       const float* d_uniforms, const uint8_t* d_mode,
                                       float temperature, int32_t* d_n_accepted,
                                       int32_t* d_correction, void* stream);
-
-/* Measurement hook: launch the GEMM kernel of one projection alone, exactly
- * as spade_verify launches it for B requests of gamma drafts, `launches`
- * times (layer = i mod n_layers), on the workspace's current operands.
- * kind: 0 QKV (+RoPE, KV append), 1 O (+residual), 2 gate/up (+SiLU),
- * 3 down (+residual), 4 LM head.  It overwrites workspace activations and
- * cache rows past lens, so run it between verify calls, not inside a round. */
-spade_status spade_profile_gemm(spade_model m, spade_kv kv, int kind, int B, int gamma, int launches,
-                                void* stream);
-
-/* Inspection hook (host only, no device): the tiling the wide-row GEMM picks
- * for a bf16 projection launch of `rows` rows (> 16), `n_units` 16-row weight
- * panels and `k` inputs (a multiple of 256) on `n_cu` compute units, with
- * every setting at its default and buffers large enough for any k-split.
- * kind as for spade_profile_gemm.  Writes the 16-row tiles per workgroup,
- * the panels per wave and the k-splits; SPADE_EINVAL on a null pointer or
- * a shape out of range. */
-spade_status spade_wide_tiling(int kind, int rows, int n_units, int k, int n_cu, int* row_tiles, int* panels,
-                               int* k_splits);
 
 /* Read and clear the device error word.  Synchronises the stream. */
 spade_status spade_get_device_error(spade_model m, uint32_t* h_flags, void* stream);

@@ -6,9 +6,10 @@ The edge side runs a draft model autoregressively: one draft token is one
 the argmax, or the Gumbel-max draw keyed by a uniform), followed by
 ``spade_softmax`` for the distribution q the token was drawn from (sampling)
 and a commit.  The cloud side is one ``spade_verify`` over the pending token
-and the gamma drafts.  After each call both caches keep the accepted prefix
-and the correction (Algorithm 1: m <- m + k + 1); when every draft was
-accepted the draft model first runs its last draft, which it never appended.
+and the gamma drafts, followed by ``spade_kv_commit`` (Algorithm 1: m <- m +
+k + 1, on the device).  The draft's cache is then cut back to the same
+accepted prefix plus the correction; when every draft was accepted the draft
+model first runs its last draft, which it never appended.
 
 Uniforms are consumed in a fixed order -- one per draft step, then gamma + 1
 per cloud call -- from a device array, so a CPU run of the same loop
@@ -103,10 +104,10 @@ def run_algorithm1(target: spade.Model, draft: spade.Model, prompt, gamma: int, 
         t.call(gamma, drafts, q if mode == SAMPLE else None, uni[pos:pos + gamma + 1], temperature)
         pos += gamma + 1
         calls += 1
+        t.kv.commit(t.n, t.corr)  # m <- m + k + 1 on the device
         n = int(t.n.item())
         corr = int(t.corr.item())
         new_len = start + n + 1
-        t.kv.set_state(np.array([new_len], np.int32), np.array([corr], np.int32))
         if n == gamma and gamma > 0:  # the draft never appended d_gamma: run it now
             d.call(0, None, None, half, temperature)
         d.kv.set_state(np.array([new_len], np.int32), np.array([corr], np.int32))

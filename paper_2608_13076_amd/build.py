@@ -16,7 +16,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspade.so")
-SOURCES = ["kernels.hip", "verify_fused.hip", "api.cpp"]
+SOURCES = ["kernels.hip", "api.cpp"]
 ARCH = os.environ.get("SPADE_OFFLOAD_ARCH", "gfx950")
 
 

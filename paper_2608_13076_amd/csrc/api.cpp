@@ -33,6 +33,16 @@ spade_status hipfail(hipError_t e, const char* what) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Set the host bound of lens[0..B) to the device values (synchronises).
+spade_status refresh_bound(spade_kv kv, int B, hipStream_t st) {
+  std::vector<int32_t> h(B);
+  hipError_t e = hipMemcpyAsync(h.data(), kv->lens, (size_t)B * 4, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hipfail(e, "reading lens");
+  for (int b = 0; b < B; ++b) kv->lens_ub[b] = std::max(0, (int)h[b]);
+  return SPADE_OK;
+}
+
 spade_status check_config(const spade_config* c) {
   if (!c) return fail(SPADE_EINVAL, "null config");
   if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->head_dim < 1 || c->d_ffn < 1 || c->vocab < 2)
@@ -90,11 +100,9 @@ ArenaLayout layout_of(const Dims& D) {
 }
 
 struct WsPlan {
-  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, bar, fused, split_cnt,
+  size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, split_cnt,
       split_part, wide_cnt, wide_part, corr_lse, corr_part, corr_cnt, prefill_tok, prefill_cnt, total;
   size_t wide_items, wide_floats;
-  FusedArena fa;
-  bool has_fused;
   int max_units;
   size_t act_split, actf_split;
   int Mmax, NCmax, Rmax;
@@ -130,7 +138,6 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.stats = take((size_t)p.Mmax * std::max(NU, kMaxStatGroups) * 3 * 4);  // NU = panels of the LM head
   p.rope = take((size_t)max_len * (D.hd / 2) * 2 * 4);
   p.err = take(4);
-  p.bar = take(kBarBytes);
   p.max_units = std::max(std::max(D.d + 2 * D.dkv, 2 * D.F), D.Vpad) / 16;
   p.split_cnt = take((size_t)p.max_units * 4);
   p.split_part = take((size_t)p.max_units * 8 * 256 * 4);
@@ -151,12 +158,6 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.corr_cnt = take((size_t)max_batch * 4);
   p.prefill_tok = take((size_t)p.Mmax * 4);
   p.prefill_cnt = take((size_t)max_batch * 4);
-  // the single-launch pass handles bf16 weights and cache with head_dim 128
-  p.has_fused = wb && D.kvdt == SPADE_BF16 && D.hd == 128;
-  if (p.has_fused) {
-    p.fa = fused_arena_of(D.L, D.d, D.F);
-    p.fused = take(p.fa.total);
-  }
   p.total = off;
   return p;
 }
@@ -216,7 +217,6 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->wide_p = 0;
   m->wide_ks = 0;
   m->split_ks = 0;
-  m->attn_cpw = 0;
   m->attn_merge = 0;
   m->corr_split = 0;
   m->attn_grouped = 0;
@@ -224,14 +224,6 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
   }
-  // the single-launch verify pass needs cooperative launches (all workgroups
-  // resident); it is off by default (the per-stage path is faster at the
-  // measured shapes), SPADE_FUSED=1 or spade_model_set_fused turns it on
-  int coop = 0;
-  (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, m->device);
-  m->fused_ok = false;
-  if (const char* ev = std::getenv("SPADE_FUSED"))
-    if (std::atoi(ev) != 0 && coop != 0) m->fused_ok = true;
   const WsPlan p = plan_ws(m->dims, max_batch, max_gamma, max_len);
   Workspace& w = m->ws;
   uint8_t* b = m->work;
@@ -259,9 +251,6 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.stats = (float*)(b + p.stats);
   w.rope = (float*)(b + p.rope);
   w.err = (uint32_t*)(b + p.err);
-  w.bar = (uint32_t*)(b + p.bar);
-  w.fused = p.has_fused ? b + p.fused : nullptr;
-  w.fa = p.fa;
   w.act_split = p.act_split;
   w.actf_split = p.actf_split;
   w.Mmax = p.Mmax;
@@ -284,7 +273,6 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   if (e == hipSuccess && p.wide_items > 0) e = hipMemset(w.wide_cnt, 0, p.wide_items * 4);
   if (e == hipSuccess) e = hipMemset(w.corr_cnt, 0, (size_t)max_batch * 4);
   if (e == hipSuccess) e = hipMemset(w.err, 0, 4);
-  if (e == hipSuccess) e = hipMemset(w.bar, 0, kBarBytes);
   // activation buffers start at zero so rows past M never feed NaNs
   if (e == hipSuccess) e = hipMemset(b, 0, p.ssq);
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -327,6 +315,8 @@ spade_status spade_kv_create(spade_model m, void* d_kv, int max_batch, int max_l
   kv->stride = kv_stride_of(max_len);
   kv->lens_ub = new (std::nothrow) int[max_batch]();
   kv->last_rows = m->max_gamma + 1;
+  kv->last_B = 0;
+  kv->verified = false;
   kv->snap_ub = new (std::nothrow) int[max_batch]();
   if (!kv->lens_ub || !kv->snap_ub) {
     delete[] kv->lens_ub;
@@ -358,6 +348,7 @@ spade_status spade_kv_set_state(spade_kv kv, int B, const int32_t* h_lens, const
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hipfail(e, "kv_set_state");
   for (int b = 0; b < B; ++b) kv->lens_ub[b] = h_lens[b];
+  kv->verified = false;
   return SPADE_OK;
 }
 
@@ -390,6 +381,7 @@ spade_status spade_kv_restore(spade_kv kv, int B, const int32_t* d_lens, const i
   hipError_t e = launch_copy_state(B, kv->lens, kv->pending, d_lens, d_pending, st);
   if (e != hipSuccess) return hipfail(e, "kv_restore");
   for (int b = 0; b < B; ++b) kv->lens_ub[b] = kv->snap_ub[b];
+  kv->verified = false;
   return SPADE_OK;
 }
 
@@ -416,6 +408,7 @@ spade_status spade_prefill(spade_model m, spade_kv kv, int b, const int32_t* d_t
   }
   hipError_t e = launch_advance(kv, b, 0, d_tokens + n_cache, st);
   if (e != hipSuccess) return hipfail(e, "prefill");
+  kv->verified = false;
   return SPADE_OK;
 }
 
@@ -431,12 +424,24 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
   if (d_draft_probs && !d_uniforms) return fail(SPADE_EINVAL, "sampling needs uniforms");
   if (!(temperature > 0.f && std::isfinite(temperature)))
     return fail(SPADE_EINVAL, "temperature must be finite and > 0");
-  for (int b = 0; b < B; ++b)
-    if (kv->lens_ub[b] + gamma + 1 > kv->max_len)
-      return fail(SPADE_ECAPACITY, "request %d: %d cached + %d rows exceed max_len %d", b, kv->lens_ub[b],
-                  gamma + 1, kv->max_len);
   hipStream_t st = (hipStream_t)stream;
+  bool refreshed = false;
+  for (int b = 0; b < B; ++b)
+    if (kv->lens_ub[b] + gamma + 1 > kv->max_len) {
+      // the host bound grows by gamma + 1 per commit while the lengths grow
+      // by k + 1: read the device lengths once before giving up
+      if (!refreshed) {
+        spade_status rs = refresh_bound(kv, B, st);
+        if (rs != SPADE_OK) return rs;
+        refreshed = true;
+      }
+      if (kv->lens_ub[b] + gamma + 1 > kv->max_len)
+        return fail(SPADE_ECAPACITY, "request %d: %d cached + %d rows exceed max_len %d", b, kv->lens_ub[b],
+                    gamma + 1, kv->max_len);
+    }
   kv->last_rows = gamma + 1;
+  kv->last_B = B;
+  kv->verified = true;
   ForwardCall fc{};
   fc.b0 = 0;
   fc.nb = B;
@@ -453,7 +458,7 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
   ac.V = m->dims.V;
   ac.logits = fc.logits_out;
   ac.stats = m->ws.stats;
-  ac.NU = std::min(m->dims.Vpad / 16, m->gemm_wgs);  // LM-head workgroups (fused: n_cu, set there)
+  ac.NU = std::min(m->dims.Vpad / 16, m->gemm_wgs);  // LM-head workgroups
   ac.panels = lm_stats_panels(m, B * (gamma + 1));
   ac.drafts = d_draft_tokens;
   ac.q = d_draft_probs;
@@ -462,27 +467,9 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma, const in
   ac.inv_T = fc.inv_T;
   ac.n_out = d_n_accepted;
   ac.corr_out = d_correction;
-  hipError_t e;
-  if (fused_eligible(m, kv, fc)) {
-    e = launch_verify_fused(m, kv, fc, ac, st);
-  } else {
-    e = launch_forward(m, kv, fc, st);
-    if (e == hipSuccess) e = launch_accept(m, ac, st);
-  }
+  hipError_t e = launch_forward(m, kv, fc, st);
+  if (e == hipSuccess) e = launch_accept(m, ac, st);
   if (e != hipSuccess) return hipfail(e, "verify");
-  return SPADE_OK;
-}
-
-spade_status spade_model_set_fused(spade_model m, int enable) {
-  if (!m) return fail(SPADE_EINVAL, "null model");
-  if (!enable) {
-    m->fused_ok = false;
-    return SPADE_OK;
-  }
-  int coop = 0;
-  if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, m->device) != hipSuccess || !coop)
-    return fail(SPADE_EUNSUPPORTED, "device has no cooperative launch");
-  m->fused_ok = true;
   return SPADE_OK;
 }
 
@@ -516,13 +503,6 @@ spade_status spade_model_set_correction_slices(spade_model m, int mode) {
   return SPADE_OK;
 }
 
-spade_status spade_model_set_attn_chunks(spade_model m, int chunks) {
-  if (!m) return fail(SPADE_EINVAL, "null model");
-  if (chunks < 0 || chunks > kAttnMaxChunks) return fail(SPADE_EINVAL, "chunks must be in [0, %d]", kAttnMaxChunks);
-  m->attn_cpw = chunks;
-  return SPADE_OK;
-}
-
 spade_status spade_model_set_wide_k_splits(spade_model m, int splits) {
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (splits != 0 && splits != 1 && splits != 2 && splits != 4) return fail(SPADE_EINVAL, "splits must be 0, 1, 2 or 4");
@@ -546,6 +526,7 @@ spade_status spade_prefill_batch(spade_model m, spade_kv kv, int B, const int32_
   }
   hipError_t e = launch_prefill_batch(m, kv, B, d_tokens, ld, n_cache.data(), (hipStream_t)stream);
   if (e != hipSuccess) return hipfail(e, "prefill_batch");
+  kv->verified = false;
   return SPADE_OK;
 }
 
@@ -570,11 +551,14 @@ spade_status spade_model_set_split_k(spade_model m, int splits) {
 spade_status spade_kv_commit(spade_kv kv, int B, const int32_t* d_n_accepted, const int32_t* d_correction,
                              void* stream) {
   if (!kv || !d_n_accepted || !d_correction) return fail(SPADE_EINVAL, "null pointer");
-  if (B < 1 || B > kv->max_batch) return fail(SPADE_ECAPACITY, "B out of range");
-  hipError_t e = launch_commit(kv, B, d_n_accepted, d_correction, (hipStream_t)stream);
+  if (!kv->verified) return fail(SPADE_EINVAL, "kv_commit needs a spade_verify on this cache since the last commit");
+  if (B < 1 || B > kv->last_B) return fail(SPADE_EINVAL, "B=%d: the last spade_verify covered %d requests", B, kv->last_B);
+  // the kernel clamps each k to [0, gamma] of that call, so the lengths grow
+  // by at most gamma + 1
+  hipError_t e = launch_commit(kv, B, kv->last_rows, d_n_accepted, d_correction, (hipStream_t)stream);
   if (e != hipSuccess) return hipfail(e, "kv_commit");
-  // n_accepted <= max_gamma, so the bound grows by at most max_gamma + 1
   for (int b = 0; b < B; ++b) kv->lens_ub[b] += kv->last_rows;
+  kv->verified = false;
   return SPADE_OK;
 }
 

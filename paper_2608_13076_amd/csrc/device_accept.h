@@ -1,8 +1,8 @@
 // Accept / reject and the correction draw for one request (Sec. III-C;
 // Algorithm 1, the verify / accept / sample / correct steps), run by one
-// workgroup of NT threads.  Shared by the stand-alone accept kernel and the
-// persistent verify kernel (COH: logits and LM-head statistics were written
-// by other workgroups of the same launch and are read with sc1 loads).
+// workgroup of NT threads (COH: logits and LM-head statistics are read with
+// sc1 loads, for a caller whose other workgroups wrote them in the same
+// launch).
 #pragma once
 
 #include "device_util.h"

@@ -1,7 +1,6 @@
 // Verify attention for a bf16 cache with head_dim 128 (Sec. III-A: the
 // gamma+1 appended rows of a request attend causally to its cached keys and
-// to each other), shared by the per-stage kernels and the persistent verify
-// kernel.
+// to each other).
 //
 // Work item: (request, head, chunk of CK keys), one 8-wave workgroup.  Row i
 // of the request sits at position L + i and sees keys <= L + i.  Scores
@@ -68,62 +67,6 @@ __device__ __forceinline__ AttnItem attn_item(bool valid, int bl, int h, int c, 
   it.kc = (const uint16_t*)kc + head_off;
   it.vc = (const uint16_t*)vc + head_off;
   return it;
-}
-
-template <int CK>
-__device__ __forceinline__ void attn_zero_regs(AttnRegs<CK>& r) {
-#pragma unroll
-  for (int grp = 0; grp < CK / 128; ++grp)
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) r.kf[grp][ks] = make_uint4(0, 0, 0, 0);
-#pragma unroll
-  for (int ks = 0; ks < CK / 32; ++ks) r.vf[ks] = make_uint4(0, 0, 0, 0);
-}
-
-// Keys of this lane in [kb, ke) (plain loads).  V^T vectors load whole when
-// all their 8 keys are in [kb, ke); K rows at or past k_hi are not read.
-template <int CK>
-__device__ __forceinline__ void attn_load_plain(const AttnItem& it, int stride, int kb, int ke, int wave, int lane,
-                                                AttnRegs<CK>& r) {
-  const int g = lane >> 4, kl = lane & 15;
-#pragma unroll
-  for (int grp = 0; grp < CK / 128; ++grp) {
-    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
-    if (key >= kb && key < ke && key < it.k_hi) {
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) r.kf[grp][ks] = *(const uint4*)(it.kc + (size_t)key * kAttnHd + 32 * ks + 8 * g);
-    }
-  }
-  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
-#pragma unroll
-  for (int ks = 0; ks < CK / 32; ++ks) {
-    const int kv0 = it.k_lo + 32 * ks + 8 * g;
-    if (kv0 >= kb && kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
-  }
-}
-
-// The keys this verify call appended, [L, k_hi), written earlier in the same
-// launch by other workgroups: sc1 loads (rk, rv: resources over this (request,
-// head)'s K and V^T rows).  A V^T vector holding any such key loads whole.
-template <int CK>
-__device__ __forceinline__ void attn_load_new(const AttnItem& it, Rsrc rk, Rsrc rv, int stride, int wave, int lane,
-                                              AttnRegs<CK>& r) {
-  const int g = lane >> 4, kl = lane & 15;
-#pragma unroll
-  for (int grp = 0; grp < CK / 128; ++grp) {
-    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
-    if (key >= it.L && key < it.k_hi) {
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        r.kf[grp][ks] = ld_b128<true>(rk, (uint32_t)(key * kAttnHd + 32 * ks + 8 * g) * 2u);
-    }
-  }
-#pragma unroll
-  for (int ks = 0; ks < CK / 32; ++ks) {
-    const int kv0 = it.k_lo + 32 * ks + 8 * g;
-    if (kv0 + 8 > it.L && kv0 < it.k_hi)
-      r.vf[ks] = ld_b128<true>(rv, (uint32_t)((16 * wave + kl) * stride + kv0) * 2u);
-  }
 }
 
 // Zero the V^T entries of keys at or past k_hi (their P is zero, but the
@@ -205,144 +148,17 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v + dpp_f32<0x140>(v);
 }
 
-// This lane's query slices of the request's rotated queries for this head
-// (q: row 0, rows q_stride floats apart): row kl, features 32 ks + 8 g .. + 8
-// for ks = 0..3 (rows >= R and inactive items: zeros).  Issued before the
-// K/V loads, so the wait for them does not wait for the cache rows.
-__device__ __forceinline__ void attn_load_q(const AttnItem& it, const float* q, int q_stride, int R, int lane,
-                                            float4 (&qr)[8]) {
-  const int g = lane >> 4, kl = lane & 15;
-  const bool ok = it.active && kl < R;
-  const Rsrc rq = wave_rsrc(q);  // wave-uniform base, per-lane offsets
-  const uint32_t base = (uint32_t)(kl * q_stride + 8 * g) * 4u;
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    qr[2 * ks] = __builtin_bit_cast(float4, ld_b128<false>(rq, ok ? base + (uint32_t)(32 * ks) * 4u : kOob));
-    qr[2 * ks + 1] = __builtin_bit_cast(float4, ld_b128<false>(rq, ok ? base + (uint32_t)(32 * ks + 4) * 4u : kOob));
-  }
-}
-
-// Workgroup barrier.  LDSBAR: orders LDS accesses only, so loads and stores
-// to global memory stay in flight across it (a full __syncthreads waits for
-// pending global stores, and so for every older load as well).
-template <bool LDSBAR>
-__device__ __forceinline__ void attn_bar() {
-  if constexpr (LDSBAR) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-  } else {
-    __syncthreads();
-  }
-}
-
-// One chunk with K/V fragments in r and query slices in qr (attn_load_q).
-// Returns this lane's unnormalised chunk outputs: rows 4g + i (i = 0..3),
-// feature 16 wave + kl.  Threads tid < R also set sm.m[tid] / sm.l[tid], the
-// row max / sum (for a row that sees no key of the chunk -inf / 0).  All 512
-// threads call it (it synchronises).
+// One chunk of the verify attention: the K fragments come from attn_load_k,
+// the queries from LDS (sqh / sql, their bf16 terms staged by the caller with
+// attn_stage_q: row i, feature f at [i][f], rows past R zero), and the V^T
+// fragments are requested only after the score products, into the registers
+// the K fragments held, so a wave holds one of the two at a time.
 //
 // Chunk softmax: each lane holds the scores of rows 4g..4g+3 for its keys;
 // row maxima and sums reduce over the 16 lanes of a row (DPP) and then over
 // the eight waves (LDS, in wave order).  Probabilities (exp2 of the
 // log2(e)-scaled difference) go to LDS once, as two bf16 terms, and every
 // wave reads them as the A operand of O = P V.
-template <int CK, bool LDSBAR = false>
-__device__ __forceinline__ floatx4 attn_chunk(const AttnItem& it, const float4 (&qr)[8], int R, float scale,
-                                              const AttnRegs<CK>& r, AttnSmem<CK>& sm) {
-  constexpr int NG = CK / 128;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int g = lane >> 4, kl = lane & 15;
-  uint4 qh[4], ql[4];
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const float4 x0 = qr[2 * ks], x1 = qr[2 * ks + 1];
-    const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-    attn_split2(xs, qh[ks], ql[ks]);
-  }
-  // S = Q K^T; D[i][j] sits in lane j + 16*(i/4), register i%4: rows 4g..4g+3 of key kl
-  float sv[NG][4];
-#pragma unroll
-  for (int grp = 0; grp < NG; ++grp) {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql[ks]),
-                                                    __builtin_bit_cast(bf16x8, r.kf[grp][ks]), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh[ks]),
-                                                    __builtin_bit_cast(bf16x8, r.kf[grp][ks]), acc, 0, 0, 0);
-    }
-    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = 4 * g + i;
-      sv[grp][i] = (key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
-    }
-  }
-  // row maxima: over the wave's keys, then over the waves
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float mx = sv[0][i];
-#pragma unroll
-    for (int grp = 1; grp < NG; ++grp) mx = fmaxf(mx, sv[grp][i]);
-    mx = row16_max(mx);
-    if (kl == 0) sm.pm[4 * g + i][wave] = mx;
-  }
-  attn_bar<LDSBAR>();
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 4 * g + i;
-    const float4 a = *(const float4*)&sm.pm[row][0];
-    const float4 b = *(const float4*)&sm.pm[row][4];
-    const float M = fmaxf(fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)), fmaxf(fmaxf(b.x, b.y), fmaxf(b.z, b.w)));
-    float sum = 0.f;
-#pragma unroll
-    for (int grp = 0; grp < NG; ++grp) {
-      // masked keys: exp2(-inf) = 0
-      const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[grp][i] - M) * 1.44269504088896341f);
-      sum += e;
-      const uint16_t h = f2bf_num(e);
-      const int kc = (CK / 8) * wave + 16 * grp + kl;
-      sm.ph[row][kc] = h;
-      sm.pl[row][kc] = f2bf_num(e - bf2f(h));
-    }
-    sum = row16_sum(sum);
-    if (kl == 0) sm.ps[row][wave] = sum;
-  }
-  attn_bar<LDSBAR>();
-  if (tid < R) {
-    float l = 0.f, M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < 8; ++w) {
-      l += sm.ps[tid][w];
-      M = fmaxf(M, sm.pm[tid][w]);
-    }
-    sm.m[tid] = M;
-    sm.l[tid] = l;
-  }
-  // O = P V for features 16 wave .. 16 wave + 15, key steps in order
-  floatx4 o = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < CK / 32; ++ks) {
-    const uint4 ph = *(const uint4*)&sm.ph[kl][32 * ks + 8 * g];
-    const uint4 pl = *(const uint4*)&sm.pl[kl][32 * ks + 8 * g];
-    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
-                                                0, 0, 0);
-    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
-                                                0, 0, 0);
-  }
-  return o;
-}
-
-// Low-register variant of attn_chunk for launches with many chunks per
-// compute unit: the K fragments come from attn_load_k, the queries from LDS
-// (sqh / sql, their bf16 terms staged by the caller with attn_stage_q: row i,
-// feature f at [i][f], rows past R zero),
-// and the V^T fragments are requested only after the score products, into the
-// registers the K fragments held, so a wave holds one of the two at a time.
-// Scores, softmax, P V and the returned partial are computed by the same
-// instructions in the same order as attn_chunk with attn_load_plain's
-// fragments.
 template <int CK>
 __device__ __forceinline__ void attn_load_k(const AttnItem& it, int wave, int lane, uint4 (&kf)[CK / 128][4]) {
   const int g = lane >> 4, kl = lane & 15;
@@ -502,7 +318,7 @@ __device__ __forceinline__ void attn_merge_pair(Rsrc rpo, const AttnMergeSmem& m
   if (ob < nout) out(ob, Ob);
 }
 
-// Publish this chunk's partial (o: attn_chunk's result) with write-through
+// Publish this chunk's partial (o: the chunk function's result) with write-through
 // stores, arrive on the counter of its (request, head) once the stores have
 // landed, and, in the workgroup that arrives last, merge the request's
 // chunks and pass each merged output o = row * kAttnHd + dd to out(o, value).
@@ -511,7 +327,7 @@ __device__ __forceinline__ void attn_merge_pair(Rsrc rpo, const AttnMergeSmem& m
 // resets the counter.  part_o / part_ml: [bh][NC][Rmax][kAttnHd] /
 // [bh][NC][Rmax][2].  All 512 threads call it; inactive items only
 // synchronise.
-// Store this chunk's partial (o: attn_chunk's result; m / l from sa) with
+// Store this chunk's partial (o: the chunk function's result; m / l from sa) with
 // write-through stores, without waiting for them.
 template <int CK>
 __device__ __forceinline__ void attn_publish(const AttnItem& it, floatx4 o, const AttnSmem<CK>& sa, float* part_o,
@@ -604,11 +420,10 @@ __device__ __forceinline__ void attn_merge(size_t bh, int nc, AttnMergeSmem& ms,
 // with n_mine, and, in the workgroup whose arrival completes the request's
 // chunks, merge them and pass each merged output o = row * kAttnHd + dd to
 // out(o, value).  The completing arrival resets the counter.  All 512 threads
-// call it.  COH: read the partials with sc1 loads (the single-launch pass,
-// where an earlier stage of the same launch may have cached their lines); a
-// per-stage launch reads them with plain loads (no workgroup of the launch
-// reads a partial before its write-through store has landed, and the launch
-// starts with the L2 invalidated).
+// call it.  COH: read the partials with sc1 loads; without it they are read
+// with plain loads, which is enough within one launch (no workgroup of the
+// launch reads a partial before its write-through store has landed, and the
+// launch starts with the L2 invalidated).
 template <bool COH = true, class Out>
 __device__ __forceinline__ void attn_arrive_merge(const AttnItem& it, int n_mine, AttnMergeSmem& ms, float* part_o,
                                                   float* part_ml, uint32_t* attn_cnt, int H, int NC, int Rmax, int R,

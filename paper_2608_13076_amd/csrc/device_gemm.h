@@ -1,5 +1,4 @@
-// Skinny GEMM engine with fused epilogues, shared by the per-stage kernels
-// and the persistent verify kernel.
+// Skinny GEMM engine with fused epilogues.
 //
 // The arena stores a weight matrix as panels of 16 rows, each panel as its
 // k-blocks (256 k for bf16, 128 for f32) of 8 KB.  Slice j of a k-block holds

@@ -26,7 +26,6 @@
 //   attn_merge_kernel  a second launch (several rounds of chunk workgroups)
 //   attn_g_kernel  grouped-query models: a chunk for all query heads of a
 //                  K/V head in one workgroup (merged by attn_merge_kernel)
-//   attn_bp_kernel runs of several chunks per workgroup (selectable)
 //   attn_kernel / attn_combine_kernel  f32 cache or other head sizes:
 //                  128-key chunks, then the chunk-order merge
 //   accept_kernel  per request: vocabulary-wide max / log-sum-exp / argmax
@@ -85,12 +84,25 @@ struct EmbedParams {
   size_t act_split;
   float* ssq;
   uint32_t* err;
+  int32_t* lens;   // global [Bmax] cached lengths
+  int len_limit;   // lens[b] + R may not exceed this (cache capacity, attention coverage)
 };
 
 template <bool WBF16>
 __global__ void __launch_bounds__(256) embed_kernel(EmbedParams p) {
   const int m = blockIdx.x;
   const int bl = m / p.R, i = m % p.R;
+  // A length the host could not bound (lens written outside the library's
+  // calls): clamp it so every later kernel of the call stays inside the cache
+  // and the attention's chunk grid, and flag the call.  The later kernels run
+  // after this one on the same stream.
+  if (i == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    const int L = p.lens[p.b0 + bl];
+    if (L < 0 || L > p.len_limit - p.R) {
+      flag_error(p.err, SPADE_DERR_CAPACITY);
+      p.lens[p.b0 + bl] = L < 0 ? 0 : p.len_limit - p.R;
+    }
+  }
   int t;
   if (p.tokens) t = p.tokens[m];
   else t = (i == 0) ? p.pending[p.b0 + bl] : p.drafts[bl * (p.R - 1) + i - 1];
@@ -99,7 +111,7 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedParams p) {
     t = t < 0 ? 0 : p.V - 1;
   }
   // one column per thread; the sixteen lanes of a panel sum x^2 in a fixed
-  // butterfly order (the same order as the single-launch pass)
+  // butterfly order
   const int npan = p.d / 16;
   for (int n0 = (int)(blockIdx.y * blockDim.x); n0 < p.d; n0 += (int)(blockDim.x * gridDim.y)) {
     const int n = n0 + (int)threadIdx.x;
@@ -709,68 +721,6 @@ __global__ void __launch_bounds__(kAttnThreads) attn_merge_kernel(AttnParams p) 
   });
 }
 
-// The same over runs of chunks: the workgroup of run r of (request b, head h)
-// (attn_work) computes chunks [r cpw, min((r + 1) cpw, nc_b)) in order, requesting the
-// K/V of the next chunk before it computes the current one, so its loads stay
-// in flight through the chunk's products, softmax and partial stores (the
-// barriers inside order LDS only).  Each chunk's partial and the merge are
-// exactly those of the one-chunk kernel; the workgroup arrives once with the
-// number of chunks it published.
-template <bool ABF16, int CK>
-__device__ __forceinline__ void attn_run_chunk(const AttnParams& p, const AttnItem& it0, int c, int c1,
-                                               const float4 (&qr)[8], AttnRegs<CK>& cur, AttnRegs<CK>& nxt,
-                                               AttnSmem<CK>& sm) {
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  // chunk c's K/V (and the previous chunk's stores) have landed; every wave
-  // is done with the previous chunk's LDS
-  __builtin_amdgcn_s_waitcnt(0);
-  attn_bar<true>();
-  AttnItem it = it0;
-  it.c = c;
-  it.k_lo = c * CK;
-  it.k_hi = min(it.k_lo + CK, it0.L + p.R);
-  if (c + 1 < c1) {
-    AttnItem in = it0;
-    in.c = c + 1;
-    in.k_lo = (c + 1) * CK;
-    in.k_hi = min(in.k_lo + CK, it0.L + p.R);
-    attn_zero_regs(nxt);
-    attn_load_plain(in, p.kv_stride, in.k_lo, (in.k_hi + 7) & ~7, wave, lane, nxt);
-  }
-  attn_mask_tail(it, lane, cur);
-  const floatx4 o = attn_chunk<CK, true>(it, qr, p.R, p.scale, cur, sm);
-  attn_publish<CK>(it, o, sm, p.part_o, p.part_ml, p.H, p.NC, p.Rmax, p.R);
-}
-
-template <bool ABF16, int CK>
-__global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
-attn_bp_kernel(AttnParams p, int cpw) {
-  __shared__ AttnSmem<CK> sm;
-  __shared__ AttnMergeSmem ms;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const AttnWork wk = attn_work((int)blockIdx.x, (p.NC + cpw - 1) / cpw, p.Hkv, p.G, p.nb);
-  if (!wk.ok) return;
-  const int bl = wk.bl, h = wk.h, bg = p.b0 + bl;
-  const int c0 = wk.r * cpw;
-  const AttnItem it0 = attn_item<CK>(true, bl, h, c0, p.lens[bg], p.R, p.kc, p.vc,
-                                     ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * kAttnHd);
-  if (!it0.active) return;  // past the request's last key: uniform, before any barrier
-  const int c1 = min(c0 + cpw, it0.nc);
-  float4 qr[8];
-  attn_load_q(it0, p.q + (size_t)(bl * p.R) * p.d + h * kAttnHd, p.d, p.R, lane, qr);
-  AttnRegs<CK> ra, rb;
-  attn_zero_regs(ra);
-  attn_load_plain(it0, p.kv_stride, it0.k_lo, (it0.k_hi + 7) & ~7, wave, lane, ra);
-  for (int c = c0; c < c1; c += 2) {
-    attn_run_chunk<ABF16, CK>(p, it0, c, c1, qr, ra, rb, sm);
-    if (c + 1 < c1) attn_run_chunk<ABF16, CK>(p, it0, c + 1, c1, qr, rb, ra, sm);
-  }
-  attn_arrive_merge<false>(it0, c1 - c0, ms, p.part_o, p.part_ml, p.cnt, p.H, p.NC, p.Rmax, p.R, [&](int oi, float O) {
-    const int row = oi / kAttnHd, dd = oi - row * kAttnHd;
-    store_act<ABF16>(p.act_out, p.act_split, (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
-  });
-}
-
 // ---------------------------------------------------------------------------
 // Accept / reject and the correction draw (device_accept.h), one workgroup per
 // request.
@@ -829,10 +779,19 @@ __global__ void __launch_bounds__(256) softmax_rows_kernel(const float* logits, 
 // ---------------------------------------------------------------------------
 // Small kernels: commit, lens advance, packing.
 // ---------------------------------------------------------------------------
-__global__ void commit_kernel(int B, int32_t* lens, int32_t* pending, const int32_t* n, const int32_t* corr) {
+// Context update m <- m + k + 1 with k clamped to the rows of the last verify
+// call (k in [0, R - 1]); a k outside that range (a buffer the verify call did
+// not write) is flagged.
+__global__ void commit_kernel(int B, int R, int32_t* lens, int32_t* pending, const int32_t* n, const int32_t* corr,
+                              uint32_t* err) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b < B) {
-    lens[b] += n[b] + 1;
+    int k = n[b];
+    if (k < 0 || k > R - 1) {
+      flag_error(err, SPADE_DERR_COMMIT);
+      k = k < 0 ? 0 : R - 1;
+    }
+    lens[b] += k + 1;
     pending[b] = corr[b];
   }
 }
@@ -1331,11 +1290,7 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   ep.act_split = W.act_split;
   ep.ssq = W.ssq;
   ep.err = W.err;
-  // one workgroup per (row, 256 columns)
-  const dim3 egrid(M, (D.d + 255) / 256);
-  if (wb) hipLaunchKernelGGL(embed_kernel<true>, egrid, dim3(256), 0, st, ep);
-  else hipLaunchKernelGGL(embed_kernel<false>, egrid, dim3(256), 0, st, ep);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  ep.lens = kv->lens;
 
   const size_t kv_layer = (size_t)kv->max_batch * D.KVH * kv->stride * D.hd;  // elements
   const size_t kv_elt = D.kvdt == SPADE_BF16 ? 2 : 4;
@@ -1348,11 +1303,13 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   const int CK = mfma_attn ? kAttnChunkKeys : kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
-  // chunks per workgroup of the bf16 attention: fixed (> 0), else one (the
-  // low-register one-chunk kernel with the merge below beat runs of chunks
-  // at every measured shape: C4 13.53 vs 14.2-18.0 ms, 8B-GQA batched 13.67
-  // vs 14.73)
-  const int cpw = md->attn_cpw > 0 ? md->attn_cpw : 1;
+  // every request's keys must fit the cache and the chunks launched below
+  ep.len_limit = std::min(kv->max_len, NC * CK);
+  // one workgroup per (row, 256 columns)
+  const dim3 egrid(M, (D.d + 255) / 256);
+  if (wb) hipLaunchKernelGGL(embed_kernel<true>, egrid, dim3(256), 0, st, ep);
+  else hipLaunchKernelGGL(embed_kernel<false>, egrid, dim3(256), 0, st, ep);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   // one chunk per workgroup: merge by the last chunk to arrive, or, when the
   // call has at least four chunks per compute unit (several rounds of chunk
   // workgroups), in a second launch (measured: C4 12.78 -> 12.25 ms, C5
@@ -1392,12 +1349,7 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     const dim3 agrid(NC, D.H, fc.nb);
     const bool kvb = D.kvdt == SPADE_BF16;
     ap.nb = fc.nb;
-    if (mfma_attn && cpw > 1) {
-      const dim3 rgrid(attn_grid((NC + cpw - 1) / cpw, D.KVH, D.H / D.KVH, fc.nb));
-      if (wb) hipLaunchKernelGGL((attn_bp_kernel<true, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
-      else hipLaunchKernelGGL((attn_bp_kernel<false, kAttnChunkKeys>), rgrid, dim3(kAttnThreads), 0, st, ap, cpw);
-      e = hipGetLastError();
-    } else if (mfma_attn && two_pass) {
+    if (mfma_attn && two_pass) {
       // grouped-query models: one workgroup per K/V head and chunk for the
       // G query heads when their G R rows fit three 16-row tiles (8B-GQA
       // batched: 13.42 -> 13.09 ms)
@@ -1537,8 +1489,9 @@ hipError_t launch_softmax(const float* logits, int rows, int V, float invT, floa
   return hipGetLastError();
 }
 
-hipError_t launch_commit(spade_kv kv, int B, const int32_t* n, const int32_t* corr, hipStream_t st) {
-  hipLaunchKernelGGL(commit_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, kv->lens, kv->pending, n, corr);
+hipError_t launch_commit(spade_kv kv, int B, int R, const int32_t* n, const int32_t* corr, hipStream_t st) {
+  hipLaunchKernelGGL(commit_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, R, kv->lens, kv->pending, n, corr,
+                     kv->model->ws.err);
   return hipGetLastError();
 }
 

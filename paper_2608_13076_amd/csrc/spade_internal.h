@@ -21,8 +21,6 @@ constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
 constexpr int kAttnChunk = 128;      // keys per workgroup of the generic attention (f32 cache or head_dim != 128)
 constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
 constexpr int kMaxLen = kAttnChunk * kAttnMaxChunks;
-constexpr uint32_t kFusedLdsBytes = 159 * 1024;  // dynamic LDS of the single-launch verify kernel
-constexpr size_t kBarBytes = 4096;               // its grid-barrier words
 constexpr int kMaxStatGroups = 2048;             // LM-head statistics entries per row (workgroups)
 inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
 
@@ -67,47 +65,6 @@ __host__ __device__ inline int panel_row(int kind, int p, int r, int d_model, in
   return p * 16 + r;
 }
 
-// Activation arena of the single-launch verify pass.  Every buffer one stage
-// writes and a later stage of the same launch reads has its own region per
-// layer (and one for the embedding), so no L2 holds a line of it before it is
-// written: readers use plain cached loads, writers write-through stores.
-constexpr int kFusedRows = 16;  // rows (requests x (gamma + 1)) of the single-launch pass
-struct FusedArena {
-  // per-layer block: rotated q; attention output (O operand); O output (gate/up
-  // operand) and its RMS partials; SwiGLU output (down operand); down output
-  // (next QKV / LM operand) and its RMS partials.  Split operands hold two
-  // bf16 terms, split s at element s * kFusedRows * K.
-  size_t q, act_o, act_no, ssq_o, act_f, act_nd, ssq_d, layer_bytes;
-  size_t e_act, e_ssq;  // embedding output, after the layer blocks
-  size_t total;
-};
-
-inline size_t fused_align(size_t x) { return (x + 255) & ~(size_t)255; }
-
-inline FusedArena fused_arena_of(int L, int d, int F) {
-  FusedArena a{};
-  const size_t rows = kFusedRows;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    const size_t o = off;
-    off += fused_align(bytes);
-    return o;
-  };
-  a.q = take(rows * d * 4);
-  a.act_o = take(rows * d * 4);
-  a.act_no = take(rows * d * 4);
-  a.ssq_o = take(rows * (d / 16) * 4);
-  a.act_f = take(rows * F * 4);
-  a.act_nd = take(rows * d * 4);
-  a.ssq_d = take(rows * (d / 16) * 4);
-  a.layer_bytes = off;
-  off = a.layer_bytes * L;
-  a.e_act = take(rows * d * 4);
-  a.e_ssq = take(rows * (d / 16) * 4);
-  a.total = off;
-  return a;
-}
-
 struct Dims {
   int L, d, H, hd, F, V, Vpad, wdt, kvdt;
   int KVH, dkv;  // K/V heads (grouped-query attention: H / KVH query heads each) and their width KVH * hd
@@ -136,8 +93,6 @@ struct Workspace {
   float* stats;       // [Mmax][groups][3] LM-head per-workgroup max / sumexp / argmax
   float* rope;        // [max_len][hd/2][2] cos, sin
   uint32_t* err;      // device error word
-  uint32_t* bar;      // grid-barrier words of the single-launch verify pass (kept at zero between calls)
-  uint8_t* fused;     // activation arena of the single-launch verify pass (NULL if the model cannot use it)
   uint32_t* split_cnt;  // [max units / 2] arrival counters of the split-K GEMM (kept at zero between calls)
   float* split_part;    // [max units][8][256] published sums and range partials of the split-K GEMM
   uint32_t* wide_cnt;   // [wide_items] arrival counters of the k-split wide-row GEMM (kept at zero between calls)
@@ -148,7 +103,6 @@ struct Workspace {
   uint32_t* corr_cnt;   // [Bmax] arrival counters of the correction slices (kept at zero between calls)
   int32_t* prefill_tok; // [Mmax] token ids of one batched-prefill forward
   int32_t* prefill_cnt; // [Bmax] prompt tokens to cache per request (batched prefill)
-  FusedArena fa;
   size_t act_split;   // elements between splits of act_n / act_o
   size_t actf_split;  // elements between splits of act_f
   int Mmax, NCmax, Rmax;
@@ -167,12 +121,10 @@ struct spade_model_s {
   int device;
   int n_cu;      // compute units of the device
   int gemm_wgs;  // persistent GEMM workgroups
-  bool fused_ok; // cooperative launches available and the single-launch verify pass enabled
   int wide_rt;   // 16-row tiles per workgroup of the wide-row GEMM: 0 chosen per launch, 1..3 fixed, -1 off
   int wide_p;    // panels per wave of the wide-row GEMM: 0 chosen per launch, 1..2 fixed
   int wide_ks;   // k-splits of its O and down projections: 0 chosen per launch, 1 off, 2 or 4 fixed
   int split_ks;  // k-splits of the split-K GEMM: 0 chosen per launch, 2 or 4 where it qualifies, -1 off
-  int attn_cpw;  // attention chunks per workgroup (bf16 cache, head_dim 128): 0 chosen per call, >= 1 fixed
   int attn_merge;  // merge of one-chunk attention partials: 0 chosen per call, 1 last arrival, 2 second launch
   int attn_grouped;  // grouped-query chunks (one workgroup per K/V head and chunk): 0 where they apply, 1 off
   int corr_split;  // correction draws of sampling requests: 0/2 over vocabulary slices, 1 in the accept workgroup
@@ -188,6 +140,8 @@ struct spade_kv_s {
   int stride;    // positions per (request, head) row of the cache: max_len rounded up to 32
   int* lens_ub;  // host upper bound of lens per request
   int last_rows; // rows (gamma + 1) of the last spade_verify on this cache: what a commit can add at most
+  int last_B;    // requests of that call
+  bool verified; // a spade_verify ran since the last commit or state change
   int* snap_ub;  // lens_ub at the last snapshot
 };
 
@@ -232,15 +186,11 @@ hipError_t launch_softmax(const float* logits, int rows, int V, float invT, floa
 hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_t* tokens, int ld,
                                 const int* n_cache, hipStream_t st);
 int prefill_batch_rows(spade_model md, int B);
-// single-launch verify pass (verify_fused.hip): eligibility and launch
-bool fused_eligible(spade_model m, spade_kv kv, const ForwardCall& fc);
-hipError_t launch_verify_fused(spade_model m, spade_kv kv, const ForwardCall& fc, const AcceptCall& ac,
-                               hipStream_t st);
 hipError_t launch_layer_gemm(spade_model m, spade_kv kv, int kind, int layer, const ForwardCall& fc,
                              hipStream_t st);
 hipError_t launch_accept(spade_model m, const AcceptCall& ac, hipStream_t st);
 hipError_t launch_pack(spade_model m, int kind, int layer, const void* src, hipStream_t st);
-hipError_t launch_commit(spade_kv kv, int B, const int32_t* n, const int32_t* corr, hipStream_t st);
+hipError_t launch_commit(spade_kv kv, int B, int R, const int32_t* n, const int32_t* corr, hipStream_t st);
 hipError_t launch_advance(spade_kv kv, int b, int count, const int32_t* pending_src, hipStream_t st);
 hipError_t launch_copy_state(int B, int32_t* lens, int32_t* pending, const int32_t* src_lens,
                              const int32_t* src_pending, hipStream_t st);

@@ -23,17 +23,21 @@ F32, BF16 = 0, 1
 KINDS = {"wq": 0, "wk": 1, "wv": 2, "wo": 3, "wg": 4, "wu": 5, "wd": 6,
          "g_attn": 7, "g_ffn": 8, "embed": 9, "g_final": 10, "lm_head": 11}
 GLOBAL_KINDS = ("embed", "g_final", "lm_head")
-DERR_TOKEN, DERR_NAN, DERR_RESIDUAL, DERR_NOQ = 1, 2, 4, 8
+DERR_TOKEN, DERR_NAN, DERR_RESIDUAL, DERR_NOQ, DERR_CAPACITY, DERR_COMMIT = 1, 2, 4, 8, 16, 32
 
+# include/spade.h: the calls of the method
 EXPORTED = (
     "spade_weight_bytes", "spade_workspace_bytes", "spade_kv_bytes", "spade_model_create",
     "spade_model_load_tensor", "spade_kv_create", "spade_kv_set_state", "spade_kv_get_state",
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
-    "spade_accept_from_logits", "spade_profile_gemm", "spade_get_device_error", "spade_last_error",
-    "spade_model_destroy", "spade_kv_destroy", "spade_model_set_fused", "spade_model_set_wide_tiles",
-    "spade_model_set_wide_k_splits", "spade_model_set_split_k", "spade_softmax", "spade_prefill_batch",
-    "spade_wide_tiling", "spade_model_set_attn_chunks", "spade_model_set_attn_merge",
-    "spade_model_set_correction_slices", "spade_model_set_attn_grouped",
+    "spade_accept_from_logits", "spade_get_device_error", "spade_last_error",
+    "spade_model_destroy", "spade_kv_destroy", "spade_softmax", "spade_prefill_batch",
+)
+# include/spade_tuning.h: schedule controls and measurement hooks
+EXPORTED_TUNING = (
+    "spade_model_set_wide_tiles", "spade_model_set_wide_k_splits", "spade_model_set_split_k",
+    "spade_model_set_attn_merge", "spade_model_set_correction_slices", "spade_model_set_attn_grouped",
+    "spade_profile_gemm", "spade_wide_tiling",
 )
 
 
@@ -90,10 +94,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_accept_from_logits": (I, [P, I, I, I, P, P, P, P, P, F, P, P, P]),
         "spade_profile_gemm": (I, [P, P, I, I, I, I, P]),
         "spade_get_device_error": (I, [P, P, P]),
-        "spade_model_set_fused": (I, [P, I]),
         "spade_model_set_wide_tiles": (I, [P, I, I]),
         "spade_model_set_wide_k_splits": (I, [P, I]),
-        "spade_model_set_attn_chunks": (I, [P, I]),
         "spade_model_set_attn_merge": (I, [P, I]),
         "spade_model_set_correction_slices": (I, [P, I]),
         "spade_model_set_attn_grouped": (I, [P, I]),
@@ -179,11 +181,6 @@ class Model:
         for kind, layer, arr in tensors:
             self.load_numpy(kind, layer, arr)
 
-    def set_fused(self, enable: bool) -> None:
-        """Single persistent launch per verify call where the shape allows it
-        (default), or one kernel per stage."""
-        _check(self.lib.spade_model_set_fused(self.handle, 1 if enable else 0))
-
     def set_wide_tiles(self, row_tiles: int, panels: int = 0) -> None:
         """Tiling of the batched projections: 16-row tiles per workgroup (0
         chosen per launch, 1..3 fixed, -1 skinny engine once per 32 rows) and
@@ -204,11 +201,6 @@ class Model:
         """Correction draw of sampling requests: 0 or 2 over vocabulary slices
         in a second launch, 1 in the accept workgroup."""
         _check(self.lib.spade_model_set_correction_slices(self.handle, int(mode)))
-
-    def set_attn_chunks(self, chunks: int) -> None:
-        """Attention chunks (256 keys) per workgroup: 0 chosen per call, n >= 1
-        fixed."""
-        _check(self.lib.spade_model_set_attn_chunks(self.handle, int(chunks)))
 
     def set_wide_k_splits(self, splits: int) -> None:
         """K splits of the batched O and down projections on the wide-row

@@ -1,6 +1,6 @@
 """Stored draft tokens for the full-size workloads whose recipe needs the
-verifier's own greedy chain (written by tests/golden/make_golden.py, which
-calls only the oracle).  Reading them needs no oracle."""
+verifier (written by tests/golden/make_golden.py, which calls only the
+oracle).  Reading them needs no oracle."""
 
 from __future__ import annotations
 
@@ -23,11 +23,14 @@ def load_golden(name: str):
 
 
 def load_drafts(w, inp) -> str:
-    """Replace inp.drafts (and q rows when stored) by the golden drafts of
-    workload w; returns a short description of where the drafts came from."""
+    """Replace inp.drafts (and the q rows of draft_model workloads) by the
+    stored first-round drafts of workload w; returns a short description of
+    where the drafts came from."""
     g = load_golden(w.name)
     if g is None or g.get("seed") != w.seed:
         return "uniform random ids (no stored chain drafts)"
     import numpy as np
     inp.drafts[:] = np.asarray(g["drafts"], dtype=np.int32)
+    if g.get("draft_probs_file"):
+        inp.draft_probs = np.load(os.path.join(HERE, g["draft_probs_file"]))
     return g.get("recipe", "stored")

@@ -15,6 +15,17 @@ from synth.inputs import draw_from, softmax64
 
 LOGIT_TOL = {"f32": 1e-4, "bf16": 5e-2}
 
+# one JSON line per parity check (decided / excluded / in-band mismatch
+# counts), printed as the check runs and again in pytest's terminal summary
+PARITY_LINES: List[str] = []
+
+
+def report_parity(name: str, counts: dict) -> None:
+    import json
+    line = json.dumps({"parity": name, **counts})
+    PARITY_LINES.append(line)
+    print(line, flush=True)
+
 
 @dataclass
 class OracleRun:

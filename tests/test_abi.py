@@ -19,8 +19,8 @@ def lib():
     return spade.load_library()
 
 
-def _declared():
-    src = open(os.path.join(ROOT, "include", "spade.h")).read()
+def _declared(header="spade.h"):
+    src = open(os.path.join(ROOT, "include", header)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(spade_[a-z_]+)\s*\(", src)))
 
@@ -31,6 +31,11 @@ def test_exports_every_declared_symbol(lib):
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(spade.EXPORTED)
+    tuning = _declared("spade_tuning.h")
+    for n in tuning:
+        assert hasattr(lib, n), n
+    assert set(tuning) == set(spade.EXPORTED_TUNING)
+    assert not set(tuning) & set(names)
 
 
 def test_buffer_sizes(lib):
@@ -89,7 +94,6 @@ def test_host_validation_without_device(lib):
     assert lib.spade_prefill(None, None, 0, None, 3, None) == -1
     assert lib.spade_kv_create(None, None, 1, 8, None, None, ctypes.byref(out)) == -1
     assert lib.spade_model_set_wide_k_splits(None, 2) == -1
-    assert lib.spade_model_set_attn_chunks(None, 1) == -1
     assert lib.spade_model_set_attn_merge(None, 1) == -1
     assert lib.spade_model_set_correction_slices(None, 1) == -1
     assert lib.spade_model_set_attn_grouped(None, 1) == -1

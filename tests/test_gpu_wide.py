@@ -61,27 +61,24 @@ def test_wide_tilings_bit_identical_and_match_oracle(w):
 
 
 @pytest.mark.parametrize("batch", [1, 6])
-def test_attention_runs_bit_identical(batch):
-    """The verify attention with one 256-key chunk per workgroup (merged by the
-    last chunk workgroup to finish, or in a second launch) and with runs of
-    2, 3, 4 or 9 chunks per workgroup (the next chunk's keys and values
-    fetched while the current one is computed), and the per-call choice, give
-    bit-for-bit the same logits, n_accepted and corrections: every chunk's
-    partial and the merge in chunk order are the same whichever workgroup
-    computes them.  Contexts up to 2100 keys (9 chunks); batch 1 runs the
-    skinny projections, batch 6 the wide-row ones."""
+def test_attention_merges_bit_identical_and_vs_oracle(batch):
+    """The verify attention (one 256-key chunk per workgroup) with its chunk
+    partials merged by the last chunk workgroup to finish, in a second launch,
+    and by the per-call choice gives bit-for-bit the same logits, n_accepted
+    and corrections (every chunk's partial and the chunk-order merge are the
+    same whichever workgroup runs them), and matches the oracle.  Contexts up
+    to 2100 keys (9 chunks); batch 1 runs the skinny projections, batch 6 the
+    wide-row ones."""
     base = {w.name: w for w in mini_workloads()}["mini_bf16_wide_b5"]
     w = base.with_(name=f"mini_bf16_long_b{batch}", batch=batch, gamma=4,
                    ctx=(2000, 2100) if batch == 1 else (90, 2100), mode="greedy", draft_recipe="random",
                    seed=2018 + batch)
     weights = ModelWeights(w.model, w.seed)
     inp = make_inputs(w)
+    orun = oracle_run(w, inp, weights=weights)
     model, kv = gpu_setup(w, weights)
     kv.prefill_batch(inp.prompts)
     from paper_2608_13076_amd import spade
-    for bad in (-1, 129):
-        with pytest.raises(spade.SpadeError):
-            model.set_attn_chunks(bad)
     for bad in (-1, 3, 8):
         with pytest.raises(spade.SpadeError):
             model.set_wide_k_splits(bad)
@@ -89,16 +86,20 @@ def test_attention_runs_bit_identical(batch):
         with pytest.raises(spade.SpadeError):
             model.set_attn_merge(bad)
     runs = {}
-    for cpw, merge in ((1, 1), (1, 2), (2, 0), (3, 0), (4, 0), (9, 0), (0, 0), (1, 1)):
-        print(f"[{w.name}] lens {inp.lens.tolist()} attention chunks per workgroup {cpw}, merge {merge}", flush=True)
-        model.set_attn_chunks(cpw)
+    for merge in (1, 2, 0, 1):
+        print(f"[{w.name}] lens {inp.lens.tolist()} attention merge {merge}", flush=True)
         model.set_attn_merge(merge)
-        runs[(cpw, merge)] = gpu_verify(model, kv, inp)[:3]
-    ref = runs[(1, 1)]
+        runs[merge] = gpu_verify(model, kv, inp)[:3]
+    ref = runs[1]
     assert np.isfinite(ref[0]).all()
     for cfg, (lg, n, c) in runs.items():
         assert np.array_equal(lg.view(np.uint32), ref[0].view(np.uint32)), cfg
         assert np.array_equal(n, ref[1]) and np.array_equal(c, ref[2]), cfg
+    p = compare(orun, *runs[2])
+    print(f"[{w.name}] vs oracle: logit err {p.logit_err:.2e}, stable n/corr {p.stable_n}/{p.stable_corr}, "
+          f"excluded n/corr {p.excluded_n}/{p.excluded_corr}", flush=True)
+    assert p.logit_err < LOGIT_TOL[w.model.weight_dtype]
+    assert not p.stable_n_fail and not p.stable_corr_fail, p
     assert model.device_error() == 0
 
 
@@ -108,13 +109,14 @@ def test_grouped_attention_bit_identical(gamma, kv_heads):
     heads of a K/V head, the G (gamma+1) rows packed into one to three 16-row
     tiles) give the per-head chunks' logits, n_accepted and corrections bit
     for bit, with the second-launch merge forced so both run: G = 4 and 2,
-    rows per request 3 to 16, one to three tiles."""
+    rows per request 3 to 16, one to three tiles; both match the oracle."""
     import dataclasses
     base = {w.name: w for w in mini_workloads()}["mini_gqa_mixed_b5"]
     w = base.with_(name=f"mini_gqa_g{gamma}_kvh{kv_heads}", model=dataclasses.replace(base.model, n_kv_heads=kv_heads),
                    gamma=gamma, seed=3000 + gamma + kv_heads)
     weights = ModelWeights(w.model, w.seed)
     inp = make_inputs(w)
+    orun = oracle_run(w, inp, weights=weights)  # also fills the chain drafts of inp
     model, kv = gpu_setup(w, weights)
     kv.prefill_batch(inp.prompts)
     from paper_2608_13076_amd import spade
@@ -130,4 +132,10 @@ def test_grouped_attention_bit_identical(gamma, kv_heads):
     assert np.isfinite(a[0]).all()
     assert np.array_equal(a[0].view(np.uint32), b[0].view(np.uint32))
     assert np.array_equal(a[1], b[1]) and np.array_equal(a[2], b[2])
+    # and the grouped chunks against the oracle
+    p = compare(orun, *b)
+    print(f"[{w.name}] grouped vs oracle: logit err {p.logit_err:.2e}, stable n/corr {p.stable_n}/"
+          f"{p.stable_corr}, excluded n/corr {p.excluded_n}/{p.excluded_corr}", flush=True)
+    assert p.logit_err < LOGIT_TOL[w.model.weight_dtype]
+    assert not p.stable_n_fail and not p.stable_corr_fail, p
     assert model.device_error() == 0

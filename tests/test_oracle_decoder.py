@@ -228,7 +228,8 @@ def test_bf16_widening_matches_torch_for_every_pattern():
     bfloat16 -> float64 conversion (NaN patterns stay NaN)."""
     from oracle.decoder import bf16_bits_to_f64
     bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
-    got = bf16_bits_to_f64(bits)
+    with np.errstate(invalid="ignore"):  # NaN patterns
+        got = bf16_bits_to_f64(bits)
     ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
     nan = np.isnan(ref)
     assert np.array_equal(np.isnan(got), nan)
