@@ -262,6 +262,22 @@ spade_status spade_accept_from_logits(spade_model m, int B, int gamma, int V, co
                                       float temperature, int32_t* d_n_accepted,
                                       int32_t* d_correction, void* stream);
 
+/* spade_accept_from_logits for callers that cannot allocate -- code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc --
+ * and have no model: the same accept/reject and correction draw (the sliced
+ * draw of a call that may sample) with the library's own static device
+ * scratch (about 260 KB per device, held until the process ends) instead of
+ * a model's workspace.  B <= 64 (else SPADE_ECAPACITY), gamma + 1 <= 16;
+ * other arguments as in spade_accept_from_logits.  d_err: device uint32 the
+ * call ORs the SPADE_DERR_* bits into (the caller clears it).  Calls no
+ * allocating routine.  Calls on one device share its scratch: calls that
+ * overlap on one device (different streams, no ordering) race. */
+spade_status spade_accept_from_logits_noalloc(int B, int gamma, int V, const float* d_logits,
+                                              const int32_t* d_draft_tokens, const float* d_draft_probs,
+                                              const float* d_uniforms, const uint8_t* d_mode,
+                                              float temperature, int32_t* d_n_accepted,
+                                              int32_t* d_correction, uint32_t* d_err, void* stream);
+
 /* Read and clear the device error word.  Synchronises the stream. */
 spade_status spade_get_device_error(spade_model m, uint32_t* h_flags, void* stream);
 

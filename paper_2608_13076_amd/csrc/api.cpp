@@ -592,6 +592,37 @@ spade_status spade_accept_from_logits(spade_model m, int B, int gamma, int V, co
   return SPADE_OK;
 }
 
+spade_status spade_accept_from_logits_noalloc(int B, int gamma, int V, const float* d_logits,
+                                              const int32_t* d_draft_tokens, const float* d_draft_probs,
+                                              const float* d_uniforms, const uint8_t* d_mode, float temperature,
+                                              int32_t* d_n_accepted, int32_t* d_correction, uint32_t* d_err,
+                                              void* stream) {
+  if (!d_logits || !d_mode || !d_n_accepted || !d_correction || !d_err) return fail(SPADE_EINVAL, "null pointer");
+  if (B < 1 || B > kNoAllocMaxB)
+    return fail(SPADE_ECAPACITY, "B=%d: the static scratch holds at most %d requests", B, kNoAllocMaxB);
+  if (gamma < 0 || gamma + 1 > kMaxR) return fail(SPADE_ECAPACITY, "gamma out of range");
+  if (gamma > 0 && !d_draft_tokens) return fail(SPADE_EINVAL, "draft tokens required when gamma > 0");
+  if (V < 2) return fail(SPADE_EINVAL, "V must be >= 2");
+  if (d_draft_probs && !d_uniforms) return fail(SPADE_EINVAL, "sampling needs uniforms");
+  if (!(temperature > 0.f && std::isfinite(temperature)))
+    return fail(SPADE_EINVAL, "temperature must be finite and > 0");
+  AcceptCall ac{};
+  ac.B = B;
+  ac.gamma = gamma;
+  ac.V = V;
+  ac.logits = d_logits;
+  ac.drafts = d_draft_tokens;
+  ac.q = d_draft_probs;
+  ac.u = d_uniforms;
+  ac.mode = d_mode;
+  ac.inv_T = 1.0f / temperature;
+  ac.n_out = d_n_accepted;
+  ac.corr_out = d_correction;
+  hipError_t e = launch_accept_noalloc(ac, d_err, (hipStream_t)stream);
+  if (e != hipSuccess) return hipfail(e, "accept_from_logits_noalloc");
+  return SPADE_OK;
+}
+
 spade_status spade_profile_gemm(spade_model m, spade_kv kv, int kind, int B, int gamma, int launches,
                                 void* stream) {
   if (!m || !kv) return fail(SPADE_EINVAL, "null pointer");

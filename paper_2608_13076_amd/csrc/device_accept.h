@@ -206,10 +206,12 @@ __device__ __forceinline__ void accept_request(const AcceptParams& p, int b, Acc
   if (!sample) {
     corr = sm.rarg[n];
   } else if (p.corr_slices > 0) {
-    // correct_slices draws it after this launch
+    // correct_slices draws it after this launch; its arrival counter starts
+    // that launch at zero
     if (tid == 0) {
       p.corr_lse[b] = sm.rlse[n];
       p.n_out[b] = n;
+      p.corr_cnt[b] = 0u;
     }
     return;
   } else {

@@ -47,6 +47,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 
 namespace spade {
 
@@ -1427,6 +1428,88 @@ hipError_t launch_accept(spade_model md, const AcceptCall& ac, hipStream_t st) {
   hipLaunchKernelGGL(accept_kernel, dim3(ac.B), dim3(kAcceptThreads), 0, st, p);
   if (split) {
     const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(correct_kernel, dim3(p.corr_slices, ac.B), dim3(kCorrThreads), 0, st, p);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of spade_accept_from_logits_noalloc, for callers that cannot
+// allocate: the sliced correction draw's per-request arrival counters,
+// log-sum-exps and per-slice winners for up to kNoAllocMaxB requests, in a
+// file-scope device array.  Each device holds its own copy at its own
+// address (looked up once per device); every call on a device uses that copy,
+// so calls that overlap on one device race.  The accept kernel zeroes a
+// request's counter before the correction launch uses it.
+// ---------------------------------------------------------------------------
+struct NoAllocScratch {
+  uint32_t cnt[kNoAllocMaxB];
+  float lse[kNoAllocMaxB];
+  float part[kNoAllocMaxB * kCorrMaxSlices * 4];
+};
+static __device__ __align__(256) uint8_t scratch[sizeof(NoAllocScratch)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's copy of `scratch` (the host symbol is a
+// stand-in, never a device address).
+hipError_t scratch_address(uint8_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (ptr == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = (uint8_t*)g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+size_t noalloc_scratch_bytes() { return sizeof(NoAllocScratch); }
+
+hipError_t launch_accept_noalloc(const AcceptCall& ac, uint32_t* err, hipStream_t st) {
+  uint8_t* base = nullptr;
+  hipError_t e = scratch_address(&base);
+  if (e != hipSuccess) return e;
+  AcceptParams p{};
+  p.logits = ac.logits;
+  p.stats = nullptr;
+  p.B = ac.B;
+  p.V = ac.V;
+  p.gamma = ac.gamma;
+  p.R = ac.gamma + 1;
+  p.drafts = ac.drafts;
+  p.q = ac.q;
+  p.u = ac.u;
+  p.mode = ac.mode;
+  p.inv_T = ac.inv_T;
+  p.n_out = ac.n_out;
+  p.corr_out = ac.corr_out;
+  p.err = err;
+  // a call that may sample draws its corrections over vocabulary slices,
+  // with this device's scratch
+  const bool may_sample = ac.u != nullptr && (ac.q != nullptr || ac.gamma == 0);
+  if (may_sample) {
+    p.corr_slices = std::min(kCorrMaxSlices, (ac.V + kCorrSliceTokens - 1) / kCorrSliceTokens);
+    p.corr_cnt = (uint32_t*)(base + offsetof(NoAllocScratch, cnt));
+    p.corr_lse = (float*)(base + offsetof(NoAllocScratch, lse));
+    p.corr_part = (float*)(base + offsetof(NoAllocScratch, part));
+  }
+  hipLaunchKernelGGL(accept_kernel, dim3(ac.B), dim3(kAcceptThreads), 0, st, p);
+  if (may_sample) {
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(correct_kernel, dim3(p.corr_slices, ac.B), dim3(kCorrThreads), 0, st, p);
   }

@@ -17,6 +17,7 @@ constexpr int kWideMinRows = 16;     // bf16 projections with more rows use the 
 constexpr int kPrefillRows = 16;     // tokens per prefill forward
 constexpr int kMaxR = 16;            // rows per request in one forward (gamma <= 15)
 constexpr int kCorrMaxSlices = 256; // vocabulary slices of one correction draw
+constexpr int kNoAllocMaxB = 64;     // requests of one spade_accept_from_logits_noalloc call
 constexpr int kActSplits = 2;        // bf16 terms per fp32 activation (hi, lo)
 constexpr int kAttnChunk = 128;      // keys per workgroup of the generic attention (f32 cache or head_dim != 128)
 constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
@@ -189,6 +190,9 @@ int prefill_batch_rows(spade_model md, int B);
 hipError_t launch_layer_gemm(spade_model m, spade_kv kv, int kind, int layer, const ForwardCall& fc,
                              hipStream_t st);
 hipError_t launch_accept(spade_model m, const AcceptCall& ac, hipStream_t st);
+// accept / correction with the library's static device scratch (no workspace)
+hipError_t launch_accept_noalloc(const AcceptCall& ac, uint32_t* err, hipStream_t st);
+size_t noalloc_scratch_bytes();
 hipError_t launch_pack(spade_model m, int kind, int layer, const void* src, hipStream_t st);
 hipError_t launch_commit(spade_kv kv, int B, int R, const int32_t* n, const int32_t* corr, hipStream_t st);
 hipError_t launch_advance(spade_kv kv, int b, int count, const int32_t* pending_src, hipStream_t st);

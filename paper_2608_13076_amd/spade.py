@@ -32,6 +32,7 @@ EXPORTED = (
     "spade_kv_snapshot", "spade_kv_restore", "spade_prefill", "spade_verify", "spade_kv_commit",
     "spade_accept_from_logits", "spade_get_device_error", "spade_last_error",
     "spade_model_destroy", "spade_kv_destroy", "spade_softmax", "spade_prefill_batch",
+    "spade_accept_from_logits_noalloc",
 )
 # include/spade_tuning.h: schedule controls and measurement hooks
 EXPORTED_TUNING = (
@@ -92,6 +93,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_verify": (I, [P, P, I, I, P, P, P, P, F, P, P, P, P]),
         "spade_kv_commit": (I, [P, I, P, P, P]),
         "spade_accept_from_logits": (I, [P, I, I, I, P, P, P, P, P, F, P, P, P]),
+        "spade_accept_from_logits_noalloc": (I, [I, I, I, P, P, P, P, P, F, P, P, P, P]),
         "spade_profile_gemm": (I, [P, P, I, I, I, I, P]),
         "spade_get_device_error": (I, [P, P, P]),
         "spade_model_set_wide_tiles": (I, [P, I, I]),
@@ -334,6 +336,18 @@ def verify(model: Model, kv: KVCache, buf: VerifyBuffers, temperature: float = 1
     _check(model.lib.spade_verify(model.handle, kv.handle, buf.B, buf.gamma, _ptr(buf.drafts), _ptr(buf.q),
                                   _ptr(buf.u), _ptr(buf.mode), float(temperature), _ptr(buf.n),
                                   _ptr(buf.corr), _ptr(buf.logits), _stream()))
+
+
+def accept_from_logits_noalloc(logits: torch.Tensor, drafts: torch.Tensor, draft_probs, uniforms,
+                               modes: torch.Tensor, temperature: float, n: torch.Tensor, corr: torch.Tensor,
+                               err: torch.Tensor) -> None:
+    """spade_accept_from_logits_noalloc on the current stream: writes n and
+    corr, ORs error bits into err (int32 [1]); allocates nothing."""
+    B, R, V = logits.shape
+    _check(load_library().spade_accept_from_logits_noalloc(B, R - 1, V, _ptr(logits), _ptr(drafts),
+                                                           _ptr(draft_probs), _ptr(uniforms), _ptr(modes),
+                                                           float(temperature), _ptr(n), _ptr(corr), _ptr(err),
+                                                           _stream()))
 
 
 def softmax_into(logits: torch.Tensor, out: torch.Tensor, temperature: float = 1.0) -> None:
