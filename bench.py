@@ -171,6 +171,131 @@ def summarize_counters(fetch_dir: str, write_dir: str, cmd_fetch: str, cmd_write
     return 0
 
 
+STEP_PASSES = (("FETCH_SIZE",), ("WRITE_SIZE",),
+               ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE",
+                "SQ_LDS_BANK_CONFLICT", "SQ_INSTS_LDS"),
+               ("TCC_HIT_sum", "TCC_MISS_sum"))
+N_SIMD = 1024  # 256 compute units x 4 SIMDs
+MFMA_PEAK_TFLOPS = 2500.0  # dense bf16
+
+
+def kernel_alg_bytes(name: str, w, lens) -> int:
+    """Algorithmic bytes of one launch of a verify-step kernel: a projection
+    GEMM's weights once plus its fp32 input and output rows; the attention's
+    cached and new K/V rows of one layer."""
+    import re
+    name = name.replace("void ", "", 1).replace("spade::", "")
+    m = w.model
+    d, f, v = m.d_model, m.d_ffn, m.vocab
+    dkv = m.kv_heads * m.head_dim
+    M = w.batch * (w.gamma + 1)
+    kind = None
+    t = re.search(r"<([^>]*)>", name)
+    args = [a.strip() for a in t.group(1).split(",")] if t else []
+    if name.startswith("gemm_wide_kernel") and len(args) >= 3:
+        kind = int(args[2])
+    elif name.startswith("gemm_kernel") and len(args) >= 4:
+        kind = int(args[3])
+    elif name.startswith("gemm_split_kernel") and len(args) >= 2:
+        kind = int(args[1])
+    if kind is not None:
+        n_out, k_in = [(d + 2 * dkv, d), (d, d), (2 * f, d), (d, f), (v, d)][kind]
+        return n_out * k_in * 2 + M * k_in * 4 + M * (n_out // (2 if kind == 2 else 1)) * 4
+    if name.startswith(("attn_lr_kernel", "attn_g_kernel", "attn_kernel")):
+        return sum(int(l) + w.gamma + 1 for l in lens) * 2 * dkv * 2
+    return 0
+
+
+def summarize_step_counters(workload_name: str, dirs, cmds) -> int:
+    """Per-kernel counters of one verify step (the dispatches after the last
+    calibration copy) from the rocprofv3 --pmc passes of --counters-step."""
+    import csv
+    import glob
+    from synth import make_inputs, workload
+    w = workload(workload_name)
+    inp = make_inputs(w)
+
+    def rows(d):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        return list(csv.DictReader(open(f)))
+
+    per = {}  # kernel -> counter -> [values]
+    meta = {}
+    copy = {}
+    for d in dirs:
+        rs = rows(d)
+        cut = max(int(r["Dispatch_Id"]) for r in rs if "neg" in r["Kernel_Name"])
+        for r in rs:
+            did = int(r["Dispatch_Id"])
+            name = r["Kernel_Name"]
+            val = float(r["Counter_Value"])
+            if did == cut:
+                copy.setdefault(r["Counter_Name"], []).append(val)
+                continue
+            if did < cut:
+                continue
+            per.setdefault(name, {}).setdefault(r["Counter_Name"], {}).setdefault(did, 0.0)
+            per[name][r["Counter_Name"]][did] += val
+            mm = meta.setdefault(name, {"dur": {}, "vgpr": r["VGPR_Count"], "agpr": r["Accum_VGPR_Count"],
+                                        "lds": r["LDS_Block_Size"], "grid": r["Grid_Size"]})
+            mm["dur"][did] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3
+    f_fetch = COPY_BYTES / (sum(copy["FETCH_SIZE"]) * 1024) * 1024
+    f_write = COPY_BYTES / (sum(copy["WRITE_SIZE"]) * 1024) * 1024
+
+    def avg(name, c):
+        vals = per.get(name, {}).get(c)
+        return sum(vals.values()) / len(vals) if vals else None
+
+    out = os.path.join(ROOT, "profiles", f"{workload_name}_counters.md")
+    lines = [f"# Hardware counters of one verify step: {w.description}", "",
+             "Four rocprofv3 counter passes of `bench.py --counters-step` (a calibration copy of "
+             f"{COPY_BYTES} bytes read and written, then one verify step), from the repository root:", ""]
+    lines += [f"    {c}" for c in cmds]
+    lines += ["", f"Calibration: FETCH_SIZE counts {f_fetch:.1f} bytes per KiB unit, WRITE_SIZE {f_write:.1f} "
+              "(HBM traffic = counter x that).  MFMA TFLOP/s = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 / duration "
+              "(the matrix operations executed, both bf16 terms of each activation counted), and its fraction "
+              f"of the {MFMA_PEAK_TFLOPS:.0f} TFLOP/s dense bf16 peak.  Durations are those of the counter runs "
+              "(kernels serialised).  Averages per launch.", "",
+              "| kernel | launches | us | alg. MB | HBM read MB | HBM write MB | traffic / alg. | HBM TB/s | "
+              "MFMA TFLOP/s | MFMA frac | L2 hit | LDS bank conflicts / LDS instr | VGPRs |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    order = sorted(per, key=lambda n: -sum(meta[n]["dur"].values()))
+    for name in order:
+        mm = meta[name]
+        n = len(mm["dur"])
+        us = sum(mm["dur"].values()) / n
+        alg = kernel_alg_bytes(name, w, inp.lens)
+        fe = avg(name, "FETCH_SIZE")
+        wr = avg(name, "WRITE_SIZE")
+        rd_b = fe * f_fetch if fe is not None else None
+        wr_b = wr * f_write if wr is not None else None
+        mops = avg(name, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        hit = avg(name, "TCC_HIT_sum")
+        miss = avg(name, "TCC_MISS_sum")
+        bank = avg(name, "SQ_LDS_BANK_CONFLICT")
+        ldsi = avg(name, "SQ_INSTS_LDS")
+
+        def fmt(x, p=1):
+            return "-" if x is None else f"{x:.{p}f}"
+        tb = (rd_b + wr_b) / (us * 1e-6) / 1e12 if rd_b is not None and wr_b is not None else None
+        ratio = (rd_b + wr_b) / alg if alg and rd_b is not None and wr_b is not None else None
+        tf = mops * 512 / (us * 1e-6) / 1e12 if mops is not None else None
+        mb = f"{tf / MFMA_PEAK_TFLOPS:.3f}" if tf is not None else "-"
+        hr = f"{100 * hit / (hit + miss):.1f}%" if hit is not None and miss is not None and hit + miss > 0 else "-"
+        lb = f"{bank / ldsi:.2f}" if bank is not None and ldsi else "-"
+        short = name.replace("void ", "", 1).replace("spade::", "").split("(")[0]
+        lines.append(f"| `{short}` | {n} | {us:.1f} | {fmt(alg / 1e6 if alg else None)} | {fmt(rd_b / 1e6 if rd_b else None)} | "
+                     f"{fmt(wr_b / 1e6 if wr_b else None)} | {fmt(ratio, 2)} | {fmt(tb, 2)} | {fmt(tf)} | {mb} | {hr} | "
+                     f"{lb} | {mm['vgpr']} |")
+    lines += ["", "Kernel names: `gemm_wide_kernel<row tiles, panels per wave, kind, k-splits>`, "
+              "`gemm_kernel<bf16, row tiles, operand in LDS, kind>`, `gemm_split_kernel<k-splits, kind>` with kind "
+              "0 QKV, 1 O, 2 gate/up, 3 down, 4 LM head; attention kernels read one layer's K/V.", ""]
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -186,9 +311,17 @@ def main() -> int:
                     help="counter-collection run: a calibration copy, then the gate/up GEMM launches; no timing")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH", "CMD_WRITE"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc runs of --counters")
+    ap.add_argument("--counters-step", action="store_true",
+                    help="counter-collection run: one warm-up step, a calibration copy, one verify step; no timing")
+    ap.add_argument("--summarize-step-counters", nargs=8, metavar=("D1", "D2", "D3", "D4", "C1", "C2", "C3", "C4"),
+                    help="write profiles/<workload>_counters.md from the four rocprofv3 --pmc passes of "
+                         "--counters-step (output dirs, then the commands)")
     args = ap.parse_args()
     if args.summarize_counters:
         return summarize_counters(*args.summarize_counters)
+    if args.summarize_step_counters:
+        a = args.summarize_step_counters
+        return summarize_step_counters(args.workload, a[:4], a[4:])
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark measures one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
@@ -227,7 +360,13 @@ def main() -> int:
         log("counter run done: 1 calibration copy, 4 gate/up launches")
         return 0
     t0 = time.perf_counter()
-    kv.prefill_batch(inp.prompts)  # all requests' chunks in one forward each
+    if args.counters_step:
+        # the cache's contents do not change what the counters measure: set the
+        # lengths directly (a zero-filled cache) instead of prefilling
+        kv.buf.zero_()
+        kv.set_state(inp.lens, inp.pending)
+    else:
+        kv.prefill_batch(inp.prompts)  # all requests' chunks in one forward each
     log(f"prefill of {inp.lens.tolist()} tokens in {time.perf_counter() - t0:.1f}s")
     lens0, pend0 = kv.snapshot(w.batch)
     buf = spade.VerifyBuffers(model, inp.drafts, inp.draft_probs, inp.uniforms, inp.modes, want_logits=False)
@@ -237,6 +376,17 @@ def main() -> int:
         kv.commit(buf.n, buf.corr)
         kv.restore(lens0, pend0)
 
+    if args.counters_step:
+        step()
+        torch.cuda.synchronize()
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)  # calibration (and the marker before the measured step)
+        torch.cuda.synchronize()
+        step()
+        torch.cuda.synchronize()
+        log("counter run done: 1 warm-up step, 1 calibration copy, 1 step")
+        return 0
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
