@@ -296,6 +296,33 @@ def summarize_step_counters(workload_name: str, dirs, cmds) -> int:
     return 0
 
 
+def prefill_flops(m, lens) -> float:
+    """Dense flops of caching the prompts: 2 per weight and token for the
+    projections, and 4 hd per (query, key) pair and head for the causal scores
+    and weighted values (a prompt of n tokens has n (n + 1) / 2 pairs)."""
+    dkv = m.kv_heads * m.head_dim
+    per_tok = m.n_layers * 2 * (m.d_model * (m.d_model + 2 * dkv) + m.d_model * m.d_model + 3 * m.d_model * m.d_ffn)
+    pairs = sum(int(n) * (int(n) + 1) // 2 for n in lens)
+    return float(per_tok * sum(int(n) for n in lens) + m.n_layers * m.n_heads * 4 * m.head_dim * pairs)
+
+
+def time_prefill(model, kv, inp, w) -> dict:
+    """The same prompts again, into an empty cache (same contents and state
+    afterwards), timed around the call (host to device copy of the ids and the
+    final synchronisation included)."""
+    import torch
+    zeros = np.zeros(w.batch, dtype=np.int32)
+    kv.set_state(zeros, zeros)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    kv.prefill_batch(inp.prompts)
+    t = time.perf_counter() - t0
+    tokens = int(sum(len(p) - 1 for p in inp.prompts))
+    fl = prefill_flops(w.model, [len(p) - 1 for p in inp.prompts])
+    return {"tokens": tokens, "s": round(t, 4), "tokens_per_s": round(tokens / t, 1),
+            "tflops": round(fl / t / 1e12, 1), "frac_bf16_peak": round(fl / t / 1e12 / MFMA_PEAK_TFLOPS, 4)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -368,6 +395,10 @@ def main() -> int:
     else:
         kv.prefill_batch(inp.prompts)  # all requests' chunks in one forward each
     log(f"prefill of {inp.lens.tolist()} tokens in {time.perf_counter() - t0:.1f}s")
+    prefill = None
+    if not args.counters_step:
+        prefill = time_prefill(model, kv, inp, w)
+        log(f"prefill (warm): {prefill}")
     lens0, pend0 = kv.snapshot(w.batch)
     buf = spade.VerifyBuffers(model, inp.drafts, inp.draft_probs, inp.uniforms, inp.modes, want_logits=False)
 
@@ -455,6 +486,7 @@ def main() -> int:
         "hbm_frac_whole_pass": round(gbs / HBM_PEAK_GBS, 4),
         "emitted_tokens_per_call": float(np.mean(n_acc + 1)),
         "roofline": roof,
+        "prefill": prefill,
     }
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle on {args.cpu_layers} layers")

@@ -219,13 +219,16 @@ spade_status spade_verify(spade_model m, spade_kv kv, int B, int gamma,
 /* Prefill of B requests at once: request b caches h_n_tokens[b] - 1 prompt
  * tokens (row b of d_tokens, device int32 [B][ld], ld >= every count) after
  * its current length, and its last prompt token becomes pending -- the same
- * cache contents and state as spade_prefill of each request.  Every forward
- * takes the next R = 16 tokens of every request (the GEMMs read each weight
- * once for all B * R rows; the workspace holds max_batch * 16 rows); a request
- * whose prompt is used up contributes placeholder rows, written past its
- * length, so each request needs R free positions beyond its prompt
- * (lens + h_n_tokens[b] - 1 + R <= max_len, else SPADE_ECAPACITY).  Counts
- * are read from host memory (h_n_tokens) before the call returns. */
+ * cache contents and state as spade_prefill of each request.  Each forward
+ * takes R rows from each of a range of consecutive requests (the GEMMs read
+ * each weight once for all rows of the forward): with a bf16 cache and
+ * head_dim 128 up to all of a request's prompt, within the workspace's
+ * prefill rows (max_batch * max_len rounded up to 16, at most 2048, and at
+ * least max_batch * 16); otherwise 16 per request.  A request whose prompt
+ * runs out inside a forward contributes placeholder rows, written past its
+ * length and only where the cache has room.  Needs lens + h_n_tokens[b] <=
+ * max_len (else SPADE_ECAPACITY).  Counts are read from host memory
+ * (h_n_tokens) before the call returns. */
 spade_status spade_prefill_batch(spade_model m, spade_kv kv, int B, const int32_t* d_tokens, int ld,
                                  const int32_t* h_n_tokens, void* stream);
 

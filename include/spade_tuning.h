@@ -70,6 +70,20 @@ spade_status spade_model_set_correction_slices(spade_model m, int mode);
  * same under both modes.  Other values return SPADE_EINVAL. */
 spade_status spade_model_set_attn_grouped(spade_model m, int mode);
 
+/* Prompt rows per request of a prefill forward (spade_prefill,
+ * spade_prefill_batch; Sec. III-A: the context is run through the verifier
+ * once before the first verification).  With a bf16 cache and head_dim 128,
+ * rows = 0 (the default) lets a forward take as many prompt rows as the
+ * workspace holds (up to 2048 rows in all), so the projections multiply each
+ * weight tile with thousands of rows and run at matrix-core speed, and the
+ * attention of rows past the first 16 runs on the prefill attention kernel
+ * (16-row tiles, each computed as a verify call of its own); rows > 0 caps
+ * the rows per request (at most 16: the verify attention kernels, 16 rows
+ * per forward).  Other caches always take 16.  The cache contents, and so
+ * every later result, are bit-for-bit the same under every setting.  rows < 0
+ * returns SPADE_EINVAL. */
+spade_status spade_model_set_prefill_rows(spade_model m, int rows);
+
 /* K splitting of the batched O and down projections on the wide-row GEMM.
  * Their weights have few panels (d_model / 16), so one workgroup per panel
  * group leaves most compute units idle; with `splits` = 2 or 4 each

@@ -101,23 +101,28 @@ ArenaLayout layout_of(const Dims& D) {
 
 struct WsPlan {
   size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, split_cnt,
-      split_part, wide_cnt, wide_part, corr_lse, corr_part, corr_cnt, prefill_tok, prefill_cnt, total;
+      split_part, wide_cnt, wide_part, corr_lse, corr_part, corr_cnt, prefill_tok, prefill_cnt, prefill_base, total;
   size_t wide_items, wide_floats;
   int max_units;
   size_t act_split, actf_split;
-  int Mmax, NCmax, Rmax;
+  int Mmax, Mrows, NCmax, Rmax;
 };
 
 WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   WsPlan p{};
   p.Rmax = std::max(max_gamma + 1, kPrefillRows);
-  // rows of one forward: a verify call, or a batched prefill of 16 tokens per request
+  // rows of a verify call, or of a batched prefill of 16 tokens per request
   p.Mmax = std::max(max_batch * (max_gamma + 1), max_batch * kPrefillRows);
+  // rows of any forward: a bf16 cache with head_dim 128 also takes prefill
+  // forwards of up to kPrefillMaxRows prompt rows (no more than the caches hold)
+  p.Mrows = p.Mmax;
+  if (D.kvdt == SPADE_BF16 && D.hd == kAttnHd)
+    p.Mrows = std::max(p.Mmax, (int)std::min<long>(kPrefillMaxRows, (long)max_batch * ((max_len + 15) / 16 * 16)));
   p.NCmax = std::min(kAttnMaxChunks, (max_len + kAttnChunk - 1) / kAttnChunk);
   const bool wb = D.wdt == SPADE_BF16;
   const size_t ae = wb ? 2 * kActSplits : 4;  // bf16 terms or one float
-  p.act_split = (size_t)p.Mmax * D.d;
-  p.actf_split = (size_t)p.Mmax * D.F;
+  p.act_split = (size_t)p.Mrows * D.d;
+  p.actf_split = (size_t)p.Mrows * D.F;
   const int NU = D.Vpad / 16;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -125,12 +130,12 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
     off += align256(bytes);
     return o;
   };
-  p.x = take((size_t)p.Mmax * D.d * 4);
-  p.act_n = take((size_t)p.Mmax * D.d * ae);
-  p.act_o = take((size_t)p.Mmax * D.d * ae);
-  p.act_f = take((size_t)p.Mmax * D.F * ae);
-  p.ssq = take((size_t)p.Mmax * (D.d / 16) * 4);
-  p.q = take((size_t)p.Mmax * D.d * 4);
+  p.x = take((size_t)p.Mrows * D.d * 4);
+  p.act_n = take((size_t)p.Mrows * D.d * ae);
+  p.act_o = take((size_t)p.Mrows * D.d * ae);
+  p.act_f = take((size_t)p.Mrows * D.F * ae);
+  p.ssq = take((size_t)p.Mrows * (D.d / 16) * 4);
+  p.q = take((size_t)p.Mrows * D.d * 4);
   p.attn_o = take((size_t)max_batch * D.H * p.NCmax * p.Rmax * D.hd * 4);
   p.attn_ml = take((size_t)max_batch * D.H * p.NCmax * p.Rmax * 2 * 4);
   p.attn_cnt = take((size_t)max_batch * D.H * 4);
@@ -156,8 +161,9 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   p.corr_lse = take((size_t)max_batch * 4);
   p.corr_part = take((size_t)max_batch * kCorrMaxSlices * 4 * 4);
   p.corr_cnt = take((size_t)max_batch * 4);
-  p.prefill_tok = take((size_t)p.Mmax * 4);
+  p.prefill_tok = take((size_t)p.Mrows * 4);
   p.prefill_cnt = take((size_t)max_batch * 4);
+  p.prefill_base = take((size_t)max_batch * 4);
   p.total = off;
   return p;
 }
@@ -220,6 +226,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->attn_merge = 0;
   m->corr_split = 0;
   m->attn_grouped = 0;
+  m->prefill_rows = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -247,6 +254,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.corr_cnt = (uint32_t*)(b + p.corr_cnt);
   w.prefill_tok = (int32_t*)(b + p.prefill_tok);
   w.prefill_cnt = (int32_t*)(b + p.prefill_cnt);
+  w.prefill_base = (int32_t*)(b + p.prefill_base);
   w.logits = (float*)(b + p.logits);
   w.stats = (float*)(b + p.stats);
   w.rope = (float*)(b + p.rope);
@@ -254,6 +262,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.act_split = p.act_split;
   w.actf_split = p.actf_split;
   w.Mmax = p.Mmax;
+  w.Mrows = p.Mrows;
   w.NCmax = p.NCmax;
   w.Rmax = p.Rmax;
 
@@ -393,20 +402,7 @@ spade_status spade_prefill(spade_model m, spade_kv kv, int b, const int32_t* d_t
   const int n_cache = n_tokens - 1;
   if (kv->lens_ub[b] + n_cache + 1 > kv->max_len)
     return fail(SPADE_ECAPACITY, "prefill of %d tokens overflows max_len %d", n_tokens, kv->max_len);
-  hipStream_t st = (hipStream_t)stream;
-  for (int s = 0; s < n_cache; s += kPrefillRows) {
-    ForwardCall fc{};
-    fc.b0 = b;
-    fc.nb = 1;
-    fc.R = std::min(kPrefillRows, n_cache - s);
-    fc.tokens = d_tokens + s;
-    fc.want_logits = false;
-    hipError_t e = launch_forward(m, kv, fc, st);
-    if (e == hipSuccess) e = launch_advance(kv, b, fc.R, nullptr, st);
-    if (e != hipSuccess) return hipfail(e, "prefill");
-    kv->lens_ub[b] += fc.R;
-  }
-  hipError_t e = launch_advance(kv, b, 0, d_tokens + n_cache, st);
+  hipError_t e = launch_prefill_one(m, kv, b, d_tokens, n_cache, (hipStream_t)stream);
   if (e != hipSuccess) return hipfail(e, "prefill");
   kv->verified = false;
   return SPADE_OK;
@@ -496,6 +492,13 @@ spade_status spade_model_set_attn_grouped(spade_model m, int mode) {
   return SPADE_OK;
 }
 
+spade_status spade_model_set_prefill_rows(spade_model m, int rows) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (rows < 0) return fail(SPADE_EINVAL, "rows must be >= 0");
+  m->prefill_rows = rows;
+  return SPADE_OK;
+}
+
 spade_status spade_model_set_correction_slices(spade_model m, int mode) {
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
@@ -515,14 +518,13 @@ spade_status spade_prefill_batch(spade_model m, spade_kv kv, int B, const int32_
   if (!m || !kv || !d_tokens || !h_n_tokens) return fail(SPADE_EINVAL, "null pointer");
   if (kv->model != m) return fail(SPADE_EINVAL, "kv belongs to another model");
   if (B < 1 || B > kv->max_batch || B > m->max_batch) return fail(SPADE_ECAPACITY, "B=%d out of range", B);
-  const int R = prefill_batch_rows(m, B);
   std::vector<int> n_cache(B);
   for (int b = 0; b < B; ++b) {
     if (h_n_tokens[b] < 1 || h_n_tokens[b] > ld) return fail(SPADE_EINVAL, "request %d: n_tokens must be in [1, ld]", b);
     n_cache[b] = h_n_tokens[b] - 1;
-    if (kv->lens_ub[b] + n_cache[b] + R > kv->max_len)
-      return fail(SPADE_ECAPACITY, "request %d: %d cached + %d prompt tokens + %d rows of slack exceed max_len %d", b,
-                  kv->lens_ub[b], n_cache[b], R, kv->max_len);
+    if (kv->lens_ub[b] + n_cache[b] + 1 > kv->max_len)
+      return fail(SPADE_ECAPACITY, "request %d: %d cached + %d prompt tokens overflow max_len %d", b, kv->lens_ub[b],
+                  h_n_tokens[b], kv->max_len);
   }
   hipError_t e = launch_prefill_batch(m, kv, B, d_tokens, ld, n_cache.data(), (hipStream_t)stream);
   if (e != hipSuccess) return hipfail(e, "prefill_batch");

@@ -20,7 +20,6 @@
 
 namespace spade {
 
-constexpr int kAttnHd = 128;
 constexpr int kAttnRows = 16;  // rows per request (gamma + 1 <= 16)
 constexpr int kAttnThreads = 512;
 
@@ -174,16 +173,16 @@ __device__ __forceinline__ void attn_load_k(const AttnItem& it, int wave, int la
   }
 }
 
+// Scores of one chunk, scaled and masked: sv[grp][i] is row 4g + i and key
+// k_lo + (CK/8) wave + 16 grp + kl of the lane (-inf past k_hi or after the
+// row's position).
 template <int CK>
-__device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
-                                                 const uint16_t (*sqh)[kAttnQPitch],
-                                                 const uint16_t (*sql)[kAttnQPitch], int R, float scale, int stride,
-                                                 AttnSmem<CK>& sm) {
+__device__ __forceinline__ void attn_scores(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
+                                            const uint16_t (*sqh)[kAttnQPitch], const uint16_t (*sql)[kAttnQPitch],
+                                            float scale, float (&sv)[CK / 128][4]) {
   constexpr int NG = CK / 128;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, kl = lane & 15;
-  const int ke = (it.k_hi + 7) & ~7;
-  float sv[NG][4];
 #pragma unroll
   for (int grp = 0; grp < NG; ++grp) {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -203,9 +202,14 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
       sv[grp][i] = (key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
     }
   }
-  // the V^T fragments, after the score products (the K registers are free)
-  __builtin_amdgcn_sched_barrier(0);
-  AttnRegs<CK> r;
+}
+
+// V^T fragments of a chunk: 8-key granules below k_hi rounded up to 8 (zero
+// past them).
+template <int CK>
+__device__ __forceinline__ void attn_load_v(const AttnItem& it, int wave, int lane, int stride, AttnRegs<CK>& r) {
+  const int g = lane >> 4, kl = lane & 15;
+  const int ke = (it.k_hi + 7) & ~7;
   const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
 #pragma unroll
   for (int ks = 0; ks < CK / 32; ++ks) {
@@ -213,7 +217,15 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
     r.vf[ks] = make_uint4(0, 0, 0, 0);
     if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
   }
-  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Chunk softmax of the scores: probabilities to sm.ph / sm.pl, and the row
+// max and row sum of rows < R to sm.m / sm.l (read after a barrier).
+template <int CK>
+__device__ __forceinline__ void attn_softmax(const float (&sv)[CK / 128][4], int R, AttnSmem<CK>& sm) {
+  constexpr int NG = CK / 128;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, kl = lane & 15;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     float mx = sv[0][i];
@@ -253,7 +265,14 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
     sm.m[tid] = M;
     sm.l[tid] = l;
   }
-  attn_mask_tail(it, lane, r);
+}
+
+// O = P V over the chunk (P from sm.ph / sm.pl, V^T fragments masked past
+// k_hi): row 4g + i, feature 16 wave + kl in o[i].
+template <int CK>
+__device__ __forceinline__ floatx4 attn_pv(const AttnSmem<CK>& sm, const AttnRegs<CK>& r) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, kl = lane & 15;
   floatx4 o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ks = 0; ks < CK / 32; ++ks) {
@@ -265,6 +284,24 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
                                                 0, 0, 0);
   }
   return o;
+}
+
+template <int CK>
+__device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
+                                                 const uint16_t (*sqh)[kAttnQPitch],
+                                                 const uint16_t (*sql)[kAttnQPitch], int R, float scale, int stride,
+                                                 AttnSmem<CK>& sm) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  float sv[CK / 128][4];
+  attn_scores<CK>(it, kf, sqh, sql, scale, sv);
+  // the V^T fragments, after the score products (the K registers are free)
+  __builtin_amdgcn_sched_barrier(0);
+  AttnRegs<CK> r;
+  attn_load_v<CK>(it, wave, lane, stride, r);
+  __builtin_amdgcn_sched_barrier(0);
+  attn_softmax<CK>(sv, R, sm);
+  attn_mask_tail(it, lane, r);
+  return attn_pv<CK>(sm, r);
 }
 
 // Last-arrival merge of the chunks of one (request, head).
@@ -285,6 +322,14 @@ __device__ __forceinline__ void attn_load16(Rsrc rpo, int c0, int nc, int Rmax, 
   }
 }
 
+// One chunk's term of a merged output: O + w v (a zero weight adds zero
+// whatever v holds), rounded after the product and after the sum, never
+// fused, so every merge gives the same bits.
+__device__ __forceinline__ float attn_acc1(float O, float v, float w) {
+#pragma clang fp contract(off)
+  return O + (w != 0.f ? v * w : 0.f);
+}
+
 // add chunks c0 .. c0 + 15 of output o to O, in chunk order
 __device__ __forceinline__ void attn_acc16(const AttnMergeSmem& ms, int c0, int nc, int o, const float (&v)[16],
                                            float& O) {
@@ -292,10 +337,7 @@ __device__ __forceinline__ void attn_acc16(const AttnMergeSmem& ms, int c0, int 
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     const int c = c0 + j;
-    if (c < nc) {
-      const float w = ms.sc[c][row];
-      O += w != 0.f ? v[j] * w : 0.f;
-    }
+    if (c < nc) O = attn_acc1(O, v[j], ms.sc[c][row]);
   }
 }
 
@@ -350,6 +392,62 @@ __device__ __forceinline__ void attn_publish(const AttnItem& it, floatx4 o, cons
   }
 }
 
+// Merge weights of one row's nc chunks, by one wave (chunk c on lane c % 64,
+// slot c / 64): w_c = exp(m_c - max) / sum_c(l_c exp(m_c - max)), the sum
+// taken per lane in slot order and then across the lanes by butterfly.
+// ml(c, ok, m, l) fetches chunk c's row max and row sum (ok false: no such
+// chunk, values unused); put(c, w) receives each weight after every fetch.
+template <class ML, class PUT>
+__device__ __forceinline__ void attn_row_weights(int nc, ML&& ml, PUT&& put) {
+  const int lane = threadIdx.x & 63;
+  constexpr int NJ = kAttnMaxChunks / 64;
+  float mc[NJ], lc[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int c = lane + 64 * j;
+    const bool ok = c < nc;
+    float m, l;
+    ml(c, ok, m, l);
+    mc[j] = ok ? m : -INFINITY;
+    lc[j] = l;
+  }
+  float Mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) Mx = fmaxf(Mx, mc[j]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, off));
+  float Ls = 0.f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    mc[j] = (mc[j] == -INFINITY) ? 0.f : expf(mc[j] - Mx);
+    Ls += lc[j] * mc[j];
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) Ls += __shfl_xor(Ls, off);
+  const float inv = 1.0f / Ls;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int c = lane + 64 * j;
+    if (c < nc) put(c, mc[j] * inv);
+  }
+}
+
+// Merge weights of the nc chunks of R rows into ms.sc (attn_row_weights, one
+// wave per row: rows wave and wave + 8); ml(c, row, ok, m, l) as there.  All
+// 512 threads call it; the caller synchronises before reading ms.sc.
+template <class ML>
+__device__ __forceinline__ void attn_merge_weights(AttnMergeSmem& ms, int nc, int R, ML&& ml) {
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int row = wave + 8 * k;
+    if (row < R)  // uniform across the wave
+      attn_row_weights(
+          nc, [&](int c, bool ok, float& m, float& l) { ml(c, row, ok, m, l); },
+          [&](int c, float w) { ms.sc[c][row] = w; });
+  }
+}
+
 // Merge the nc chunk partials of (request, head) bh in chunk order and pass
 // each merged output o = row * kAttnHd + dd to out(o, value).  Merge weights
 // of a row: one wave, chunks over its lanes; the weight of chunk c is
@@ -366,46 +464,11 @@ __device__ __forceinline__ void attn_merge(size_t bh, int nc, AttnMergeSmem& ms,
   float va[16], vb[16];
   attn_load16<COH>(rpo, 0, nc, Rmax, tid, tid < nout, va);
   attn_load16<COH>(rpo, 0, nc, Rmax, tid + 512, tid + 512 < nout, vb);
-  constexpr int NJ = kAttnMaxChunks / 64;
-  float mc[2][NJ], lc[2][NJ];
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int row = wave + 8 * k;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int c = lane + 64 * j;
-      const bool ok = row < R && c < nc;
-      const uint32_t off = ok ? (uint32_t)((c * Rmax + row) * 2) * 4u : kOob;
-      const float m = ld_f32<COH>(rpm, off);
-      mc[k][j] = ok ? m : -INFINITY;
-      lc[k][j] = ld_f32<COH>(rpm, off == kOob ? kOob : off + 4u);
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int row = wave + 8 * k;
-    if (row < R) {  // uniform across the wave
-      float Mx = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) Mx = fmaxf(Mx, mc[k][j]);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, off));
-      float Ls = 0.f;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        mc[k][j] = (mc[k][j] == -INFINITY) ? 0.f : expf(mc[k][j] - Mx);
-        Ls += lc[k][j] * mc[k][j];
-      }
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) Ls += __shfl_xor(Ls, off);
-      const float inv = 1.0f / Ls;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        const int c = lane + 64 * j;
-        if (c < nc) ms.sc[c][row] = mc[k][j] * inv;
-      }
-    }
-  }
+  attn_merge_weights(ms, nc, R, [&](int c, int row, bool ok, float& m, float& l) {
+    const uint32_t off = ok ? (uint32_t)((c * Rmax + row) * 2) * 4u : kOob;
+    m = ld_f32<COH>(rpm, off);
+    l = ld_f32<COH>(rpm, off == kOob ? kOob : off + 4u);
+  });
   __syncthreads();
   attn_merge_pair<COH>(rpo, ms, nc, Rmax, nout, tid, va, vb, out);
   for (int oa = tid + 1024; oa < nout; oa += 1024) {
@@ -633,6 +696,316 @@ __device__ __forceinline__ void attn_publish_grp(const AttnItem& it, int kvh, in
     float* pml = part_ml + ((bh * NC + it.c) * Rmax + row) * 2;
     __hip_atomic_store(pml, sa.m[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(pml + 1, sa.l[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Prefill attention: R prompt rows of a request (R > 16), appended at
+// positions L .. L + R - 1, each attending causally to the cache and the
+// rows before it.  The rows form 16-row tiles; tile t is computed as a verify
+// call of its own (L + 16 t cached keys, up to 16 rows), operation for
+// operation, so each row gets the verify path's result bit for bit: the same
+// 256-key chunks, the same scores (the query's two bf16 terms against 16 keys
+// per MFMA output tile, four 32-feature steps each), the same chunk softmax
+// (row max and row sum over each 32-key slice, then over the eight slices in
+// order), the same probabilities' two bf16 terms against V^T in 32-key steps,
+// the same merge weights (attn_row_weights) and the same chunk-order sum
+// (attn_acc1).  A row's result does not depend on which other rows share its
+// tile: every product and reduction of a chunk is per row, and chunks past a
+// row's position get weight zero.
+//
+// Where the verify kernel spreads one chunk over eight waves, here one wave
+// runs a whole tile: the eight 32-key slices of a chunk one after another,
+// with no barrier between them.  The W waves of a workgroup take W
+// consecutive tiles of one (request, head) and share every K and V^T block:
+// SK keys at a time, staged through a two-slot LDS ring (rows of 16-byte
+// pieces XOR-swizzled by row, so the 16 rows a fragment read touches hit
+// distinct banks), the next block's loads in flight while the current one is
+// used.  Each chunk is walked twice: the first walk keeps every chunk's row
+// max and row sum in LDS, the merge weights follow from them, and the second
+// walk recomputes each chunk's probabilities, multiplies them with V and adds
+// the result, times its weight, to the tile's running sums in registers.
+// ---------------------------------------------------------------------------
+template <int W, int SK>
+struct AttnPfSmem {
+  static_assert(SK == 64 || SK == 128, "staged blocks of 64 or 128 keys");
+  uint4 st[2][SK * 16];                    // K: SK rows of 16 pieces; V^T: 128 rows of SK / 8 pieces
+  uint16_t ph[W][16][40], pl[W][16][40];  // one 32-key step's probabilities, per wave (rows padded by 16 bytes)
+};
+
+// Dynamic LDS of the prefill attention: per wave, chunk and row a (max, sum)
+// pair, then the merge weight in .x.
+__host__ __device__ inline unsigned attn_prefill_dyn_bytes(int W, int NC) { return (unsigned)W * NC * 16 * 8; }
+
+// piece c (8 features) of staged K row r; piece c (8 keys) of staged V^T row f
+__device__ __forceinline__ int pf_k_at(int r, int c) { return r * 16 + (c ^ (r & 15)); }
+template <int SK>
+__device__ __forceinline__ int pf_v_at(int f, int c) {
+  constexpr int CPR = SK / 8;
+  return f * CPR + (CPR == 16 ? (c ^ (f & 15)) : (c ^ ((f >> 1) & 7)));
+}
+
+// This thread's share of staged block b of chunk c: K (b < 256 / SK: keys
+// c * 256 + b * SK ..) or V^T (keys c * 256 + (b - 256 / SK) * SK ..).  Keys
+// at or past k_hi (V^T: 8-key pieces past ke) read as zero.
+template <int W, int SK>
+__device__ __forceinline__ void pf_fetch(int c, int b, int k_hi, int ke, const uint16_t* kc, const uint16_t* vc,
+                                         int stride, uint4 (&r)[SK * 16 / (64 * W)]) {
+  constexpr int PER = SK * 16 / (64 * W), NB = 256 / SK, CPR = SK / 8;
+  const bool is_v = b >= NB;
+  const int k0 = c * 256 + (is_v ? b - NB : b) * SK;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = (int)threadIdx.x + 64 * W * q;
+    r[q] = make_uint4(0, 0, 0, 0);
+    if (!is_v) {
+      const int row = e >> 4, pc = e & 15;
+      if (k0 + row < k_hi) r[q] = *(const uint4*)(kc + (size_t)(k0 + row) * kAttnHd + pc * 8);
+    } else {
+      const int f = e / CPR, pc = e % CPR, key = k0 + 8 * pc;
+      if (key + 8 <= ke) r[q] = *(const uint4*)(vc + (size_t)f * stride + key);
+    }
+  }
+}
+
+template <int W, int SK>
+__device__ __forceinline__ void pf_stash(AttnPfSmem<W, SK>& s, int slot, int b, const uint4 (&r)[SK * 16 / (64 * W)]) {
+  constexpr int PER = SK * 16 / (64 * W), NB = 256 / SK, CPR = SK / 8;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = (int)threadIdx.x + 64 * W * q;
+    s.st[slot][b < NB ? pf_k_at(e >> 4, e & 15) : pf_v_at<SK>(e / CPR, e % CPR)] = r[q];
+  }
+}
+
+// Wave-local ordering of LDS traffic between the lanes of one wave.
+__device__ __forceinline__ void pf_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// q: this request's query rows ([R][d], head h's features at h * kAttnHd);
+// kc / vc: K rows and V^T rows of (request, K/V head); L: the request's
+// cached keys; t0: the group's first tile (tile t0 + wave for this wave).
+// out(row, dd, value) receives every output of the group's rows (row counted
+// from the request's first prompt row).  mlw: W * NCP * 16 pairs; NCP bounds
+// the chunks of any tile.  All 64 W threads call it.
+template <int W, int SK, class Out>
+__device__ __forceinline__ void attn_prefill_tiles(AttnPfSmem<W, SK>& s, float2* mlw, int NCP, const float* q,
+                                                   int d, int h, const uint16_t* kc, const uint16_t* vc, int L,
+                                                   int R, int t0, float scale, int stride, Out&& out) {
+  constexpr int NB = 256 / SK, SPB = SK / 32, PER = SK * 16 / (64 * W);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int g = lane >> 4, kl = lane & 15;
+  const int ntile = (R + 15) / 16;
+  const int tl = t0 + wave;                            // this wave's tile
+  const int Rt = tl < ntile ? min(16, R - 16 * tl) : 0;  // its rows (0: idle)
+  const int Lt = L + 16 * tl;
+  const int nct = Rt > 0 ? (Lt + Rt + 255) / 256 : 0;
+  // the group's furthest key: the end of its last tile
+  const int tlast = min(t0 + W, ntile) - 1;
+  const int kend = L + 16 * tlast + min(16, R - 16 * tlast);
+  const int ncg = (kend + 255) / 256;
+  float2* ml = mlw + (size_t)wave * NCP * 16;
+
+  // this lane's query fragments (row kl of the tile, features 32 ks + 8 g ..),
+  // as two bf16 terms; rows past the tile: zeros
+  uint4 qh[4], ql[4];
+  {
+    const bool ok = kl < Rt;
+    const float* qr = q + (size_t)(16 * tl + kl) * d + h * kAttnHd;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = 0.f;
+      if (ok) {
+        const float4 a = *(const float4*)(qr + 32 * ks + 8 * g), b = *(const float4*)(qr + 32 * ks + 8 * g + 4);
+        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+      }
+      attn_split2(x, qh[ks], ql[ks]);
+    }
+  }
+
+  // scores of staged K block b (slices b * SPB ..) of chunk c into sv
+  auto scores = [&](const uint4* blk, int c, int b, float (&sv)[8][2][4]) {
+    const int k_lo = c * 256, k_hi = min(k_lo + 256, Lt + Rt);
+#pragma unroll
+    for (int j = 0; j < SPB; ++j) {
+      const int vw = b * SPB + j;  // the slice (the verify kernel's wave)
+#pragma unroll
+      for (int grp = 0; grp < 2; ++grp) {
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        const int r = 32 * j + 16 * grp + kl;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const uint4 kf = blk[pf_k_at(r, 4 * ks + g)];
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql[ks]),
+                                                        __builtin_bit_cast(bf16x8, kf), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh[ks]),
+                                                        __builtin_bit_cast(bf16x8, kf), acc, 0, 0, 0);
+        }
+        const int key = k_lo + 32 * vw + 16 * grp + kl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          sv[vw][grp][i] = (key < k_hi && key <= Lt + 4 * g + i) ? acc[i] * scale : -INFINITY;
+      }
+    }
+  };
+  // chunk softmax of sv: probabilities in place, and each row's max and sum
+  auto softmax = [&](float (&sv)[8][2][4], float (&m)[4], float (&l)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float mw[8];
+#pragma unroll
+      for (int vw = 0; vw < 8; ++vw) mw[vw] = row16_max(fmaxf(sv[vw][0][i], sv[vw][1][i]));
+      const float M = fmaxf(fmaxf(fmaxf(mw[0], mw[1]), fmaxf(mw[2], mw[3])), fmaxf(fmaxf(mw[4], mw[5]), fmaxf(mw[6], mw[7])));
+      float lsum = 0.f, mm = -INFINITY;
+#pragma unroll
+      for (int vw = 0; vw < 8; ++vw) {
+        float sum = 0.f;
+#pragma unroll
+        for (int grp = 0; grp < 2; ++grp) {
+          const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[vw][grp][i] - M) * 1.44269504088896341f);
+          sum += e;
+          sv[vw][grp][i] = e;
+        }
+        lsum += row16_sum(sum);
+        mm = fmaxf(mm, mw[vw]);
+      }
+      m[i] = mm;
+      l[i] = lsum;
+    }
+  };
+
+  uint4 pre[PER];
+  // first walk: every chunk's row max and row sum
+  pf_fetch<W, SK>(0, 0, kend, 0, kc, vc, stride, pre);
+  pf_stash(s, 0, 0, pre);
+  __syncthreads();
+  int slot = 0;
+  for (int c = 0; c < ncg; ++c) {
+    float sv[8][2][4];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const bool more = b + 1 < NB || c + 1 < ncg;
+      if (more) pf_fetch<W, SK>(b + 1 < NB ? c : c + 1, b + 1 < NB ? b + 1 : 0, kend, 0, kc, vc, stride, pre);
+      if (c < nct) scores(s.st[slot], c, b, sv);
+      if (more) pf_stash(s, slot ^ 1, 0, pre);
+      __syncthreads();
+      slot ^= 1;
+    }
+    if (c < nct) {
+      float m[4], l[4];
+      softmax(sv, m, l);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (kl == 0 && 4 * g + i < Rt) ml[c * 16 + 4 * g + i] = make_float2(m[i], l[i]);
+    }
+  }
+  // merge weights of this wave's rows, in place of (max, sum)
+  pf_wave_sync();
+  for (int row = 0; row < Rt; ++row)
+    attn_row_weights(
+        nct,
+        [&](int c, bool ok, float& m, float& l) {
+          const float2 v = ok ? ml[c * 16 + row] : make_float2(0.f, 0.f);
+          m = v.x;
+          l = v.y;
+        },
+        [&](int c, float w) { ml[c * 16 + row].x = w; });
+  pf_wave_sync();
+
+  // second walk: K blocks (scores, softmax), then V^T blocks (P V), per chunk
+  const int keg = (kend + 7) & ~7;
+  float O[8][4];
+#pragma unroll
+  for (int fb = 0; fb < 8; ++fb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) O[fb][i] = 0.f;
+  pf_fetch<W, SK>(0, 0, kend, keg, kc, vc, stride, pre);
+  pf_stash(s, slot, 0, pre);
+  __syncthreads();
+  for (int c = 0; c < ncg; ++c) {
+    const int k_lo = c * 256, k_hi = min(k_lo + 256, Lt + Rt);
+    float sv[8][2][4];
+    floatx4 o[8];
+#pragma unroll
+    for (int fb = 0; fb < 8; ++fb) o[fb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < 2 * NB; ++b) {
+      const bool more = b + 1 < 2 * NB || c + 1 < ncg;
+      if (more) pf_fetch<W, SK>(b + 1 < 2 * NB ? c : c + 1, b + 1 < 2 * NB ? b + 1 : 0, kend, keg, kc, vc, stride, pre);
+      if (c < nct) {
+        if (b < NB) {
+          scores(s.st[slot], c, b, sv);
+          if (b == NB - 1) {
+            float m[4], l[4];
+            softmax(sv, m, l);
+          }
+        } else {
+          const uint4* blk = s.st[slot];
+#pragma unroll
+          for (int j = 0; j < SPB; ++j) {
+            const int ks = (b - NB) * SPB + j;  // 32-key step of the chunk
+            // this step's probabilities, as two bf16 terms, through LDS into
+            // the A-operand layout (row kl, keys 8 g ..)
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const float e = sv[ks][grp][i];
+                const uint16_t hb = f2bf_num(e);
+                s.ph[wave][4 * g + i][16 * grp + kl] = hb;
+                s.pl[wave][4 * g + i][16 * grp + kl] = f2bf_num(e - bf2f(hb));
+              }
+            pf_wave_sync();
+            const uint4 pa_h = *(const uint4*)&s.ph[wave][kl][8 * g];
+            const uint4 pa_l = *(const uint4*)&s.pl[wave][kl][8 * g];
+            const int kv0 = k_lo + 32 * ks + 8 * g;
+#pragma unroll
+            for (int fb = 0; fb < 8; ++fb) {
+              uint4 vf = blk[pf_v_at<SK>(16 * fb + kl, 4 * j + g)];
+              if (kv0 + 8 > k_hi) {  // this tile's keys only (the verify kernel's tail mask)
+                uint32_t wv[4] = {vf.x, vf.y, vf.z, vf.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const int p0 = kv0 + 2 * e;
+                  if (p0 >= k_hi) wv[e] = 0u;
+                  else if (p0 + 1 >= k_hi) wv[e] &= 0xffffu;
+                }
+                vf = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+              }
+              o[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pa_l),
+                                                              __builtin_bit_cast(bf16x8, vf), o[fb], 0, 0, 0);
+              o[fb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pa_h),
+                                                              __builtin_bit_cast(bf16x8, vf), o[fb], 0, 0, 0);
+            }
+            pf_wave_sync();
+          }
+        }
+      }
+      if (more) pf_stash(s, slot ^ 1, b + 1 < 2 * NB ? b + 1 : 0, pre);
+      __syncthreads();
+      slot ^= 1;
+    }
+    if (c < nct) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 4 * g + i;
+        const float w = row < Rt ? ml[c * 16 + row].x : 0.f;
+#pragma unroll
+        for (int fb = 0; fb < 8; ++fb) O[fb][i] = attn_acc1(O[fb][i], o[fb][i], w);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * g + i;
+    if (row < Rt)
+#pragma unroll
+      for (int fb = 0; fb < 8; ++fb) out(16 * tl + row, 16 * fb + kl, O[fb][i]);
   }
 }
 

@@ -722,6 +722,32 @@ __global__ void __launch_bounds__(kAttnThreads) attn_merge_kernel(AttnParams p) 
   });
 }
 
+// Prefill attention of a forward with more than 16 rows per request
+// (device_attn.h: attn_prefill_tiles): workgroup (group of W 16-row tiles,
+// query head, request), one wave per tile.  Every tile group and query head
+// of one (request, K/V head) runs on the same XCD, so that pair's keys and
+// values, read by all of them, stay in one L2; on each XCD the groups with
+// the most chunks start first.  Dynamic LDS: attn_prefill_dyn_bytes(W, NC).
+template <bool ABF16, int W, int SK>
+__global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2)))
+attn_prefill_kernel(AttnParams p, int ngrp) {
+  __shared__ AttnPfSmem<W, SK> s;
+  extern __shared__ uint4 lds_dyn[];
+  const int i = blockIdx.x, x = i & 7, j = i >> 3;
+  const int per = p.G * ngrp;
+  const int pair = 8 * (j / per) + x, rem = j % per;
+  if (pair >= p.nb * p.Hkv) return;
+  const int gq = rem / ngrp, grp = ngrp - 1 - rem % ngrp;
+  const int bl = pair / p.Hkv, kvh = pair % p.Hkv, h = kvh * p.G + gq, bg = p.b0 + bl;
+  const size_t head_off = ((size_t)bg * p.Hkv + kvh) * p.kv_stride * kAttnHd;
+  attn_prefill_tiles<W, SK>(s, (float2*)lds_dyn, p.NC, p.q + (size_t)bl * p.R * p.d, p.d, h,
+                            (const uint16_t*)p.kc + head_off, (const uint16_t*)p.vc + head_off, p.lens[bg], p.R,
+                            grp * W, p.scale, p.kv_stride, [&](int row, int dd, float O) {
+                              store_act<ABF16>(p.act_out, p.act_split,
+                                               (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
+                            });
+}
+
 // ---------------------------------------------------------------------------
 // Accept / reject and the correction draw (device_accept.h), one workgroup per
 // request.
@@ -813,30 +839,38 @@ __global__ void advance_kernel(int b, int count, int32_t* lens, int32_t* pending
   }
 }
 
-// Batched prefill: the next R prompt tokens of every request (0 past a
-// request's end: a placeholder row, written past its length), each
-// request's length advanced by its real tokens, and the pending tokens.
+// Batched prefill.  A forward takes the next R prompt tokens of requests
+// [b0, b0 + nb), each from the offset it has reached (its length now minus
+// its length when the prefill began; 0 past its end: a placeholder row,
+// written past its length); each length then advances by its real tokens;
+// last, the pending tokens.
 struct PrefillCounts {
   int n[64];
 };
 
-__global__ void prefill_counts_kernel(PrefillCounts c, int b0, int nb, int32_t* dst) {
+__global__ void prefill_counts_kernel(PrefillCounts c, int b0, int nb, int32_t* dst, const int32_t* lens,
+                                      int32_t* base) {
   const int i = threadIdx.x;
-  if (i < nb) dst[b0 + i] = c.n[i];
+  if (i < nb) {
+    dst[b0 + i] = c.n[i];
+    base[b0 + i] = lens[b0 + i];
+  }
 }
 
-__global__ void prefill_gather_kernel(const int32_t* tokens, int ld, const int32_t* n_cache, int B, int R, int c0,
-                                      int32_t* out) {
+__global__ void prefill_gather_kernel(const int32_t* tokens, int ld, const int32_t* n_cache, const int32_t* base,
+                                      const int32_t* lens, int b0, int nb, int R, int32_t* out) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= B * R) return;
-  const int b = m / R, pos = c0 + m % R;
-  out[m] = pos < n_cache[b] ? tokens[(size_t)b * ld + pos] : 0;
+  if (m >= nb * R) return;
+  const int b = b0 + m / R, pos = lens[b] - base[b] + m % R;
+  out[m] = (pos >= 0 && pos < n_cache[b]) ? tokens[(size_t)b * ld + pos] : 0;
 }
 
-__global__ void prefill_advance_kernel(int B, int R, int c0, const int32_t* n_cache, int32_t* lens) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b < B) {
-    const int rem = n_cache[b] - c0;
+__global__ void prefill_advance_kernel(int b0, int nb, int R, const int32_t* n_cache, const int32_t* base,
+                                       int32_t* lens) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < nb) {
+    const int b = b0 + i;
+    const int rem = n_cache[b] - (lens[b] - base[b]);
     lens[b] += rem <= 0 ? 0 : (rem < R ? rem : R);
   }
 }
@@ -1123,6 +1157,24 @@ hipError_t launch_wide(spade_model md, int kind, const GemmParams& gp, hipStream
   }
 }
 
+hipError_t launch_attn_prefill(const AttnParams& ap, bool abf16, hipStream_t st) {
+  constexpr int W = kPrefillAttnTiles, SK = kPrefillAttnKeys;
+  const int most = (int)attn_prefill_dyn_bytes(W, kAttnMaxChunks);
+  static hipError_t attr_b = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_prefill_kernel<true, W, SK>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, most);
+  static hipError_t attr_f = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_prefill_kernel<false, W, SK>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, most);
+  if (attr_b != hipSuccess) return attr_b;
+  if (attr_f != hipSuccess) return attr_f;
+  if (ap.NC > kAttnMaxChunks) return hipErrorInvalidValue;
+  const int ngrp = ((ap.R + 15) / 16 + W - 1) / W;
+  const dim3 grid(8 * ((ap.nb * ap.Hkv + 7) / 8) * ap.G * ngrp);
+  const unsigned dyn = attn_prefill_dyn_bytes(W, ap.NC);
+  if (abf16) hipLaunchKernelGGL((attn_prefill_kernel<true, W, SK>), grid, dim3(64 * W), dyn, st, ap, ngrp);
+  else hipLaunchKernelGGL((attn_prefill_kernel<false, W, SK>), grid, dim3(64 * W), dyn, st, ap, ngrp);
+  return hipGetLastError();
+}
+
 template <int HD, int RMAX>
 hipError_t launch_attn_r(const AttnParams& ap, bool kvbf16, bool abf16, dim3 grid, hipStream_t st) {
   if (kvbf16 && abf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, true, true>), grid, dim3(256), 0, st, ap);
@@ -1300,8 +1352,12 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
   // head_dim 128 the 8-wave MFMA kernel, else kAttnChunk
   int max_keys = 0;
   for (int b = fc.b0; b < fc.b0 + fc.nb; ++b) max_keys = std::max(max_keys, kv->lens_ub[b] + fc.R);
-  const bool mfma_attn = D.kvdt == SPADE_BF16 && D.hd == kAttnHd && fc.R <= kAttnRows;
-  const int CK = mfma_attn ? kAttnChunkKeys : kAttnChunk;
+  const bool tiled = D.kvdt == SPADE_BF16 && D.hd == kAttnHd;
+  const bool mfma_attn = tiled && fc.R <= kAttnRows;
+  // more rows per request than one verify call: the prefill attention
+  const bool prefill_attn = fc.R > kAttnRows;
+  if (prefill_attn && (!tiled || fc.tokens == nullptr || fc.want_logits)) return hipErrorInvalidValue;
+  const int CK = tiled ? kAttnChunkKeys : kAttnChunk;
   const int NC = (max_keys + CK - 1) / CK;
   if (NC > W.NCmax || NC > kAttnMaxChunks) return hipErrorInvalidValue;
   // every request's keys must fit the cache and the chunks launched below
@@ -1350,7 +1406,9 @@ hipError_t launch_forward(spade_model md, spade_kv kv, const ForwardCall& fc, hi
     const dim3 agrid(NC, D.H, fc.nb);
     const bool kvb = D.kvdt == SPADE_BF16;
     ap.nb = fc.nb;
-    if (mfma_attn && two_pass) {
+    if (prefill_attn) {
+      e = launch_attn_prefill(ap, wb, st);
+    } else if (mfma_attn && two_pass) {
       // grouped-query models: one workgroup per K/V head and chunk for the
       // G query heads when their G R rows fit three 16-row tiles (8B-GQA
       // batched: 13.42 -> 13.09 ms)
@@ -1585,6 +1643,32 @@ hipError_t launch_copy_state(int B, int32_t* lens, int32_t* pending, const int32
   return hipGetLastError();
 }
 
+namespace {
+
+// Prompt rows of one prefill forward, per request and in all.  A bf16 cache
+// with head_dim 128 takes up to the workspace's rows (the prefill attention
+// covers any number of rows per request; the projections then run on the
+// wide-row GEMM, every weight tile read once per launch for all rows); other
+// caches take kPrefillRows per request (the verify attention's limit).  A
+// model setting can lower the rows per request.
+void prefill_caps(spade_model md, int* r_cap, int* m_cap) {
+  const Dims& D = md->dims;
+  const bool tiled = D.kvdt == SPADE_BF16 && D.hd == kAttnHd;
+  int r = tiled ? md->ws.Mrows : kPrefillRows;
+  if (md->prefill_rows > 0) r = std::min(r, md->prefill_rows);
+  *m_cap = tiled ? md->ws.Mrows : md->ws.Mmax;
+  *r_cap = std::min(r, *m_cap);
+}
+
+}  // namespace
+
+// Requests go through in index order, in ranges [b0, b0 + nb) with R rows
+// each: a range starts at the first request with tokens left (R = its
+// remaining tokens, up to the caps) and takes in the next requests while all
+// nb R rows fit the workspace, every request of the range has R free
+// positions in the cache, and at least half the rows are real tokens.  Rows
+// depend only on their own token and position, so the cache comes out the
+// same as from spade_prefill of each request.
 hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_t* tokens, int ld,
                                 const int* n_cache, hipStream_t st) {
   const Workspace& W = md->ws;
@@ -1592,29 +1676,52 @@ hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_
     PrefillCounts c{};
     const int nb = std::min(64, B - b0);
     for (int i = 0; i < nb; ++i) c.n[i] = n_cache[b0 + i];
-    hipLaunchKernelGGL(prefill_counts_kernel, dim3(1), dim3(64), 0, st, c, b0, nb, W.prefill_cnt);
+    hipLaunchKernelGGL(prefill_counts_kernel, dim3(1), dim3(64), 0, st, c, b0, nb, W.prefill_cnt, kv->lens,
+                       W.prefill_base);
   }
-  int mx = 0;
-  for (int b = 0; b < B; ++b) mx = std::max(mx, n_cache[b]);
-  const int R = std::max(1, std::min(kPrefillRows, W.Mmax / B));
+  int r_cap, m_cap;
+  prefill_caps(md, &r_cap, &m_cap);
+  std::vector<int> rem(n_cache, n_cache + B);
   hipError_t e = hipGetLastError();
-  for (int c0 = 0; c0 < mx && e == hipSuccess; c0 += R) {
-    hipLaunchKernelGGL(prefill_gather_kernel, dim3((B * R + 255) / 256), dim3(256), 0, st, tokens, ld, W.prefill_cnt,
-                       B, R, c0, W.prefill_tok);
+  int b0 = 0;
+  while (e == hipSuccess) {
+    while (b0 < B && rem[b0] == 0) ++b0;
+    if (b0 == B) break;
+    int R = std::min(rem[b0], r_cap), nb = 1;
+    int top = kv->lens_ub[b0];  // the longest cached length of the range
+    while (b0 + nb < B) {
+      const int c = b0 + nb;
+      const int R2 = std::max(R, std::min(rem[c], r_cap));
+      const int top2 = std::max(top, kv->lens_ub[c]);
+      if ((long)(nb + 1) * R2 > m_cap || top2 + R2 > kv->max_len) break;
+      long real2 = 0;
+      for (int b = b0; b <= c; ++b) real2 += std::min(rem[b], R2);
+      if (2 * real2 < (long)(nb + 1) * R2) break;
+      R = R2;
+      top = top2;
+      ++nb;
+    }
+    hipLaunchKernelGGL(prefill_gather_kernel, dim3((nb * R + 255) / 256), dim3(256), 0, st, tokens, ld,
+                       W.prefill_cnt, W.prefill_base, kv->lens, b0, nb, R, W.prefill_tok);
     ForwardCall fc{};
-    fc.b0 = 0;
-    fc.nb = B;
+    fc.b0 = b0;
+    fc.nb = nb;
     fc.R = R;
     fc.tokens = W.prefill_tok;
     fc.want_logits = false;
     e = launch_forward(md, kv, fc, st);
     if (e == hipSuccess) {
-      hipLaunchKernelGGL(prefill_advance_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, R, c0, W.prefill_cnt, kv->lens);
+      hipLaunchKernelGGL(prefill_advance_kernel, dim3((nb + 63) / 64), dim3(64), 0, st, b0, nb, R, W.prefill_cnt,
+                         W.prefill_base, kv->lens);
       e = hipGetLastError();
     }
     // the host bound of lens follows the device lengths (the next forward
     // sizes its attention grid from it)
-    for (int b = 0; b < B; ++b) kv->lens_ub[b] += std::max(0, std::min(R, n_cache[b] - c0));
+    for (int b = b0; b < b0 + nb; ++b) {
+      const int t = std::min(rem[b], R);
+      rem[b] -= t;
+      kv->lens_ub[b] += t;
+    }
   }
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(prefill_pending_kernel, dim3((B + 63) / 64), dim3(64), 0, st, B, tokens, ld, W.prefill_cnt,
@@ -1622,7 +1729,27 @@ hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_
   return hipGetLastError();
 }
 
-int prefill_batch_rows(spade_model md, int B) { return std::max(1, std::min(kPrefillRows, md->ws.Mmax / B)); }
+// One request: forwards of up to the caps' rows over its prompt, then its
+// last token becomes pending.
+hipError_t launch_prefill_one(spade_model md, spade_kv kv, int b, const int32_t* tokens, int n_cache,
+                              hipStream_t st) {
+  int r_cap, m_cap;
+  prefill_caps(md, &r_cap, &m_cap);
+  for (int s = 0; s < n_cache;) {
+    ForwardCall fc{};
+    fc.b0 = b;
+    fc.nb = 1;
+    fc.R = std::min(r_cap, n_cache - s);
+    fc.tokens = tokens + s;
+    fc.want_logits = false;
+    hipError_t e = launch_forward(md, kv, fc, st);
+    if (e == hipSuccess) e = launch_advance(kv, b, fc.R, nullptr, st);
+    if (e != hipSuccess) return e;
+    kv->lens_ub[b] += fc.R;
+    s += fc.R;
+  }
+  return launch_advance(kv, b, 0, tokens + n_cache, st);
+}
 
 hipError_t launch_advance(spade_kv kv, int b, int count, const int32_t* pending_src, hipStream_t st) {
   hipLaunchKernelGGL(advance_kernel, dim3(1), dim3(64), 0, st, b, count, kv->lens, kv->pending, pending_src);

@@ -14,7 +14,10 @@ constexpr int kPanel = 16;           // weight rows per MFMA tile (one panel)
 constexpr int kTileBytes = 8192;     // one panel x one k-block, in the arena
 constexpr int kMaxRowsPerGemm = 32;  // rows handled by one skinny-GEMM launch
 constexpr int kWideMinRows = 16;     // bf16 projections with more rows use the wide-row GEMM
-constexpr int kPrefillRows = 16;     // tokens per prefill forward
+constexpr int kPrefillRows = 16;     // prompt rows per request of a prefill forward on the verify attention
+constexpr int kPrefillMaxRows = 2048;  // rows of a prefill forward (bf16 cache, head_dim 128)
+constexpr int kPrefillAttnTiles = 4;   // 16-row tiles (one wave each) per workgroup of the prefill attention
+constexpr int kPrefillAttnKeys = 64;   // keys per K or V^T block it stages in LDS
 constexpr int kMaxR = 16;            // rows per request in one forward (gamma <= 15)
 constexpr int kCorrMaxSlices = 256; // vocabulary slices of one correction draw
 constexpr int kNoAllocMaxB = 64;     // requests of one spade_accept_from_logits_noalloc call
@@ -30,6 +33,7 @@ inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
 // requests of the batch.  256 keys: 78 VGPRs and 35 KB of LDS per 8-wave
 // workgroup of the one-chunk kernel, three workgroups per compute unit.
 constexpr int kAttnChunkKeys = 256;
+constexpr int kAttnHd = 128;  // head_dim of the MFMA attention kernels (bf16 cache)
 
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GU = 2, GEMM_DOWN = 3, GEMM_LM = 4 };
 
@@ -81,12 +85,12 @@ struct ArenaLayout {
 
 // Sub-buffers of the caller's workspace.
 struct Workspace {
-  float* x;           // [Mmax][d] residual stream
-  void* act_n;        // normed GEMM input, split bf16 [S][Mmax][d] or f32 [Mmax][d]
+  float* x;           // [Mrows][d] residual stream
+  void* act_n;        // normed GEMM input, split bf16 [S][Mrows][d] or f32 [Mrows][d]
   void* act_o;        // attention output (O-projection input)
-  void* act_f;        // SwiGLU output (down-projection input) [S][Mmax][F]
-  float* ssq;         // [Mmax][d/16] sum-of-squares partials of x
-  float* q;           // [Mmax][d] rotated queries
+  void* act_f;        // SwiGLU output (down-projection input) [S][Mrows][F]
+  float* ssq;         // [Mrows][d/16] sum-of-squares partials of x
+  float* q;           // [Mrows][d] rotated queries
   float* attn_o;      // [Bmax][H][NCmax][Rmax][hd] chunk partial outputs
   float* attn_ml;     // [Bmax][H][NCmax][Rmax][2] chunk max / sum
   uint32_t* attn_cnt; // [Bmax][H] arrival counters (kept at zero between calls)
@@ -102,11 +106,14 @@ struct Workspace {
   float* corr_lse;      // [Bmax] log-sum-exp of each sampling request's correction row
   float* corr_part;     // [Bmax][kCorrMaxSlices][4] per-slice winners of the correction draw
   uint32_t* corr_cnt;   // [Bmax] arrival counters of the correction slices (kept at zero between calls)
-  int32_t* prefill_tok; // [Mmax] token ids of one batched-prefill forward
+  int32_t* prefill_tok; // [Mrows] token ids of one batched-prefill forward
   int32_t* prefill_cnt; // [Bmax] prompt tokens to cache per request (batched prefill)
+  int32_t* prefill_base; // [Bmax] each request's length when its batched prefill began
   size_t act_split;   // elements between splits of act_n / act_o
   size_t actf_split;  // elements between splits of act_f
-  int Mmax, NCmax, Rmax;
+  int Mmax;   // rows of a verify call (logits, LM-head statistics)
+  int Mrows;  // rows of any forward (activations): Mmax, or more for prefill
+  int NCmax, Rmax;
 };
 
 }  // namespace spade
@@ -129,6 +136,7 @@ struct spade_model_s {
   int attn_merge;  // merge of one-chunk attention partials: 0 chosen per call, 1 last arrival, 2 second launch
   int attn_grouped;  // grouped-query chunks (one workgroup per K/V head and chunk): 0 where they apply, 1 off
   int corr_split;  // correction draws of sampling requests: 0/2 over vocabulary slices, 1 in the accept workgroup
+  int prefill_rows;  // prompt rows per request of a prefill forward: 0 as many as the workspace holds, else at most this
 };
 
 struct spade_kv_s {
@@ -186,7 +194,8 @@ int lm_stats_panels(spade_model m, int M);
 hipError_t launch_softmax(const float* logits, int rows, int V, float invT, float* out, hipStream_t st);
 hipError_t launch_prefill_batch(spade_model md, spade_kv kv, int B, const int32_t* tokens, int ld,
                                 const int* n_cache, hipStream_t st);
-int prefill_batch_rows(spade_model md, int B);
+hipError_t launch_prefill_one(spade_model md, spade_kv kv, int b, const int32_t* tokens, int n_cache,
+                              hipStream_t st);
 hipError_t launch_layer_gemm(spade_model m, spade_kv kv, int kind, int layer, const ForwardCall& fc,
                              hipStream_t st);
 hipError_t launch_accept(spade_model m, const AcceptCall& ac, hipStream_t st);

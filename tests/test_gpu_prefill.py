@@ -1,12 +1,17 @@
-"""Batched prefill (spade_prefill_batch) against per-request prefill.
+"""Prefill paths against per-request prefill at 16 rows per forward.
 
-All requests' next chunks run in one forward; a request whose prompt is used
-up contributes placeholder rows past its length.  A cached key depends only
-on its own token and the keys before it, so the cache contents, lengths and
-pending tokens must be bit-identical to prefilling each request alone, and so
-must the logits and decisions of the verify call that follows.  Ragged prompt
-lengths (including a prompt of one token: nothing to cache) and both the
-multi-head and the grouped-query mini shapes.
+spade_prefill_batch runs ranges of requests per forward; with a bf16 cache
+and head_dim 128 a forward takes up to all of a request's prompt (the
+prefill attention: 16-row tiles, each computed as a verify call of its
+own), else 16 rows per request.  A cached key depends only on its own token
+and the keys before it, so the cache contents, lengths and pending tokens
+must be bit-identical to prefilling each request alone 16 rows at a time
+(the verify attention), and so must the logits and decisions of the verify
+call that follows.  Ragged prompt lengths (including a prompt of one token:
+nothing to cache), a cap of 40 rows per request (tiles that end mid-tile,
+several forwards per request), a prompt prefilled in two parts (a second
+part that starts off a tile boundary), and the multi-head, wide and
+grouped-query mini shapes; the float32 / head_dim-64 shape keeps 16 rows.
 """
 
 import numpy as np
@@ -17,6 +22,8 @@ from tests.helpers import gpu_setup, gpu_verify
 
 pytestmark = pytest.mark.gpu
 
+MINIS = {w.name: w for w in mini_workloads()}
+
 
 @pytest.fixture(scope="module", autouse=True)
 def need_gpu():
@@ -25,41 +32,21 @@ def need_gpu():
         pytest.skip("no GPU")
 
 
-def _cases():
-    ws = {w.name: w for w in mini_workloads()}
-    return [ws["mini_bf16_mixed"], ws["mini_gqa_mixed_b5"], ws["mini_f32_greedy"]]
-
-
-@pytest.mark.parametrize("w", _cases(), ids=lambda w: w.name)
-def test_batched_prefill_equals_per_request(w):
+def _assert_same_cache(model, kv1, kv2, B, max_len):
     import torch
-    weights = ModelWeights(w.model, w.seed)
-    inp = make_inputs(w)
-    prompts = [np.asarray(p) for p in inp.prompts]
-    prompts[0] = prompts[0][:1]  # nothing to cache for request 0
-    inp.prompts = prompts
-    max_len = max(len(p) for p in prompts) + 2 * (w.gamma + 1) + 24
-    model, kv1 = gpu_setup(w, weights, max_len=max_len)
-    from paper_2608_13076_amd import spade
-    kv2 = spade.KVCache(model, w.batch, max_len)
-    print(f"[{w.name}] prompts {[len(p) for p in prompts]}", flush=True)
-    for b, p in enumerate(prompts):
-        kv1.prefill(b, p)
-    kv2.prefill_batch(prompts)
-    l1, p1 = kv1.get_state(w.batch)
-    l2, p2 = kv2.get_state(w.batch)
+    l1, p1 = kv1.get_state(B)
+    l2, p2 = kv2.get_state(B)
     np.testing.assert_array_equal(l1, l2)
     np.testing.assert_array_equal(p1, p2)
-    # cache contents up to each request's length
     half = kv1.buf.numel() // 2
     s = model.shape
     stride = (max_len + 31) // 32 * 32
     elt = torch.int16 if s.kv_dtype == "bf16" else torch.float32
-    n_el = s.n_layers * w.batch * s.kv_heads * stride * s.head_dim
+    n_el = s.n_layers * B * s.kv_heads * stride * s.head_dim
     for which, part in (("k", slice(0, half)), ("v", slice(half, 2 * half))):
-        a = kv1.buf[part].view(elt)[:n_el].view(s.n_layers, w.batch, s.kv_heads, stride * s.head_dim)
-        c = kv2.buf[part].view(elt)[:n_el].view(s.n_layers, w.batch, s.kv_heads, stride * s.head_dim)
-        for b in range(w.batch):
+        a = kv1.buf[part].view(elt)[:n_el].view(s.n_layers, B, s.kv_heads, stride * s.head_dim)
+        c = kv2.buf[part].view(elt)[:n_el].view(s.n_layers, B, s.kv_heads, stride * s.head_dim)
+        for b in range(B):
             n = int(l1[b])
             if which == "k":  # K rows [pos][hd]
                 ka = a[:, b].reshape(s.n_layers, s.kv_heads, stride, s.head_dim)[:, :, :n]
@@ -68,8 +55,70 @@ def test_batched_prefill_equals_per_request(w):
                 ka = a[:, b].reshape(s.n_layers, s.kv_heads, s.head_dim, stride)[..., :n]
                 kc = c[:, b].reshape(s.n_layers, s.kv_heads, s.head_dim, stride)[..., :n]
             assert torch.equal(ka, kc), (which, b)
+
+
+def _assert_same_verify(model, kv1, kv2, inp):
     r1 = gpu_verify(model, kv1, inp)
     r2 = gpu_verify(model, kv2, inp)
     assert np.array_equal(r1[0].view(np.uint32), r2[0].view(np.uint32))
     assert np.array_equal(r1[1], r2[1]) and np.array_equal(r1[2], r2[2])
     assert model.device_error() == 0
+
+
+def _setup(w, short_first=True):
+    weights = ModelWeights(w.model, w.seed)
+    inp = make_inputs(w)
+    prompts = [np.asarray(p) for p in inp.prompts]
+    if short_first:
+        prompts[0] = prompts[0][:1]  # nothing to cache for request 0
+    inp.prompts = prompts
+    max_len = max(len(p) for p in prompts) + 2 * (w.gamma + 1) + 24
+    model, kv1 = gpu_setup(w, weights, max_len=max_len)
+    return model, kv1, inp, prompts, max_len
+
+
+@pytest.mark.parametrize("rows", [0, 40])
+@pytest.mark.parametrize("name", ["mini_bf16_mixed", "mini_gqa_mixed_b5", "mini_bf16_wide_b5", "mini_f32_greedy"])
+def test_batched_prefill_equals_per_request(name, rows):
+    from paper_2608_13076_amd import spade
+    w = MINIS[name]
+    model, kv1, inp, prompts, max_len = _setup(w)
+    kv2 = spade.KVCache(model, w.batch, max_len)
+    print(f"[{name}] rows {rows} prompts {[len(p) for p in prompts]}", flush=True)
+    model.set_prefill_rows(16)
+    for b, p in enumerate(prompts):
+        kv1.prefill(b, p)
+    model.set_prefill_rows(rows)
+    kv2.prefill_batch(prompts)
+    _assert_same_cache(model, kv1, kv2, w.batch, max_len)
+    _assert_same_verify(model, kv1, kv2, inp)
+
+
+@pytest.mark.parametrize("name", ["mini_bf16_mixed", "mini_gqa_mixed_b5"])
+def test_prefill_in_two_parts(name):
+    """Request b's prompt in two spade_prefill calls, the second starting at
+    position 37 + b (off a tile boundary), at the default rows, against one
+    call at 16 rows per forward."""
+    from paper_2608_13076_amd import spade
+    w = MINIS[name]
+    model, kv1, inp, prompts, max_len = _setup(w, short_first=False)
+    kv2 = spade.KVCache(model, w.batch, max_len)
+    model.set_prefill_rows(16)
+    for b, p in enumerate(prompts):
+        kv1.prefill(b, p)
+    model.set_prefill_rows(0)
+    for b, p in enumerate(prompts):
+        cut = min(37 + b, len(p) - 1)
+        print(f"[{name}] request {b}: {len(p)} tokens, cut at {cut}", flush=True)
+        kv2.prefill(b, p[:cut + 1])  # caches p[:cut], p[cut] pending
+        kv2.prefill(b, p[cut:])      # caches p[cut:-1] after them
+    _assert_same_cache(model, kv1, kv2, w.batch, max_len)
+    _assert_same_verify(model, kv1, kv2, inp)
+
+
+def test_prefill_rows_setter_rejects_negative():
+    from paper_2608_13076_amd import spade
+    w = MINIS["mini_bf16_mixed"]
+    model, _, _, _, _ = _setup(w)
+    with pytest.raises(spade.SpadeError):
+        model.set_prefill_rows(-1)
