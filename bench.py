@@ -334,6 +334,8 @@ def main() -> int:
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--all-kernels", action="store_true", help="also time every other projection GEMM")
     ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="time the workload's prefill only (a cold run, then a warm one) and print it as JSON")
     ap.add_argument("--counters", action="store_true",
                     help="counter-collection run: a calibration copy, then the gate/up GEMM launches; no timing")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH", "CMD_WRITE"),
@@ -385,6 +387,16 @@ def main() -> int:
                                             4, spade._stream()))
         torch.cuda.synchronize()
         log("counter run done: 1 calibration copy, 4 gate/up launches")
+        return 0
+    if args.prefill_only:
+        kv.prefill_batch(inp.prompts)  # cold: first launches, code loading
+        pf = time_prefill(model, kv, inp, w)
+        log(f"prefill (warm): {pf}")
+        if model.device_error() != 0:
+            log("device error word set")
+            return 1
+        print(json.dumps({"workload": w.name, "prefill": pf,
+                          "prompt_tokens": [len(p) - 1 for p in inp.prompts]}), flush=True)
         return 0
     t0 = time.perf_counter()
     if args.counters_step:

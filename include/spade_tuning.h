@@ -84,6 +84,19 @@ spade_status spade_model_set_attn_grouped(spade_model m, int mode);
  * returns SPADE_EINVAL. */
 spade_status spade_model_set_prefill_rows(spade_model m, int rows);
 
+/* Projection GEMM of forwards with many rows (prefill: hundreds to thousands
+ * of prompt rows; bf16 weights).  A workgroup of four waves owns 128 rows and
+ * 256 columns and runs the k-loop in 32-k steps: the activations' step
+ * through an LDS ring filled by direct loads, the weights' straight into
+ * registers, so each weight byte is multiplied with 128 rows and each
+ * activation byte read from LDS with 256 columns.  mode 0 (the default) uses
+ * it for the QKV, O, gate/up and down projections once a launch has at least
+ * one such workgroup per compute unit; mode 1 turns it off (the wide-row GEMM
+ * runs instead); mode 2 uses it for every launch of more than 16 rows but
+ * the LM head.  Results are bit-for-bit the same under every mode.  Other
+ * values return SPADE_EINVAL. */
+spade_status spade_model_set_big_gemm(spade_model m, int mode);
+
 /* K splitting of the batched O and down projections on the wide-row GEMM.
  * Their weights have few panels (d_model / 16), so one workgroup per panel
  * group leaves most compute units idle; with `splits` = 2 or 4 each

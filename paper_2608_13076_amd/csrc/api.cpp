@@ -227,6 +227,7 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->corr_split = 0;
   m->attn_grouped = 0;
   m->prefill_rows = 0;
+  m->big_gemm = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -496,6 +497,13 @@ spade_status spade_model_set_prefill_rows(spade_model m, int rows) {
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (rows < 0) return fail(SPADE_EINVAL, "rows must be >= 0");
   m->prefill_rows = rows;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_big_gemm(spade_model m, int mode) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
+  m->big_gemm = mode;
   return SPADE_OK;
 }
 

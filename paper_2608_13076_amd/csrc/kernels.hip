@@ -20,6 +20,8 @@
 //   gemm_wide_kernel   the same epilogues for more than 16 rows: row tiles
 //                  and panels per workgroup, the operand through an LDS ring,
 //                  optional k-splits for the O and down projections
+//   gemm_big_kernel    the projections of prefill forwards (hundreds to
+//                  thousands of rows): 128 rows x 256 columns per workgroup
 //   attn_lr_kernel the bf16 / head_dim-128 verify attention, one 256-key
 //                  chunk per workgroup; merges the chunks of a (request,
 //                  head) in the last one to finish, or leaves that to
@@ -40,6 +42,7 @@
 #include "device_accept.h"
 #include "device_attn.h"
 #include "device_gemm.h"
+#include "device_gemm_big.h"
 #include "device_gemm_split.h"
 #include "device_gemm_wide.h"
 
@@ -162,6 +165,35 @@ __global__ void __launch_bounds__(kGemmWaves * 64) gemm_split_kernel(GemmParams 
 // and k-splits of a unit group share that XCD's L2.  K-splits: cnt / part
 // hold one arrival counter / kWideItemFloats published values per (unit
 // group, row group).
+// Large-M projections (device_gemm_big.h): workgroup (row group, panel
+// group).  Workgroup b runs on XCD b % 8, which owns panel groups b % 8 + 8 c;
+// its workgroups go in blocks of 4 row groups x every one of its panel
+// groups, so the workgroups that run together on an XCD share both their
+// weight panels and their activation rows in its L2.
+template <int KIND>
+__global__ void __launch_bounds__(kBigWaves * 64)
+gemm_big_kernel(GemmParams a, int NRG, int NUG) {
+  extern __shared__ uint4 lds_dyn[];
+  const int b = (int)blockIdx.x, q = b >> 3;
+  const int NC = (NUG + 7) / 8;     // panel groups per XCD
+  constexpr int RB = 4;             // row groups per block
+  const int full = NRG / RB;        // whole blocks
+  int rg, c;
+  if (q < full * RB * NC) {
+    const int blk = q / (RB * NC), w = q - blk * (RB * NC);
+    c = w / RB;
+    rg = blk * RB + (w - c * RB);
+  } else {
+    const int rbs = NRG - full * RB, w = q - full * RB * NC;  // the last, partial block
+    c = w / rbs;
+    rg = full * RB + (w - c * rbs);
+  }
+  const int ug = (b & 7) + 8 * c;
+  if (ug >= NUG) return;  // uniform, before any barrier
+  GemmBig<KIND> gb(a, *(GemmBigSmem*)lds_dyn, rg, ug);
+  gb.run();
+}
+
 template <int RT, int P, int KIND, int KS>
 __global__ void __launch_bounds__(kGemmWaves * 64)
     gemm_wide_kernel(GemmParams a, int NRG, int NUG, uint32_t* cnt, float* part) {
@@ -1175,6 +1207,29 @@ hipError_t launch_attn_prefill(const AttnParams& ap, bool abf16, hipStream_t st)
   return hipGetLastError();
 }
 
+template <int KIND>
+hipError_t launch_big_kind(const GemmParams& gp, hipStream_t st) {
+  const void* fn = reinterpret_cast<const void*>(&gemm_big_kernel<KIND>);
+  static hipError_t attr =
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GemmBigSmem));
+  if (attr != hipSuccess) return attr;
+  const int nrg = gemm_big_row_groups(gp.M), nug = gemm_big_unit_groups(gp.n_units);
+  const int grid = 8 * ((nug + 7) / 8) * nrg;
+  hipLaunchKernelGGL((gemm_big_kernel<KIND>), dim3(grid), dim3(kBigWaves * 64), sizeof(GemmBigSmem), st, gp, nrg,
+                     nug);
+  return hipGetLastError();
+}
+
+hipError_t launch_big(int kind, const GemmParams& gp, hipStream_t st) {
+  switch (kind) {
+    case GEMM_QKV: return launch_big_kind<GEMM_QKV>(gp, st);
+    case GEMM_O: return launch_big_kind<GEMM_O>(gp, st);
+    case GEMM_GU: return launch_big_kind<GEMM_GU>(gp, st);
+    case GEMM_DOWN: return launch_big_kind<GEMM_DOWN>(gp, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int HD, int RMAX>
 hipError_t launch_attn_r(const AttnParams& ap, bool kvbf16, bool abf16, dim3 grid, hipStream_t st) {
   if (kvbf16 && abf16) hipLaunchKernelGGL((attn_kernel<HD, RMAX, true, true>), grid, dim3(256), 0, st, ap);
@@ -1282,6 +1337,23 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
   }
   const int grid = std::min(units, md->gemm_wgs);
   g.NU = grid;  // LM head: one statistics entry per workgroup and row
+  if (wb && M > kWideMinRows && kind != GEMM_LM && md->big_gemm != 1) {
+    // many rows (prefill): 128-row x 256-column workgroups, once there are
+    // enough of them to fill the chip (or always, when forced)
+    const long wgs = (long)gemm_big_row_groups(M) * gemm_big_unit_groups(units);
+    if (md->big_gemm == 2 || wgs >= md->n_cu) {
+      GemmParams gp = g;
+      gp.w = wmat;
+      gp.NKB = K / KBd;
+      gp.n_units = units;
+      gp.M = M;
+      gp.m0 = 0;
+      gp.act = act;
+      gp.act_split = act_split;
+      gp.act_stride = K;
+      return launch_big(kind, gp, st);
+    }
+  }
   if (wb && M > kWideMinRows && md->wide_rt >= 0) {
     // batched rows: every row in one launch, weights streamed once
     GemmParams gp = g;

@@ -137,6 +137,7 @@ struct spade_model_s {
   int attn_grouped;  // grouped-query chunks (one workgroup per K/V head and chunk): 0 where they apply, 1 off
   int corr_split;  // correction draws of sampling requests: 0/2 over vocabulary slices, 1 in the accept workgroup
   int prefill_rows;  // prompt rows per request of a prefill forward: 0 as many as the workspace holds, else at most this
+  int big_gemm;  // large-M projection GEMM: 0 where it fills the chip, 1 off, 2 whenever more than 16 rows
 };
 
 struct spade_kv_s {

@@ -38,7 +38,7 @@ EXPORTED = (
 EXPORTED_TUNING = (
     "spade_model_set_wide_tiles", "spade_model_set_wide_k_splits", "spade_model_set_split_k",
     "spade_model_set_attn_merge", "spade_model_set_correction_slices", "spade_model_set_attn_grouped",
-    "spade_model_set_prefill_rows", "spade_profile_gemm", "spade_wide_tiling",
+    "spade_model_set_prefill_rows", "spade_model_set_big_gemm", "spade_profile_gemm", "spade_wide_tiling",
 )
 
 
@@ -102,6 +102,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_model_set_correction_slices": (I, [P, I]),
         "spade_model_set_attn_grouped": (I, [P, I]),
         "spade_model_set_prefill_rows": (I, [P, I]),
+        "spade_model_set_big_gemm": (I, [P, I]),
         "spade_model_set_split_k": (I, [P, I]),
         "spade_softmax": (I, [P, I, I, F, P, P]),
         "spade_prefill_batch": (I, [P, P, I, P, I, P, P]),
@@ -204,6 +205,11 @@ class Model:
         """Prompt rows per request of a prefill forward: 0 as many as the
         workspace holds (bf16 cache, head_dim 128), n > 0 at most n."""
         _check(self.lib.spade_model_set_prefill_rows(self.handle, int(rows)))
+
+    def set_big_gemm(self, mode: int) -> None:
+        """Projection GEMM of forwards with many rows: 0 where it fills the
+        chip, 1 off, 2 for every launch of more than 16 rows (not the LM head)."""
+        _check(self.lib.spade_model_set_big_gemm(self.handle, int(mode)))
 
     def set_correction_slices(self, mode: int) -> None:
         """Correction draw of sampling requests: 0 or 2 over vocabulary slices

@@ -77,21 +77,47 @@ def _setup(w, short_first=True):
     return model, kv1, inp, prompts, max_len
 
 
-@pytest.mark.parametrize("rows", [0, 40])
+@pytest.mark.parametrize("rows,big", [(0, 0), (0, 2), (40, 0), (40, 2)])
 @pytest.mark.parametrize("name", ["mini_bf16_mixed", "mini_gqa_mixed_b5", "mini_bf16_wide_b5", "mini_f32_greedy"])
-def test_batched_prefill_equals_per_request(name, rows):
+def test_batched_prefill_equals_per_request(name, rows, big):
+    """big = 2 forces the large-M projection GEMM onto every launch of more
+    than 16 rows (the mini shapes' launches are too small for it to be
+    chosen); the reference runs with it off."""
     from paper_2608_13076_amd import spade
     w = MINIS[name]
     model, kv1, inp, prompts, max_len = _setup(w)
     kv2 = spade.KVCache(model, w.batch, max_len)
-    print(f"[{name}] rows {rows} prompts {[len(p) for p in prompts]}", flush=True)
+    print(f"[{name}] rows {rows} big {big} prompts {[len(p) for p in prompts]}", flush=True)
     model.set_prefill_rows(16)
+    model.set_big_gemm(1)
     for b, p in enumerate(prompts):
         kv1.prefill(b, p)
     model.set_prefill_rows(rows)
+    model.set_big_gemm(big)
     kv2.prefill_batch(prompts)
+    model.set_big_gemm(0)
     _assert_same_cache(model, kv1, kv2, w.batch, max_len)
     _assert_same_verify(model, kv1, kv2, inp)
+
+
+@pytest.mark.parametrize("name", ["mini_bf16_wide_b5", "mini_gqa_mixed_b5"])
+def test_big_gemm_verify_bit_identical(name):
+    """A verify call of B (gamma + 1) > 16 rows with the large-M projection
+    GEMM forced gives the same logits and decisions as the wide-row GEMM."""
+    from paper_2608_13076_amd import spade
+    w = MINIS[name]
+    model, kv1, inp, prompts, max_len = _setup(w, short_first=False)
+    kv2 = spade.KVCache(model, w.batch, max_len)
+    kv1.prefill_batch(prompts)
+    kv2.prefill_batch(prompts)
+    model.set_big_gemm(1)
+    r1 = gpu_verify(model, kv1, inp)
+    model.set_big_gemm(2)
+    r2 = gpu_verify(model, kv2, inp)
+    model.set_big_gemm(0)
+    assert np.array_equal(r1[0].view(np.uint32), r2[0].view(np.uint32))
+    assert np.array_equal(r1[1], r2[1]) and np.array_equal(r1[2], r2[2])
+    assert model.device_error() == 0
 
 
 @pytest.mark.parametrize("name", ["mini_bf16_mixed", "mini_gqa_mixed_b5"])
@@ -116,9 +142,12 @@ def test_prefill_in_two_parts(name):
     _assert_same_verify(model, kv1, kv2, inp)
 
 
-def test_prefill_rows_setter_rejects_negative():
+def test_prefill_setters_reject_bad_values():
     from paper_2608_13076_amd import spade
     w = MINIS["mini_bf16_mixed"]
     model, _, _, _, _ = _setup(w)
     with pytest.raises(spade.SpadeError):
         model.set_prefill_rows(-1)
+    for bad in (-1, 3):
+        with pytest.raises(spade.SpadeError):
+            model.set_big_gemm(bad)
