@@ -286,22 +286,100 @@ __device__ __forceinline__ floatx4 attn_pv(const AttnSmem<CK>& sm, const AttnReg
   return o;
 }
 
+// The verify kernels' chunk: the helpers above written out in one body, the
+// same operations in the same order (composed of the helper calls, the
+// one-chunk kernel needs 80 VGPRs and spills six; written out, 76 and none).
 template <int CK>
 __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
                                                  const uint16_t (*sqh)[kAttnQPitch],
                                                  const uint16_t (*sql)[kAttnQPitch], int R, float scale, int stride,
                                                  AttnSmem<CK>& sm) {
+  constexpr int NG = CK / 128;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  float sv[CK / 128][4];
-  attn_scores<CK>(it, kf, sqh, sql, scale, sv);
+  const int g = lane >> 4, kl = lane & 15;
+  const int ke = (it.k_hi + 7) & ~7;
+  float sv[NG][4];
+#pragma unroll
+  for (int grp = 0; grp < NG; ++grp) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 qh = *(const uint4*)&sqh[kl][32 * ks + 8 * g];
+      const uint4 ql = *(const uint4*)&sql[kl][32 * ks + 8 * g];
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ql),
+                                                    __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qh),
+                                                    __builtin_bit_cast(bf16x8, kf[grp][ks]), acc, 0, 0, 0);
+    }
+    const int key = it.k_lo + (CK / 8) * wave + 16 * grp + kl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 4 * g + i;
+      sv[grp][i] = (key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
+    }
+  }
   // the V^T fragments, after the score products (the K registers are free)
   __builtin_amdgcn_sched_barrier(0);
   AttnRegs<CK> r;
-  attn_load_v<CK>(it, wave, lane, stride, r);
+  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
+#pragma unroll
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const int kv0 = it.k_lo + 32 * ks + 8 * g;
+    r.vf[ks] = make_uint4(0, 0, 0, 0);
+    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
+  }
   __builtin_amdgcn_sched_barrier(0);
-  attn_softmax<CK>(sv, R, sm);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float mx = sv[0][i];
+#pragma unroll
+    for (int grp = 1; grp < NG; ++grp) mx = fmaxf(mx, sv[grp][i]);
+    mx = row16_max(mx);
+    if (kl == 0) sm.pm[4 * g + i][wave] = mx;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * g + i;
+    const float4 a = *(const float4*)&sm.pm[row][0];
+    const float4 b = *(const float4*)&sm.pm[row][4];
+    const float M = fmaxf(fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)), fmaxf(fmaxf(b.x, b.y), fmaxf(b.z, b.w)));
+    float sum = 0.f;
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp) {
+      const float e = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((sv[grp][i] - M) * 1.44269504088896341f);
+      sum += e;
+      const uint16_t h = f2bf_num(e);
+      const int kc = (CK / 8) * wave + 16 * grp + kl;
+      sm.ph[row][kc] = h;
+      sm.pl[row][kc] = f2bf_num(e - bf2f(h));
+    }
+    sum = row16_sum(sum);
+    if (kl == 0) sm.ps[row][wave] = sum;
+  }
+  __syncthreads();
+  if (tid < R) {
+    float l = 0.f, M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      l += sm.ps[tid][w];
+      M = fmaxf(M, sm.pm[tid][w]);
+    }
+    sm.m[tid] = M;
+    sm.l[tid] = l;
+  }
   attn_mask_tail(it, lane, r);
-  return attn_pv<CK>(sm, r);
+  floatx4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < CK / 32; ++ks) {
+    const uint4 ph = *(const uint4*)&sm.ph[kl][32 * ks + 8 * g];
+    const uint4 pl = *(const uint4*)&sm.pl[kl][32 * ks + 8 * g];
+    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pl), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
+                                                0, 0, 0);
+    o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ph), __builtin_bit_cast(bf16x8, r.vf[ks]), o,
+                                                0, 0, 0);
+  }
+  return o;
 }
 
 // Last-arrival merge of the chunks of one (request, head).
