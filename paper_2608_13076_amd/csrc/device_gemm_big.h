@@ -148,6 +148,14 @@ struct GemmBig {
     ((x[MT][0] = ds_read16<MT * 1024>(base), x[MT][1] = ds_read16<kBigRT * 1024 + MT * 1024>(base)), ...);
   }
 
+  // wait until at most N of this wave's LDS reads are outstanding; the
+  // fragments x depend on the wait
+  template <int N>
+  __device__ __forceinline__ static void lds_wait_n(u32x4b (&x)[S]) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x[s]) : "n"(N));
+  }
+
   // the MFMAs of slice t: fragments of its ring slot (this wave's row
   // tiles), weights w
   __device__ __forceinline__ void mma(int t, const uint4 (&w)[4]) {
@@ -155,18 +163,21 @@ struct GemmBig {
         lds_ring + (uint32_t)(t % kBigSlots) * (uint32_t)(S * kBigRT * 1024) + (uint32_t)mt0 * 1024u + frag_off;
     u32x4b x[4][S];
     read_frags(base, x, std::make_integer_sequence<int, 4>{});
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int s = 0; s < S; ++s) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[mt][s]));
+    // row tile mt's two fragments are the reads 2 mt and 2 mt + 1 of eight:
+    // its MFMAs start once those have landed (LDS reads complete in order)
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
+      if (mt == 0) lds_wait_n<6>(x[0]);
+      else if (mt == 1) lds_wait_n<4>(x[1]);
+      else if (mt == 2) lds_wait_n<2>(x[2]);
+      else lds_wait_n<0>(x[3]);
 #pragma unroll
       for (int p = 0; p < 4; ++p)
 #pragma unroll
         for (int s = S - 1; s >= 0; --s)
           acc[mt][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, x[mt][s]),
                                                                __builtin_bit_cast(bf16x8, w[p]), acc[mt][p], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);  // keep row tile mt's MFMAs before the next wait
     }
   }
 
