@@ -30,13 +30,17 @@
 //                  K/V head in one workgroup (merged by attn_merge_kernel)
 //   attn_kernel / attn_combine_kernel  f32 cache or other head sizes:
 //                  128-key chunks, then the chunk-order merge
+//   attn_prefill_kernel  prefill forwards of more than 16 rows per request:
+//                  one wave per 16-row tile, each tile computed as a verify
+//                  call of its own, K / V^T blocks shared through LDS
 //   accept_kernel  per request: vocabulary-wide max / log-sum-exp / argmax
 //                  per row, the accept chain, the Gumbel-max correction draw
 //   correct_kernel that draw over vocabulary slices (calls that may sample)
 //   commit_kernel  lens += n + 1, pending = correction
 //   copy_state_kernel / advance_kernel  cache-state copies and single-request
 //                  prefill bookkeeping
-//   prefill_*_kernel   batched prefill: counts, token gather, advance, pending
+//   prefill_*_kernel   batched prefill: counts and start lengths, token
+//                  gather, advance, pending
 //   softmax_rows_kernel  softmax of logits / T (the draft side of Algorithm 1)
 //   pack_kernel    row-major weights -> tiled arena
 #include "device_accept.h"
