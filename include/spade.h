@@ -114,7 +114,10 @@ typedef struct {
 size_t spade_weight_bytes(const spade_config* cfg);
 
 /* Bytes of the workspace for calls with up to max_batch requests of up to
- * max_gamma drafts each and caches of up to max_len positions. */
+ * max_gamma drafts each and caches of up to max_len positions.  With a bf16
+ * cache and head_dim 128 its activation arrays also hold a prefill forward:
+ * min(2048, max_batch * max_len rounded up to 16) rows (about 220 MB at the
+ * 7B shape, 363 MB at the 33B shape). */
 size_t spade_workspace_bytes(const spade_config* cfg, int max_batch, int max_gamma, int max_len);
 
 /* Bytes of a KV cache holding max_batch requests of max_len positions.  With
