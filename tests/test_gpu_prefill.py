@@ -120,6 +120,39 @@ def test_big_gemm_verify_bit_identical(name):
     assert model.device_error() == 0
 
 
+@pytest.mark.parametrize("big", [0, 2])
+def test_batched_prefill_ragged_ranges(big):
+    """Eight requests of lengths 1 .. 700 (one-token prompts inside ranges,
+    whose rows are all placeholders) in caches with little room past the
+    longest prompt, so the range scheduler must leave out requests whose
+    placeholder rows would not fit; forwards of more rows than one request
+    holds.  The cache and a verify call after it must equal 16-row prefill
+    request by request bit for bit."""
+    from paper_2608_13076_amd import spade
+    from synth import ModelWeights, make_inputs
+    w = MINIS["mini_bf16_mixed"].with_(batch=8)
+    weights = ModelWeights(w.model, w.seed)
+    inp = make_inputs(w)
+    rng = np.random.default_rng(11)
+    lengths = [1, 700, 1, 33, 17, 600, 2, 401]
+    inp.prompts = [rng.integers(0, w.model.vocab, size=n).astype(np.int32) for n in lengths]
+    inp.lens = np.array([n - 1 for n in lengths], dtype=np.int32)
+    inp.pending = np.array([p[-1] for p in inp.prompts], dtype=np.int32)
+    max_len = max(lengths) + 2 * (w.gamma + 1) + 2
+    model, kv1 = gpu_setup(w, weights, max_len=max_len)
+    kv2 = spade.KVCache(model, w.batch, max_len)
+    model.set_prefill_rows(16)
+    model.set_big_gemm(1)
+    for b, p in enumerate(inp.prompts):
+        kv1.prefill(b, p)
+    model.set_prefill_rows(0)
+    model.set_big_gemm(big)
+    kv2.prefill_batch(inp.prompts)
+    model.set_big_gemm(0)
+    _assert_same_cache(model, kv1, kv2, w.batch, max_len)
+    _assert_same_verify(model, kv1, kv2, inp)
+
+
 @pytest.mark.parametrize("name", ["mini_bf16_mixed", "mini_gqa_mixed_b5"])
 def test_prefill_in_two_parts(name):
     """Request b's prompt in two spade_prefill calls, the second starting at
