@@ -999,14 +999,20 @@ hipError_t launch_split_ks(const GemmParams& gp, uint32_t* cnt, float* part, int
 }
 
 // k-splits for a bf16 projection with <= 16 rows whose whole operand does
-// not fit in LDS: the fewest (2 or 4) whose split fits, with at most
-// kSplitMaxGroups panel groups per workgroup; 0 when none qualifies (or the
-// whole operand fits).  fixed > 0 forces that count where it qualifies.
+// not fit in LDS, or whose panels are no more than the compute units: the
+// fewest (2 or 4) whose split fits, with at most kSplitMaxGroups panel
+// groups per workgroup; 0 when none qualifies (or the whole operand fits and
+// the panels outnumber the compute units).  fixed > 0 forces that count
+// where it qualifies.
 int split_k_choice(const GemmParams& gp, int n_cu, int fixed) {
   if (gp.M > 16) return 0;
   const uint32_t whole = gemm_lds_a_bytes(gp.M, gp.act_stride, 1);
   const bool whole_fits = whole <= kGemmLdsABytes && gemm_lds_a_ok(gp.act_stride, 1);
-  if (whole_fits && fixed <= 0) return 0;
+  // an operand that fits one LDS copy needs no split, unless the panels are
+  // too few for one per compute unit (the 7B O projection: 256 panels, one
+  // 128 KB stream per workgroup; two k-splits: 3.520 -> 3.506 ms per 7B
+  // batch-1 verify step)
+  if (whole_fits && fixed <= 0 && gp.n_units > n_cu) return 0;
   for (int ks = 2; ks <= 4; ks *= 2) {
     if (fixed > 0 && ks != fixed) continue;
     const int G = n_cu / ks;
