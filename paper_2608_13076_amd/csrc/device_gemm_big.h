@@ -72,6 +72,7 @@ struct GemmBig {
   floatx4 acc[4][4], tot[4][4];
   uint4 wq[D][4];      // weight fragments of the slices in flight
   int rnext, bnd;      // next k-range, its first k-block
+  int T;               // slices of the k-loop
 
   __device__ __forceinline__ GemmBig(const GemmParams& a_, GemmBigSmem& sm_, int rg, int ug) : a(a_), sm(sm_) {
     tid = threadIdx.x;
@@ -83,6 +84,7 @@ struct GemmBig {
     mt0 = 4 * (wave % kBigRowWaves);
     u0 = ug * kBigUnits + (wave / kBigRowWaves) * 4;
     NKB = a.NKB;
+    T = NKB * 8;
     lds_ring = (uint32_t)(size_t)(__attribute__((address_space(3))) void*)&sm.ring[0][0][0][0];
     frag_off = (uint32_t)(kl * 64 + 16 * (g ^ (((kl >> 1) ^ (kl >> 2)) & 3)));
     ract = make_rsrc((const uint8_t*)a.act + (size_t)a.m0 * a.act_stride * 2,
@@ -109,7 +111,9 @@ struct GemmBig {
   // ring slot t % kBigSlots: each wave moves two of the 16 (split, row tile)
   // blocks, one 16-byte piece per lane (lane l: row l / 4, piece l % 4 of the
   // swizzled block).  Rows past M repeat row M - 1: finite values whose
-  // products are never stored.
+  // products are never stored.  Slices past the k-loop read zeros (an offset
+  // past the resource) into a slot no later slice reads: every load is
+  // issued unconditionally, so the compiler's wait counts stay exact.
   __device__ __forceinline__ void fill(int t) const {
     const int kb = t >> 3, j = t & 7;
     const int slot = t % kBigSlots;
@@ -122,16 +126,18 @@ struct GemmBig {
       const int row = row0 + mt * 16 + r;
       const int grow = row < a.M ? row : a.M - 1;
       const uint32_t off =
-          (uint32_t)(((size_t)s * a.act_split + (size_t)grow * a.act_stride + kb * 256 + j * 32 + lp * 8) * 2);
+          t < T ? (uint32_t)(((size_t)s * a.act_split + (size_t)grow * a.act_stride + kb * 256 + j * 32 + lp * 8) * 2)
+                : kOob;
       __attribute__((address_space(3))) void* dst =
           (__attribute__((address_space(3))) void*)&sm.ring[slot][s][mt][0];
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ract, dst, 16, off, 0, 0, 0);
     }
   }
 
-  // weight fragments of slice t for this wave's four panels
+  // weight fragments of slice t for this wave's four panels (zeros past the
+  // k-loop: the offset is past the resource)
   __device__ __forceinline__ void issue_w(int t, uint4 (&w)[4]) const {
-    const uint32_t off = (uint32_t)((t >> 3) * kTileBytes + (t & 7) * 1024 + lane * 16);
+    const uint32_t off = t < T ? (uint32_t)((t >> 3) * kTileBytes + (t & 7) * 1024 + lane * 16) : kOob;
 #pragma unroll
     for (int p = 0; p < 4; ++p) w[p] = ld_b128<false>(rw[p], off);
   }
@@ -200,44 +206,40 @@ struct GemmBig {
   }
 
   // slice t = 8 kb + J: wait for this wave's share of its fill and for its
-  // weights (the slices after it have at most D - 1 groups of six loads in
-  // flight), publish the slot to every wave (bare barrier: the ring is read
-  // with inline asm and written by direct loads each wave has waited for),
+  // weights (the D - 1 slices after it have their six loads each in flight),
+  // publish the slot to every wave (bare barrier: the ring is read with
+  // inline asm and written by direct loads each wave has waited for),
   // request slice t + D into slot (t + D) % kBigSlots -- the slot of slice
   // t - 1, which every wave finished reading before this barrier -- then the
   // MFMAs, then the weights of slice t + D into the registers just used.
   template <int J>
-  __device__ __forceinline__ void slice(int kb, int T) {
+  __device__ __forceinline__ void slice(int kb) {
     const int t = kb * 8 + J;
-    if (t + D - 1 < T) wait_vmcnt<(D - 1) * 6>();
-    else wait_vmcnt<0>();
+    wait_vmcnt<(D - 1) * 6>();
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if (t + D < T) fill(t + D);
+    fill(t + D);
     mma(t, wq[J % D]);
     __builtin_amdgcn_sched_barrier(0);
-    if (t + D < T) issue_w(t + D, wq[J % D]);
+    issue_w(t + D, wq[J % D]);
   }
 
   template <int... I>
-  __device__ __forceinline__ void kblock(int kb, int T, std::integer_sequence<int, I...>) {
-    (slice<I>(kb, T), ...);
+  __device__ __forceinline__ void kblock(int kb, std::integer_sequence<int, I...>) {
+    (slice<I>(kb), ...);
   }
 
   __device__ __forceinline__ void run() {
-    const int T = NKB * 8;
     // prologue: the first D slices (each one fill, then its weights: the
     // waits count two fill loads and four weight loads per slice)
 #pragma unroll
     for (int i = 0; i < D; ++i) {
-      if (i < T) {
-        fill(i);
-        issue_w(i, wq[i]);
-      }
+      fill(i);
+      issue_w(i, wq[i]);
     }
     for (int kb = 0; kb < NKB; ++kb) {
-      kblock(kb, T, std::make_integer_sequence<int, 8>{});
+      kblock(kb, std::make_integer_sequence<int, 8>{});
       range_end(kb);
     }
     // the ring is idle once every fill has landed and every wave is past its
