@@ -85,7 +85,7 @@ spade_status spade_model_set_attn_grouped(spade_model m, int mode);
 spade_status spade_model_set_prefill_rows(spade_model m, int rows);
 
 /* Projection GEMM of forwards with many rows (prefill: hundreds to thousands
- * of prompt rows; bf16 weights).  A workgroup of four waves owns 128 rows and
+ * of prompt rows; bf16 weights).  A workgroup of eight waves owns 128 rows and
  * 256 columns and runs the k-loop in 32-k steps: the activations' step
  * through an LDS ring filled by direct loads, the weights' straight into
  * registers, so each weight byte is multiplied with 128 rows and each
@@ -96,6 +96,23 @@ spade_status spade_model_set_prefill_rows(spade_model m, int rows);
  * the LM head.  Results are bit-for-bit the same under every mode.  Other
  * values return SPADE_EINVAL. */
 spade_status spade_model_set_big_gemm(spade_model m, int mode);
+
+/* Projection GEMM of batched verification calls of up to 144 rows (e.g. 16
+ * requests of gamma + 1 = 9 rows; bf16 weights).  A workgroup of eight waves
+ * owns every row of the call and 256 columns, so each weight byte enters one
+ * compute unit once per launch; the k-loop runs in 32-k steps with the
+ * activations' step in an LDS ring filled by direct loads and the weights'
+ * straight into registers.  The k-loop is split over 1-8 workgroups per
+ * panel group (whole k-ranges of the eight); each stores its sums in the
+ * workspace, and a second launch, one workgroup per panel group and 16-row
+ * tile, adds them in range order and runs the epilogue.  mode 0 (the
+ * default) uses it for the O, gate/up and down projections of 129 to 144
+ * rows; mode 1 turns it off (the wide-row GEMM runs instead); mode 2 uses it
+ * for every QKV, O, gate/up and down launch of 17 to 144 rows.  k_splits 0
+ * chooses the split count per launch, 1..8 fixes it.  Results are
+ * bit-for-bit the same under every setting.  Other values return
+ * SPADE_EINVAL. */
+spade_status spade_model_set_mid_gemm(spade_model m, int mode, int k_splits);
 
 /* K splitting of the batched O and down projections on the wide-row GEMM.
  * Their weights have few panels (d_model / 16), so one workgroup per panel

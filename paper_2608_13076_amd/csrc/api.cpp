@@ -101,8 +101,8 @@ ArenaLayout layout_of(const Dims& D) {
 
 struct WsPlan {
   size_t x, act_n, act_o, act_f, ssq, q, attn_o, attn_ml, attn_cnt, logits, stats, rope, err, split_cnt,
-      split_part, wide_cnt, wide_part, corr_lse, corr_part, corr_cnt, prefill_tok, prefill_cnt, prefill_base, total;
-  size_t wide_items, wide_floats;
+      split_part, wide_cnt, wide_part, mid_part, corr_lse, corr_part, corr_cnt, prefill_tok, prefill_cnt, prefill_base, total;
+  size_t wide_items, wide_floats, mid_items;
   int max_units;
   size_t act_split, actf_split;
   int Mmax, Mrows, NCmax, Rmax;
@@ -158,6 +158,11 @@ WsPlan plan_ws(const Dims& D, int max_batch, int max_gamma, int max_len) {
   }
   p.wide_cnt = take(p.wide_items * 4);
   p.wide_part = take(p.wide_floats * 4);
+  // medium-M projections (forwards of 17 to 144 rows): one block of published
+  // sums per 256-column panel group of the widest projection
+  if (wb && p.Mrows > kWideMinRows)
+    p.mid_items = (size_t)((std::max(D.d + 2 * D.dkv, 2 * D.F) / 16 + 15) / 16);
+  p.mid_part = take(p.mid_items * mid_split_floats() * 4);
   p.corr_lse = take((size_t)max_batch * 4);
   p.corr_part = take((size_t)max_batch * kCorrMaxSlices * 4 * 4);
   p.corr_cnt = take((size_t)max_batch * 4);
@@ -228,6 +233,8 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   m->attn_grouped = 0;
   m->prefill_rows = 0;
   m->big_gemm = 0;
+  m->mid_gemm = 0;
+  m->mid_ks = 0;
   if (const char* ev = std::getenv("SPADE_GEMM_WGS")) {
     const int v = std::atoi(ev);
     if (v > 0) m->gemm_wgs = std::min(v, kMaxStatGroups);
@@ -250,6 +257,8 @@ spade_status spade_model_create(const spade_config* cfg, void* d_weights, void* 
   w.wide_part = (float*)(b + p.wide_part);
   w.wide_items = p.wide_items;
   w.wide_floats = p.wide_floats;
+  w.mid_items = p.mid_items;
+  w.mid_part = p.mid_items > 0 ? (float*)(b + p.mid_part) : nullptr;
   w.corr_lse = (float*)(b + p.corr_lse);
   w.corr_part = (float*)(b + p.corr_part);
   w.corr_cnt = (uint32_t*)(b + p.corr_cnt);
@@ -504,6 +513,15 @@ spade_status spade_model_set_big_gemm(spade_model m, int mode) {
   if (!m) return fail(SPADE_EINVAL, "null model");
   if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
   m->big_gemm = mode;
+  return SPADE_OK;
+}
+
+spade_status spade_model_set_mid_gemm(spade_model m, int mode, int k_splits) {
+  if (!m) return fail(SPADE_EINVAL, "null model");
+  if (mode < 0 || mode > 2) return fail(SPADE_EINVAL, "mode must be 0, 1 or 2");
+  if (k_splits < 0 || k_splits > 8) return fail(SPADE_EINVAL, "k_splits must be 0..8");
+  m->mid_gemm = mode;
+  m->mid_ks = k_splits;
   return SPADE_OK;
 }
 

@@ -47,6 +47,7 @@
 #include "device_attn.h"
 #include "device_gemm.h"
 #include "device_gemm_big.h"
+#include "device_gemm_mid.h"
 #include "device_gemm_split.h"
 #include "device_gemm_wide.h"
 
@@ -196,6 +197,33 @@ gemm_big_kernel(GemmParams a, int NRG, int NUG) {
   if (ug >= NUG) return;  // uniform, before any barrier
   GemmBig<KIND> gb(a, *(GemmBigSmem*)lds_dyn, rg, ug);
   gb.run();
+}
+
+// Batched-verification projections of up to 144 rows
+// (device_gemm_mid.h), first pass: workgroup b = (panel group b / KS, k-split
+// b % KS) publishes its sums into part (kMidItemFloats per panel group).
+template <int KIND>
+__global__ void __launch_bounds__(kMidWaves * 64)
+gemm_mid_kernel(GemmParams a, int NUG, int KS, float* part) {
+  extern __shared__ uint4 lds_dyn[];
+  const int b = (int)blockIdx.x;
+  const int ug = b / KS, ks = b - ug * KS;
+  if (ug >= NUG) return;  // uniform, before any barrier
+  GemmMid<KIND> g(a, *(GemmMidSmem*)lds_dyn, ug, ks, KS, part + (size_t)ug * kMidItemFloats);
+  g.run();
+}
+
+// Second pass: workgroup b = (panel group b / kMidRT, row tile b % kMidRT)
+// adds the published sums in range order and runs the epilogue.
+template <int KIND>
+__global__ void __launch_bounds__(kMidWaves * 64)
+gemm_mid_finish_kernel(GemmParams a, int NUG, int KS, const float* part) {
+  __shared__ float rinv[16];
+  const int b = (int)blockIdx.x;
+  const int ug = b / kMidRT, mt = b - ug * kMidRT;
+  if (ug >= NUG || mt * 16 >= a.M) return;  // uniform, before any barrier
+  GemmMidFinish<KIND> f(a, rinv, ug, mt, KS, part);
+  f.run();
 }
 
 template <int RT, int P, int KIND, int KS>
@@ -1113,6 +1141,32 @@ size_t wide_split_floats(int n_units, int M, int rt, int p) {
   return items * (size_t)8 * kGemmWaves * p * rt * 256;
 }
 
+size_t mid_split_floats() { return (size_t)kMidItemFloats; }
+
+// K-splits of a medium-M launch: the fewest that minimise the rounds of
+// workgroups (one per compute unit at a time) times the k-blocks of the
+// longest split, with a split launch charged about one and a half k-blocks
+// for its publish and combine.  A fixed count (1-8) is used as given; more
+// panel groups than the published-value buffers hold run unsplit.
+int mid_k_splits(int n_units, int NKB, int n_cu, int fixed_ks) {
+  const int G = gemm_mid_unit_groups(n_units);
+  if (fixed_ks > 0) return std::min(fixed_ks, kMidMaxSplits);
+  int best = 1;
+  double best_cost = -1.0;
+  for (int ks = 1; ks <= kMidMaxSplits && ks <= NKB; ++ks) {
+    int longest = 0;
+    for (int s = 0; s < ks; ++s)
+      longest = std::max(longest, NKB * (8 * (s + 1) / ks) / 8 - NKB * (8 * s / ks) / 8);
+    const long rounds = ((long)G * ks + n_cu - 1) / n_cu;
+    const double cost = (double)rounds * longest + (ks > 1 ? 1.5 : 0.0);
+    if (best_cost < 0 || cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best = ks;
+    }
+  }
+  return best;
+}
+
 WideChoice wide_choice(int kind, int M, int n_units, int NKB, int K, int n_cu, int fixed_rt, int fixed_p, int fixed_ks,
                        size_t cap_items, size_t cap_floats) {
   const int tiles = (M + 15) / 16;
@@ -1228,6 +1282,33 @@ hipError_t launch_big_kind(const GemmParams& gp, hipStream_t st) {
   hipLaunchKernelGGL((gemm_big_kernel<KIND>), dim3(grid), dim3(kBigWaves * 64), sizeof(GemmBigSmem), st, gp, nrg,
                      nug);
   return hipGetLastError();
+}
+
+template <int KIND>
+hipError_t launch_mid_kind(const GemmParams& gp, int ks, float* part, hipStream_t st) {
+  const void* fn = reinterpret_cast<const void*>(&gemm_mid_kernel<KIND>);
+  static hipError_t attr =
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(GemmMidSmem));
+  if (attr != hipSuccess) return attr;
+  if (gp.M > kMidRT * 16 || ks < 1 || ks > kMidMaxSplits) return hipErrorInvalidValue;
+  const int nug = gemm_mid_unit_groups(gp.n_units);
+  hipLaunchKernelGGL((gemm_mid_kernel<KIND>), dim3(nug * ks), dim3(kMidWaves * 64), sizeof(GemmMidSmem), st, gp, nug,
+                     ks, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((gemm_mid_finish_kernel<KIND>), dim3(nug * kMidRT), dim3(kMidWaves * 64), 0, st, gp, nug, ks,
+                     (const float*)part);
+  return hipGetLastError();
+}
+
+hipError_t launch_mid(int kind, const GemmParams& gp, int ks, float* part, hipStream_t st) {
+  switch (kind) {
+    case GEMM_QKV: return launch_mid_kind<GEMM_QKV>(gp, ks, part, st);
+    case GEMM_O: return launch_mid_kind<GEMM_O>(gp, ks, part, st);
+    case GEMM_GU: return launch_mid_kind<GEMM_GU>(gp, ks, part, st);
+    case GEMM_DOWN: return launch_mid_kind<GEMM_DOWN>(gp, ks, part, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_big(int kind, const GemmParams& gp, hipStream_t st) {
@@ -1363,6 +1444,24 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
       gp.act_stride = K;
       return launch_big(kind, gp, st);
     }
+  }
+  // batched verification: every row in one workgroup per panel group (by
+  // default the O, gate/up and down projections of more than kMidMinRows
+  // rows; the QKV projection measured no faster than on the wide-row GEMM)
+  if (wb && M > kWideMinRows && M <= kMidRT * 16 && kind != GEMM_LM && md->mid_gemm != 1 &&
+      (md->mid_gemm == 2 || (M > kMidMinRows && kind != GEMM_QKV)) && W.mid_part &&
+      (size_t)gemm_mid_unit_groups(units) <= W.mid_items) {
+    GemmParams gp = g;
+    gp.w = wmat;
+    gp.NKB = K / KBd;
+    gp.n_units = units;
+    gp.M = M;
+    gp.m0 = 0;
+    gp.act = act;
+    gp.act_split = act_split;
+    gp.act_stride = K;
+    const int ks = mid_k_splits(units, gp.NKB, md->n_cu, md->mid_ks);
+    return launch_mid(kind, gp, ks, W.mid_part, st);
   }
   if (wb && M > kWideMinRows && md->wide_rt >= 0) {
     // batched rows: every row in one launch, weights streamed once

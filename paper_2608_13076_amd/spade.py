@@ -38,7 +38,8 @@ EXPORTED = (
 EXPORTED_TUNING = (
     "spade_model_set_wide_tiles", "spade_model_set_wide_k_splits", "spade_model_set_split_k",
     "spade_model_set_attn_merge", "spade_model_set_correction_slices", "spade_model_set_attn_grouped",
-    "spade_model_set_prefill_rows", "spade_model_set_big_gemm", "spade_profile_gemm", "spade_wide_tiling",
+    "spade_model_set_prefill_rows", "spade_model_set_big_gemm", "spade_model_set_mid_gemm", "spade_profile_gemm",
+    "spade_wide_tiling",
 )
 
 
@@ -103,6 +104,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "spade_model_set_attn_grouped": (I, [P, I]),
         "spade_model_set_prefill_rows": (I, [P, I]),
         "spade_model_set_big_gemm": (I, [P, I]),
+        "spade_model_set_mid_gemm": (I, [P, I, I]),
         "spade_model_set_split_k": (I, [P, I]),
         "spade_softmax": (I, [P, I, I, F, P, P]),
         "spade_prefill_batch": (I, [P, P, I, P, I, P, P]),
@@ -210,6 +212,13 @@ class Model:
         """Projection GEMM of forwards with many rows: 0 where it fills the
         chip, 1 off, 2 for every launch of more than 16 rows (not the LM head)."""
         _check(self.lib.spade_model_set_big_gemm(self.handle, int(mode)))
+
+    def set_mid_gemm(self, mode: int, k_splits: int = 0) -> None:
+        """Projection GEMM of batched calls of up to 144 rows: mode 0 the O,
+        gate/up and down projections from 129 rows, 1 off, 2 every projection
+        from 17 rows (not the LM head); k_splits 0 chosen per launch, 1..8
+        fixed."""
+        _check(self.lib.spade_model_set_mid_gemm(self.handle, int(mode), int(k_splits)))
 
     def set_correction_slices(self, mode: int) -> None:
         """Correction draw of sampling requests: 0 or 2 over vocabulary slices
