@@ -20,6 +20,10 @@
 //   gemm_wide_kernel   the same epilogues for more than 16 rows: row tiles
 //                  and panels per workgroup, the operand through an LDS ring,
 //                  optional k-splits for the O and down projections
+//   gemm_mid_kernel    batched-verification projections of up to 144 rows:
+//                  every row x 256 columns per workgroup, k-split, sums
+//                  published; gemm_mid_finish_kernel adds them in range
+//                  order and runs the epilogue
 //   gemm_big_kernel    the projections of prefill forwards (hundreds to
 //                  thousands of rows): 128 rows x 256 columns per workgroup
 //   attn_lr_kernel the bf16 / head_dim-128 verify attention, one 256-key
