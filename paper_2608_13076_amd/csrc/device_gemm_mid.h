@@ -44,7 +44,7 @@ constexpr int kMidRT = 9;                          // row tiles per workgroup (1
 constexpr int kMidP = 2;                           // panels per wave
 constexpr int kMidUnits = kMidWaves * kMidP;       // panels per workgroup
 constexpr int kMidSlots = 5;                       // activation slices in the LDS ring
-constexpr int kMidDepth = 4;                       // slices requested ahead of the one in use
+constexpr int kMidDepth = 4;                       // slices requested ahead (divides the 8 of a k-block)
 constexpr int kMidBlocks = kActSplits * kMidRT;    // 1 KB (split, row tile) blocks per slice
 constexpr int kMidMaxSplits = 8;
 
@@ -71,6 +71,7 @@ struct GemmMid {
   static constexpr int P = kMidP;
   static constexpr int NF = (kMidBlocks + kMidWaves - 1) / kMidWaves;  // fill loads per wave and slice
   static_assert(NF == 3, "fill: three loads per wave and slice");
+  static_assert(8 % D == 0, "the weight ring is indexed by the slice within its k-block");
   const GemmParams& a;
   GemmMidSmem& sm;
   int tid, lane, wave, g, kl;
