@@ -198,6 +198,8 @@ def kernel_alg_bytes(name: str, w, lens) -> int:
         kind = int(args[3])
     elif name.startswith("gemm_split_kernel") and len(args) >= 2:
         kind = int(args[1])
+    elif name.startswith("gemm_mid_kernel") and len(args) >= 1:
+        kind = int(args[0])  # the first pass; its second pass (gemm_mid_finish_kernel) counts nothing
     if kind is not None:
         n_out, k_in = [(d + 2 * dkv, d), (d, d), (2 * f, d), (d, f), (v, d)][kind]
         return n_out * k_in * 2 + M * k_in * 4 + M * (n_out // (2 if kind == 2 else 1)) * 4
@@ -288,7 +290,9 @@ def summarize_step_counters(workload_name: str, dirs, cmds) -> int:
                      f"{fmt(wr_b / 1e6 if wr_b else None)} | {fmt(ratio, 2)} | {fmt(tb, 2)} | {fmt(tf)} | {mb} | {hr} | "
                      f"{lb} | {mm['vgpr']} |")
     lines += ["", "Kernel names: `gemm_wide_kernel<row tiles, panels per wave, kind, k-splits>`, "
-              "`gemm_kernel<bf16, row tiles, operand in LDS, kind>`, `gemm_split_kernel<k-splits, kind>` with kind "
+              "`gemm_kernel<bf16, row tiles, operand in LDS, kind>`, `gemm_split_kernel<k-splits, kind>`, "
+              "`gemm_mid_kernel<kind>` (its algorithmic bytes: the whole projection's; the published sums it "
+              "writes and `gemm_mid_finish_kernel<kind>` reads back are traffic beyond them) with kind "
               "0 QKV, 1 O, 2 gate/up, 3 down, 4 LM head; attention kernels read one layer's K/V.", ""]
     with open(out, "w") as fh:
         fh.write("\n".join(lines))

@@ -106,12 +106,13 @@ spade_status spade_model_set_big_gemm(spade_model m, int mode);
  * panel group (whole k-ranges of the eight); each stores its sums in the
  * workspace, and a second launch, one workgroup per panel group and 16-row
  * tile, adds them in range order and runs the epilogue.  mode 0 (the
- * default) uses it for the O, gate/up and down projections of 129 to 144
- * rows; mode 1 turns it off (the wide-row GEMM runs instead); mode 2 uses it
- * for every QKV, O, gate/up and down launch of 17 to 144 rows.  k_splits 0
- * chooses the split count per launch, 1..8 fixes it.  Results are
- * bit-for-bit the same under every setting.  Other values return
- * SPADE_EINVAL. */
+ * default) uses it where it measured faster than the wide-row GEMM: the
+ * gate/up projection of 113 to 144 rows, the O projection of 129 to 144, the
+ * down projection of 137 to 144; mode 1 turns it off (the wide-row GEMM runs
+ * instead); mode 2 uses it for every QKV, O, gate/up and down launch of 17
+ * to 144 rows.  k_splits 0 chooses the split count per launch, 1..8 fixes
+ * it.  Results are bit-for-bit the same under every setting.  Other values
+ * return SPADE_EINVAL. */
 spade_status spade_model_set_mid_gemm(spade_model m, int mode, int k_splits);
 
 /* K splitting of the batched O and down projections on the wide-row GEMM.

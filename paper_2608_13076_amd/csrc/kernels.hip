@@ -1147,6 +1147,17 @@ size_t wide_split_floats(int n_units, int M, int rt, int p) {
 
 size_t mid_split_floats() { return (size_t)kMidItemFloats; }
 
+// Rows above which a projection runs on the medium-M GEMM by default (the
+// wide-row GEMM's time grows with the rows, the medium-M GEMM's barely).
+int mid_min_rows(int kind) {
+  switch (kind) {
+    case GEMM_GU: return 112;
+    case GEMM_O: return 128;
+    case GEMM_DOWN: return 136;
+    default: return kMidRT * 16;  // QKV, LM head: never
+  }
+}
+
 // K-splits of a medium-M launch: the fewest that minimise the rounds of
 // workgroups (one per compute unit at a time) times the k-blocks of the
 // longest split, with a split launch charged about one and a half k-blocks
@@ -1450,11 +1461,11 @@ hipError_t launch_layer_gemm(spade_model md, spade_kv kv, int kind, int layer, c
     }
   }
   // batched verification: every row in one workgroup per panel group (by
-  // default the O, gate/up and down projections of more than kMidMinRows
-  // rows; the QKV projection measured no faster than on the wide-row GEMM)
+  // default the gate/up projection of more than 112 rows, O and down of
+  // more than 128 and 136: the crossovers with the wide-row GEMM measured at
+  // the 7B shape; the QKV projection measured no faster)
   if (wb && M > kWideMinRows && M <= kMidRT * 16 && kind != GEMM_LM && md->mid_gemm != 1 &&
-      (md->mid_gemm == 2 || (M > kMidMinRows && kind != GEMM_QKV)) && W.mid_part &&
-      (size_t)gemm_mid_unit_groups(units) <= W.mid_items) {
+      (md->mid_gemm == 2 || M > mid_min_rows(kind)) && W.mid_part && (size_t)gemm_mid_unit_groups(units) <= W.mid_items) {
     GemmParams gp = g;
     gp.w = wmat;
     gp.NKB = K / KBd;

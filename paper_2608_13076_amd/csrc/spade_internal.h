@@ -14,7 +14,6 @@ constexpr int kPanel = 16;           // weight rows per MFMA tile (one panel)
 constexpr int kTileBytes = 8192;     // one panel x one k-block, in the arena
 constexpr int kMaxRowsPerGemm = 32;  // rows handled by one skinny-GEMM launch
 constexpr int kWideMinRows = 16;     // bf16 projections with more rows use the wide-row GEMM
-constexpr int kMidMinRows = 128;     // O, gate/up and down projections of more rows (up to 144): the medium-M GEMM
 constexpr int kPrefillRows = 16;     // prompt rows per request of a prefill forward on the verify attention
 constexpr int kPrefillMaxRows = 2048;  // rows of a prefill forward (bf16 cache, head_dim 128)
 constexpr int kPrefillAttnTiles = 4;   // 16-row tiles (one wave each) per workgroup of the prefill attention
@@ -141,7 +140,7 @@ struct spade_model_s {
   int corr_split;  // correction draws of sampling requests: 0/2 over vocabulary slices, 1 in the accept workgroup
   int prefill_rows;  // prompt rows per request of a prefill forward: 0 as many as the workspace holds, else at most this
   int big_gemm;  // large-M projection GEMM: 0 where it fills the chip, 1 off, 2 whenever more than 16 rows
-  int mid_gemm;  // medium-M GEMM: 0 O, gate/up, down from kMidMinRows + 1 to 144 rows, 1 off, 2 every projection of 17-144
+  int mid_gemm;  // medium-M GEMM: 0 O, gate/up, down above mid_min_rows (to 144 rows), 1 off, 2 every projection of 17-144
   int mid_ks;    // its k-splits: 0 chosen per launch, 1..8 fixed
 };
 
@@ -197,6 +196,7 @@ WideChoice wide_choice(int kind, int M, int n_units, int NKB, int K, int n_cu, i
                        size_t cap_items, size_t cap_floats);
 size_t wide_split_floats(int n_units, int M, int rt, int p);
 int mid_k_splits(int n_units, int NKB, int n_cu, int fixed_ks);
+int mid_min_rows(int kind);  // rows above which a projection kind runs on the medium-M GEMM by default
 size_t mid_split_floats();  // published floats per panel group of a medium-M launch
 int lm_stats_panels(spade_model m, int M);
 hipError_t launch_softmax(const float* logits, int rows, int V, float invT, float* out, hipStream_t st);

@@ -214,8 +214,8 @@ class Model:
         _check(self.lib.spade_model_set_big_gemm(self.handle, int(mode)))
 
     def set_mid_gemm(self, mode: int, k_splits: int = 0) -> None:
-        """Projection GEMM of batched calls of up to 144 rows: mode 0 the O,
-        gate/up and down projections from 129 rows, 1 off, 2 every projection
+        """Projection GEMM of batched calls of up to 144 rows: mode 0 gate/up
+        from 113 rows, O from 129, down from 137, 1 off, 2 every projection
         from 17 rows (not the LM head); k_splits 0 chosen per launch, 1..8
         fixed."""
         _check(self.lib.spade_model_set_mid_gemm(self.handle, int(mode), int(k_splits)))
