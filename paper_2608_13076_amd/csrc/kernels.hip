@@ -1161,8 +1161,8 @@ int mid_min_rows(int kind) {
 // K-splits of a medium-M launch: the fewest that minimise the rounds of
 // workgroups (one per compute unit at a time) times the k-blocks of the
 // longest split, with a split launch charged about one and a half k-blocks
-// for its publish and combine.  A fixed count (1-8) is used as given; more
-// panel groups than the published-value buffers hold run unsplit.
+// for the range partials it adds to what the second pass reads back.  A
+// fixed count (1-8) is used as given.
 int mid_k_splits(int n_units, int NKB, int n_cu, int fixed_ks) {
   const int G = gemm_mid_unit_groups(n_units);
   if (fixed_ks > 0) return std::min(fixed_ks, kMidMaxSplits);
