@@ -121,11 +121,16 @@ size_t spade_weight_bytes(const spade_config* cfg);
 size_t spade_workspace_bytes(const spade_config* cfg, int max_batch, int max_gamma, int max_len);
 
 /* Bytes of a KV cache holding max_batch requests of max_len positions.  With
- * S = max_len rounded up to a multiple of 32: K is
- * [n_layers][max_batch][n_heads][S][head_dim] (a row per position) and V,
- * stored transposed, is [n_layers][max_batch][n_heads][head_dim][S] (a row
- * per feature), so the verify kernels read both as contiguous 16-byte
- * fragments.  max_len <= 16384. */
+ * S = max_len rounded up to a multiple of 256 and KVH the K/V heads: K is
+ * [n_layers][max_batch][KVH][S][head_dim] (a row per position); V is
+ * [n_layers][max_batch][KVH][S / 256] blocks of head_dim x 256 elements.  In
+ * a bf16 cache a block holds the B operands of the attention's O = P V in
+ * MFMA order: 1 KB fragments [head_dim / 16][8], fragment (t, s) covering
+ * features 16 t .. + 15 and positions 32 s .. + 31 of the block, its 16-byte
+ * piece 16 j + i holding positions 32 s + 8 j .. + 7 of feature 16 t + i; in
+ * a float32 cache a block is [head_dim][256].  So one wave's fragment load is
+ * 1 KB contiguous and one 256-key chunk of V one contiguous block.
+ * max_len <= 16384. */
 size_t spade_kv_bytes(const spade_config* cfg, int max_batch, int max_len);
 
 /* Create a model over caller-owned device buffers: d_weights of

@@ -205,17 +205,19 @@ __device__ __forceinline__ void attn_scores(const AttnItem& it, const uint4 (&kf
 }
 
 // V^T fragments of a chunk: 8-key granules below k_hi rounded up to 8 (zero
-// past them).
+// past them).  A chunk's keys lie in one V block, where the fragment of
+// (feature tile = wave, 32-key step) is 1 KB contiguous (v_cache_index).
 template <int CK>
-__device__ __forceinline__ void attn_load_v(const AttnItem& it, int wave, int lane, int stride, AttnRegs<CK>& r) {
+__device__ __forceinline__ void attn_load_v(const AttnItem& it, int wave, int lane, AttnRegs<CK>& r) {
+  static_assert(kVBlock % CK == 0, "a chunk within one V block");
   const int g = lane >> 4, kl = lane & 15;
   const int ke = (it.k_hi + 7) & ~7;
-  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
+  const uint16_t* vfr = it.vc + v_cache_index(16 * wave + kl, it.k_lo + 8 * g, kAttnHd);
 #pragma unroll
   for (int ks = 0; ks < CK / 32; ++ks) {
     const int kv0 = it.k_lo + 32 * ks + 8 * g;
     r.vf[ks] = make_uint4(0, 0, 0, 0);
-    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
+    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vfr + ks * 512);
   }
 }
 
@@ -318,15 +320,17 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
       sv[grp][i] = (key < it.k_hi && key <= it.L + row) ? acc[i] * scale : -INFINITY;
     }
   }
-  // the V^T fragments, after the score products (the K registers are free)
+  // the V^T fragments, after the score products (the K registers are free);
+  // fragment (wave, 32-key step ks) of the chunk's V block is 512 elements
+  // after step ks - 1's
   __builtin_amdgcn_sched_barrier(0);
   AttnRegs<CK> r;
-  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
+  const uint16_t* vfr = it.vc + v_cache_index(16 * wave + kl, it.k_lo + 8 * g, kAttnHd);
 #pragma unroll
   for (int ks = 0; ks < CK / 32; ++ks) {
     const int kv0 = it.k_lo + 32 * ks + 8 * g;
     r.vf[ks] = make_uint4(0, 0, 0, 0);
-    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
+    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vfr + ks * 512);
   }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -678,12 +682,12 @@ __device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (
     }
   __builtin_amdgcn_sched_barrier(0);
   AttnRegs<CK> r;
-  const uint16_t* vrow = it.vc + (size_t)(16 * wave + kl) * stride;
+  const uint16_t* vfr = it.vc + v_cache_index(16 * wave + kl, it.k_lo + 8 * g, kAttnHd);
 #pragma unroll
   for (int ks = 0; ks < CK / 32; ++ks) {
     const int kv0 = it.k_lo + 32 * ks + 8 * g;
     r.vf[ks] = make_uint4(0, 0, 0, 0);
-    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vrow + kv0);
+    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vfr + ks * 512);
   }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -841,7 +845,7 @@ __device__ __forceinline__ void pf_fetch(int c, int b, int k_hi, int ke, const u
       if (k0 + row < k_hi) r[q] = *(const uint4*)(kc + (size_t)(k0 + row) * kAttnHd + pc * 8);
     } else {
       const int f = e / CPR, pc = e % CPR, key = k0 + 8 * pc;
-      if (key + 8 <= ke) r[q] = *(const uint4*)(vc + (size_t)f * stride + key);
+      if (key + 8 <= ke) r[q] = *(const uint4*)(vc + v_cache_index(f, key, kAttnHd));
     }
   }
 }

@@ -349,7 +349,7 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   float* po = p.part_o + ((bh * p.NC + c) * p.Rmax) * HD;
   float* pml = p.part_ml + ((bh * p.NC + c) * p.Rmax) * 2;
   const size_t kbase = ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * HD;  // K rows [key][HD]
-  const size_t vbase = kbase;                                       // V^T rows [feature][kv_stride]
+  const size_t vbase = kbase;  // V blocks of kVBlock positions (v_cache_index, v_cache_index_f32)
 
   if (k_lo < k_hi) {
     if constexpr (KVBF16) {
@@ -372,7 +372,7 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
       const int kv0 = kw + 8 * g;  // first of this lane's 8 keys
 #pragma unroll
       for (int ft = 0; ft < FT; ++ft) {
-        const uint16_t* vp = vc + vbase + (size_t)(16 * ft + kl) * p.kv_stride + kv0;
+        const uint16_t* vp = vc + vbase + v_cache_index(16 * ft + kl, kv0, HD);
         if (kv0 + 8 <= k_hi) {
           vf[ft] = *(const uint4*)vp;
         } else {
@@ -507,7 +507,7 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
       float vt[DPV][KPW];  // V^T: this lane's features over the wave's keys
 #pragma unroll
       for (int e = 0; e < DPV; ++e) {
-        const float* vp = vc + vbase + (size_t)(lane * DPV + e) * p.kv_stride + kw;
+        const float* vp = vc + vbase + v_cache_index_f32(lane * DPV + e, kw, HD);
 #pragma unroll
         for (int j = 0; j < KPW; j += 4) {
           if (kw + j + 4 <= k_hi) {

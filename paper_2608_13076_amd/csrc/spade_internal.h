@@ -26,7 +26,25 @@ constexpr int kAttnChunk = 128;      // keys per workgroup of the generic attent
 constexpr int kAttnMaxChunks = 128;  // chunks per (request, head)
 constexpr int kMaxLen = kAttnChunk * kAttnMaxChunks;
 constexpr int kMaxStatGroups = 2048;             // LM-head statistics entries per row (workgroups)
-inline int kv_stride_of(int max_len) { return (max_len + 31) / 32 * 32; }
+// The V cache is stored in blocks of kVBlock positions (head_dim x kVBlock
+// elements, one contiguous run per (request, K/V head)); positions per
+// (request, K/V head) of either cache: max_len rounded up to a whole block.
+constexpr int kVBlock = 256;
+inline int kv_stride_of(int max_len) { return (max_len + kVBlock - 1) / kVBlock * kVBlock; }
+// Element (feature f, position pos) of a (request, K/V head) V region of a
+// bf16 cache: a block is the B operands of O = P V in MFMA order, fragment
+// (16-feature tile f / 16, 32-position step p / 32) of 1 KB, whose lane
+// 16 ((p / 8) % 4) + f % 16 holds positions 8 ((p / 8) % 4) .. + 7 of the step
+// (p = pos % kVBlock), so one wave's fragment load reads 1 KB contiguous.
+__host__ __device__ inline size_t v_cache_index(int f, int pos, int hd) {
+  const int p = pos % kVBlock;
+  return (size_t)(pos / kVBlock) * hd * kVBlock +
+         (size_t)(((((f >> 4) * (kVBlock / 32) + (p >> 5)) * 64 + ((p >> 3) & 3) * 16 + (f & 15)) * 8) + (p & 7));
+}
+// ... and of a float32 cache: a block is [head_dim][kVBlock].
+__host__ __device__ inline size_t v_cache_index_f32(int f, int pos, int hd) {
+  return ((size_t)(pos / kVBlock) * hd + f) * kVBlock + (pos % kVBlock);
+}
 
 // Keys per chunk of the bf16 / head_dim-128 verify attention.  A constant:
 // a request's attention (and so its logits) must not depend on the other

@@ -219,3 +219,51 @@ def gpu_setup_streaming(w, max_len: int, max_batch: Optional[int] = None):
             print(f"  [{w.name}] weights of layer {layer} loaded", flush=True)
     kv = spade.KVCache(model, max_batch or w.batch, max_len)
     return model, kv
+
+
+# The cache layout (include/spade.h, spade_kv_bytes): K rows
+# [position][head_dim]; V in blocks of V_BLOCK positions -- bf16: the B
+# operands of O = P V in MFMA order, 1 KB fragments (16-feature tile,
+# 32-position step) whose lane 16 ((p / 8) % 4) + f % 16 holds positions
+# 8 ((p / 8) % 4) .. + 7; float32: [head_dim][V_BLOCK]; positions per (request,
+# K/V head): max_len rounded up to a whole block.
+V_BLOCK = 256
+
+
+def kv_stride(max_len: int) -> int:
+    return (max_len + V_BLOCK - 1) // V_BLOCK * V_BLOCK
+
+
+def v_phys_index(shape, S: int) -> np.ndarray:
+    """[head_dim, S]: the element offset of (feature, position) in a
+    (request, K/V head) region of the V cache."""
+    hd = shape.head_dim
+    f = np.arange(hd)[:, None]
+    pos = np.arange(S)[None, :]
+    blk, p = pos // V_BLOCK, pos % V_BLOCK
+    if shape.kv_dtype == "bf16":
+        return blk * hd * V_BLOCK + (((f // 16) * (V_BLOCK // 32) + p // 32) * 64 + ((p // 8) % 4) * 16 + f % 16) * 8 + p % 8
+    return (blk * hd + f) * V_BLOCK + p
+
+
+def kv_views(kv, shape, max_len: int):
+    """K as [layer][request][K/V head][position][head_dim] and V as
+    [layer][request][K/V head][region] views of the cache (v_phys_index maps
+    a region's elements)."""
+    import torch
+    S = kv_stride(max_len)
+    dt = torch.int16 if shape.kv_dtype == "bf16" else torch.float32
+    half = kv.buf.numel() // 2
+    n = shape.n_layers * kv.max_batch * shape.kv_heads * S * shape.head_dim
+    k = kv.buf[:half].view(dt)[:n].view(shape.n_layers, kv.max_batch, shape.kv_heads, S, shape.head_dim)
+    v = kv.buf[half:].view(dt)[:n].view(shape.n_layers, kv.max_batch, shape.kv_heads, S * shape.head_dim)
+    return k, v
+
+
+def v_by_position(v, shape, max_len: int):
+    """[..., region] -> [..., head_dim, position] (a copy)."""
+    import torch
+    S = kv_stride(max_len)
+    idx = torch.as_tensor(v_phys_index(shape, S).reshape(-1), device=v.device)
+    return v[..., idx].reshape(*v.shape[:-1], shape.head_dim, S)
+

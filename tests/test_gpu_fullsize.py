@@ -27,7 +27,7 @@ import pytest
 
 from synth import make_inputs, workload
 from tests.golden.drafts import HERE as GOLDEN_DIR, load_golden
-from tests.helpers import gpu_prefill, gpu_setup_streaming, gpu_verify, report_parity
+from tests.helpers import gpu_prefill, gpu_setup_streaming, gpu_verify, kv_stride, report_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -295,7 +295,7 @@ def _check_layer0_keys(w, inp, kv, max_len, n_samples=24):
     E = bf16_bits_to_f64(emb) if emb.dtype == np.uint16 else emb.astype(np.float64)
     Wk = bf16_bits_to_f64(wk) if wk.dtype == np.uint16 else wk.astype(np.float64)
     KVH = m.kv_heads
-    stride = (max_len + 31) // 32 * 32
+    stride = kv_stride(max_len)
     kcache = kv.buf[: kv.buf.numel() // 2].view(torch.int16 if m.kv_dtype == "bf16" else torch.float32)
     rng = np.random.default_rng(5)
     for _ in range(n_samples):

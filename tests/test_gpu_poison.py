@@ -19,7 +19,7 @@ import numpy as np
 import pytest
 
 from synth import ModelWeights, make_inputs, mini_workloads
-from tests.helpers import gpu_setup, gpu_verify
+from tests.helpers import gpu_setup, gpu_verify, kv_stride, kv_views, v_phys_index
 
 pytestmark = pytest.mark.gpu
 
@@ -34,16 +34,9 @@ def need_gpu():
 
 
 def _views(kv, shape, max_len):
-    """K as [layer][request][K/V head][S][hd] and V^T as [layer][request][K/V
-    head][hd][S] over the cache buffer (S = max_len rounded up to 32)."""
-    import torch
-    S = (max_len + 31) // 32 * 32
-    dt = torch.int16 if shape.kv_dtype == "bf16" else torch.float32
-    half = kv.buf.numel() // 2
-    n = shape.n_layers * kv.max_batch * shape.kv_heads * S * shape.head_dim
-    k = kv.buf[:half].view(dt)[:n].view(shape.n_layers, kv.max_batch, shape.kv_heads, S, shape.head_dim)
-    v = kv.buf[half:].view(dt)[:n].view(shape.n_layers, kv.max_batch, shape.kv_heads, shape.head_dim, S)
-    return k, v
+    """K as [layer][request][K/V head][position][hd] and V as [layer][request]
+    [K/V head][region] over the cache buffer."""
+    return kv_views(kv, shape, max_len)
 
 
 def _nan_value(shape):
@@ -60,6 +53,7 @@ def _two_rounds(w, weights, fill, merge, grouped):
     if w.model.kv_heads != w.model.n_heads:
         model.set_attn_grouped(grouped)
     k, v = _views(kv, w.model, max_len)
+    vidx = v_phys_index(w.model, kv_stride(max_len))
     if fill == "nan":
         k.fill_(_nan_value(w.model))
         v.fill_(_nan_value(w.model))
@@ -74,7 +68,8 @@ def _two_rounds(w, weights, fill, merge, grouped):
     if fill == "nan":  # the rolled-back drafts' rows and everything after them
         for b in range(w.batch):
             k[:, b, :, int(lens[b]):, :] = _nan_value(w.model)
-            v[:, b, :, :, int(lens[b]):] = _nan_value(w.model)
+            past = torch.as_tensor(vidx[:, int(lens[b]):].reshape(-1), device=v.device)
+            v[:, b, :, past] = _nan_value(w.model)
     inp2 = make_inputs(w, round_index=1)
     r2 = gpu_verify(model, kv, inp2)
     err = model.device_error()

@@ -18,7 +18,7 @@ import numpy as np
 import pytest
 
 from synth import ModelWeights, make_inputs, mini_workloads
-from tests.helpers import gpu_setup, gpu_verify
+from tests.helpers import gpu_setup, gpu_verify, kv_views, v_by_position
 
 pytestmark = pytest.mark.gpu
 
@@ -38,23 +38,14 @@ def _assert_same_cache(model, kv1, kv2, B, max_len):
     l2, p2 = kv2.get_state(B)
     np.testing.assert_array_equal(l1, l2)
     np.testing.assert_array_equal(p1, p2)
-    half = kv1.buf.numel() // 2
     s = model.shape
-    stride = (max_len + 31) // 32 * 32
-    elt = torch.int16 if s.kv_dtype == "bf16" else torch.float32
-    n_el = s.n_layers * B * s.kv_heads * stride * s.head_dim
-    for which, part in (("k", slice(0, half)), ("v", slice(half, 2 * half))):
-        a = kv1.buf[part].view(elt)[:n_el].view(s.n_layers, B, s.kv_heads, stride * s.head_dim)
-        c = kv2.buf[part].view(elt)[:n_el].view(s.n_layers, B, s.kv_heads, stride * s.head_dim)
-        for b in range(B):
-            n = int(l1[b])
-            if which == "k":  # K rows [pos][hd]
-                ka = a[:, b].reshape(s.n_layers, s.kv_heads, stride, s.head_dim)[:, :, :n]
-                kc = c[:, b].reshape(s.n_layers, s.kv_heads, stride, s.head_dim)[:, :, :n]
-            else:  # V stored transposed: [hd][stride] per head
-                ka = a[:, b].reshape(s.n_layers, s.kv_heads, s.head_dim, stride)[..., :n]
-                kc = c[:, b].reshape(s.n_layers, s.kv_heads, s.head_dim, stride)[..., :n]
-            assert torch.equal(ka, kc), (which, b)
+    k1, v1 = kv_views(kv1, s, max_len)
+    k2, v2 = kv_views(kv2, s, max_len)
+    for b in range(B):
+        n = int(l1[b])
+        assert torch.equal(k1[:, b, :, :n], k2[:, b, :, :n]), ("k", b)
+        assert torch.equal(v_by_position(v1[:, b], s, max_len)[..., :n], v_by_position(v2[:, b], s, max_len)[..., :n]), \
+            ("v", b)
 
 
 def _assert_same_verify(model, kv1, kv2, inp):
