@@ -10,8 +10,9 @@
 // [16 w, 16 w + 16) over every key of the chunk), so each wave ends with
 // final chunk outputs and no cross-wave sum is needed.  Both products use
 // MFMA 16x16x32 bf16 with Q and P split into two bf16 terms (hi + lo).  K is
-// stored as rows [pos][hd] and V transposed, rows [feature][stride], so both
-// B operands are 16-byte loads.  A chunk writes its unnormalised output, row
+// stored as rows [pos][hd] and V in blocks of 256 positions in the order of
+// the B operands of O = P V (v_cache_index), so both B operands are 16-byte
+// loads.  A chunk writes its unnormalised output, row
 // max and row sum; the chunks of a (request, head) are merged in chunk order
 // with weights exp(m_c - max) / sum_c(l_c exp(m_c - max)).
 #pragma once
@@ -294,7 +295,7 @@ __device__ __forceinline__ floatx4 attn_pv(const AttnSmem<CK>& sm, const AttnReg
 template <int CK>
 __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
                                                  const uint16_t (*sqh)[kAttnQPitch],
-                                                 const uint16_t (*sql)[kAttnQPitch], int R, float scale, int stride,
+                                                 const uint16_t (*sql)[kAttnQPitch], int R, float scale,
                                                  AttnSmem<CK>& sm) {
   constexpr int NG = CK / 128;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -651,7 +652,7 @@ template <int CK, int T>
 __device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (&kf)[CK / 128][4],
                                                const uint16_t (*sqh)[kAttnQPitch],
                                                const uint16_t (*sql)[kAttnQPitch], int R, int NR, float scale,
-                                               int stride, AttnSmemG<CK, T>& sm, floatx4 (&o)[T]) {
+                                               AttnSmemG<CK, T>& sm, floatx4 (&o)[T]) {
   constexpr int NG = CK / 128;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, kl = lane & 15;
@@ -832,7 +833,7 @@ __device__ __forceinline__ int pf_v_at(int f, int c) {
 // at or past k_hi (V^T: 8-key pieces past ke) read as zero.
 template <int W, int SK>
 __device__ __forceinline__ void pf_fetch(int c, int b, int k_hi, int ke, const uint16_t* kc, const uint16_t* vc,
-                                         int stride, uint4 (&r)[SK * 16 / (64 * W)]) {
+                                         uint4 (&r)[SK * 16 / (64 * W)]) {
   constexpr int PER = SK * 16 / (64 * W), NB = 256 / SK, CPR = SK / 8;
   const bool is_v = b >= NB;
   const int k0 = c * 256 + (is_v ? b - NB : b) * SK;
@@ -876,7 +877,7 @@ __device__ __forceinline__ void pf_wave_sync() {
 template <int W, int SK, class Out>
 __device__ __forceinline__ void attn_prefill_tiles(AttnPfSmem<W, SK>& s, float2* mlw, int NCP, const float* q,
                                                    int d, int h, const uint16_t* kc, const uint16_t* vc, int L,
-                                                   int R, int t0, float scale, int stride, Out&& out) {
+                                                   int R, int t0, float scale, Out&& out) {
   constexpr int NB = 256 / SK, SPB = SK / 32, PER = SK * 16 / (64 * W);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int g = lane >> 4, kl = lane & 15;
@@ -963,7 +964,7 @@ __device__ __forceinline__ void attn_prefill_tiles(AttnPfSmem<W, SK>& s, float2*
 
   uint4 pre[PER];
   // first walk: every chunk's row max and row sum
-  pf_fetch<W, SK>(0, 0, kend, 0, kc, vc, stride, pre);
+  pf_fetch<W, SK>(0, 0, kend, 0, kc, vc, pre);
   pf_stash(s, 0, 0, pre);
   __syncthreads();
   int slot = 0;
@@ -972,7 +973,7 @@ __device__ __forceinline__ void attn_prefill_tiles(AttnPfSmem<W, SK>& s, float2*
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const bool more = b + 1 < NB || c + 1 < ncg;
-      if (more) pf_fetch<W, SK>(b + 1 < NB ? c : c + 1, b + 1 < NB ? b + 1 : 0, kend, 0, kc, vc, stride, pre);
+      if (more) pf_fetch<W, SK>(b + 1 < NB ? c : c + 1, b + 1 < NB ? b + 1 : 0, kend, 0, kc, vc, pre);
       if (c < nct) scores(s.st[slot], c, b, sv);
       if (more) pf_stash(s, slot ^ 1, 0, pre);
       __syncthreads();
@@ -1006,7 +1007,7 @@ __device__ __forceinline__ void attn_prefill_tiles(AttnPfSmem<W, SK>& s, float2*
   for (int fb = 0; fb < 8; ++fb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) O[fb][i] = 0.f;
-  pf_fetch<W, SK>(0, 0, kend, keg, kc, vc, stride, pre);
+  pf_fetch<W, SK>(0, 0, kend, keg, kc, vc, pre);
   pf_stash(s, slot, 0, pre);
   __syncthreads();
   for (int c = 0; c < ncg; ++c) {
@@ -1018,7 +1019,7 @@ __device__ __forceinline__ void attn_prefill_tiles(AttnPfSmem<W, SK>& s, float2*
 #pragma unroll
     for (int b = 0; b < 2 * NB; ++b) {
       const bool more = b + 1 < 2 * NB || c + 1 < ncg;
-      if (more) pf_fetch<W, SK>(b + 1 < 2 * NB ? c : c + 1, b + 1 < 2 * NB ? b + 1 : 0, kend, keg, kc, vc, stride, pre);
+      if (more) pf_fetch<W, SK>(b + 1 < 2 * NB ? c : c + 1, b + 1 < 2 * NB ? b + 1 : 0, kend, keg, kc, vc, pre);
       if (c < nct) {
         if (b < NB) {
           scores(s.st[slot], c, b, sv);

@@ -724,7 +724,7 @@ attn_lr_kernel(AttnParams p) {
   attn_load_k<CK>(it, wave, lane, kf);
   attn_stage_q(sqh, sql, qrow, 4 * f4, qv);
   __syncthreads();
-  const floatx4 o = attn_chunk_lr<CK>(it, kf, sqh, sql, p.R, p.scale, p.kv_stride, sm);
+  const floatx4 o = attn_chunk_lr<CK>(it, kf, sqh, sql, p.R, p.scale, sm);
   if constexpr (!ARRIVE) {  // attn_merge_kernel merges after this launch
     attn_publish<CK>(it, o, sm, p.part_o, p.part_ml, p.H, p.NC, p.Rmax, p.R);
     return;
@@ -770,7 +770,7 @@ attn_g_kernel(AttnParams p) {
   for (int j = 0; j < T; ++j) attn_stage_q(sqh, sql, (tid >> 5) + 16 * j, 4 * f4, qv[j]);
   __syncthreads();
   floatx4 o[T];
-  attn_chunk_grp<CK, T>(it, kf, sqh, sql, p.R, NR, p.scale, p.kv_stride, sm, o);
+  attn_chunk_grp<CK, T>(it, kf, sqh, sql, p.R, NR, p.scale, sm, o);
   attn_publish_grp<CK, T>(it, kvh, p.G, o, sm, p.part_o, p.part_ml, p.H, p.NC, p.Rmax, p.R);
 }
 
@@ -810,7 +810,7 @@ attn_prefill_kernel(AttnParams p, int ngrp) {
   const size_t head_off = ((size_t)bg * p.Hkv + kvh) * p.kv_stride * kAttnHd;
   attn_prefill_tiles<W, SK>(s, (float2*)lds_dyn, p.NC, p.q + (size_t)bl * p.R * p.d, p.d, h,
                             (const uint16_t*)p.kc + head_off, (const uint16_t*)p.vc + head_off, p.lens[bg], p.R,
-                            grp * W, p.scale, p.kv_stride, [&](int row, int dd, float O) {
+                            grp * W, p.scale, [&](int row, int dd, float O) {
                               store_act<ABF16>(p.act_out, p.act_split,
                                                (size_t)(bl * p.R + row) * p.d + h * kAttnHd + dd, O);
                             });
