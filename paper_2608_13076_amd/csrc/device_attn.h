@@ -169,7 +169,7 @@ __device__ __forceinline__ void attn_load_k(const AttnItem& it, int wave, int la
     for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = make_uint4(0, 0, 0, 0);
     if (key < it.k_hi) {
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = *(const uint4*)(it.kc + (size_t)key * kAttnHd + 32 * ks + 8 * g);
+      for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = ld_stream_g128(it.kc + (size_t)key * kAttnHd + 32 * ks + 8 * g);
     }
   }
 }
@@ -218,7 +218,7 @@ __device__ __forceinline__ void attn_load_v(const AttnItem& it, int wave, int la
   for (int ks = 0; ks < CK / 32; ++ks) {
     const int kv0 = it.k_lo + 32 * ks + 8 * g;
     r.vf[ks] = make_uint4(0, 0, 0, 0);
-    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vfr + ks * 512);
+    if (kv0 + 8 <= ke) r.vf[ks] = ld_stream_g128(vfr + ks * 512);
   }
 }
 
@@ -331,7 +331,7 @@ __device__ __forceinline__ floatx4 attn_chunk_lr(const AttnItem& it, const uint4
   for (int ks = 0; ks < CK / 32; ++ks) {
     const int kv0 = it.k_lo + 32 * ks + 8 * g;
     r.vf[ks] = make_uint4(0, 0, 0, 0);
-    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vfr + ks * 512);
+    if (kv0 + 8 <= ke) r.vf[ks] = ld_stream_g128(vfr + ks * 512);
   }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -688,7 +688,7 @@ __device__ __forceinline__ void attn_chunk_grp(const AttnItem& it, const uint4 (
   for (int ks = 0; ks < CK / 32; ++ks) {
     const int kv0 = it.k_lo + 32 * ks + 8 * g;
     r.vf[ks] = make_uint4(0, 0, 0, 0);
-    if (kv0 + 8 <= ke) r.vf[ks] = *(const uint4*)(vfr + ks * 512);
+    if (kv0 + 8 <= ke) r.vf[ks] = ld_stream_g128(vfr + ks * 512);
   }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll

@@ -333,7 +333,7 @@ struct Gemm {
     const uint8_t* tile = a.w + ((size_t)u * NKB + kbl + (ok ? k : 0)) * kTileBytes;
     const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) w[j] = ld_b128<false>(r, (uint32_t)(lane * 16 + j * 1024));
+    for (int j = 0; j < 8; ++j) w[j] = ld_stream_b128(r, (uint32_t)(lane * 16 + j * 1024));
   }
 
   // activation operand of k-block kbl + k (k >= cnt: zeros)

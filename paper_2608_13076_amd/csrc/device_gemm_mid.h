@@ -171,7 +171,7 @@ struct GemmMid {
   __device__ __forceinline__ void issue_w(int t, uint4 (&w)[P]) const {
     const uint32_t off = t < T ? (uint32_t)((kb0 + (t >> 3)) * kTileBytes + (t & 7) * 1024 + lane * 16) : kOob;
 #pragma unroll
-    for (int p = 0; p < P; ++p) w[p] = ld_b128<false>(rw[p], off);
+    for (int p = 0; p < P; ++p) w[p] = ld_stream_b128(rw[p], off);
   }
 
   template <int OFF>

@@ -111,7 +111,7 @@ struct GemmSplit {
     const uint8_t* tile = a.w + ((size_t)(ok ? u : 0) * NKB + kbl + (ok ? k : 0)) * kTileBytes;
     const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) w[q] = ld_b128<false>(r, (uint32_t)(lane * 16 + q * 1024));
+    for (int q = 0; q < 8; ++q) w[q] = ld_stream_b128(r, (uint32_t)(lane * 16 + q * 1024));
   }
 
   // copy k-blocks [kb0, kb0 + nkbs) of rows 0..M-1 of every split into LDS:
