@@ -140,7 +140,7 @@ struct GemmWide {
       const uint8_t* tile = a.w + ((size_t)(ok ? u : 0) * NKB + (ok ? kb : 0)) * kTileBytes;
       const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) w[p][j] = ld_b128<false>(r, (uint32_t)(lane * 16 + j * 1024));
+      for (int j = 0; j < 8; ++j) w[p][j] = ld_stream_b128(r, (uint32_t)(lane * 16 + j * 1024));
     }
   }
 

@@ -55,8 +55,10 @@ __device__ __forceinline__ uint4 ld_b128(Rsrc r, uint32_t off) {
 // nt cache policy: a streaming read.  With every compute unit streaming lines
 // that no other workgroup reads, HBM delivers about 7.0 TB/s with it against
 // about 6.1 TB/s without (one to four 8-wave workgroups per CU, plain and
-// direct-to-LDS buffer loads alike).  Weight tiles, each read by one workgroup
-// once per call, are loaded with it.
+// direct-to-LDS buffer loads alike).  The weight tiles of the verify-call
+// GEMMs are loaded with it (each is read by one workgroup, or by the few row
+// groups of a wide-row launch, once per call); the big prefill GEMM, whose
+// tiles many row-tile workgroups re-read through L2, runs slower with it.
 constexpr int kAuxStream = 2;
 
 __device__ __forceinline__ uint4 ld_stream_b128(Rsrc r, uint32_t off) {
