@@ -504,13 +504,6 @@ struct Gemm {
       sm.rinv[row] = (a.ssq_in != nullptr && row < a.M) ? 1.0f / sqrtf(s * a.inv_din + a.eps) : 1.0f;
   }
 
-  // The first three weight tiles: needs nothing the previous stage produces.
-  __device__ __forceinline__ void prefetch() {
-    issue_w(0, w0);
-    issue_w(1, w1);
-    issue_w(2, w2);
-  }
-
   template <int P>
   __device__ __forceinline__ void step(int t) {
     if constexpr (P == 0) step_impl(t, w0, e0, e2);
@@ -545,19 +538,30 @@ struct Gemm {
     }
   }
 
-  // Everything after prefetch(): operands, row scales, the item loop.  The
-  // first item needs all of the prologue; starting the loop with nothing in
-  // flight lets the loop head take its wait counts from the loop body.
+  // The whole launch: operands, row scales, the item loop.  Request order
+  // (scheduling barriers keep it): weight tiles 0 and 1, the operand copy, the
+  // epilogue inputs and the row partials, weight tile 2.  Every workgroup
+  // starts at once, so whatever is requested behind the first weight tiles
+  // queues behind the whole chip's: the operand comes after two tiles (it
+  // waited behind three before, or the weights behind the operand: both
+  // measured slower).  Loads complete in issue order, so the prologue waits
+  // for all but tile 2's eight loads, and the loop starts with a tile in
+  // flight.
   __device__ __forceinline__ void run() {
-    // prologue: operand copy, epilogue inputs and row partials in one round trip
+    issue_w(0, w0);
+    issue_w(1, w1);
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (ALDS) fill_lds_a();
     else issue_a_t(0, av);
     e0 = epi_load(0);
     e1 = epi_load(1);
     float sv[kSsqFirst];
     ssq_issue(sv);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_w(2, w2);
+    __builtin_amdgcn_sched_barrier(0);
     row_scales(sv);
-    __builtin_amdgcn_s_waitcnt(0);
+    wait_vmcnt<8>();
     __syncthreads();
     items();
     finish();

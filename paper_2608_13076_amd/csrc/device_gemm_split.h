@@ -196,12 +196,6 @@ struct GemmSplit {
     acc = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  __device__ __forceinline__ void prefetch() {
-    issue_w(0, w0);
-    issue_w(1, w1);
-    issue_w(2, w2);
-  }
-
   template <int P>
   __device__ __forceinline__ void step(int t) {
     if constexpr (P == 0) step_impl(t, w0);
@@ -258,13 +252,22 @@ struct GemmSplit {
     }
   }
 
+  // Request order: weight tile 0, this split's operand copy, weight tiles 1
+  // and 2 (the operand waits behind one tile of every workgroup's instead of
+  // three); the prologue waits for all but tiles 1 and 2.
   __device__ __forceinline__ void run() {
+    issue_w(0, w0);
+    __builtin_amdgcn_sched_barrier(0);
     fill_lds_a();
+    __builtin_amdgcn_sched_barrier(0);
+    issue_w(1, w1);
+    issue_w(2, w2);
+    __builtin_amdgcn_sched_barrier(0);
     for (int r = tid >> 4; r < 16; r += 32) {
       const float ri = gemm_row_rinv(a, r, tid & 15);
       if ((tid & 15) == 0) sm.rinv[r] = ri;
     }
-    __builtin_amdgcn_s_waitcnt(0);
+    wait_vmcnt<16>();
     __syncthreads();
     // item count padded to a multiple of 3 with no exits inside the loop
     const int Tpad = (T + 2) / 3 * 3;

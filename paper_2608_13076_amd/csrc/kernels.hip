@@ -152,7 +152,6 @@ __global__ void __launch_bounds__(kGemmWaves * 64) gemm_kernel(GemmParams a) {
   __shared__ GemmSmem<MT> sm;
   extern __shared__ uint4 lds_dyn[];
   Gemm<WBF16, MT, ALDS, KIND, false> g(a, sm, (uint8_t*)lds_dyn, (int)blockIdx.x, (int)gridDim.x);
-  g.prefetch();
   g.run();
 }
 
@@ -164,7 +163,6 @@ template <int KS, int KIND>
 __global__ void __launch_bounds__(kGemmWaves * 64) gemm_split_kernel(GemmParams a, uint32_t* cnt, float* part, int G) {
   extern __shared__ uint4 lds_dyn[];
   GemmSplit<KS, KIND> g(a, *(GemmSplitSmem*)lds_dyn, (uint8_t*)lds_dyn + kSplitSmemBytes, cnt, part, G);
-  g.prefetch();
   g.run();
 }
 
