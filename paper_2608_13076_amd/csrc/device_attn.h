@@ -28,8 +28,11 @@ template <int CK>
 struct AttnSmem {
   static_assert(CK == 128 || CK == 256, "chunk of 128 or 256 keys");
   // probabilities as two bf16 terms (the A operand of O = P V); rows padded by
-  // 16 bytes so the 16 rows of a fragment read start in different banks
-  uint16_t ph[kAttnRows][CK + 8], pl[kAttnRows][CK + 8];
+  // 16 bytes so the 16 rows of a fragment read start in different banks; 16-byte
+  // aligned, so each lane's fragment is one ds_read_b128 (with the alignment of
+  // uint16_t alone it becomes two ds_read2_b32, whose 64 lanes conflict)
+  alignas(16) uint16_t ph[kAttnRows][CK + 8];
+  alignas(16) uint16_t pl[kAttnRows][CK + 8];
   float pm[kAttnRows][8], ps[kAttnRows][8];  // per-wave row max / row sum
   float m[kAttnRows], l[kAttnRows];
 };
@@ -615,7 +618,8 @@ __device__ __forceinline__ void attn_publish_merge(const AttnItem& it, floatx4 o
 // the caller with attn_stage_q.  o[t]: rows 16 t + 4 g + i (i = 0..3), feature 16 wave + kl.
 template <int CK, int T>
 struct AttnSmemG {
-  uint16_t ph[16 * T][CK + 8], pl[16 * T][CK + 8];
+  alignas(16) uint16_t ph[16 * T][CK + 8];
+  alignas(16) uint16_t pl[16 * T][CK + 8];
   float pm[16 * T][8], ps[16 * T][8];
   float m[16 * T], l[16 * T];
 };

@@ -706,7 +706,8 @@ __global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_
 attn_lr_kernel(AttnParams p) {
   __shared__ AttnSmem<CK> sm;
   __shared__ AttnMergeSmem ms;
-  __shared__ uint16_t sqh[kAttnRows][kAttnQPitch], sql[kAttnRows][kAttnQPitch];
+  __shared__ alignas(16) uint16_t sqh[kAttnRows][kAttnQPitch];
+  __shared__ alignas(16) uint16_t sql[kAttnRows][kAttnQPitch];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const AttnWork wk = attn_work((int)blockIdx.x, p.NC, p.Hkv, p.G, p.nb);
   if (!wk.ok) return;
@@ -741,7 +742,8 @@ __global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_
 attn_g_kernel(AttnParams p) {
   constexpr int CK = kAttnChunkKeys;
   __shared__ AttnSmemG<CK, T> sm;
-  __shared__ uint16_t sqh[16 * T][kAttnQPitch], sql[16 * T][kAttnQPitch];
+  __shared__ alignas(16) uint16_t sqh[16 * T][kAttnQPitch];
+  __shared__ alignas(16) uint16_t sql[16 * T][kAttnQPitch];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const AttnWork wk = attn_work((int)blockIdx.x, p.NC, p.Hkv, 1, p.nb);
   if (!wk.ok) return;
