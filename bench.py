@@ -289,7 +289,7 @@ def summarize_step_counters(workload_name: str, dirs, cmds) -> int:
         lines.append(f"| `{short}` | {n} | {us:.1f} | {fmt(alg / 1e6 if alg else None)} | {fmt(rd_b / 1e6 if rd_b else None)} | "
                      f"{fmt(wr_b / 1e6 if wr_b else None)} | {fmt(ratio, 2)} | {fmt(tb, 2)} | {fmt(tf)} | {mb} | {hr} | "
                      f"{lb} | {mm['vgpr']} |")
-    lines += ["", "Kernel names: `gemm_wide_kernel<row tiles, panels per wave, kind, k-splits>`, "
+    lines += ["", "Kernel names: `gemm_wide_kernel<row tiles, panels per wave, kind, k-splits, non-temporal weight loads>`, "
               "`gemm_kernel<bf16, row tiles, operand in LDS, kind>`, `gemm_split_kernel<k-splits, kind>`, "
               "`gemm_mid_kernel<kind>` (its algorithmic bytes: the whole projection's; the published sums it "
               "writes and `gemm_mid_finish_kernel<kind>` reads back are traffic beyond them) with kind "

@@ -68,7 +68,10 @@ constexpr int kWideItemFloats = 8 * kGemmWaves * P * RT * 256;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <int RT, int P, int KIND, int KS = 1>
+// NT: the weight tiles are loaded with the non-temporal policy (launches of
+// few row groups, whose tiles are read about once); without it they stay in
+// L2 for the other row groups of a many-row launch.
+template <int RT, int P, int KIND, int KS = 1, bool NT = true>
 struct GemmWide {
   static_assert(KS == 1 || KS == 2 || KS == 4, "k-splits");
   static constexpr int NPR = KS == 2 ? 3 : 1;  // range partials a split > 0 holds besides tot
@@ -140,7 +143,10 @@ struct GemmWide {
       const uint8_t* tile = a.w + ((size_t)(ok ? u : 0) * NKB + (ok ? kb : 0)) * kTileBytes;
       const Rsrc r = make_rsrc(tile, ok ? (uint32_t)kTileBytes : 0u);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) w[p][j] = ld_stream_b128(r, (uint32_t)(lane * 16 + j * 1024));
+      for (int j = 0; j < 8; ++j) {
+        if constexpr (NT) w[p][j] = ld_stream_b128(r, (uint32_t)(lane * 16 + j * 1024));
+        else w[p][j] = ld_b128<false>(r, (uint32_t)(lane * 16 + j * 1024));
+      }
     }
   }
 

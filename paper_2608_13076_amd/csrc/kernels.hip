@@ -228,7 +228,7 @@ gemm_mid_finish_kernel(GemmParams a, int NUG, int KS, const float* part) {
   f.run();
 }
 
-template <int RT, int P, int KIND, int KS>
+template <int RT, int P, int KIND, int KS, bool NT = true>
 __global__ void __launch_bounds__(kGemmWaves * 64)
     gemm_wide_kernel(GemmParams a, int NRG, int NUG, uint32_t* cnt, float* part) {
   extern __shared__ uint4 lds_dyn[];
@@ -238,7 +238,7 @@ __global__ void __launch_bounds__(kGemmWaves * 64)
   const int ug = (b & 7) + 8 * j;
   if (ug >= NUG) return;  // uniform, before any barrier
   const int item = ug * NRG + rg;
-  GemmWide<RT, P, KIND, KS> g(a, *(GemmWideSmem<RT>*)lds_dyn, ug, rg, ks, KS > 1 ? cnt + item : nullptr,
+  GemmWide<RT, P, KIND, KS, NT> g(a, *(GemmWideSmem<RT>*)lds_dyn, ug, rg, ks, KS > 1 ? cnt + item : nullptr,
                               KS > 1 ? part + (size_t)item * kWideItemFloats<RT, P> : nullptr);
   g.run();
 }
@@ -1097,16 +1097,30 @@ hipError_t launch_split(int kind, const GemmParams& gp, int ks, int n_cu, uint32
   }
 }
 
-template <int RT, int P, int KIND, int KS>
-hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, uint32_t* cnt, float* part, hipStream_t st) {
-  const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, P, KIND, KS>);
+template <int RT, int P, int KIND, int KS, bool NT>
+hipError_t launch_wide_nt(const GemmParams& gp, int nrg, int nug, uint32_t* cnt, float* part, hipStream_t st) {
+  const void* fn = reinterpret_cast<const void*>(&gemm_wide_kernel<RT, P, KIND, KS, NT>);
   const uint32_t lds = gemm_wide_lds_bytes(RT);
   static hipError_t attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return attr;
   const int grid = 8 * ((nug + 7) / 8) * nrg * KS;
-  hipLaunchKernelGGL((gemm_wide_kernel<RT, P, KIND, KS>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp, nrg, nug,
-                     cnt, part);
+  hipLaunchKernelGGL((gemm_wide_kernel<RT, P, KIND, KS, NT>), dim3(grid), dim3(kGemmWaves * 64), lds, st, gp, nrg,
+                     nug, cnt, part);
   return hipGetLastError();
+}
+
+// Non-temporal weight loads for launches of at most kWideNtRowGroups row
+// groups (batched verification: 1-5); a many-row launch (prefill forwards:
+// 32 and more row groups re-read every tile) keeps them in L2 (7B prefill
+// down projection 256 -> 283 us per launch with them).  K-split launches
+// are few-row ones.
+constexpr int kWideNtRowGroups = 8;
+
+template <int RT, int P, int KIND, int KS>
+hipError_t launch_wide_rt(const GemmParams& gp, int nrg, int nug, uint32_t* cnt, float* part, hipStream_t st) {
+  if constexpr (KS == 1)
+    if (nrg > kWideNtRowGroups) return launch_wide_nt<RT, P, KIND, KS, false>(gp, nrg, nug, cnt, part, st);
+  return launch_wide_nt<RT, P, KIND, KS, true>(gp, nrg, nug, cnt, part, st);
 }
 
 template <int KIND, int KS>
