@@ -121,15 +121,18 @@ size_t spade_weight_bytes(const spade_config* cfg);
 size_t spade_workspace_bytes(const spade_config* cfg, int max_batch, int max_gamma, int max_len);
 
 /* Bytes of a KV cache holding max_batch requests of max_len positions.  With
- * S = max_len rounded up to a multiple of 256 and KVH the K/V heads: K is
- * [n_layers][max_batch][KVH][S][head_dim] (a row per position); V is
- * [n_layers][max_batch][KVH][S / 256] blocks of head_dim x 256 elements.  In
- * a bf16 cache a block holds the B operands of the attention's O = P V in
- * MFMA order: 1 KB fragments [head_dim / 16][8], fragment (t, s) covering
- * features 16 t .. + 15 and positions 32 s .. + 31 of the block, its 16-byte
- * piece 16 j + i holding positions 32 s + 8 j .. + 7 of feature 16 t + i; in
- * a float32 cache a block is [head_dim][256].  So one wave's fragment load is
- * 1 KB contiguous and one 256-key chunk of V one contiguous block.
+ * S = max_len rounded up to a multiple of 256 and KVH the K/V heads, K and V
+ * are each [n_layers][max_batch][KVH][S / 256] blocks of head_dim x 256
+ * elements.  In a bf16 cache a block holds the B operands of the attention's
+ * products in MFMA order, as 1 KB fragments.  K (S = Q K^T): fragments
+ * [16][head_dim / 32], fragment (u, s) covering positions 16 u .. + 15 and
+ * features 32 s .. + 31 of the block, its 16-byte piece 16 j + i holding
+ * features 32 s + 8 j .. + 7 of position 16 u + i.  V (O = P V): fragments
+ * [head_dim / 16][8], fragment (t, s) covering features 16 t .. + 15 and
+ * positions 32 s .. + 31, its piece 16 j + i holding positions 32 s + 8 j .. + 7
+ * of feature 16 t + i.  In a float32 cache a K block is [256][head_dim] (a row
+ * per position) and a V block [head_dim][256].  So one wave's fragment load is
+ * 1 KB contiguous and one 256-key chunk of K or V one contiguous block.
  * max_len <= 16384. */
 size_t spade_kv_bytes(const spade_config* cfg, int max_batch, int max_len);
 

@@ -9,10 +9,10 @@
 // row; O = P V runs with features split over the waves (wave w: features
 // [16 w, 16 w + 16) over every key of the chunk), so each wave ends with
 // final chunk outputs and no cross-wave sum is needed.  Both products use
-// MFMA 16x16x32 bf16 with Q and P split into two bf16 terms (hi + lo).  K is
-// stored as rows [pos][hd] and V in blocks of 256 positions in the order of
-// the B operands of O = P V (v_cache_index), so both B operands are 16-byte
-// loads.  A chunk writes its unnormalised output, row
+// MFMA 16x16x32 bf16 with Q and P split into two bf16 terms (hi + lo).  K and
+// V are stored in blocks of 256 positions in the order of the B operands of
+// S = Q K^T and O = P V (k_cache_index, v_cache_index), so every B-operand
+// fragment a wave loads is 1 KB contiguous.  A chunk writes its unnormalised output, row
 // max and row sum; the chunks of a (request, head) are merged in chunk order
 // with weights exp(m_c - max) / sum_c(l_c exp(m_c - max)).
 #pragma once
@@ -49,7 +49,7 @@ struct AttnItem {
   int L;           // cached keys of the request (row i sits at L + i)
   int nc;          // chunks of the request
   int k_lo, k_hi;  // keys of this chunk: [k_lo, k_hi)
-  const uint16_t* kc;  // K rows of (request, head)
+  const uint16_t* kc;  // K blocks of (request, head) (k_cache_index)
   const uint16_t* vc;  // V^T rows of (request, head)
 };
 
@@ -172,7 +172,7 @@ __device__ __forceinline__ void attn_load_k(const AttnItem& it, int wave, int la
     for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = make_uint4(0, 0, 0, 0);
     if (key < it.k_hi) {
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = ld_stream_g128(it.kc + (size_t)key * kAttnHd + 32 * ks + 8 * g);
+      for (int ks = 0; ks < 4; ++ks) kf[grp][ks] = ld_stream_g128(it.kc + k_cache_index(32 * ks + 8 * g, key, kAttnHd));
     }
   }
 }
@@ -826,6 +826,14 @@ __host__ __device__ inline unsigned attn_prefill_dyn_bytes(int W, int NC) { retu
 
 // piece c (8 features) of staged K row r; piece c (8 keys) of staged V^T row f
 __device__ __forceinline__ int pf_k_at(int r, int c) { return r * 16 + (c ^ (r & 15)); }
+// The K piece that staging thread e moves: row r (a position of the block),
+// piece c, in the cache's fragment order (k_cache_index), so 64 consecutive
+// threads read one 1 KB fragment: 16 positions x 32 features.
+__device__ __forceinline__ void pf_k_piece(int e, int& r, int& c) {
+  const int fr = e >> 6, ln = e & 63;
+  r = 16 * (fr >> 2) + (ln & 15);
+  c = 4 * (fr & 3) + (ln >> 4);
+}
 template <int SK>
 __device__ __forceinline__ int pf_v_at(int f, int c) {
   constexpr int CPR = SK / 8;
@@ -846,8 +854,9 @@ __device__ __forceinline__ void pf_fetch(int c, int b, int k_hi, int ke, const u
     const int e = (int)threadIdx.x + 64 * W * q;
     r[q] = make_uint4(0, 0, 0, 0);
     if (!is_v) {
-      const int row = e >> 4, pc = e & 15;
-      if (k0 + row < k_hi) r[q] = *(const uint4*)(kc + (size_t)(k0 + row) * kAttnHd + pc * 8);
+      int row, pc;
+      pf_k_piece(e, row, pc);
+      if (k0 + row < k_hi) r[q] = *(const uint4*)(kc + k_cache_index(pc * 8, k0 + row, kAttnHd));
     } else {
       const int f = e / CPR, pc = e % CPR, key = k0 + 8 * pc;
       if (key + 8 <= ke) r[q] = *(const uint4*)(vc + v_cache_index(f, key, kAttnHd));
@@ -861,7 +870,9 @@ __device__ __forceinline__ void pf_stash(AttnPfSmem<W, SK>& s, int slot, int b, 
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
     const int e = (int)threadIdx.x + 64 * W * q;
-    s.st[slot][b < NB ? pf_k_at(e >> 4, e & 15) : pf_v_at<SK>(e / CPR, e % CPR)] = r[q];
+    int kr, kpc;
+    pf_k_piece(e, kr, kpc);
+    s.st[slot][b < NB ? pf_k_at(kr, kpc) : pf_v_at<SK>(e / CPR, e % CPR)] = r[q];
   }
 }
 
@@ -873,7 +884,7 @@ __device__ __forceinline__ void pf_wave_sync() {
 }
 
 // q: this request's query rows ([R][d], head h's features at h * kAttnHd);
-// kc / vc: K rows and V^T rows of (request, K/V head); L: the request's
+// kc / vc: the K and V blocks of (request, K/V head); L: the request's
 // cached keys; t0: the group's first tile (tile t0 + wave for this wave).
 // out(row, dd, value) receives every output of the group's rows (row counted
 // from the request's first prompt row).  mlw: W * NCP * 16 pairs; NCP bounds

@@ -144,10 +144,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& a, int u, int ml
     v = hi ? (pv * sn + v * c) : (v * c - pv * sn);
     const Rsrc rq = make_rsrc(a.q_out + (size_t)a.m0 * a.d, (uint32_t)((size_t)a.M * a.d * 4));
     st_f32<COH>(rq, (rok && sec == 0) ? (uint32_t)(ml * a.d + h * a.hd + f) * 4u : kOob, v);
-    // K rows [pos][hd]; V in blocks of kVBlock positions (v_cache_index)
+    // K and V in blocks of kVBlock positions (k_cache_index, v_cache_index;
+    // a float32 K cache is [pos][hd])
     const uint32_t head = (uint32_t)(bg * a.Hkv + h) * (uint32_t)a.kv_stride * (uint32_t)a.hd;
     const uint32_t vel = (uint32_t)(a.kv_bf16 ? v_cache_index(f, pos, a.hd) : v_cache_index_f32(f, pos, a.hd));
-    const uint32_t elem = sec == 1 ? head + (uint32_t)(pos * a.hd + f) : head + vel;
+    const uint32_t kel = (uint32_t)(a.kv_bf16 ? k_cache_index(f, pos, a.hd) : (size_t)pos * a.hd + f);
+    const uint32_t elem = head + (sec == 1 ? kel : vel);
     const Rsrc rkv = make_rsrc(sec == 1 ? a.kc : a.vc, a.kv_bytes);
     const bool kok = rok && sec > 0;
     if (a.kv_bf16) st_b16<COH>(rkv, kok ? elem * 2u : kOob, f2bf(v));

@@ -346,7 +346,8 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   const size_t bh = (size_t)bl * p.H + h;
   float* po = p.part_o + ((bh * p.NC + c) * p.Rmax) * HD;
   float* pml = p.part_ml + ((bh * p.NC + c) * p.Rmax) * 2;
-  const size_t kbase = ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * HD;  // K rows [key][HD]
+  // K blocks (k_cache_index; a float32 K cache: rows [key][HD])
+  const size_t kbase = ((size_t)bg * p.Hkv + h / p.G) * p.kv_stride * HD;
   const size_t vbase = kbase;  // V blocks of kVBlock positions (v_cache_index, v_cache_index_f32)
 
   if (k_lo < k_hi) {
@@ -363,7 +364,7 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
         const int key = kw + 16 * grp + kl;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          kf[grp][ks] = key < k_hi ? *(const uint4*)(kc + kbase + (size_t)key * HD + 32 * ks + 8 * g)
+          kf[grp][ks] = key < k_hi ? *(const uint4*)(kc + kbase + k_cache_index(32 * ks + 8 * g, key, HD))
                                    : make_uint4(0, 0, 0, 0);
       }
       uint4 vf[FT];

@@ -45,6 +45,17 @@ __host__ __device__ inline size_t v_cache_index(int f, int pos, int hd) {
 __host__ __device__ inline size_t v_cache_index_f32(int f, int pos, int hd) {
   return ((size_t)(pos / kVBlock) * hd + f) * kVBlock + (pos % kVBlock);
 }
+// Element (feature f, position pos) of a (request, K/V head) K region of a
+// bf16 cache, in blocks of kVBlock positions: a block is the B operands of
+// S = Q K^T in MFMA order, fragment (16-position group p / 16, 32-feature
+// step f / 32) of 1 KB, whose lane 16 ((f / 8) % 4) + p % 16 holds features
+// 8 ((f / 8) % 4) .. + 7 of position p (p = pos % kVBlock), so one wave's
+// fragment load reads 1 KB contiguous.  A float32 K cache is [position][head_dim].
+__host__ __device__ inline size_t k_cache_index(int f, int pos, int hd) {
+  const int p = pos % kVBlock;
+  return (size_t)(pos / kVBlock) * hd * kVBlock +
+         (size_t)(((((p >> 4) * (hd >> 5) + (f >> 5)) * 64 + ((f >> 3) & 3) * 16 + (p & 15)) * 8) + (f & 7));
+}
 
 // Keys per chunk of the bf16 / head_dim-128 verify attention.  A constant:
 // a request's attention (and so its logits) must not depend on the other

@@ -221,12 +221,14 @@ def gpu_setup_streaming(w, max_len: int, max_batch: Optional[int] = None):
     return model, kv
 
 
-# The cache layout (include/spade.h, spade_kv_bytes): K rows
-# [position][head_dim]; V in blocks of V_BLOCK positions -- bf16: the B
-# operands of O = P V in MFMA order, 1 KB fragments (16-feature tile,
+# The cache layout (include/spade.h, spade_kv_bytes): K and V in blocks of
+# V_BLOCK positions.  bf16 K: the B operands of S = Q K^T in MFMA order, 1 KB
+# fragments (16-position group, 32-feature step) whose lane 16 ((f / 8) % 4)
+# + p % 16 holds features 8 ((f / 8) % 4) .. + 7; float32 K: [V_BLOCK][head_dim].
+# bf16 V: the B operands of O = P V, 1 KB fragments (16-feature tile,
 # 32-position step) whose lane 16 ((p / 8) % 4) + f % 16 holds positions
-# 8 ((p / 8) % 4) .. + 7; float32: [head_dim][V_BLOCK]; positions per (request,
-# K/V head): max_len rounded up to a whole block.
+# 8 ((p / 8) % 4) .. + 7; float32 V: [head_dim][V_BLOCK].  Positions per
+# (request, K/V head): max_len rounded up to a whole block.
 V_BLOCK = 256
 
 
@@ -246,18 +248,37 @@ def v_phys_index(shape, S: int) -> np.ndarray:
     return (blk * hd + f) * V_BLOCK + p
 
 
+def k_phys_index(shape, S: int) -> np.ndarray:
+    """[S, head_dim]: the element offset of (position, feature) in a
+    (request, K/V head) region of the K cache."""
+    hd = shape.head_dim
+    pos = np.arange(S)[:, None]
+    f = np.arange(hd)[None, :]
+    if shape.kv_dtype == "bf16":
+        blk, p = pos // V_BLOCK, pos % V_BLOCK
+        return blk * hd * V_BLOCK + (((p // 16) * (hd // 32) + f // 32) * 64 + ((f // 8) % 4) * 16 + p % 16) * 8 + f % 8
+    return pos * hd + f
+
+
 def kv_views(kv, shape, max_len: int):
-    """K as [layer][request][K/V head][position][head_dim] and V as
-    [layer][request][K/V head][region] views of the cache (v_phys_index maps
-    a region's elements)."""
+    """K and V as [layer][request][K/V head][region] views of the cache
+    (k_phys_index and v_phys_index map a region's elements)."""
     import torch
     S = kv_stride(max_len)
     dt = torch.int16 if shape.kv_dtype == "bf16" else torch.float32
     half = kv.buf.numel() // 2
     n = shape.n_layers * kv.max_batch * shape.kv_heads * S * shape.head_dim
-    k = kv.buf[:half].view(dt)[:n].view(shape.n_layers, kv.max_batch, shape.kv_heads, S, shape.head_dim)
+    k = kv.buf[:half].view(dt)[:n].view(shape.n_layers, kv.max_batch, shape.kv_heads, S * shape.head_dim)
     v = kv.buf[half:].view(dt)[:n].view(shape.n_layers, kv.max_batch, shape.kv_heads, S * shape.head_dim)
     return k, v
+
+
+def k_by_position(k, shape, max_len: int):
+    """[..., region] -> [..., position, head_dim] (a copy)."""
+    import torch
+    S = kv_stride(max_len)
+    idx = torch.as_tensor(k_phys_index(shape, S).reshape(-1), device=k.device)
+    return k[..., idx].reshape(*k.shape[:-1], S, shape.head_dim)
 
 
 def v_by_position(v, shape, max_len: int):

@@ -27,7 +27,7 @@ import pytest
 
 from synth import make_inputs, workload
 from tests.golden.drafts import HERE as GOLDEN_DIR, load_golden
-from tests.helpers import gpu_prefill, gpu_setup_streaming, gpu_verify, kv_stride, report_parity
+from tests.helpers import gpu_prefill, gpu_setup_streaming, gpu_verify, k_phys_index, kv_stride, report_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -307,8 +307,9 @@ def _check_layer0_keys(w, inp, kv, max_len, n_samples=24):
         cs, sn = rope_tables(np.array([pos]), m.head_dim, m.rope_theta)
         k = bf16_round(apply_rope(k, cs, sn))[0]
         for hh in (0, KVH - 1):
-            off = ((b * KVH + hh) * stride + pos) * m.head_dim
-            row = kcache[off: off + m.head_dim].cpu().numpy()
+            off = (b * KVH + hh) * stride * m.head_dim
+            idx = torch.as_tensor(off + k_phys_index(m, stride)[pos], device=kcache.device)
+            row = kcache[idx].cpu().numpy()
             got = (row.view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
             # equal up to one bf16 rounding step of float32 differences
             np.testing.assert_allclose(got, k[hh], rtol=2 ** -7, atol=1e-6)

@@ -19,7 +19,7 @@ import numpy as np
 import pytest
 
 from synth import ModelWeights, make_inputs, mini_workloads
-from tests.helpers import gpu_setup, gpu_verify, kv_stride, kv_views, v_phys_index
+from tests.helpers import gpu_setup, gpu_verify, k_phys_index, kv_stride, kv_views, v_phys_index
 
 pytestmark = pytest.mark.gpu
 
@@ -34,8 +34,7 @@ def need_gpu():
 
 
 def _views(kv, shape, max_len):
-    """K as [layer][request][K/V head][position][hd] and V as [layer][request]
-    [K/V head][region] over the cache buffer."""
+    """K and V as [layer][request][K/V head][region] over the cache buffer."""
     return kv_views(kv, shape, max_len)
 
 
@@ -54,6 +53,7 @@ def _two_rounds(w, weights, fill, merge, grouped):
         model.set_attn_grouped(grouped)
     k, v = _views(kv, w.model, max_len)
     vidx = v_phys_index(w.model, kv_stride(max_len))
+    kidx = k_phys_index(w.model, kv_stride(max_len))
     if fill == "nan":
         k.fill_(_nan_value(w.model))
         v.fill_(_nan_value(w.model))
@@ -67,7 +67,8 @@ def _two_rounds(w, weights, fill, merge, grouped):
     lens, _ = kv.get_state(w.batch)
     if fill == "nan":  # the rolled-back drafts' rows and everything after them
         for b in range(w.batch):
-            k[:, b, :, int(lens[b]):, :] = _nan_value(w.model)
+            kpast = torch.as_tensor(kidx[int(lens[b]):, :].reshape(-1), device=k.device)
+            k[:, b, :, kpast] = _nan_value(w.model)
             past = torch.as_tensor(vidx[:, int(lens[b]):].reshape(-1), device=v.device)
             v[:, b, :, past] = _nan_value(w.model)
     inp2 = make_inputs(w, round_index=1)

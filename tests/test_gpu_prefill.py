@@ -18,7 +18,7 @@ import numpy as np
 import pytest
 
 from synth import ModelWeights, make_inputs, mini_workloads
-from tests.helpers import gpu_setup, gpu_verify, kv_views, v_by_position
+from tests.helpers import gpu_setup, gpu_verify, k_by_position, kv_views, v_by_position
 
 pytestmark = pytest.mark.gpu
 
@@ -43,7 +43,8 @@ def _assert_same_cache(model, kv1, kv2, B, max_len):
     k2, v2 = kv_views(kv2, s, max_len)
     for b in range(B):
         n = int(l1[b])
-        assert torch.equal(k1[:, b, :, :n], k2[:, b, :, :n]), ("k", b)
+        assert torch.equal(k_by_position(k1[:, b], s, max_len)[..., :n, :], k_by_position(k2[:, b], s, max_len)[..., :n, :]), \
+            ("k", b)
         assert torch.equal(v_by_position(v1[:, b], s, max_len)[..., :n], v_by_position(v2[:, b], s, max_len)[..., :n]), \
             ("v", b)
 
