@@ -517,15 +517,20 @@ struct Gemm {
   // inputs of item t + 2 into enew, finish the unit with ecur
   __device__ __forceinline__ void step_impl(int t, uint4 (&w)[8], EpiIn& ecur, EpiIn& enew) {
     const int k = t - (t / nkw) * nkw;
-    if constexpr (ALDS) read_a_lds(k);
-    mma(w, av);
+    // a padding item (t >= T, the same in every wave) only keeps the loads'
+    // count: its MFMAs and its unit's sum would be discarded
+    const bool live = t < T;
+    if (live) {
+      if constexpr (ALDS) read_a_lds(k);
+      mma(w, av);
+    }
     // the refills below reuse the registers just consumed: keep them after
     // the MFMAs so no fourth tile is ever live
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (!ALDS) issue_a_t(t + 1, av);
     issue_w(t + 3, w);
     enew = epi_load(t + 2);
-    if (k == nkw - 1) unit_end(t, ecur);
+    if (live && k == nkw - 1) unit_end(t, ecur);
   }
 
   // The item loop (no exits inside; the item count is padded to a multiple of

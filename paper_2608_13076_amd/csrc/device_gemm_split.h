@@ -205,11 +205,16 @@ struct GemmSplit {
 
   __device__ __forceinline__ void step_impl(int t, uint4 (&w)[8]) {
     const int k = t - (t / nkw) * nkw;
-    read_a_lds(k);
-    mma(w);
+    // a padding item (t >= T, the same in every wave) only keeps the loads'
+    // count: its MFMAs and its group's sum would be discarded
+    const bool live = t < T;
+    if (live) {
+      read_a_lds(k);
+      mma(w);
+    }
     __builtin_amdgcn_sched_barrier(0);
     issue_w(t + 3, w);
-    if (k == nkw - 1) group_end(t);
+    if (live && k == nkw - 1) group_end(t);
   }
 
   // the last arrival of group grp: continue split 0's running sum over the
